@@ -1,0 +1,62 @@
+"""Plants plausible mistakes in a copy of the oracle (on the CPU) and checks that
+at least one pin catches each.  The oracle module on disk is never modified."""
+import os
+import sys
+import types
+
+import pytest
+
+import oracle_pins
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = open(os.path.join(ROOT, "oracle", "nlr.py")).read()
+
+# (name, original text, mutated text)
+MUTATIONS = [
+    ("sign of the 2 Ahat U term", "return 2.0 * AU + np.outer", "return -2.0 * AU + np.outer"),
+    ("dropped 1 s^T term", " + np.outer(np.ones(U.shape[0]), U.T @ ybar)", ""),
+    ("dropped ybar p^T term", "2.0 * AU + np.outer(ybar, colsum) +", "2.0 * AU +"),
+    ("p and s swapped", "np.outer(ybar, colsum) + np.outer(np.ones(U.shape[0]), U.T @ ybar)",
+     "np.outer(ybar, U.T @ ybar) + np.outer(np.ones(U.shape[0]), colsum)"),
+    ("beta/sqrt(n) in ybar", "(beta / n) * constraint_g(U)", "(beta / np.sqrt(n)) * constraint_g(U)"),
+    ("y not scaled in ybar", "return y / np.sqrt(n) + (beta / n)", "return y + (beta / n)"),
+    ("projection by K not sqrt(K)", "return np.sqrt(K) * Vp / nrm", "return K * Vp / nrm"),
+    ("no positive part", "W = np.maximum(U - alpha * G, 0.0)", "W = U - alpha * G"),
+    ("ascent instead of descent", "W = np.maximum(U - alpha * G, 0.0)", "W = np.maximum(U + alpha * G, 0.0)"),
+    ("c = K/a", "c = float(np.sqrt(K / a))", "c = float(K / a)"),
+    ("dual step sign", "y = y + (beta / sqrtn) * q", "y = y - (beta / sqrtn) * q"),
+    ("dual step scale", "y = y + (beta / sqrtn) * q", "y = y + beta * q"),
+    ("dual step uses stale residual", "q = constraint_g(U)  # p = U^T 1", "q = constraint_g(res.U)  # p = U^T 1"),
+    ("movement not divided by sqrt(K)", "np.linalg.norm(U_new - U) / np.sqrt(K)", "np.linalg.norm(U_new - U)"),
+    ("no centring", "Xc = X - xbar[None, :]", "Xc = X"),
+    ("squared spectral norm", "return float(np.sqrt(max(lam, 0.0)))", "return float(max(lam, 0.0))"),
+    ("penalty without 1/2", "0.5 * beta * (hU @ hU)", "beta * (hU @ hU)"),
+    ("residual without -1", "return U @ U.sum(axis=0) - 1.0", "return U @ U.sum(axis=0)"),
+    ("h not scaled", "return constraint_g(U) / np.sqrt(U.shape[0])", "return constraint_g(U)"),
+    ("Lipschitz bound without the beta term", "2.0 * np.linalg.norm(y) + beta * (6.0 * K + 2.0))", "2.0 * np.linalg.norm(y))"),
+    ("argmax over columns", "np.argmax(np.asarray(U), axis=1)", "np.argmax(np.asarray(U), axis=0)"),
+    ("objective sign", "return float(-np.sum(Theta * Theta) + y @ hU", "return float(np.sum(Theta * Theta) + y @ hU"),
+]
+
+
+def _load_mutant(monkeypatch, orig, new):
+    assert orig in SRC, f"mutation anchor not found: {orig!r}"
+    mod = types.ModuleType("oracle_nlr_mutant")
+    mod.__file__ = "<mutant>"
+    monkeypatch.setitem(sys.modules, mod.__name__, mod)
+    exec(compile(SRC.replace(orig, new), "<mutant>", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name,orig,new", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_mutation_is_caught(monkeypatch, name, orig, new):
+    mutant = _load_mutant(monkeypatch, orig, new)
+    monkeypatch.setattr(oracle_pins, "nlr", mutant)
+    caught = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin()
+        except Exception as e:  # any failure (assertion, error) counts as caught
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin catches the planted mistake: {name}"
