@@ -1,0 +1,206 @@
+#!/usr/bin/env python3
+"""Benchmark of the NLR iteration on one MI355X.
+
+A "step" is one full iteration of Algorithm 1 (pass A, Theta reduction,
+control, fused pass B, control) over the whole synthetic Gaussian-mixture
+matrix, which is resident in HBM before timing starts.  `value` is
+points*iterations per second over the timed run.  The `roofline` object
+describes the dominant kernel, timed with HIP events on the library's stream
+inside the same timed region; `cpu_baseline` times the fp64 oracle on a
+bounded sample of the same workload on the host cores.
+
+Usage: python bench.py [--gpus 1] [--steps 50] [--warmup 3] [--workload gmm10m]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "NLR points·iters/sec + achieved HBM GB/s (n=1e7,d=128,K=64, fp32)"
+HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def eprint(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(kind: str, n: int, d: int, r: int, dual_frac: float = 0.0) -> float:
+    """Bytes each kernel must move per launch (fp32 = 4 B), independent of caching."""
+    if kind == "pass_b":      # read Xhat, read U, write W over U, read ytilde
+        return 4.0 * (n * d + 2 * n * r + n)
+    if kind == "pass_a":      # read Xhat, read U, read ytilde (+ write it on dual steps)
+        return 4.0 * (n * d + n * r + n) + 4.0 * n * dual_frac
+    if kind == "step":        # whole iteration, two-pass structure
+        return 4.0 * (2 * n * d + 3 * n * r + 2 * n) + 4.0 * n * dual_frac
+    raise ValueError(kind)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("k_iter.hip", "nlr_internal.hpp"):
+        with open(os.path.join(ROOT, "paper_2609_36074_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM traffic of `kernel` from the committed rocprofv3 --pmc summary, or None
+    when there is none or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            t = json.load(f)
+        if t.get("kernel_source_hash") != kernel_source_hash():
+            return None
+        return float(t["bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def cpu_baseline(workload, n_sample: int, iters: int) -> dict:
+    """Times the fp64 oracle's iteration loop on a bounded sample of the workload."""
+    import numpy as np
+
+    from oracle import nlr as onlr
+    from synth import make_workload
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    X, Z, _, wl = make_workload(workload, n=n_sample)
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    U0 = onlr.project_omega(Z.astype(np.float64), wl.K)
+    alpha = onlr.default_step_size(wl.K)
+    t0 = time.perf_counter()
+    onlr.run(Xh, U0, wl.K, alpha, 1.0, T=iters, T_min=iters, project_init=False)
+    dt = time.perf_counter() - t0
+    return {"value": n_sample * iters / dt, "unit": "points*iters/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"fp64 oracle loop, {iters} iterations on the first {n_sample} rows of the same "
+                      f"seeded {workload} mixture (d={wl.d}, K=r={wl.K}); {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="gmm10m")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=2_000_000)
+    ap.add_argument("--cpu-iters", type=int, default=8)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}): the NLR path here is the "
+              "single-GPU kernel set; multi-GPU row sharding is described in DESIGN.md but not built.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_36074_amd import nlr
+    from synth import WORKLOADS, make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = WORKLOADS[args.workload]
+    n, d, r, K = wl.n, wl.d, wl.r, wl.K
+    eprint(f"[bench] generating {args.workload}: n={n} d={d} K=r={K}")
+    t0 = time.perf_counter()
+    X, Z, _, _ = make_workload(wl)
+    eprint(f"[bench] generated in {time.perf_counter() - t0:.1f} s; uploading")
+    dev = torch.device("cuda:0")
+    Xt = torch.from_numpy(X).to(dev)
+    Ut = torch.from_numpy(Z).to(dev)
+    del X, Z
+    torch.cuda.synchronize()
+    alpha = 1.0 / (2.0 * (2.0 + 1.0 * (6.0 * K + 2.0)))  # half the Prop. 1 step bound at y = 0, beta = 1
+    steps, warm = args.steps, args.warmup
+    ctx = nlr.Context(Xt, K, Ut, alpha=alpha, beta=1.0, eps_d=1e-4, eps_c=1e-4, T_min=1 << 30)
+    eprint("[bench] init done; warmup")
+    if warm > 0:
+        ctx.run(warm)
+    torch.cuda.synchronize()
+
+    ctx.set_profiling(True)
+    stream = ctx.stream
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    done, last = ctx.run(steps)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t_ms = ev0.elapsed_time(ev1)
+    kt = ctx.kernel_times()
+    ctx.set_profiling(False)
+    assert done == steps, (done, steps)
+    hist = ctx.history(steps)
+    dual_frac = float(np.mean([h["dual_step"] for h in hist])) if hist else 0.0
+
+    value = n * steps / (t_ms / 1e3)
+    step_bytes = algorithmic_bytes("step", n, d, r, dual_frac)
+    eff_gbs = step_bytes * steps / (t_ms / 1e3) / 1e9
+    flops = 4.0 * n * d * r
+    kinfo = {k: {"total_ms": v[0], "launches": v[1], "avg_ms": (v[0] / v[1]) if v[1] else None}
+             for k, v in kt.items() if v[1]}
+    dom = max(("pass_a", "pass_b"), key=lambda k: kinfo.get(k, {"total_ms": 0})["total_ms"])
+    dom_ms = kinfo[dom]["avg_ms"]
+    dom_bytes = algorithmic_bytes(dom, n, d, r, dual_frac)
+    achieved = dom_bytes / (dom_ms / 1e3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": load_traffic(dom, args.workload),
+                "kernel": dom, "avg_launch_ms": round(dom_ms, 4),
+                "algorithmic_bytes_per_launch": dom_bytes,
+                "mfma_tflops": round(2.0 * n * d * r / (dom_ms / 1e3) / 1e12, 2),
+                "mfma_frac": round(2.0 * n * d * r / (dom_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4)}
+    eprint(f"[bench] {steps} steps in {t_ms:.2f} ms -> {t_ms / steps:.3f} ms/step, {value:.3e} pts*it/s, "
+           f"effective {eff_gbs:.0f} GB/s ({eff_gbs / HBM_PEAK_GBS:.1%} of HBM), "
+           f"{flops * steps / (t_ms / 1e3) / 1e12:.1f} TFLOP/s")
+    for k, v in kinfo.items():
+        eprint(f"[bench]   {k:13s} {v['avg_ms'] * 1e3:9.1f} us x {v['launches']}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        eprint("[bench] cpu baseline (fp64 oracle) ...")
+        cpu = cpu_baseline(args.workload, min(args.cpu_sample, n), args.cpu_iters)
+        eprint(f"[bench] cpu baseline {cpu['value']:.3e} pts*it/s on {cpu['cores']} threads")
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "points*iters/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": t_ms / steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "n": n, "d": d, "K": K, "r": r, "alpha": alpha, "beta": 1.0,
+                   "eps_d": 1e-4, "eps_c": 1e-4, "dual_step_fraction": dual_frac},
+        "achieved_hbm_gbs": round(eff_gbs, 1),
+        "hbm_frac": round(eff_gbs / HBM_PEAK_GBS, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kinfo,
+    }
+    print(json.dumps(out), flush=True)
+    ctx.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,180 @@
+/*
+ * nlr.h — C ABI of the MI355X (gfx950) NLR K-means iteration library (libnlr.so).
+ *
+ * The library runs the spectrally normalised nonnegative low-rank (NLR)
+ * projected-gradient iteration for the K-means SDP relaxation (GEM-KMeans):
+ *
+ *   minimise  fhat_y(U) = <Ahat, U U^T> + y^T h(U) + beta/2 ||h(U)||^2
+ *   over      Omega = { U in R^{n x r} : U >= 0, ||U||_F^2 = K },
+ *   with      Ahat = -Xhat Xhat^T,  h(U) = (U U^T 1 - 1) / sqrt(n)
+ *
+ * (paper Section 2, eq. Kmeans_NLR; Section 3, eq. normalized).  One
+ * iteration is Algorithm 1 (Section 4.3): Theta = Xhat^T U; the gradient step
+ * and positive part of eq. (gpu-positive-update) fused with the statistics of
+ * eq. (fused-statistics); the normalising multiplier, movement estimate
+ * (eq. movement-estimate), gated dual ascent and stopping rule.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All matrices are row-major and contiguous.  X is n x d, U is n x r.
+ * - Pointers named X, U, y, labels, workspace are DEVICE pointers owned by
+ *   the caller; the library never allocates, frees or retains device memory
+ *   beyond the lifetime the caller gives it.  Pointers must be 4-byte aligned
+ *   (16-byte alignment enables vector loads), the workspace 256-byte aligned.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Every kernel is enqueued on it; host-visible results are synchronised on
+ *   it only where a function says so.
+ * - Functions return nlr_status.  Argument errors are detected before any
+ *   HIP call and leave device memory untouched.  A HIP failure or a
+ *   normalisation breakdown makes the context sticky-failed: later calls on
+ *   it return NLR_ESTATE (nlr_destroy still works).
+ * - A context is not thread-safe; two contexts may share a device and stream.
+ * - The dual buffer y holds the STORED dual ytilde = y_math / sqrt(n), and the
+ *   penalty is applied as beta / n (Section 3, Appendix C "Storage and
+ *   parameter conventions").
+ */
+#ifndef NLR_H
+#define NLR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct nlr_ctx nlr_ctx; /* opaque host-side handle: scalars + borrowed pointers */
+
+typedef enum {
+  NLR_OK = 0,
+  NLR_EINVAL = 1,       /* invalid argument (nothing enqueued) */
+  NLR_EWORKSPACE = 2,   /* workspace NULL, misaligned or smaller than nlr_workspace_bytes */
+  NLR_EBREAKDOWN = 3,   /* normalisation breakdown: ||W_+||_F <= 1e-20 (Algorithm 1) */
+  NLR_EDEGENERATE = 4,  /* centred data is zero, so a = ||X_c||_2 = 0 (Section 3 needs a > 0) */
+  NLR_EHIP = 5,         /* a HIP runtime call failed */
+  NLR_ESTATE = 6,       /* context failed earlier, or was used out of order */
+  NLR_EUNSUPPORTED = 7  /* shape outside the compiled kernel family (see nlr_init) */
+} nlr_status;
+
+/* Algorithm parameters (Algorithm 1 "Require" line).  The paper fixes no
+ * values; alpha must be > 0 and finite, beta > 0, eps_d >= 0, eps_c >= 0,
+ * T_min >= 0. */
+typedef struct {
+  double alpha;   /* primal step size */
+  double beta;    /* augmentation (penalty) parameter; the kernels use beta/n */
+  double eps_d;   /* dual-ascent tolerance: dual step iff Delta < eps_d^2 K */
+  double eps_c;   /* convergence tolerance on movement and feasibility */
+  int32_t T_min;  /* stop only once at least T_min iterations are done */
+  int32_t reserved;
+} nlr_params;
+
+/* Per-iteration record.  For iteration t (0-based; it maps U_t to U_{t+1}):
+ *   objective, theta_fro2 : fhat_{y_t}(U_t) and ||Xhat^T U_t||_F^2 (eq. normalized)
+ *   a, b, h               : ||W||_F^2, ||U_t||_F^2, <W, U_t>_F, FP64 (eq. fused-statistics)
+ *   c                     : FP32(sqrt(K)/sqrt(a)) computed from an FP64 ratio (Appendix B, Alg. 2)
+ *   delta                 : sqrt(max(c^2 a + b - 2 c h, 0) / K) with the rounded c (eq. movement-estimate)
+ *   dual_step             : Delta < eps_d^2 K, the dual step taken at the end of iteration t
+ *   rho                   : ||q_{t+1}||_2 / sqrt(n), q = U p - 1 of U_{t+1}
+ *   stop                  : the stopping rule of Section 4.3 fired at iteration t
+ *   breakdown             : normalisation breakdown at iteration t (U then holds W) */
+typedef struct {
+  int64_t t;
+  double objective;
+  double theta_fro2;
+  double a, b, h;
+  double delta;
+  double rho;
+  float c;
+  int32_t dual_step;
+  int32_t stop;
+  int32_t breakdown;
+} nlr_iter_stats;
+
+/* nlr_init flags */
+enum {
+  NLR_INIT_U_IN_OMEGA = 1, /* U already lies in Omega: skip the projection (resume) */
+  NLR_INIT_KEEP_Y = 2,     /* keep the caller's y instead of zeroing it (resume) */
+  NLR_INIT_X_NORMALISED = 4 /* X already holds Xhat: skip centring and spectral normalisation */
+};
+
+/* Bytes of device workspace nlr_init needs for an (n, d, r) problem.  Depends
+ * only on (n, d, r).  Returns 0 when the shape is invalid or unsupported. */
+size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r);
+
+/* Prepares a problem and enqueues the initialisation on `stream`:
+ *   1. centring and spectral normalisation of X in place (Section 3):
+ *      xbar (FP64 column means), C = X_c^T X_c (FP64), a = sqrt(lambda_max(C))
+ *      by power iteration, X <- (X - 1 xbar^T) / a   [skipped with X_NORMALISED]
+ *   2. U <- Pi_Omega(U) = sqrt(K) U_+ / ||U_+||_F (eq. projected-primal-step)
+ *      [skipped with U_IN_OMEGA]; p = U^T 1
+ *   3. y <- 0 [skipped with KEEP_Y]
+ * X: device n*d floats (in: data, out: Xhat).  U: device n*r floats (in: U_0,
+ * e.g. the paper's random start Z with N(0,1) entries; out: Pi_Omega(U_0)).
+ * y: device n floats (stored dual).  Requires 1 <= K <= r <= 256, r <= n,
+ * 1 <= d <= 4096, n < 2^40 (r > 256 returns NLR_EUNSUPPORTED).  Synchronises `stream` once at the end to report
+ * NLR_EDEGENERATE / NLR_EBREAKDOWN (U_0 with no positive entry).  On success
+ * *ctx receives a new context. */
+nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, int32_t r,
+                    float* U, float* y, const nlr_params* params, uint32_t flags,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Replaces the algorithm parameters of a context (takes effect at the next step). */
+nlr_status nlr_set_params(nlr_ctx* ctx, const nlr_params* params);
+
+/* One iteration of Algorithm 1, enqueued asynchronously.  On return U holds
+ * U_{t+1} and y the stored dual after the (gated) dual step.  When `stats` is
+ * non-NULL the stream is synchronised and the iteration's record written.
+ * Returns NLR_EBREAKDOWN if the iteration broke down (only known when stats
+ * is non-NULL; otherwise reported by the next synchronising call). */
+nlr_status nlr_step(nlr_ctx* ctx, nlr_iter_stats* stats);
+
+/* Up to T iterations of Algorithm 1, stopping early by the rule of Section
+ * 4.3 (movement < min(eps_d, eps_c), rho < eps_c, t+1 >= T_min).  The device
+ * decides; the host polls a flag every 32 iterations and synchronises once
+ * at the end.  *iters_done (nullable) receives the iterations done by this
+ * call; *last (nullable) the record of the last one.  nlr_run(T) and T calls
+ * of nlr_step give bitwise-identical U and y. */
+nlr_status nlr_run(nlr_ctx* ctx, int32_t T, int32_t* iters_done, nlr_iter_stats* last);
+
+/* Row-argmax labels of the current U: labels[i] = argmax_j U_ij, lowest j on
+ * ties (int32, device pointer, n entries).  Asynchronous. */
+nlr_status nlr_labels(nlr_ctx* ctx, int32_t* labels);
+
+/* Copies the records of the most recent iterations (oldest first, at most the
+ * last 4096) into host memory `out` (capacity `max_records`); *count receives
+ * the number written.  Synchronises the stream. */
+nlr_status nlr_history(nlr_ctx* ctx, nlr_iter_stats* out, int32_t max_records, int32_t* count);
+
+/* Synchronises and returns the spectral normaliser a = ||X_c||_2 and, when
+ * xbar_host is non-NULL, the d column means (FP64) found by nlr_init. */
+nlr_status nlr_normaliser(nlr_ctx* ctx, double* a, double* xbar_host);
+
+/* Diagnostic read-back (synchronises): what = 0 copies Theta = Xhat^T U of the
+ * latest iteration as d*r row-major floats; 1 copies p = U^T 1 (r floats) of
+ * the current U; 2 copies s = U^T ybar (r floats) of the latest iteration. */
+nlr_status nlr_inspect(nlr_ctx* ctx, int32_t what, void* host_dst, size_t bytes);
+
+/* Per-kernel timing with HIP events recorded on the context's stream around
+ * every launch made by nlr_step / nlr_run (off by default).  enable = 0 turns
+ * it off and clears the totals. */
+nlr_status nlr_set_profiling(nlr_ctx* ctx, int32_t enable);
+
+/* Kernel timing totals since profiling was enabled (synchronises).  For kernel
+ * k < *n_kernels: names[k] (static string), total_ms[k], launches[k].
+ * Arrays must hold NLR_MAX_KERNEL_KINDS entries. */
+#define NLR_MAX_KERNEL_KINDS 16
+nlr_status nlr_kernel_times(nlr_ctx* ctx, const char** names, double* total_ms,
+                            int64_t* launches, int32_t* n_kernels);
+
+/* Releases the host-side handle (device memory stays the caller's). */
+void nlr_destroy(nlr_ctx* ctx);
+
+const char* nlr_status_string(nlr_status s);
+
+/* Library build identification (static string). */
+const char* nlr_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NLR_H */

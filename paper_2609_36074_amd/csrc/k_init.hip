@@ -1,0 +1,418 @@
+// Initialisation kernels for gfx950: centring and spectral normalisation
+// (Section 3: X_c = X - 1 xbar^T, a = ||X_c||_2, Xhat = X_c / a), projection of
+// the starting factor onto Omega (eq. projected-primal-step) and p = U^T 1.
+//
+// a is found as sqrt(lambda_max(C)) with C = X_c^T X_c (FP64), by the power
+// method: C is first squared kSquarings times with trace normalisation
+// (B_{k+1} = (B_k / tr B_k)^2, i.e. the power C^(2^k) up to scale), the column
+// of the last B with the largest diagonal entry starts kPowerIters ordinary
+// power iterations on C, and the Rayleigh quotient of the final unit vector is
+// lambda_max.  Appendix D notes C is reused from this normalisation by the
+// data-informed initialisation.
+#include "nlr_internal.hpp"
+
+namespace nlr {
+
+__global__ void k_ctl_init(Bufs B, float gamma_f) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    DevCtl* c = B.ctl;
+    c->stop = 0;
+    c->breakdown = 0;
+    c->gate = 0;
+    c->degenerate = 0;
+    c->t_done = 0;
+    c->pad64 = 0;
+    c->c_f = 1.0f;
+    c->pad_f = gamma_f;
+    c->pad_i0 = c->pad_i1 = 0;
+    c->a = c->b = c->h = 0.0;
+    c->Delta = c->delta = 0.0;
+    c->rho = c->objective = c->theta_fro2 = 0.0;
+    c->spectral_a = 1.0;
+  }
+}
+
+__global__ void k_clear_stop(Bufs B) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) B.ctl->stop = 0;
+}
+
+// Column sums of X over row chunks (FP64).  Threads map to (column, row offset).
+__global__ __launch_bounds__(kThreads) void k_colsum(Geometry g, Bufs B) {
+  __shared__ double red[kThreads];
+  const int tid = threadIdx.x;
+  const int64_t n = g.n;
+  const int d = g.d;
+  const int64_t r0 = (int64_t)blockIdx.x * n / g.GI;
+  const int64_t r1 = (int64_t)(blockIdx.x + 1) * n / g.GI;
+  double* out = B.i_colsum + (int64_t)blockIdx.x * d;
+  if (d <= kThreads) {
+    const int rstep = kThreads / d;
+    const int col = tid % d;
+    const int rsub = tid / d;
+    double acc = 0.0;
+    if (rsub < rstep)
+      for (int64_t i = r0 + rsub; i < r1; i += rstep) acc += (double)B.X[i * d + col];
+    red[tid] = acc;
+    __syncthreads();
+    if (tid < d) {
+      double t = 0.0;
+      for (int k = 0; k < rstep; ++k) t += red[tid + k * d];
+      out[tid] = t;
+    }
+  } else {
+    for (int col = tid; col < d; col += kThreads) {
+      double acc = 0.0;
+      for (int64_t i = r0; i < r1; ++i) acc += (double)B.X[i * d + col];
+      out[col] = acc;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_colmean(Geometry g, Bufs B) {
+  const int j = blockIdx.x * kThreads + threadIdx.x;
+  if (j >= g.d) return;
+  double t = 0.0;
+  for (int gx = 0; gx < g.GI; ++gx) t += B.i_colsum[(int64_t)gx * g.d + j];
+  B.i_xbar[j] = t / (double)g.n;
+}
+
+// Partial centred Gram blocks: block (bi, bj) of sum over the chunk's rows of
+// (x - xbar)(x - xbar)^T, FP64.  Thread (ta, tb) owns entries (32 bi + ta, 32 bj + 4 tb + e).
+__global__ __launch_bounds__(kThreads) void k_gram(Geometry g, Bufs B) {
+  __shared__ double xa[64][33];
+  __shared__ double xb[64][33];
+  const int tid = threadIdx.x;
+  const int d = g.d;
+  const int bi = blockIdx.y / g.gblk;
+  const int bj = blockIdx.y - bi * g.gblk;
+  const int64_t n = g.n;
+  const int64_t r0 = (int64_t)blockIdx.x * n / g.GG;
+  const int64_t r1 = (int64_t)(blockIdx.x + 1) * n / g.GG;
+  const int ta = tid >> 3, tb = tid & 7;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int64_t t0 = r0; t0 < r1; t0 += 64) {
+    __syncthreads();
+    for (int v = tid; v < 64 * 32; v += kThreads) {
+      const int rr = v >> 5, cc = v & 31;
+      const int64_t i = t0 + rr;
+      const int ca = bi * 32 + cc, cb = bj * 32 + cc;
+      double va = 0.0, vb = 0.0;
+      if (i < r1) {
+        if (ca < d) va = (double)B.X[i * d + ca] - B.i_xbar[ca];
+        if (cb < d) vb = (double)B.X[i * d + cb] - B.i_xbar[cb];
+      }
+      xa[rr][cc] = va;
+      xb[rr][cc] = vb;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int rr = 0; rr < 64; ++rr) {
+      const double a = xa[rr][ta];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] += a * xb[rr][4 * tb + e];
+    }
+  }
+  double* out = B.i_gram + (int64_t)blockIdx.x * d * d;
+  const int ia = bi * 32 + ta;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int jb = bj * 32 + 4 * tb + e;
+    if (ia < d && jb < d) out[(int64_t)ia * d + jb] = acc[e];
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_gram_reduce(Geometry g, Bufs B) {
+  const int64_t dd = (int64_t)g.d * g.d;
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= dd) return;
+  double t = 0.0;
+  for (int gx = 0; gx < g.GG; ++gx) t += B.i_gram[(int64_t)gx * dd + e];
+  B.i_C[e] = t;
+}
+
+// scal[slot] = 1 / trace(M) (0 when the trace is not positive).
+__global__ __launch_bounds__(kThreads) void k_trace(Geometry g, const double* __restrict__ M, double* scal, int slot) {
+  __shared__ double red[8];
+  double t = 0.0;
+  for (int i = threadIdx.x; i < g.d; i += kThreads) t += M[(int64_t)i * g.d + i];
+  t = block_sum_d(t, red);
+  if (threadIdx.x == 0) scal[slot] = (t > 0.0 && isfinite(t)) ? 1.0 / t : 0.0;
+}
+
+// out = (in * scal[slot])^2 for a symmetric d x d matrix (32 x 32 tiles).
+__global__ __launch_bounds__(kThreads) void k_square(Geometry g, const double* __restrict__ in, double* __restrict__ out,
+                                                     const double* scal, int slot) {
+  __shared__ double As[32][33];
+  __shared__ double Bs[32][33];
+  const int d = g.d;
+  const int tid = threadIdx.x;
+  const int ty = tid >> 3, tx = tid & 7;
+  const int bi = blockIdx.y, bj = blockIdx.x;
+  const double s = scal[slot];
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int k0 = 0; k0 < d; k0 += 32) {
+    __syncthreads();
+    for (int v = tid; v < 32 * 32; v += kThreads) {
+      const int rr = v >> 5, cc = v & 31;
+      const int ia = bi * 32 + rr, ka = k0 + cc;
+      const int kb = k0 + rr, jb = bj * 32 + cc;
+      As[rr][cc] = (ia < d && ka < d) ? in[(int64_t)ia * d + ka] * s : 0.0;
+      Bs[rr][cc] = (kb < d && jb < d) ? in[(int64_t)kb * d + jb] * s : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int k = 0; k < 32; ++k) {
+      const double a = As[ty][k];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] += a * Bs[k][4 * tx + e];
+    }
+  }
+  const int ia = bi * 32 + ty;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int jb = bj * 32 + 4 * tx + e;
+    if (ia < d && jb < d) out[(int64_t)ia * d + jb] = acc[e];
+  }
+}
+
+// Power iterations on C from the dominant column of Bf; a = sqrt(Rayleigh quotient).
+__global__ __launch_bounds__(kThreads) void k_power(Geometry g, Bufs B, const double* __restrict__ Bf) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  double* v = reinterpret_cast<double*>(smem_raw);  // d
+  double* w = v + g.d;                               // d
+  __shared__ double red[8];
+  __shared__ double sh[2];
+  __shared__ int shi[1];
+  const int d = g.d;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const double* C = B.i_C;
+  // start column: largest diagonal of Bf, lowest index on ties
+  if (tid == 0) {
+    double best = -1.0;
+    int arg = 0;
+    for (int j = 0; j < d; ++j) {
+      const double x = Bf[(int64_t)j * d + j];
+      if (x > best) {
+        best = x;
+        arg = j;
+      }
+    }
+    shi[0] = arg;
+  }
+  __syncthreads();
+  const int j0 = shi[0];
+  double nn = 0.0;
+  for (int i = tid; i < d; i += kThreads) {
+    v[i] = Bf[(int64_t)i * d + j0];
+    nn += v[i] * v[i];
+  }
+  nn = block_sum_d(nn, red);
+  if (tid == 0) sh[0] = nn;
+  __syncthreads();
+  double inv = (sh[0] > 0.0) ? 1.0 / sqrt(sh[0]) : 0.0;
+  for (int i = tid; i < d; i += kThreads) v[i] *= inv;
+  __syncthreads();
+  double lam = 0.0;
+  for (int it = 0; it <= kPowerIters; ++it) {
+    // w = C v, one wave per row, lanes stride the columns
+    for (int i = wave; i < d; i += 4) {
+      double t = 0.0;
+      for (int j = lane; j < d; j += 64) t += C[(int64_t)i * d + j] * v[j];
+      for (int m = 32; m >= 1; m >>= 1) t += shfl_xor_d(t, m);
+      if (lane == 0) w[i] = t;
+    }
+    __syncthreads();
+    double vw = 0.0, ww = 0.0;
+    for (int i = tid; i < d; i += kThreads) {
+      vw += v[i] * w[i];
+      ww += w[i] * w[i];
+    }
+    vw = block_sum_d(vw, red);
+    ww = block_sum_d(ww, red);
+    if (tid == 0) {
+      sh[0] = vw;
+      sh[1] = ww;
+    }
+    __syncthreads();
+    lam = sh[0];  // Rayleigh quotient of the unit vector v
+    if (it == kPowerIters) break;
+    inv = (sh[1] > 0.0) ? 1.0 / sqrt(sh[1]) : 0.0;
+    for (int i = tid; i < d; i += kThreads) v[i] = w[i] * inv;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const double a = (lam > 0.0) ? sqrt(lam) : 0.0;
+    B.ctl->spectral_a = a;
+    if (!(a > 0.0) || !isfinite(a)) B.ctl->degenerate = 1;
+  }
+}
+
+// X <- (X - 1 xbar^T) / a in place; 256 rows per workgroup.
+__global__ __launch_bounds__(kThreads) void k_normalise(Geometry g, Bufs B) {
+  if (B.ctl->degenerate) return;
+  const double a = B.ctl->spectral_a;
+  const int d = g.d;
+  const int64_t row0 = (int64_t)blockIdx.x * 256;
+  const int64_t rows = (g.n - row0) < 256 ? (g.n - row0) : 256;
+  const int tot = (int)rows * d;
+  float* base = B.X + row0 * d;
+  for (int e = threadIdx.x; e < tot; e += kThreads) {
+    const int col = e % d;
+    base[e] = (float)(((double)base[e] - B.i_xbar[col]) / a);
+  }
+}
+
+// Projection statistics over row chunks: sum of (u_+)^2 and column sums of u_+.
+__global__ __launch_bounds__(kThreads) void k_proj_partial(Geometry g, Bufs B) {
+  __shared__ double red[kThreads];
+  __shared__ double red8[8];
+  const int tid = threadIdx.x;
+  const int64_t n = g.n;
+  const int r = g.r;
+  const int64_t r0 = (int64_t)blockIdx.x * n / g.GI;
+  const int64_t r1 = (int64_t)(blockIdx.x + 1) * n / g.GI;
+  double* out = B.i_proj + (int64_t)blockIdx.x * (4 + g.r32);
+  const int rstep = kThreads / r;   // r <= 256
+  const int col = tid % r;
+  const int rsub = tid / r;
+  double cs = 0.0, sq = 0.0;
+  if (rsub < rstep)
+    for (int64_t i = r0 + rsub; i < r1; i += rstep) {
+      const float u = fmaxf(B.U[i * r + col], 0.f);
+      cs += (double)u;
+      sq += (double)u * (double)u;
+    }
+  red[tid] = cs;
+  __syncthreads();
+  if (tid < r) {
+    double t = 0.0;
+    for (int k = 0; k < rstep; ++k) t += red[tid + k * r];
+    out[4 + tid] = t;
+  }
+  const double tsq = block_sum_d(sq, red8);
+  if (tid == 0) {
+    out[0] = tsq;
+    out[1] = out[2] = out[3] = 0.0;
+  }
+}
+
+// c_f = FP32(sqrt(K) / ||U_+||_F) (1 when U is already in Omega); p = FP32(c colsum).
+__global__ __launch_bounds__(kThreads) void k_proj_ctl(Geometry g, Bufs B, double K, int in_omega) {
+  __shared__ double red[8];
+  __shared__ double cbuf[1];
+  const int tid = threadIdx.x;
+  const int stride = 4 + g.r32;
+  double S = 0.0;
+  for (int gx = tid; gx < g.GI; gx += kThreads) S += B.i_proj[(int64_t)gx * stride];
+  S = block_sum_d(S, red);
+  if (tid == 0) {
+    double c = 1.0;
+    if (!in_omega) {
+      const double nu = sqrt(S);
+      if (!(nu > 1e-20) || !isfinite(S)) {
+        B.ctl->breakdown = 1;
+        c = 0.0;
+      } else {
+        c = (double)(float)(sqrt(K) / nu);
+      }
+    }
+    cbuf[0] = c;
+    B.i_scal[0] = c;
+  }
+  __syncthreads();
+  const double c = cbuf[0];
+  for (int col = tid; col < g.r32; col += kThreads) {
+    double t = 0.0;
+    if (col < g.r)
+      for (int gx = 0; gx < g.GI; ++gx) t += B.i_proj[(int64_t)gx * stride + 4 + col];
+    B.p[col] = (col < g.r) ? (float)(c * t) : 0.f;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_proj_apply(Geometry g, Bufs B) {
+  if (B.ctl->breakdown) return;
+  const float cf = (float)B.i_scal[0];
+  const int64_t tot = g.n * (int64_t)g.r;
+  for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < tot; e += (int64_t)gridDim.x * kThreads)
+    B.U[e] = cf * fmaxf(B.U[e], 0.f);
+}
+
+__global__ __launch_bounds__(kThreads) void k_zero_y(Geometry g, Bufs B) {
+  for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < g.n; e += (int64_t)gridDim.x * kThreads)
+    B.y[e] = 0.f;
+}
+
+// ---------------------------------------------------------------------------
+hipError_t launch_ctl_init(const Bufs& b, float gamma_f, hipStream_t st) {
+  hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, b, gamma_f);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_stop(const Bufs& b, hipStream_t st) {
+  hipLaunchKernelGGL(k_clear_stop, dim3(1), dim3(64), 0, st, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_colsum(const Geometry& g, const Bufs& b, hipStream_t st) {
+  hipLaunchKernelGGL(k_colsum, dim3(g.GI), dim3(kThreads), 0, st, g, b);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_colmean, dim3((g.d + kThreads - 1) / kThreads), dim3(kThreads), 0, st, g, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_gram(const Geometry& g, const Bufs& b, hipStream_t st) {
+  hipLaunchKernelGGL(k_gram, dim3(g.GG, g.gblk * g.gblk), dim3(kThreads), 0, st, g, b);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t dd = (int64_t)g.d * g.d;
+  hipLaunchKernelGGL(k_gram_reduce, dim3((unsigned)((dd + kThreads - 1) / kThreads)), dim3(kThreads), 0, st, g, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_spectral(const Geometry& g, const Bufs& b, hipStream_t st) {
+  // B_0 = C; scal[k] = 1/tr(B_k); B_{k+1} = (B_k scal[k])^2, ping-ponging B0/B1.
+  hipLaunchKernelGGL(k_trace, dim3(1), dim3(kThreads), 0, st, g, (const double*)b.i_C, b.i_scal, 1);
+  const double* in = b.i_C;
+  double* bufs[2] = {b.i_B0, b.i_B1};
+  const dim3 grid(g.gblk, g.gblk);
+  for (int k = 0; k < kSquarings; ++k) {
+    double* out = bufs[k & 1];
+    hipLaunchKernelGGL(k_square, grid, dim3(kThreads), 0, st, g, in, out, (const double*)b.i_scal, 1 + k);
+    hipLaunchKernelGGL(k_trace, dim3(1), dim3(kThreads), 0, st, g, (const double*)out, b.i_scal, 2 + k);
+    in = out;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t lds = 2 * (size_t)g.d * sizeof(double);
+  if (lds > (64u << 10)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_power), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_power, dim3(1), dim3(kThreads), lds, st, g, b, in);
+  return hipGetLastError();
+}
+
+hipError_t launch_normalise(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int64_t blocks = (g.n + 255) / 256;
+  hipLaunchKernelGGL(k_normalise, dim3((unsigned)blocks), dim3(kThreads), 0, st, g, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_project(const Geometry& g, const Bufs& b, double K, int in_omega, hipStream_t st) {
+  hipLaunchKernelGGL(k_proj_partial, dim3(g.GI), dim3(kThreads), 0, st, g, b);
+  hipLaunchKernelGGL(k_proj_ctl, dim3(1), dim3(kThreads), 0, st, g, b, K, in_omega);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || in_omega) return e;
+  hipLaunchKernelGGL(k_proj_apply, dim3(2048), dim3(kThreads), 0, st, g, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_y(const Geometry& g, const Bufs& b, hipStream_t st) {
+  hipLaunchKernelGGL(k_zero_y, dim3(1024), dim3(kThreads), 0, st, g, b);
+  return hipGetLastError();
+}
+
+}  // namespace nlr

@@ -1,0 +1,754 @@
+// Per-iteration kernels of the NLR iteration (Algorithm 1, Section 4) for gfx950.
+//
+// One iteration is
+//   pass A        Theta partials = Xhat^T U over row chunks (fp32 matrix cores),
+//                 fused with the row work that ends the previous iteration and
+//                 prepares this one: u = fl(c_f w) (lazy normalisation), q = u.p - 1,
+//                 gated dual step ytilde += (beta/n) q, ybar = ytilde + (beta/n) q,
+//                 s partials = U^T ybar, ||q||^2 and ytilde^T q partials
+//                 (eq. gpu-vectors; Appendix C call sites 2, 3, 7-11);
+//   reduce_theta  fixed-order FP64 sum of the Theta partials, ||Theta||_F^2;
+//   ctl_a         s, rho, objective fhat (eq. normalized), stopping rule (Section 4.3);
+//   pass B        G = Xhat Theta on fp32 matrix cores with the epilogue of
+//                 eq. (entrywise-fusion): w = max(u + 2 alpha G - alpha ybar p - alpha s, 0),
+//                 FP64 statistics a = ||W||^2, b = ||U||^2, h = <W, U> (eq. fused-statistics)
+//                 and column sums of W, W stored over U in place;
+//   ctl_b         a, b, h, column sums -> c_f = FP32(sqrt(K)/sqrt(a)), breakdown test,
+//                 Delta = max(c^2 a + b - 2 c h, 0), delta, dual gate Delta < eps_d^2 K,
+//                 p = FP32(c * colsum) (eq. movement-estimate, Appendix B Alg. 2 (d)-(f)).
+// The rescale U <- c W is never a separate pass: every consumer reads fl(c_f w).
+// "finish" is pass A without the matrix product: it materialises U = fl(c_f w)
+// and applies the pending end-of-iteration work, so a host call always returns
+// a materialised factor.
+#include "nlr_internal.hpp"
+
+namespace nlr {
+
+__device__ __forceinline__ bool halted(const DevCtl* ctl) {
+  return (ctl->stop | ctl->breakdown) != 0;
+}
+
+// ---------------------------------------------------------------------------
+// Tile staging: rows [row0, row0+kTPA) x cols [c0, c0+cw) of a row-major matrix
+// with leading dimension ld, multiplied by `scale`, into LDS with row stride ls.
+// Rows >= n and cols >= cmax are zero-filled.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void stage_tile(float* __restrict__ dst, int ls, const float* __restrict__ src,
+                                           int64_t ld, int64_t n, int64_t row0, int c0, int cw,
+                                           int cmax, float scale, bool vec) {
+  if (vec) {
+    const int cw4 = cw >> 2;
+    const int total = kTPA * cw4;
+    for (int v = threadIdx.x; v < total; v += kThreads) {
+      const int row = v / cw4;
+      const int c = (v - row * cw4) * 4;
+      const int64_t gr = row0 + row;
+      f32x4 x = {0.f, 0.f, 0.f, 0.f};
+      if (gr < n && c0 + c < cmax) {
+        x = *reinterpret_cast<const f32x4*>(src + gr * ld + c0 + c);
+        x.x = x.x * scale;
+        x.y = x.y * scale;
+        x.z = x.z * scale;
+        x.w = x.w * scale;
+      }
+      *reinterpret_cast<f32x4*>(dst + row * ls + c) = x;
+    }
+  } else {
+    const int total = kTPA * cw;
+    for (int v = threadIdx.x; v < total; v += kThreads) {
+      const int row = v / cw;
+      const int c = v - row * cw;
+      const int64_t gr = row0 + row;
+      float x = 0.f;
+      if (gr < n && c0 + c < cmax) x = src[gr * ld + c0 + c] * scale;
+      dst[row * ls + c] = x;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass A.  Grid (GA, mgroups*ngroups).  Workgroup (gx, gy) owns a contiguous
+// range of kTPA-row tiles and the Theta blocks of group gy (MBG x NBG blocks of
+// 32 x 32).  Wave w owns m-block w % MBG and all NBG n-blocks, over the k-slice
+// w / MBG of each tile (KS = 4 / MBG slices).  Group 0 also does the row work.
+// FINISH: no matrix product; materialise U and do the row work only.
+// ---------------------------------------------------------------------------
+template <int MBG, int NBG, bool FINISH>
+__global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArgs S) {
+  // The finish pass runs after a stop (it still materialises U) but not after a breakdown.
+  if (FINISH ? (B.ctl->breakdown != 0) : halted(B.ctl)) return;
+  const bool stopped = FINISH && (B.ctl->stop != 0);
+  constexpr int KS = 4 / MBG;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  float* smem = reinterpret_cast<float*>(smem_raw);
+  const int xs_stride = g.xs_stride;  // MBG*32
+  const int us_stride = g.us_stride;  // r32 + 4
+  float* Xs = smem;                                  // kTPA x xs_stride
+  float* Us = Xs + (FINISH ? 0 : kTPA * xs_stride);  // kTPA x us_stride
+  float* ybar_s = Us + kTPA * us_stride;             // kTPA
+  float* p_s = ybar_s + kTPA;                        // r32
+  double* dred = reinterpret_cast<double*>(p_s + g.r32);  // 256 + 8 doubles (8-byte aligned: r32 even)
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int gx = blockIdx.x;
+  const int gy = blockIdx.y;
+  const int mg = gy / g.ngroups;
+  const int ng = gy - mg * g.ngroups;
+  const bool do_rows = (gy == 0);
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r, r32 = g.r32;
+  const int f0 = mg * MBG * 32;       // first feature of the group
+  const int c0 = ng * NBG * 32;       // first column of the group
+  const float cf = B.ctl->c_f;
+  // after a stop the end-of-iteration work was already done by pass A
+  const bool gate = (S.end_work != 0) && (B.ctl->gate != 0) && !stopped;
+  const float gam = S.gamma_f;
+
+  const int64_t tb = (int64_t)gx * g.tilesA / g.GA;
+  const int64_t te = (int64_t)(gx + 1) * g.tilesA / g.GA;
+
+  if (do_rows)
+    for (int c = tid; c < r32; c += kThreads) p_s[c] = (c < r) ? B.p[c] : 0.f;
+
+  // row-work accumulators
+  double acc_qq = 0.0, acc_yq = 0.0, acc_s = 0.0;
+  // s ownership: column sc, points ps0, ps0 + pstep, ...
+  const int pstep = kThreads / r32 > 0 ? kThreads / r32 : 1;
+  const int sc = tid % r32;
+  const int ps0 = tid / r32;
+
+  // matrix-core accumulators
+  const int mb = wave % MBG;
+  const int ks = wave / MBG;
+  f32x16 acc[NBG];
+#pragma unroll
+  for (int j = 0; j < NBG; ++j)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+
+  const int ucols = do_rows ? r32 : NBG * 32;      // staged U columns
+  const int ucol0 = do_rows ? 0 : c0;              // first staged U column
+  const int ub = do_rows ? c0 : 0;                 // offset of the group's columns in Us
+
+  for (int64_t tile = tb; tile < te; ++tile) {
+    const int64_t row0 = tile * kTPA;
+    __syncthreads();
+    if (!FINISH)
+      stage_tile(Xs, xs_stride, B.X, d, n, row0, f0, MBG * 32, d, 1.0f, g.vec_x != 0);
+    stage_tile(Us, us_stride, B.U, r, n, row0, ucol0, ucols, r, cf, g.vec_u != 0);
+    __syncthreads();
+
+    if (do_rows) {
+      // R1: four threads per row: q = u.p - 1 (FP64 dot), dual step, ybar.
+      const int tp = tid >> 2;
+      const int j4 = tid & 3;
+      double dot = 0.0;
+      for (int c = j4; c < r; c += 4) dot += (double)Us[tp * us_stride + c] * (double)p_s[c];
+      dot += shfl_xor_d(dot, 1);
+      dot += shfl_xor_d(dot, 2);
+      const int64_t gr = row0 + tp;
+      float ybar = 0.f;
+      if (gr < n) {
+        const float q = (float)(dot - 1.0);
+        float yt = B.y[gr];
+        if (gate) {
+          yt = fmaf(gam, q, yt);
+          if (j4 == 0) B.y[gr] = yt;
+        }
+        ybar = fmaf(gam, q, yt);
+        if (j4 == 0) {
+          acc_qq += (double)q * (double)q;
+          acc_yq += (double)yt * (double)q;
+        }
+      }
+      if (j4 == 0) ybar_s[tp] = ybar;
+      if (FINISH) {
+        // materialise U = fl(c_f w) from the staged tile
+        const int64_t rows_here = (n - row0) < kTPA ? (n - row0) : kTPA;
+        const int64_t total = rows_here * r;
+        for (int64_t v = tid; v < total; v += kThreads) {
+          const int rr = (int)(v / r);
+          const int cc = (int)(v - (int64_t)rr * r);
+          B.U[(row0 + rr) * r + cc] = Us[rr * us_stride + cc];
+        }
+      }
+      __syncthreads();
+      if (!FINISH && sc < r) {
+        // R2: s_c += ybar_p u_pc
+        for (int pt = ps0; pt < kTPA; pt += pstep)
+          acc_s += (double)ybar_s[pt] * (double)Us[pt * us_stride + sc];
+      }
+    }
+
+    if (!FINISH) {
+      // Theta_blk += Xs^T Us over this wave's k-slice (2 rows per instruction).
+      const int kbeg = ks * (kTPA / KS);
+      const int kend = kbeg + kTPA / KS;
+      const int lr = lane >> 5;   // row within the pair
+      const int lc = lane & 31;
+#pragma unroll 4
+      for (int k = kbeg; k < kend; k += 2) {
+        const float a = Xs[(k + lr) * xs_stride + mb * 32 + lc];
+#pragma unroll
+        for (int j = 0; j < NBG; ++j) {
+          const float bv = Us[(k + lr) * us_stride + ub + j * 32 + lc];
+          acc[j] = mfma32x32x2(a, bv, acc[j]);
+        }
+      }
+    }
+  }
+
+  // ---- write partials ----
+  if (!FINISH) {
+    // combine k-slices (waves with the same m-block) in a fixed order
+    __syncthreads();
+    float* comb = smem;  // MBG * NBG * 16 * 64 floats
+    for (int slice = 1; slice < KS; ++slice) {
+      if (ks == slice) {
+#pragma unroll
+        for (int j = 0; j < NBG; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) comb[((mb * NBG + j) * 16 + v) * 64 + lane] = acc[j][v];
+      }
+      __syncthreads();
+      if (ks == 0) {
+#pragma unroll
+        for (int j = 0; j < NBG; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[j][v] += comb[((mb * NBG + j) * 16 + v) * 64 + lane];
+      }
+      __syncthreads();
+    }
+    if (ks == 0) {
+      float* part = B.theta_part + (int64_t)gx * g.d32 * r32;
+      const int lr = lane >> 5, lc = lane & 31;
+#pragma unroll
+      for (int j = 0; j < NBG; ++j) {
+        const int col = c0 + j * 32 + lc;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int f = f0 + mb * 32 + 8 * (v >> 2) + 4 * lr + (v & 3);
+          if (f < g.d32 && col < r32) part[(int64_t)f * r32 + col] = acc[j][v];
+        }
+      }
+    }
+  }
+  if (do_rows) {
+    const double qq = block_sum_d(acc_qq, dred + 256);
+    const double yq = block_sum_d(acc_yq, dred + 256);
+    if (tid == 0) {
+      B.row_part[2 * gx + 0] = qq;
+      B.row_part[2 * gx + 1] = yq;
+    }
+    if (!FINISH) {
+      // s: threads sharing a column reduce in a fixed order
+      __syncthreads();
+      dred[tid] = acc_s;
+      __syncthreads();
+      if (tid < r32) {
+        double t = 0.0;
+        for (int k = 0; k < pstep; ++k) t += dred[tid + k * r32];
+        B.s_part[(int64_t)gx * r32 + tid] = t;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Theta = sum of the pass-A partials (fixed order, FP64), written in the pass-B
+// operand layout, plus per-workgroup ||Theta||_F^2 partials.
+// Layout: chunk ch of 32 features, quarter j (4 features), m-block mb, lane l,
+// element e  <->  Theta[32 ch + 16 (l/32) + 4 j + e][32 mb + l%32].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B) {
+  if (halted(B.ctl)) return;
+  __shared__ double red[8];
+  const int64_t tot = (int64_t)g.d32 * g.r32;
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  double sum = 0.0;
+  if (e < tot) {
+    const float* src = B.theta_part + e;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    int gx = 0;
+    for (; gx + 4 <= g.GA; gx += 4) {
+      s0 += (double)src[(int64_t)(gx + 0) * tot];
+      s1 += (double)src[(int64_t)(gx + 1) * tot];
+      s2 += (double)src[(int64_t)(gx + 2) * tot];
+      s3 += (double)src[(int64_t)(gx + 3) * tot];
+    }
+    for (; gx < g.GA; ++gx) s0 += (double)src[(int64_t)gx * tot];
+    sum = (s0 + s1) + (s2 + s3);
+    const int f = (int)(e / g.r32);
+    const int c = (int)(e - (int64_t)f * g.r32);
+    const int ch = f >> 5, fin = f & 31;
+    const int hh = fin >> 4, j = (fin & 15) >> 2, ee = fin & 3;
+    const int mbk = c >> 5, l = hh * 32 + (c & 31);
+    const int64_t idx = ((((int64_t)ch * 4 + j) * g.NB + mbk) * 64 + l) * 4 + ee;
+    B.theta[idx] = (float)sum;
+  }
+  const double t2 = block_sum_d(sum * sum, red);
+  if (threadIdx.x == 0) B.th2_part[blockIdx.x] = t2;
+}
+
+// ---------------------------------------------------------------------------
+// Control after pass A (one workgroup): s, rho, objective, stopping rule of the
+// previous iteration.  finish = the call after the finish pass.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs S, int finish) {
+  DevCtl* ctl = B.ctl;
+  if (ctl->breakdown) return;
+  if (ctl->stop) {
+    // stopped earlier in this call: the finish pass only materialised U
+    if (finish && threadIdx.x == 0) ctl->c_f = 1.0f;
+    return;
+  }
+  __shared__ double red[8];
+  const int tid = threadIdx.x;
+  if (!finish) {
+    for (int c = tid; c < g.r32; c += kThreads) {
+      double t = 0.0;
+      for (int gx = 0; gx < g.GA; ++gx) t += B.s_part[(int64_t)gx * g.r32 + c];
+      B.s[c] = (c < g.r) ? (float)t : 0.f;
+    }
+  }
+  double qq = 0.0, yq = 0.0, th2 = 0.0;
+  for (int gx = tid; gx < g.GA; gx += kThreads) {
+    qq += B.row_part[2 * gx];
+    yq += B.row_part[2 * gx + 1];
+  }
+  if (!finish)
+    for (int k = tid; k < g.RT; k += kThreads) th2 += B.th2_part[k];
+  qq = block_sum_d(qq, red);
+  yq = block_sum_d(yq, red);
+  th2 = block_sum_d(th2, red);
+  if (tid == 0) {
+    const double rho = sqrt(qq * S.inv_n);
+    ctl->rho = rho;
+    const int64_t t = ctl->t_done;
+    if (S.end_work && t > 0) {
+      nlr_iter_stats* prev = &B.hist[(t - 1) % kHistCap];
+      const int stop = (ctl->Delta < S.eps_d * S.eps_d * S.K) && (ctl->delta < S.eps_c) &&
+                       (rho < S.eps_c) && (t >= S.T_min);
+      prev->rho = rho;
+      prev->stop = stop;
+      if (stop) ctl->stop = 1;
+    }
+    if (!finish && !ctl->stop) {
+      const double obj = -th2 + yq + 0.5 * S.beta * S.inv_n * qq;
+      ctl->objective = obj;
+      ctl->theta_fro2 = th2;
+      nlr_iter_stats* cur = &B.hist[t % kHistCap];
+      cur->t = t;
+      cur->objective = obj;
+      cur->theta_fro2 = th2;
+      cur->a = cur->b = cur->h = cur->delta = 0.0;
+      cur->rho = 0.0;
+      cur->c = 0.f;
+      cur->dual_step = 0;
+      cur->stop = 0;
+      cur->breakdown = 0;
+    }
+    if (finish) ctl->c_f = 1.0f;
+  }
+}
+
+// Reduce-scatter of LEN per-lane values across the lanes that differ in bits
+// MASK, MASK/2, ...: afterwards a lane holds LEN >> steps sums, of the upper half
+// when its bit is set and of the lower half otherwise.
+template <int LEN, int MASK>
+__device__ __forceinline__ void reduce_scatter(float* wv, int li) {
+  if constexpr (LEN > 1 && MASK > 0) {
+    const bool up = (li & MASK) != 0;
+#pragma unroll
+    for (int k = 0; k < LEN / 2; ++k) {
+      const float send = up ? wv[k] : wv[k + LEN / 2];
+      const float keep = up ? wv[k + LEN / 2] : wv[k];
+      wv[k] = keep + shfl_xor_f(send, MASK);
+    }
+    reduce_scatter<LEN / 2, MASK / 2>(wv, li);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass B.  Grid GB, persistent over 128-row super-tiles; wave w computes rows
+// [32w, 32w+32) of each super-tile for all r32 columns:
+//   acc (D layout) = Theta^T (A operand, from LDS or global) x Xhat^T (B operand,
+//   lane l loads row l%32, features 32ch + 16 (l/32) + [0, 16)).
+// Epilogue per element: w = max(u + 2 alpha acc - alpha ybar p - alpha s, 0).
+// ---------------------------------------------------------------------------
+template <int NB, bool THETA_LDS, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_pass_b(Geometry g, Bufs B, StepArgs S) {
+  if (halted(B.ctl)) return;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  float* th_s = reinterpret_cast<float*>(smem_raw);                 // d32*r32 if THETA_LDS
+  float* ps = th_s + (THETA_LDS ? g.d32 * g.r32 : 0);               // r32
+  float* ss = ps + g.r32;                                           // r32
+  double* colred = reinterpret_cast<double*>(ss + g.r32);          // 4 x r32
+  double* dred = colred + 4 * g.r32;                                // 8
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int h = lane >> 5;
+  const int li = lane & 31;
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r, r32 = g.r32;
+  const int nch = g.nch;
+  const float cf = B.ctl->c_f;
+  const float gam = S.gamma_f;
+  const float two_alpha = S.two_alpha_f;
+  const float neg_alpha = -S.alpha_f;
+
+  if (THETA_LDS) {
+    const int tot4 = (g.d32 * r32) >> 2;
+    const f32x4* src = reinterpret_cast<const f32x4*>(B.theta);
+    f32x4* dst = reinterpret_cast<f32x4*>(th_s);
+    for (int v = tid; v < tot4; v += kThreads) dst[v] = src[v];
+  }
+  for (int c = tid; c < r32; c += kThreads) {
+    ps[c] = B.p[c];
+    ss[c] = B.s[c];
+  }
+  __syncthreads();
+  const float* theta = THETA_LDS ? th_s : B.theta;
+
+  double sa = 0.0, sb = 0.0, sh = 0.0;
+  // column sums: per 32-column block, a 16-value reduce-scatter over lane bits
+  // 16, 8, 4, 2 leaves one value per lane; lanes l and l^1 then share a column
+  double colacc[NB];
+#pragma unroll
+  for (int m = 0; m < NB; ++m) colacc[m] = 0.0;
+  int base = 0;  // local index (8 qd + e ordering) of the value this lane keeps
+  {
+    if (li & 16) base += 8;
+    if (li & 8) base += 4;
+    if (li & 4) base += 2;
+    if (li & 2) base += 1;
+  }
+
+  const int64_t sb0 = (int64_t)blockIdx.x * g.tilesB / g.GB;
+  const int64_t sb1 = (int64_t)(blockIdx.x + 1) * g.tilesB / g.GB;
+  for (int64_t st = sb0; st < sb1; ++st) {
+    const int64_t pt = st * kTPB + wave * 32 + li;
+    const bool vpt = pt < n;
+    f32x16 acc[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+
+    const float* xrow = B.X + (vpt ? pt : 0) * (int64_t)d;
+    for (int ch = 0; ch < nch; ++ch) {
+      const int fb = ch * 32 + h * 16;
+      float xv[16];
+      if (VEC) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          f32x4 t = {0.f, 0.f, 0.f, 0.f};
+          if (vpt && fb + 4 * q < d) t = *reinterpret_cast<const f32x4*>(xrow + fb + 4 * q);
+          xv[4 * q + 0] = t.x;
+          xv[4 * q + 1] = t.y;
+          xv[4 * q + 2] = t.z;
+          xv[4 * q + 3] = t.w;
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) xv[q] = (vpt && fb + q < d) ? xrow[fb + q] : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int m = 0; m < NB; ++m) {
+          const f32x4 a = *reinterpret_cast<const f32x4*>(theta + ((((int64_t)ch * 4 + j) * NB + m) * 64 + lane) * 4);
+          acc[m] = mfma32x32x2(a.x, xv[4 * j + 0], acc[m]);
+          acc[m] = mfma32x32x2(a.y, xv[4 * j + 1], acc[m]);
+          acc[m] = mfma32x32x2(a.z, xv[4 * j + 2], acc[m]);
+          acc[m] = mfma32x32x2(a.w, xv[4 * j + 3], acc[m]);
+        }
+      }
+    }
+
+    // ---- epilogue ----
+    // lane holds row pt and columns 32 m + 8 qd + 4 h + e (m < NB, qd < 4, e < 4)
+    // (the opaque copy keeps the p/s reads inside the tile loop instead of
+    // hoisting 2*16*NB loop-invariant registers out of it)
+    const float* psl = ps;
+    const float* ssl = ss;
+    asm volatile("" : "+v"(psl), "+v"(ssl));
+    float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
+    auto load_u4 = [&](int c, float out[4]) {
+      if (VEC) {
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+        if (vpt && c < r) t = *reinterpret_cast<const f32x4*>(urow + c);
+        out[0] = t.x * cf;
+        out[1] = t.y * cf;
+        out[2] = t.z * cf;
+        out[3] = t.w * cf;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) out[e] = (vpt && c + e < r) ? urow[c + e] * cf : 0.f;
+      }
+    };
+    // q = u.p - 1 (fp32 dot over the lane's half of the row, then the other half)
+    float dotf = 0.f;
+#pragma unroll
+    for (int m = 0; m < NB; ++m)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int c = 32 * m + 8 * qd + 4 * h;
+        float u4[4];
+        load_u4(c, u4);
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+        dotf = fmaf(u4[0], pv.x, dotf);
+        dotf = fmaf(u4[1], pv.y, dotf);
+        dotf = fmaf(u4[2], pv.z, dotf);
+        dotf = fmaf(u4[3], pv.w, dotf);
+      }
+    dotf += shfl_xor_f(dotf, 32);
+    float ybar = 0.f;
+    if (vpt) ybar = fmaf(gam, dotf - 1.0f, B.y[pt]);
+#pragma unroll
+    for (int m = 0; m < NB; ++m) {
+      float wv[16];
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int c = 32 * m + 8 * qd + 4 * h;
+        float u4[4];
+        load_u4(c, u4);
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+        const f32x4 sv = *reinterpret_cast<const f32x4*>(ssl + c);
+        const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+        const float se[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float uu = u4[e];
+          float t = fmaf(two_alpha, acc[m][4 * qd + e], uu);
+          t = fmaf(neg_alpha, ybar * pe[e], t);
+          t = fmaf(neg_alpha, se[e], t);
+          float w = fmaxf(t, 0.f);
+          if (!vpt || c + e >= r) w = 0.f;
+          wv[4 * qd + e] = w;
+          const double wd = (double)w, ud = (double)uu;
+          sa = fma(wd, wd, sa);
+          sb = fma(ud, ud, sb);
+          sh = fma(wd, ud, sh);
+        }
+        if (vpt) {
+          if (VEC) {
+            if (c < r) {
+              f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
+              *reinterpret_cast<f32x4*>(urow + c) = o;
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (c + e < r) urow[c + e] = wv[4 * qd + e];
+          }
+        }
+      }
+      reduce_scatter<16, 16>(wv, li);
+      colacc[m] += (double)wv[0];
+    }
+  }
+
+  // ---- workgroup partials ----
+  for (int c = tid; c < 4 * r32; c += kThreads) colred[c] = 0.0;
+  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < NB; ++m) {
+    const double v = colacc[m] + shfl_xor_d(colacc[m], 1);
+    if ((li & 1) == 0) {
+      const int col = 32 * m + 8 * (base >> 2) + 4 * h + (base & 3);
+      colred[wave * r32 + col] = v;
+    }
+  }
+  __syncthreads();
+  double* out = B.b_part + (int64_t)blockIdx.x * (4 + r32);
+  for (int c = tid; c < r32; c += kThreads)
+    out[4 + c] = ((colred[c] + colred[r32 + c]) + colred[2 * r32 + c]) + colred[3 * r32 + c];
+  const double ta = block_sum_d(sa, dred);
+  const double tb2 = block_sum_d(sb, dred);
+  const double th = block_sum_d(sh, dred);
+  if (tid == 0) {
+    out[0] = ta;
+    out[1] = tb2;
+    out[2] = th;
+    out[3] = 0.0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Control after pass B (one workgroup): Algorithm 2 steps (d)-(f).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs S) {
+  DevCtl* ctl = B.ctl;
+  if (halted(ctl)) return;
+  __shared__ double red[8];
+  __shared__ double cbuf[1];
+  const int tid = threadIdx.x;
+  const int stride = 4 + g.r32;
+  double a = 0.0, b = 0.0, h = 0.0;
+  for (int gx = tid; gx < g.GB; gx += kThreads) {
+    const double* pp = B.b_part + (int64_t)gx * stride;
+    a += pp[0];
+    b += pp[1];
+    h += pp[2];
+  }
+  a = block_sum_d(a, red);
+  b = block_sum_d(b, red);
+  h = block_sum_d(h, red);
+  if (tid == 0) {
+    const double nu = sqrt(a);
+    const int64_t t = ctl->t_done;
+    nlr_iter_stats* rec = &B.hist[t % kHistCap];
+    rec->a = a;
+    rec->b = b;
+    rec->h = h;
+    if (!(nu > 1e-20) || !isfinite(a)) {
+      ctl->breakdown = 1;
+      rec->breakdown = 1;
+      cbuf[0] = 0.0;
+    } else {
+      const float cf = (float)(sqrt(S.K) / nu);
+      const double c = (double)cf;
+      double D = c * c * a + b - 2.0 * c * h;
+      if (D < 0.0) D = 0.0;
+      const double delta = sqrt(D) / sqrt(S.K);
+      const int gate = D < S.eps_d * S.eps_d * S.K;
+      ctl->a = a;
+      ctl->b = b;
+      ctl->h = h;
+      ctl->Delta = D;
+      ctl->delta = delta;
+      ctl->gate = gate;
+      ctl->c_f = cf;
+      ctl->t_done = t + 1;
+      rec->c = cf;
+      rec->delta = delta;
+      rec->dual_step = gate;
+      cbuf[0] = c;
+    }
+  }
+  __syncthreads();
+  const double c = cbuf[0];
+  if (c > 0.0) {
+    for (int col = tid; col < g.r32; col += kThreads) {
+      double t = 0.0;
+      for (int gx = 0; gx < g.GB; ++gx) t += B.b_part[(int64_t)gx * stride + 4 + col];
+      B.p[col] = (col < g.r) ? (float)(c * t) : 0.f;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Row-argmax labels, lowest index on ties.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_labels(Geometry g, const float* __restrict__ U,
+                                                     int32_t* __restrict__ labels) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= g.n) return;
+  const float* row = U + i * g.r;
+  float best = row[0];
+  int arg = 0;
+  for (int c = 1; c < g.r; ++c) {
+    const float v = row[c];
+    if (v > best) {
+      best = v;
+      arg = c;
+    }
+  }
+  labels[i] = arg;
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+// Kernels whose dynamic LDS exceeds 64 KiB need the per-function limit raised
+// (gfx950 has 160 KiB of LDS per workgroup).
+template <typename F>
+static hipError_t allow_lds(F* kern, size_t lds) {
+  if (lds <= (64u << 10)) return hipSuccess;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)lds);
+}
+
+template <int MBG, int NBG, bool FIN>
+static hipError_t pass_a_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  const dim3 grid(g.GA, FIN ? 1 : g.mgroups * g.ngroups);
+  const size_t lds = g.ldsA_bytes;
+  hipError_t e = allow_lds(k_pass_a<MBG, NBG, FIN>, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_pass_a<MBG, NBG, FIN>), grid, dim3(kThreads), lds, st, g, b, a);
+  return hipGetLastError();
+}
+
+template <int MBG, bool FIN>
+static hipError_t pass_a_nbg(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  switch (g.NBG) {
+    case 1: return pass_a_launch<MBG, 1, FIN>(g, b, a, st);
+    case 2: return pass_a_launch<MBG, 2, FIN>(g, b, a, st);
+    case 4: return pass_a_launch<MBG, 4, FIN>(g, b, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish, hipStream_t st) {
+  if (finish) return pass_a_nbg<4, true>(g, b, a, st);
+  switch (g.MBG) {
+    case 1: return pass_a_nbg<1, false>(g, b, a, st);
+    case 2: return pass_a_nbg<2, false>(g, b, a, st);
+    case 4: return pass_a_nbg<4, false>(g, b, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, hipStream_t st) {
+  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT), dim3(kThreads), 0, st, g, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish, hipStream_t st) {
+  hipLaunchKernelGGL(k_ctl_a, dim3(1), dim3(kThreads), 0, st, g, b, a, finish ? 1 : 0);
+  return hipGetLastError();
+}
+
+template <int NB>
+static hipError_t pass_b_nb(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  const size_t lds = g.ldsB_bytes;
+  const dim3 grid(g.GB), blk(kThreads);
+  const bool vec = g.vec_x && g.vec_u;
+  if (lds > (64u << 10)) return hipErrorInvalidValue;  // the layout keeps pass B under 64 KiB
+  if (g.theta_lds) {
+    if (vec) hipLaunchKernelGGL((k_pass_b<NB, true, true>), grid, blk, lds, st, g, b, a);
+    else hipLaunchKernelGGL((k_pass_b<NB, true, false>), grid, blk, lds, st, g, b, a);
+  } else {
+    if (vec) hipLaunchKernelGGL((k_pass_b<NB, false, true>), grid, blk, lds, st, g, b, a);
+    else hipLaunchKernelGGL((k_pass_b<NB, false, false>), grid, blk, lds, st, g, b, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  switch (g.NB) {
+    case 1: return pass_b_nb<1>(g, b, a, st);
+    case 2: return pass_b_nb<2>(g, b, a, st);
+    case 4: return pass_b_nb<4>(g, b, a, st);
+    case 8: return pass_b_nb<8>(g, b, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_ctl_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_ctl_b, dim3(1), dim3(kThreads), 0, st, g, b, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_labels(const Geometry& g, const Bufs& b, int32_t* labels, hipStream_t st) {
+  const int64_t blocks = (g.n + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL(k_labels, dim3((unsigned)blocks), dim3(kThreads), 0, st, g, (const float*)b.U, labels);
+  return hipGetLastError();
+}
+
+}  // namespace nlr

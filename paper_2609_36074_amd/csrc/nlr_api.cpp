@@ -1,0 +1,554 @@
+// Host controller behind the C ABI of include/nlr.h: argument validation,
+// launch geometry, workspace layout and the iteration state machine.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "nlr.h"
+#include "nlr_internal.hpp"
+
+namespace nlr {
+
+static int32_t round_up(int32_t x, int32_t m) { return (x + m - 1) / m * m; }
+static int32_t next_pow2(int32_t x) {
+  int32_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K) {
+  Geometry g;
+  std::memset(&g, 0, sizeof(g));
+  g.n = n;
+  g.d = d;
+  g.r = r;
+  g.K = K;
+  g.d32 = round_up(d, 32);
+  g.MB = g.d32 / 32;
+  g.NB = next_pow2((r + 31) / 32);  // 1, 2, 4 or 8 column blocks
+  g.r32 = 32 * g.NB;
+  // pass A groups: MBG in {1, 2, 4}, NBG in {1, 2, 4}
+  g.MBG = g.MB >= 3 ? 4 : g.MB;
+  g.NBG = g.NB >= 4 ? 4 : g.NB;
+  g.mgroups = (g.MB + g.MBG - 1) / g.MBG;
+  g.ngroups = (g.NB + g.NBG - 1) / g.NBG;
+  g.tilesA = (n + kTPA - 1) / kTPA;
+  {
+    const int64_t part_bytes = (int64_t)g.d32 * g.r32 * 4;
+    int64_t lim = (int64_t)64 << 20;
+    int64_t ga = lim / part_bytes;
+    if (ga < 16) ga = 16;
+    if (ga > 1024) ga = 1024;
+    if (ga > g.tilesA) ga = g.tilesA;
+    g.GA = (int32_t)ga;
+  }
+  g.xs_stride = g.MBG * 32;
+  g.us_stride = g.r32 + 4;
+  {
+    const int64_t floats = (int64_t)kTPA * g.xs_stride + (int64_t)kTPA * g.us_stride + kTPA + g.r32;
+    int64_t bytes = floats * 4 + (256 + 8) * 8;
+    const int64_t comb = (int64_t)g.MBG * g.NBG * 16 * 64 * 4;
+    if (comb > floats * 4) bytes = comb + (256 + 8) * 8 + 64;  // combine scratch overlaps the tiles
+    g.ldsA_bytes = (int32_t)((bytes + 15) & ~15);
+  }
+  g.RT = (int32_t)(((int64_t)g.d32 * g.r32 + kThreads - 1) / kThreads);
+  g.tilesB = (n + kTPB - 1) / kTPB;
+  g.GB = (int32_t)(g.tilesB < 1536 ? g.tilesB : 1536);
+  g.nch = g.d32 / 32;
+  g.theta_lds = ((int64_t)g.d32 * g.r32 * 4 <= (64 << 10)) ? 1 : 0;
+  g.ldsB_bytes = (int32_t)((g.theta_lds ? (int64_t)g.d32 * g.r32 * 4 : 0) + 2 * g.r32 * 4 +
+                           (4 * g.r32 + 8) * 8);
+  // init reductions
+  {
+    int64_t gi = (n + 255) / 256;
+    if (gi > 512) gi = 512;
+    g.GI = (int32_t)gi;
+    const int64_t dd8 = (int64_t)d * d * 8;
+    int64_t gg = ((int64_t)64 << 20) / (dd8 > 0 ? dd8 : 1);
+    if (gg < 1) gg = 1;
+    if (gg > 256) gg = 256;
+    const int64_t t64 = (n + 63) / 64;
+    if (gg > t64) gg = t64;
+    g.GG = (int32_t)gg;
+    g.gblk = g.d32 / 32;
+  }
+  g.vec_x = (d % 4 == 0) ? 1 : 0;
+  g.vec_u = (r % 4 == 0) ? 1 : 0;
+  return g;
+}
+
+size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> char* {
+    char* p = base ? base + off : nullptr;
+    off += align256(bytes);
+    return p;
+  };
+  Bufs b;
+  std::memset(&b, 0, sizeof(b));
+  const size_t d = (size_t)g.d, r32 = (size_t)g.r32;
+  b.ctl = reinterpret_cast<DevCtl*>(take(sizeof(DevCtl)));
+  b.hist = reinterpret_cast<nlr_iter_stats*>(take(sizeof(nlr_iter_stats) * kHistCap));
+  b.theta = reinterpret_cast<float*>(take((size_t)g.d32 * r32 * 4));
+  b.p = reinterpret_cast<float*>(take(r32 * 4));
+  b.s = reinterpret_cast<float*>(take(r32 * 4));
+  b.th2_part = reinterpret_cast<double*>(take((size_t)g.RT * 8));
+  b.b_part = reinterpret_cast<double*>(take((size_t)g.GB * (4 + r32) * 8));
+  b.row_part = reinterpret_cast<double*>(take((size_t)g.GA * 2 * 8));
+  b.s_part = reinterpret_cast<double*>(take((size_t)g.GA * r32 * 8));
+  b.i_xbar = reinterpret_cast<double*>(take(d * 8));
+  // union: pass-A Theta partials | init temporaries
+  const size_t u_iter = align256((size_t)g.GA * g.d32 * r32 * 4);
+  size_t u_init = 0;
+  u_init += align256((size_t)g.GI * d * 8);            // colsum
+  u_init += align256((size_t)g.GG * d * d * 8);         // gram partials
+  u_init += 3 * align256(d * d * 8);                    // C, B0, B1
+  u_init += align256(2 * (kSquarings + 2) * 8);         // scal
+  u_init += align256((size_t)g.GI * (4 + r32) * 8);     // projection partials
+  const size_t ubytes = u_iter > u_init ? u_iter : u_init;
+  char* ub = take(ubytes);
+  b.theta_part = reinterpret_cast<float*>(ub);
+  if (base) {
+    size_t o = 0;
+    auto sub = [&](size_t bytes) -> char* {
+      char* p = ub + o;
+      o += align256(bytes);
+      return p;
+    };
+    b.i_colsum = reinterpret_cast<double*>(sub((size_t)g.GI * d * 8));
+    b.i_gram = reinterpret_cast<double*>(sub((size_t)g.GG * d * d * 8));
+    b.i_C = reinterpret_cast<double*>(sub(d * d * 8));
+    b.i_B0 = reinterpret_cast<double*>(sub(d * d * 8));
+    b.i_B1 = reinterpret_cast<double*>(sub(d * d * 8));
+    b.i_scal = reinterpret_cast<double*>(sub(2 * (kSquarings + 2) * 8));
+    b.i_proj = reinterpret_cast<double*>(sub((size_t)g.GI * (4 + r32) * 8));
+  }
+  if (out) *out = b;
+  return off;
+}
+
+}  // namespace nlr
+
+using namespace nlr;
+
+enum KernelKind {
+  KK_PASS_A = 0,
+  KK_REDUCE_THETA,
+  KK_CTL_A,
+  KK_PASS_B,
+  KK_CTL_B,
+  KK_FINISH,
+  KK_CTL_FINISH,
+  KK_COUNT
+};
+static const char* kKernelNames[KK_COUNT] = {"pass_a", "reduce_theta", "ctl_a", "pass_b",
+                                             "ctl_b",  "finish",       "ctl_finish"};
+
+struct nlr_ctx {
+  Geometry g;
+  Bufs b;
+  hipStream_t stream;
+  int device;
+  nlr_params prm;
+  bool pending;       // end-of-iteration work of the latest pass B not yet applied
+  bool failed;        // sticky failure
+  bool breakdown;
+  int64_t t_host;     // last known iteration counter
+  bool t_host_valid;
+  DevCtl* host_ctl;   // pinned mirror of the control block
+  // profiling
+  bool prof;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::pair<int, int>> ev_pairs;  // (kind, index of start event)
+  size_t ev_used;
+  double prof_ms[KK_COUNT];
+  int64_t prof_n[KK_COUNT];
+};
+
+static nlr_status hip_fail(nlr_ctx* c) {
+  if (c) c->failed = true;
+  return NLR_EHIP;
+}
+
+static bool params_ok(const nlr_params* p) {
+  if (!p) return false;
+  if (!(p->alpha > 0.0) || !std::isfinite(p->alpha)) return false;
+  if (!(p->beta > 0.0) || !std::isfinite(p->beta)) return false;
+  if (!(p->eps_d >= 0.0) || !(p->eps_c >= 0.0)) return false;
+  if (std::isnan(p->eps_d) || std::isnan(p->eps_c)) return false;
+  if (p->T_min < 0) return false;
+  return true;
+}
+
+static bool shape_ok(int64_t n, int32_t d, int32_t r) {
+  return n >= 1 && d >= 1 && d <= 4096 && r >= 1 && r <= n && n < ((int64_t)1 << 40);
+}
+
+static StepArgs make_step_args(const nlr_ctx* c, int end_work) {
+  StepArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.alpha_f = (float)c->prm.alpha;
+  a.two_alpha_f = (float)(2.0 * c->prm.alpha);
+  a.gamma_f = (float)(c->prm.beta / (double)c->g.n);
+  a.beta = c->prm.beta;
+  a.eps_d = c->prm.eps_d;
+  a.eps_c = c->prm.eps_c;
+  a.K = (double)c->g.K;
+  a.inv_n = 1.0 / (double)c->g.n;
+  a.T_min = c->prm.T_min;
+  a.end_work = end_work;
+  return a;
+}
+
+// ---- profiling helpers ----
+static hipError_t prof_begin(nlr_ctx* c, int kind, int* slot) {
+  *slot = -1;
+  if (!c->prof) return hipSuccess;
+  if (c->ev_used + 2 > c->ev_pool.size()) {
+    for (int k = 0; k < 64; ++k) {
+      hipEvent_t e;
+      hipError_t err = hipEventCreate(&e);
+      if (err != hipSuccess) return err;
+      c->ev_pool.push_back(e);
+    }
+  }
+  *slot = (int)c->ev_used;
+  c->ev_used += 2;
+  c->ev_pairs.push_back({kind, *slot});
+  return hipEventRecord(c->ev_pool[*slot], c->stream);
+}
+static hipError_t prof_end(nlr_ctx* c, int slot) {
+  if (slot < 0) return hipSuccess;
+  return hipEventRecord(c->ev_pool[slot + 1], c->stream);
+}
+static hipError_t prof_collect(nlr_ctx* c) {
+  if (!c->prof || c->ev_pairs.empty()) return hipSuccess;
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return e;
+  for (auto& pr : c->ev_pairs) {
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, c->ev_pool[pr.second], c->ev_pool[pr.second + 1]);
+    if (e != hipSuccess) return e;
+    c->prof_ms[pr.first] += ms;
+    c->prof_n[pr.first] += 1;
+  }
+  c->ev_pairs.clear();
+  c->ev_used = 0;
+  return hipSuccess;
+}
+
+#define LAUNCH(kind, expr)                              \
+  do {                                                  \
+    int slot_;                                          \
+    if (prof_begin(c, kind, &slot_) != hipSuccess)      \
+      return hip_fail(c);                               \
+    if ((expr) != hipSuccess) return hip_fail(c);       \
+    if (prof_end(c, slot_) != hipSuccess)               \
+      return hip_fail(c);                               \
+  } while (0)
+
+static nlr_status enqueue_iteration(nlr_ctx* c) {
+  const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
+  LAUNCH(KK_PASS_A, launch_pass_a(c->g, c->b, a, false, c->stream));
+  LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, c->stream));
+  LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
+  LAUNCH(KK_PASS_B, launch_pass_b(c->g, c->b, a, c->stream));
+  LAUNCH(KK_CTL_B, launch_ctl_b(c->g, c->b, a, c->stream));
+  c->pending = true;
+  return NLR_OK;
+}
+
+static nlr_status enqueue_finish(nlr_ctx* c) {
+  const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
+  LAUNCH(KK_FINISH, launch_pass_a(c->g, c->b, a, true, c->stream));
+  LAUNCH(KK_CTL_FINISH, launch_ctl_a(c->g, c->b, a, true, c->stream));
+  c->pending = false;
+  return NLR_OK;
+}
+
+static nlr_status read_ctl(nlr_ctx* c) {
+  if (hipMemcpyAsync(c->host_ctl, c->b.ctl, sizeof(DevCtl), hipMemcpyDeviceToHost, c->stream) != hipSuccess)
+    return hip_fail(c);
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+  c->t_host = c->host_ctl->t_done;
+  c->t_host_valid = true;
+  return NLR_OK;
+}
+
+static nlr_status read_record(nlr_ctx* c, int64_t t, nlr_iter_stats* out) {
+  if (hipMemcpyAsync(out, c->b.hist + (t % kHistCap), sizeof(nlr_iter_stats), hipMemcpyDeviceToHost,
+                     c->stream) != hipSuccess)
+    return hip_fail(c);
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+  return NLR_OK;
+}
+
+extern "C" {
+
+size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r) {
+  if (!shape_ok(n, d, r) || r > kMaxR) return 0;
+  const Geometry g = make_geometry(n, d, r, 1);
+  return carve_workspace(g, nullptr, nullptr);
+}
+
+nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, int32_t r, float* U, float* y,
+                    const nlr_params* params, uint32_t flags, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  if (!ctx) return NLR_EINVAL;
+  *ctx = nullptr;
+  if (!X || !U || !y || !params_ok(params)) return NLR_EINVAL;
+  if (!shape_ok(n, d, r) || K < 1 || K > r) return NLR_EINVAL;
+  if (flags & ~(uint32_t)(NLR_INIT_U_IN_OMEGA | NLR_INIT_KEEP_Y | NLR_INIT_X_NORMALISED)) return NLR_EINVAL;
+  if (((uintptr_t)X & 3) || ((uintptr_t)U & 3) || ((uintptr_t)y & 3)) return NLR_EINVAL;
+  if (r > kMaxR) return NLR_EUNSUPPORTED;
+  const Geometry g0 = make_geometry(n, d, r, K);
+  const size_t need = carve_workspace(g0, nullptr, nullptr);
+  if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
+
+  nlr_ctx* c = new (std::nothrow) nlr_ctx();
+  if (!c) return NLR_EHIP;
+  c->g = g0;
+  // vector loads need 16-byte aligned row starts
+  if (((uintptr_t)X & 15) != 0) c->g.vec_x = 0;
+  if (((uintptr_t)U & 15) != 0) c->g.vec_u = 0;
+  carve_workspace(c->g, reinterpret_cast<char*>(workspace), &c->b);
+  c->b.X = X;
+  c->b.U = U;
+  c->b.y = y;
+  c->stream = reinterpret_cast<hipStream_t>(stream);
+  c->prm = *params;
+  c->pending = false;
+  c->failed = false;
+  c->breakdown = false;
+  c->t_host = 0;
+  c->t_host_valid = true;
+  c->prof = false;
+  c->ev_used = 0;
+  for (int k = 0; k < KK_COUNT; ++k) {
+    c->prof_ms[k] = 0.0;
+    c->prof_n[k] = 0;
+  }
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return NLR_EHIP;
+  }
+  if (hipHostMalloc(reinterpret_cast<void**>(&c->host_ctl), sizeof(DevCtl), hipHostMallocDefault) != hipSuccess) {
+    delete c;
+    return NLR_EHIP;
+  }
+  const Geometry& g = c->g;
+  const Bufs& b = c->b;
+  hipStream_t st = c->stream;
+  auto fail = [&](nlr_status s) {
+    nlr_destroy(c);
+    return s;
+  };
+  if (launch_ctl_init(b, (float)(params->beta / (double)n), st) != hipSuccess) return fail(NLR_EHIP);
+  if (!(flags & NLR_INIT_X_NORMALISED)) {
+    if (launch_colsum(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_gram(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_spectral(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_normalise(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+  }
+  if (launch_project(g, b, (double)K, (flags & NLR_INIT_U_IN_OMEGA) ? 1 : 0, st) != hipSuccess)
+    return fail(NLR_EHIP);
+  if (!(flags & NLR_INIT_KEEP_Y))
+    if (launch_zero_y(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+  if (read_ctl(c) != NLR_OK) return fail(NLR_EHIP);
+  if (c->host_ctl->degenerate) return fail(NLR_EDEGENERATE);
+  if (c->host_ctl->breakdown) return fail(NLR_EBREAKDOWN);
+  *ctx = c;
+  return NLR_OK;
+}
+
+nlr_status nlr_set_params(nlr_ctx* c, const nlr_params* params) {
+  if (!c || !params_ok(params)) return NLR_EINVAL;
+  if (c->failed) return NLR_ESTATE;
+  c->prm = *params;
+  return NLR_OK;
+}
+
+nlr_status nlr_step(nlr_ctx* c, nlr_iter_stats* stats) {
+  if (!c) return NLR_EINVAL;
+  if (c->failed) return NLR_ESTATE;
+  if (launch_clear_stop(c->b, c->stream) != hipSuccess) return hip_fail(c);
+  nlr_status s = enqueue_iteration(c);
+  if (s != NLR_OK) return s;
+  s = enqueue_finish(c);
+  if (s != NLR_OK) return s;
+  c->t_host_valid = false;
+  if (stats) {
+    if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+    if (c->host_ctl->breakdown) {
+      c->failed = true;
+      c->breakdown = true;
+    }
+    const int64_t t = c->host_ctl->t_done - (c->host_ctl->breakdown ? 0 : 1);
+    if (read_record(c, t < 0 ? 0 : t, stats) != NLR_OK) return NLR_EHIP;
+    if (prof_collect(c) != hipSuccess) return hip_fail(c);
+    if (c->breakdown) return NLR_EBREAKDOWN;
+  }
+  return NLR_OK;
+}
+
+nlr_status nlr_run(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* last) {
+  if (!c || T < 0) return NLR_EINVAL;
+  if (c->failed) return NLR_ESTATE;
+  if (!c->t_host_valid)
+    if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+  const int64_t t0 = c->t_host;
+  if (launch_clear_stop(c->b, c->stream) != hipSuccess) return hip_fail(c);
+  for (int32_t k = 0; k < T; ++k) {
+    if (k > 0 && (k % 32) == 0) {
+      if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+      if (c->host_ctl->stop || c->host_ctl->breakdown) break;
+    }
+    nlr_status s = enqueue_iteration(c);
+    if (s != NLR_OK) return s;
+  }
+  nlr_status s = enqueue_finish(c);
+  if (s != NLR_OK) return s;
+  if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+  if (prof_collect(c) != hipSuccess) return hip_fail(c);
+  const int64_t t1 = c->host_ctl->t_done;
+  if (iters_done) *iters_done = (int32_t)(t1 - t0);
+  if (c->host_ctl->breakdown) {
+    c->failed = true;
+    c->breakdown = true;
+  }
+  if (last) {
+    if (t1 > t0 || c->host_ctl->breakdown) {
+      const int64_t t = c->host_ctl->breakdown ? t1 : t1 - 1;
+      if (read_record(c, t, last) != NLR_OK) return NLR_EHIP;
+    } else {
+      std::memset(last, 0, sizeof(*last));
+      last->t = -1;
+    }
+  }
+  return c->breakdown ? NLR_EBREAKDOWN : NLR_OK;
+}
+
+nlr_status nlr_labels(nlr_ctx* c, int32_t* labels) {
+  if (!c || !labels || ((uintptr_t)labels & 3)) return NLR_EINVAL;
+  if (c->failed) return NLR_ESTATE;
+  if (launch_labels(c->g, c->b, labels, c->stream) != hipSuccess) return hip_fail(c);
+  return NLR_OK;
+}
+
+nlr_status nlr_history(nlr_ctx* c, nlr_iter_stats* out, int32_t max_records, int32_t* count) {
+  if (!c || !out || max_records < 0 || !count) return NLR_EINVAL;
+  if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+  const int64_t t1 = c->host_ctl->t_done + (c->host_ctl->breakdown ? 1 : 0);
+  int64_t avail = t1 < kHistCap ? t1 : kHistCap;
+  if (avail > max_records) avail = max_records;
+  const int64_t first = t1 - avail;
+  std::vector<nlr_iter_stats> all(kHistCap);
+  if (hipMemcpyAsync(all.data(), c->b.hist, sizeof(nlr_iter_stats) * kHistCap, hipMemcpyDeviceToHost,
+                     c->stream) != hipSuccess)
+    return hip_fail(c);
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+  for (int64_t k = 0; k < avail; ++k) out[k] = all[(first + k) % kHistCap];
+  *count = (int32_t)avail;
+  return NLR_OK;
+}
+
+nlr_status nlr_normaliser(nlr_ctx* c, double* a, double* xbar_host) {
+  if (!c || !a) return NLR_EINVAL;
+  if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+  *a = c->host_ctl->spectral_a;
+  if (xbar_host) {
+    if (hipMemcpyAsync(xbar_host, c->b.i_xbar, sizeof(double) * c->g.d, hipMemcpyDeviceToHost, c->stream) !=
+        hipSuccess)
+      return hip_fail(c);
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+  }
+  return NLR_OK;
+}
+
+nlr_status nlr_inspect(nlr_ctx* c, int32_t what, void* host_dst, size_t bytes) {
+  if (!c || !host_dst) return NLR_EINVAL;
+  const Geometry& g = c->g;
+  if (what == 0) {
+    if (bytes < (size_t)g.d * g.r * 4) return NLR_EINVAL;
+    std::vector<float> lay((size_t)g.d32 * g.r32);
+    if (hipMemcpyAsync(lay.data(), c->b.theta, lay.size() * 4, hipMemcpyDeviceToHost, c->stream) != hipSuccess)
+      return hip_fail(c);
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+    float* out = reinterpret_cast<float*>(host_dst);
+    for (int f = 0; f < g.d; ++f)
+      for (int col = 0; col < g.r; ++col) {
+        const int ch = f >> 5, fin = f & 31, hh = fin >> 4, j = (fin & 15) >> 2, ee = fin & 3;
+        const int mbk = col >> 5, l = hh * 32 + (col & 31);
+        const size_t idx = ((((size_t)ch * 4 + j) * g.NB + mbk) * 64 + l) * 4 + ee;
+        out[(size_t)f * g.r + col] = lay[idx];
+      }
+    return NLR_OK;
+  }
+  if (what == 1 || what == 2) {
+    if (bytes < (size_t)g.r * 4) return NLR_EINVAL;
+    if (hipMemcpyAsync(host_dst, what == 1 ? c->b.p : c->b.s, (size_t)g.r * 4, hipMemcpyDeviceToHost,
+                       c->stream) != hipSuccess)
+      return hip_fail(c);
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+    return NLR_OK;
+  }
+  return NLR_EINVAL;
+}
+
+nlr_status nlr_set_profiling(nlr_ctx* c, int32_t enable) {
+  if (!c) return NLR_EINVAL;
+  if (c->prof && !enable) {
+    if (prof_collect(c) != hipSuccess) return hip_fail(c);
+  }
+  c->prof = enable != 0;
+  for (int k = 0; k < KK_COUNT; ++k) {
+    c->prof_ms[k] = 0.0;
+    c->prof_n[k] = 0;
+  }
+  c->ev_pairs.clear();
+  c->ev_used = 0;
+  return NLR_OK;
+}
+
+nlr_status nlr_kernel_times(nlr_ctx* c, const char** names, double* total_ms, int64_t* launches,
+                            int32_t* n_kernels) {
+  if (!c || !names || !total_ms || !launches || !n_kernels) return NLR_EINVAL;
+  if (prof_collect(c) != hipSuccess) return hip_fail(c);
+  for (int k = 0; k < KK_COUNT; ++k) {
+    names[k] = kKernelNames[k];
+    total_ms[k] = c->prof_ms[k];
+    launches[k] = c->prof_n[k];
+  }
+  *n_kernels = KK_COUNT;
+  return NLR_OK;
+}
+
+void nlr_destroy(nlr_ctx* c) {
+  if (!c) return;
+  for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+  if (c->host_ctl) (void)hipHostFree(c->host_ctl);
+  delete c;
+}
+
+const char* nlr_status_string(nlr_status s) {
+  switch (s) {
+    case NLR_OK: return "ok";
+    case NLR_EINVAL: return "invalid argument";
+    case NLR_EWORKSPACE: return "workspace missing, misaligned or too small";
+    case NLR_EBREAKDOWN: return "normalisation breakdown (||W_+||_F <= 1e-20)";
+    case NLR_EDEGENERATE: return "degenerate data (centred matrix is zero)";
+    case NLR_EHIP: return "HIP runtime error";
+    case NLR_ESTATE: return "context failed earlier or used out of order";
+    case NLR_EUNSUPPORTED: return "shape outside the compiled kernel family";
+  }
+  return "unknown status";
+}
+
+const char* nlr_version(void) { return "nlr-gfx950 0.1"; }
+
+}  // extern "C"

@@ -1,0 +1,166 @@
+// Internal declarations shared by the host controller and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "nlr.h"
+
+namespace nlr {
+
+constexpr int kThreads = 256;     // every kernel uses 256-thread workgroups (4 wave64)
+constexpr int kHistCap = 4096;    // per-iteration record ring
+constexpr int kTPA = 64;          // rows per pass-A tile
+constexpr int kTPB = 128;         // rows per pass-B super-tile (4 waves x 32 rows)
+constexpr int kMaxR = 256;        // largest supported rank
+constexpr int kPowerIters = 64;   // refinement power iterations after the squaring phase
+constexpr int kSquarings = 20;    // C -> C^(2^20) before the refinement
+
+// Device control block.  Written only by single-workgroup control kernels and
+// read uniformly by every kernel at entry.
+struct alignas(16) DevCtl {
+  int32_t stop;        // stopping rule fired during the current host call
+  int32_t breakdown;   // sticky: normalisation breakdown
+  int32_t gate;        // dual gate of the latest primal step
+  int32_t degenerate;  // init: a = ||X_c||_2 is zero or not finite
+  int64_t t_done;      // completed primal steps
+  int64_t pad64;
+  float c_f;           // lazy scale of the factor buffer (1 when materialised)
+  float pad_f;
+  int32_t pad_i0, pad_i1;
+  double a, b, h;      // fused statistics of the latest primal step
+  double Delta;        // squared movement estimate
+  double delta;        // movement estimate
+  double rho;          // ||q||/sqrt(n) of the current factor
+  double objective;    // fhat at the start of the latest iteration
+  double theta_fro2;
+  double spectral_a;   // ||X_c||_2
+};
+
+// Scalars of one iteration, passed by value.
+struct StepArgs {
+  float alpha_f;       // alpha
+  float two_alpha_f;   // 2 alpha
+  float gamma_f;       // beta / n (the implementation's penalty on the stored dual)
+  float pad;
+  double beta;
+  double eps_d;
+  double eps_c;
+  double K;
+  double inv_n;
+  int64_t T_min;
+  int32_t end_work;    // apply the pending end-of-iteration vector work (dual step, rho, stop test)
+  int32_t pad2;
+};
+
+// Launch geometry; a pure function of (n, d, r) so that reduction orders,
+// and therefore results, do not depend on the device.
+struct Geometry {
+  int64_t n;
+  int32_t d, r, K;
+  int32_t d32, r32;     // d, r rounded up to multiples of 32
+  int32_t MB, NB;       // 32-wide blocks of d and r
+  // pass A
+  int32_t MBG, NBG;     // m-blocks / n-blocks per workgroup group (1, 2 or 4)
+  int32_t mgroups, ngroups;
+  int32_t GA;           // row-chunk workgroups per group
+  int64_t tilesA;       // ceil(n / kTPA)
+  int32_t ldsA_bytes;   // dynamic LDS of pass A
+  int32_t xs_stride, us_stride;
+  // reduce theta
+  int32_t RT;
+  // pass B
+  int32_t GB;
+  int64_t tilesB;       // ceil(n / kTPB)
+  int32_t nch;          // 32-feature chunks of d
+  int32_t theta_lds;    // 1: Theta staged whole in LDS
+  int32_t ldsB_bytes;
+  // init
+  int32_t GI;           // row-chunk workgroups of the init reductions
+  int32_t GG;           // row-chunk workgroups of the Gram partials
+  int32_t gblk;         // 32-wide blocks of d for the Gram
+  int32_t vec_x, vec_u; // 16-byte vector loads allowed on X / U rows
+};
+
+// Pointers into caller memory and the workspace.
+struct Bufs {
+  float* X;            // n x d (Xhat after init)
+  float* U;            // n x r
+  float* y;            // n (stored dual)
+  DevCtl* ctl;
+  nlr_iter_stats* hist;   // kHistCap records
+  float* theta;        // d32*r32, pass-B operand layout
+  float* p;            // r32
+  float* s;            // r32
+  float* theta_part;   // GA x d32 x r32
+  double* row_part;    // GA x 2 (||q||^2, ytilde^T q)
+  double* s_part;      // GA x r32
+  double* th2_part;    // RT
+  double* b_part;      // GB x (4 + r32): a, b, h, -, column sums
+  // init temporaries (alias the pass-A partial region)
+  double* i_colsum;    // GI x d
+  double* i_xbar;      // d
+  double* i_gram;      // GG x d x d
+  double* i_C;         // d x d
+  double* i_B0;        // d x d
+  double* i_B1;        // d x d
+  double* i_scal;      // 2*(kSquarings+2)
+  double* i_proj;      // GI x (4 + r32)
+};
+
+Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K);
+size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
+
+// ---- kernel launchers (each returns the launch error) ----
+hipError_t launch_ctl_init(const Bufs& b, float gamma_f, hipStream_t st);
+hipError_t launch_clear_stop(const Bufs& b, hipStream_t st);
+hipError_t launch_colsum(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_gram(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_spectral(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_normalise(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_project(const Geometry& g, const Bufs& b, double K, int in_omega, hipStream_t st);
+hipError_t launch_zero_y(const Geometry& g, const Bufs& b, hipStream_t st);
+
+hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
+                         hipStream_t st);
+hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
+                        hipStream_t st);
+hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_ctl_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_labels(const Geometry& g, const Bufs& b, int32_t* labels, hipStream_t st);
+
+// ---- device helpers ----
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// D += A * B on the 32x32x2 fp32 matrix core.  Lane l supplies A[l%32][l/32]
+// and B[l/32][l%32]; lane l, register v of D holds D[8(v/4)+4(l/32)+v%4][l%32].
+__device__ __forceinline__ f32x16 mfma32x32x2(float a, float b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ double shfl_xor_d(double v, int mask) {
+  return __shfl_xor(v, mask, 64);
+}
+__device__ __forceinline__ float shfl_xor_f(float v, int mask) {
+  return __shfl_xor(v, mask, 64);
+}
+
+// Fixed-order sum of one double per thread over a 256-thread workgroup.
+// Result valid in thread 0.  `red` must hold 4 doubles of shared memory.
+__device__ __forceinline__ double block_sum_d(double v, double* red) {
+  for (int m = 32; m >= 1; m >>= 1) v += shfl_xor_d(v, m);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  double r = 0.0;
+  if (threadIdx.x == 0) r = ((red[0] + red[1]) + red[2]) + red[3];
+  __syncthreads();
+  return r;
+}
+
+}  // namespace nlr

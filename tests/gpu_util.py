@@ -1,0 +1,56 @@
+"""Helpers shared by the GPU parity tests: run the HIP path through the C ABI
+binding, run the fp64 oracle on the same seeded inputs, compare."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+from oracle import nlr as onlr
+
+U_TOL = 1e-4     # max_ij |U_gpu - U_ref| / max_ij |U_ref| per iteration
+OBJ_TOL = 1e-5   # relative error of the objective
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a, dtype=np.float32):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=dtype)).to("cuda:0")
+
+
+def make_ctx(X, Z, K, alpha, beta=1.0, eps_d=1e-4, eps_c=1e-4, T_min=0, flags=0, y0=None, stream=None):
+    from paper_2609_36074_amd import nlr
+    Xt, Ut = to_dev(X), to_dev(Z)
+    yt = None if y0 is None else to_dev(y0)
+    ctx = nlr.Context(Xt, K, Ut, yt, alpha=alpha, beta=beta, eps_d=eps_d, eps_c=eps_c, T_min=T_min,
+                      flags=flags, stream=stream)
+    return ctx
+
+
+def host(t) -> np.ndarray:
+    return t.detach().cpu().numpy().astype(np.float64)
+
+
+def rel_max_err(a, ref) -> float:
+    scale = np.abs(ref).max()
+    return float(np.abs(np.asarray(a, np.float64) - ref).max() / (scale if scale > 0 else 1.0))
+
+
+def obj_rel_err(a: float, ref: float, scale: float) -> float:
+    return abs(a - ref) / max(abs(ref), scale)
+
+
+def label_agreement(lab_gpu: np.ndarray, U_ref: np.ndarray, rel_gap: float = 2e-4):
+    """(mismatches on unambiguous rows, number of ambiguous rows).  A row is
+    ambiguous when its top-2 gap in the reference is <= rel_gap * its max."""
+    srt = np.sort(U_ref, axis=1)
+    top = srt[:, -1]
+    gap = top - (srt[:, -2] if U_ref.shape[1] > 1 else 0.0)
+    amb = gap <= rel_gap * np.maximum(top, 1e-300)
+    ref = onlr.labels(U_ref)
+    bad = (lab_gpu != ref) & ~amb
+    return int(bad.sum()), int(amb.sum())

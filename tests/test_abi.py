@@ -1,0 +1,107 @@
+"""The C ABI on the CPU: the library loads, exports every symbol include/nlr.h
+declares, and rejects bad arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36074_amd import nlr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "nlr.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\**\s*(nlr_[a-z_]+)\s*\(", src, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return nlr.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 14, names
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(nlr.EXPORTED) == names
+
+
+def test_version_and_status_strings(lib):
+    assert lib.nlr_version().decode().startswith("nlr-gfx950")
+    for s in range(8):
+        assert lib.nlr_status_string(s).decode() != "unknown status"
+    assert lib.nlr_status_string(99).decode() == "unknown status"
+
+
+def test_workspace_bytes(lib):
+    a = nlr.nlr_workspace_bytes(10_000_000, 128, 64)
+    assert a > 0 and a == nlr.nlr_workspace_bytes(10_000_000, 128, 64)
+    assert nlr.nlr_workspace_bytes(2000, 16, 4) > 0
+    assert nlr.nlr_workspace_bytes(0, 16, 4) == 0       # n < 1
+    assert nlr.nlr_workspace_bytes(100, 0, 4) == 0      # d < 1
+    assert nlr.nlr_workspace_bytes(100, 16, 0) == 0     # r < 1
+    assert nlr.nlr_workspace_bytes(3, 16, 4) == 0       # r > n
+    assert nlr.nlr_workspace_bytes(1000, 16, 257) == 0  # r above the kernel family
+    assert nlr.nlr_workspace_bytes(1000, 4097, 4) == 0  # d above the limit
+
+
+FAKE = 1 << 20  # a 256-aligned address that is never dereferenced: every call below fails validation first
+
+
+def _init(lib, X=FAKE, n=1000, d=16, K=4, r=4, U=FAKE, y=FAKE, params=None, flags=0, ws=FAKE, ws_bytes=None):
+    if params is None:
+        params = nlr.NlrParams(0.01, 1.0, 1e-4, 1e-4, 0, 0)
+    if ws_bytes is None:
+        ws_bytes = nlr.nlr_workspace_bytes(n, d, r) if r <= 256 else 1 << 30
+    ctx = ctypes.c_void_p(123)
+    st = lib.nlr_init(ctypes.byref(ctx), X, n, d, K, r, U, y, ctypes.byref(params), flags, ws, ws_bytes, None)
+    return st, ctx
+
+
+def test_init_argument_errors(lib):
+    P = nlr.NlrParams
+    assert _init(lib, X=None)[0] == nlr.NLR_EINVAL
+    assert _init(lib, U=None)[0] == nlr.NLR_EINVAL
+    assert _init(lib, y=None)[0] == nlr.NLR_EINVAL
+    assert _init(lib, K=0)[0] == nlr.NLR_EINVAL
+    assert _init(lib, K=5, r=4)[0] == nlr.NLR_EINVAL            # K > r
+    assert _init(lib, n=3, r=4, K=2)[0] == nlr.NLR_EINVAL       # r > n
+    assert _init(lib, d=0)[0] == nlr.NLR_EINVAL
+    assert _init(lib, r=300, K=4)[0] == nlr.NLR_EUNSUPPORTED
+    assert _init(lib, params=P(0.0, 1.0, 1e-4, 1e-4, 0, 0))[0] == nlr.NLR_EINVAL      # alpha <= 0
+    assert _init(lib, params=P(float("inf"), 1.0, 1e-4, 1e-4, 0, 0))[0] == nlr.NLR_EINVAL
+    assert _init(lib, params=P(0.1, -1.0, 1e-4, 1e-4, 0, 0))[0] == nlr.NLR_EINVAL     # beta <= 0
+    assert _init(lib, params=P(0.1, 1.0, -1.0, 1e-4, 0, 0))[0] == nlr.NLR_EINVAL      # eps_d < 0
+    assert _init(lib, params=P(0.1, 1.0, 1e-4, float("nan"), 0, 0))[0] == nlr.NLR_EINVAL
+    assert _init(lib, params=P(0.1, 1.0, 1e-4, 1e-4, -1, 0))[0] == nlr.NLR_EINVAL     # T_min < 0
+    assert _init(lib, flags=1 << 7)[0] == nlr.NLR_EINVAL
+    assert _init(lib, X=FAKE + 2)[0] == nlr.NLR_EINVAL                                  # misaligned
+    assert _init(lib, ws=None)[0] == nlr.NLR_EWORKSPACE
+    assert _init(lib, ws=FAKE + 64)[0] == nlr.NLR_EWORKSPACE                           # not 256-aligned
+    st, ctx = _init(lib, ws_bytes=1024)
+    assert st == nlr.NLR_EWORKSPACE and ctx.value is None
+
+
+def test_null_context_calls(lib):
+    assert lib.nlr_step(None, None) == nlr.NLR_EINVAL
+    assert lib.nlr_run(None, 5, None, None) == nlr.NLR_EINVAL
+    assert lib.nlr_labels(None, FAKE) == nlr.NLR_EINVAL
+    assert lib.nlr_set_params(None, None) == nlr.NLR_EINVAL
+    assert lib.nlr_set_profiling(None, 1) == nlr.NLR_EINVAL
+    lib.nlr_destroy(None)  # no-op
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(RuntimeError, match="missing"):
+        # a fresh loader pointed at a path with no library
+        saved = nlr._lib
+        nlr._lib = None
+        try:
+            nlr.load_library(str(tmp_path / "libnlr.so"))
+        finally:
+            nlr._lib = saved

@@ -1,0 +1,305 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle on seeded inputs.
+
+Bars (from the target of the build): per-iteration U within max relative error
+1e-4 (max_ij |U_gpu - U_ref| / max_ij |U_ref|), objective within 1e-5
+relative, labels bit-exact on rows whose top-2 gap is not within rounding.
+The dual gate is a discrete decision taken on the GPU's rounded movement
+estimate; the oracle replays the GPU's gate sequence, and every gate decision
+is checked against the oracle's own movement (disagreement allowed only
+within 1e-3 relative of eps_d).
+"""
+import numpy as np
+import pytest
+
+from gpu_util import OBJ_TOL, U_TOL, host, label_agreement, log, make_ctx, obj_rel_err, rel_max_err
+from oracle import nlr as onlr
+from synth import gaussian_mixture, make_workload, standard_normal_factor
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_36074_amd import nlr
+    nlr.load_library()
+
+
+def _tiny():
+    X, Z, lab, wl = make_workload("tiny")
+    return X, Z.astype(np.float64), lab, wl
+
+
+def _gated():
+    """A tiny mixture (seed 1) on which, with alpha = 1.8/(2 L0), beta = 2, eps_d = 3e-3, the oracle
+    takes 4 dual steps in the first 600 iterations and 358 in the first 1000, and eps_c = 1e-3 stops
+    it near iteration 1030."""
+    X, lab, _ = gaussian_mixture(2000, 16, 4, 25.0, seed=1)
+    Z = standard_normal_factor(2000, 4, seed=2).astype(np.float64)
+    K, beta = 4, 2.0
+    return X, Z, lab, K, beta, 1.8 * onlr.default_step_size(K, beta)
+
+
+# ---------------------------------------------------------------- initialisation
+@pytest.mark.parametrize("n,d", [(2000, 16), (1037, 13), (5000, 128), (300, 768)])
+def test_normaliser(n, d):
+    log(f"normaliser n={n} d={d}")
+    X, _, _ = gaussian_mixture(n, d, 3, 9.0, seed=n + d)
+    Z = standard_normal_factor(n, 4, seed=1)
+    ctx = make_ctx(X, Z, 4, 0.01)
+    a, xbar = ctx.normaliser()
+    Xh_ref, xbar_ref, a_ref = onlr.centre_and_normalise(X)
+    assert abs(a / a_ref - 1.0) < 1e-9, (a, a_ref)
+    assert np.abs(xbar - xbar_ref).max() <= 1e-12 * max(1.0, np.abs(X).max())
+    Xh = host(ctx.X)
+    # X is stored as fp32(Xhat)
+    assert np.abs(Xh - Xh_ref).max() <= 2.0 ** -23 * np.abs(Xh_ref).max()
+
+
+@pytest.mark.parametrize("n,r,K", [(2000, 4, 4), (1037, 10, 7), (999, 33, 5)])
+def test_init_projection(n, r, K):
+    log(f"projection n={n} r={r} K={K}")
+    X, _, _ = gaussian_mixture(n, 8, 3, 9.0, seed=3)
+    Z = standard_normal_factor(n, r, seed=4)
+    ctx = make_ctx(X, Z, K, 0.01)
+    U = host(ctx.U)
+    ref = onlr.project_omega(Z.astype(np.float64), K)
+    assert rel_max_err(U, ref) < 1e-6
+    p = ctx.inspect("p").astype(np.float64)
+    assert np.abs(p - U.sum(axis=0)).max() <= 1e-6 * np.abs(p).max()
+    assert np.all(host(ctx.y) == 0.0)
+
+
+# ---------------------------------------------------------------- one step
+def test_one_step_tiny():
+    X, Z, _, wl = _tiny()
+    K = wl.K
+    alpha, beta = onlr.default_step_size(K), 1.0
+    ctx = make_ctx(X, Z, K, alpha, beta)
+    U0 = host(ctx.U)
+    st = ctx.step()
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    theta = ctx.inspect("theta").astype(np.float64)
+    th_ref = Xh.T @ U0
+    assert rel_max_err(theta, th_ref) < 1e-5
+    res = onlr.run(Xh, U0, K, alpha, beta, T=1, T_min=1, project_init=False, gates=[bool(st["dual_step"])])
+    rec = res.records[0]
+    for k in ("a", "b", "h"):
+        assert abs(st[k] - getattr(rec, k)) <= 1e-6 * abs(getattr(rec, k)), k
+    assert abs(st["c"] - rec.c) <= 2e-7 * rec.c
+    assert abs(st["delta"] - rec.delta) <= 1e-4 * rec.delta + 1e-9
+    assert obj_rel_err(st["objective"], rec.objective, 1.0) < OBJ_TOL
+    assert rel_max_err(host(ctx.U), res.U) < U_TOL / 10
+    s_ref = U0.T @ onlr.effective_multiplier(U0, np.zeros(U0.shape[0]), beta)
+    assert np.abs(ctx.inspect("s") - s_ref).max() <= 1e-5 * max(1e-12, np.abs(s_ref).max()) + 1e-9
+
+
+# ---------------------------------------------------------------- trajectories
+def _trajectory(X, Z, K, alpha, beta, T, eps_d=1e-4, eps_c=1e-4, one_step_tol=None):
+    """Steps the GPU T times; returns per-iteration errors vs the oracle (gate replay)
+    and per-iteration one-step errors (oracle step from the GPU's own iterate)."""
+    ctx = make_ctx(X, Z, K, alpha, beta, eps_d=eps_d, eps_c=eps_c, T_min=T)
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    n = X.shape[0]
+    U_gpu = [host(ctx.U)]
+    y_gpu = [host(ctx.y)]
+    stats = []
+    for t in range(T):
+        stats.append(ctx.step())
+        U_gpu.append(host(ctx.U))
+        y_gpu.append(host(ctx.y))
+    gates = [bool(s["dual_step"]) for s in stats]
+    ref = onlr.run(Xh, Z, K, alpha, beta, T=T, T_min=T, eps_d=eps_d, eps_c=eps_c, gates=gates,
+                   keep_trajectory=True)
+    traj_err = [rel_max_err(U_gpu[t + 1], ref.trajectory[t]) for t in range(T)]
+    obj_err = [obj_rel_err(stats[t]["objective"], ref.records[t].objective, 1.0) for t in range(T)]
+    # gate decisions against the oracle's own movement
+    bad_gates = [t for t in range(T)
+                 if gates[t] != (ref.records[t].delta < eps_d)
+                 and abs(ref.records[t].delta - eps_d) > 1e-3 * eps_d]
+    one = []
+    if one_step_tol is not None:
+        for t in range(T):
+            y_math = onlr.dual_from_stored(y_gpu[t])
+            r1 = onlr.run(Xh, U_gpu[t], K, alpha, beta, T=1, T_min=1, project_init=False, y0=y_math,
+                          gates=[gates[t]])
+            one.append(rel_max_err(U_gpu[t + 1], r1.U))
+            ystored = onlr.stored_dual(r1.y)
+            assert np.abs(y_gpu[t + 1] - ystored).max() <= 1e-5 * max(1e-12, np.abs(ystored).max()) + 1e-12, t
+    return ctx, ref, traj_err, obj_err, bad_gates, one, U_gpu, stats
+
+
+def test_trajectory_tiny_200():
+    X, Z, lab, wl = _tiny()
+    K = wl.K
+    alpha, beta = onlr.default_step_size(K), 1.0
+    log("tiny trajectory T=200")
+    ctx, ref, traj, obj, bad_gates, one, U_gpu, stats = _trajectory(X, Z, K, alpha, beta, wl.T,
+                                                                    one_step_tol=True)
+    log(f"max traj err {max(traj):.3e}  max one-step err {max(one):.3e}  max obj err {max(obj):.3e}")
+    assert max(traj) < U_TOL, (int(np.argmax(traj)), max(traj))
+    assert max(one) < U_TOL / 10
+    assert max(obj) < OBJ_TOL
+    assert not bad_gates, bad_gates
+    labels = ctx.labels().cpu().numpy()
+    bad, amb = label_agreement(labels, ref.U)
+    log(f"labels: {bad} mismatches, {amb} ambiguous rows")
+    assert bad == 0
+
+
+def test_trajectory_with_dual_steps():
+    """Gated dual steps along a 1000-iteration trajectory."""
+    X, Z, lab, K, beta, alpha = _gated()
+    ctx, ref, traj, obj, bad_gates, one, _, stats = _trajectory(X, Z, K, alpha, beta, 1000, eps_d=3e-3,
+                                                              eps_c=1e-7, one_step_tol=True)
+    ngates = sum(s["dual_step"] for s in stats)
+    log(f"dual steps {ngates}; max traj err {max(traj):.3e} one-step {max(one):.3e} obj {max(obj):.3e}")
+    assert ngates > 200
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates, bad_gates
+
+
+@pytest.mark.parametrize("n,d,r,K", [(1037, 13, 10, 7), (777, 64, 16, 16), (4099, 128, 64, 64),
+                                     (300, 33, 33, 5), (513, 200, 100, 20), (64, 3, 1, 1),
+                                     (1500, 768, 256, 256)])
+def test_ragged_shapes(n, d, r, K):
+    log(f"ragged n={n} d={d} r={r} K={K}")
+    X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 7 + d)
+    Z = standard_normal_factor(n, r, seed=n + r).astype(np.float64)
+    alpha = onlr.default_step_size(K)
+    _, _, traj, obj, bad_gates, one, _, _ = _trajectory(X, Z, K, alpha, 1.0, 8, one_step_tol=True)
+    log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates
+
+
+def test_gmm1m_parity():
+    X, Z, lab, wl = make_workload("gmm1m")
+    Z = Z.astype(np.float64)
+    K = wl.K
+    alpha = onlr.default_step_size(K)
+    log("gmm1m trajectory T=6")
+    ctx, ref, traj, obj, bad_gates, one, _, _ = _trajectory(X, Z, K, alpha, 1.0, 6, one_step_tol=True)
+    log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    bad, amb = label_agreement(ctx.labels().cpu().numpy(), ref.U)
+    log(f"  labels: {bad} mismatches, {amb} ambiguous")
+    assert bad == 0
+
+
+# ---------------------------------------------------------------- API semantics
+def test_run_equals_steps_bitwise_and_deterministic():
+    X, Z, _, K, beta, alpha = _gated()
+    kw = dict(eps_d=3e-3, eps_c=1e-7, T_min=0)
+    a = make_ctx(X, Z, K, alpha, beta, **kw)
+    b = make_ctx(X, Z, K, alpha, beta, **kw)
+    c = make_ctx(X, Z, K, alpha, beta, **kw)
+    T = 900
+    done, _ = a.run(T)
+    assert done == T
+    done_c, _ = c.run(T)
+    for _ in range(T):
+        b.step(with_stats=False)
+    for name in ("U", "y"):
+        ua, ub, uc = host(getattr(a, name)), host(getattr(b, name)), host(getattr(c, name))
+        assert np.array_equal(ua, ub), name
+        assert np.array_equal(ua, uc), name
+    assert sum(h["dual_step"] for h in a.history()) > 50
+
+
+def test_nondefault_stream():
+    import torch
+    X, Z, _, wl = _tiny()
+    K = wl.K
+    alpha = onlr.default_step_size(K)
+    a = make_ctx(X, Z, K, alpha)
+    a.run(25)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        b = make_ctx(X, Z, K, alpha, stream=s)
+        b.run(25)
+    s.synchronize()
+    assert np.array_equal(host(a.U), host(b.U))
+
+
+def test_stop_rule():
+    X, Z, _, K, beta, alpha = _gated()
+    eps_d, eps_c = 3e-3, 1e-3
+    ctx = make_ctx(X, Z, K, alpha, beta, eps_d=eps_d, eps_c=eps_c, T_min=5)
+    done, last = ctx.run(3000)
+    log(f"stopped after {done} iterations: {last}")
+    assert done < 3000 and last["stop"] == 1
+    assert last["delta"] < min(eps_d, eps_c) and last["rho"] < eps_c and done >= 5
+    hist = ctx.history(4096)
+    assert len(hist) == done
+    for h in hist[:-1]:
+        assert not (h["delta"] < min(eps_d, eps_c) and h["rho"] < eps_c and h["t"] + 1 >= 5), h
+    # the oracle, replaying the gates, meets its own stopping rule at the same iteration
+    gates = [bool(h["dual_step"]) for h in hist]
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    ref = onlr.run(Xh, Z, K, alpha, beta, T=done, T_min=5, eps_d=eps_d, eps_c=eps_c, gates=gates)
+    rec = ref.records[-1]
+    band = 1e-3
+    assert rec.delta < min(eps_d, eps_c) * (1 + band) and rec.rho < eps_c * (1 + band)
+    assert rel_max_err(host(ctx.U), ref.U) < U_TOL
+    # the stored dual after the final (gated) step agrees too
+    ys = onlr.stored_dual(ref.y)
+    assert np.abs(host(ctx.y) - ys).max() <= 1e-4 * np.abs(ys).max()
+
+
+def test_k1_fixed_point():
+    n = 256
+    X, _, _ = gaussian_mixture(n, 5, 2, 9.0, seed=9)
+    Z = np.full((n, 1), 1.0 / np.sqrt(n))
+    ctx = make_ctx(X, Z, 1, 0.3, 2.0)
+    for _ in range(3):
+        st = ctx.step()
+        assert st["delta"] < 1e-6 and abs(st["c"] - 1.0) < 1e-6 and st["rho"] < 1e-6
+    assert np.abs(host(ctx.U) - 1.0 / np.sqrt(n)).max() < 1e-6
+
+
+def test_breakdown_and_sticky_state():
+    from paper_2609_36074_amd import nlr
+    n, K = 200, 3
+    X, _, _ = gaussian_mixture(n, 4, 2, 9.0, seed=10)
+    Z = np.ones((n, 3))
+    ctx = make_ctx(X, Z, K, 1.0 / (2 * 1.0 * (K - 1)) * 1.5, 1.0)
+    with pytest.raises(nlr.NlrError) as e:
+        ctx.step()
+    assert e.value.status == nlr.NLR_EBREAKDOWN
+    assert np.all(host(ctx.U) == 0.0)  # the unnormalised update replaced the factor
+    with pytest.raises(nlr.NlrError) as e:
+        ctx.run(3)
+    assert e.value.status == nlr.NLR_ESTATE
+
+
+def test_degenerate_and_nonpositive_start():
+    from paper_2609_36074_amd import nlr
+    X = np.ones((100, 6), dtype=np.float32) * 3.0
+    with pytest.raises(nlr.NlrError) as e:
+        make_ctx(X, np.abs(standard_normal_factor(100, 2, 1)), 2, 0.01)
+    assert e.value.status == nlr.NLR_EDEGENERATE
+    X2, _, _ = gaussian_mixture(100, 6, 2, 9.0, seed=1)
+    with pytest.raises(nlr.NlrError) as e:
+        make_ctx(X2, -np.abs(standard_normal_factor(100, 2, 1)), 2, 0.01)
+    assert e.value.status == nlr.NLR_EBREAKDOWN
+
+
+def test_resume_flags():
+    """Resuming from (U, y) with U_IN_OMEGA | KEEP_Y | X_NORMALISED continues the iteration."""
+    from paper_2609_36074_amd import nlr
+    X, Z, _, wl = _tiny()
+    K, beta = wl.K, 2.0
+    alpha = 1.8 * onlr.default_step_size(K, beta)
+    kw = dict(eps_d=3e-3, eps_c=1e-7, T_min=0)
+    a = make_ctx(X, Z, K, alpha, beta, **kw)
+    a.run(120)
+    b = make_ctx(X, Z, K, alpha, beta, **kw)
+    b.run(60)
+    flags = nlr.NLR_INIT_U_IN_OMEGA | nlr.NLR_INIT_KEEP_Y | nlr.NLR_INIT_X_NORMALISED
+    c = nlr.Context(b.X, K, b.U, b.y, alpha=alpha, beta=beta, flags=flags, **kw)
+    c.run(60)
+    # p is recomputed from the stored factor on resume, so agreement is to tolerance, not bitwise
+    assert rel_max_err(host(c.U), host(a.U)) < U_TOL
