@@ -236,28 +236,292 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
     }
   }
   if (do_rows) {
+    double* ap = B.a_part + (int64_t)gx * (4 + r32);
     const double qq = block_sum_d(acc_qq, dred + 256);
     const double yq = block_sum_d(acc_yq, dred + 256);
     if (tid == 0) {
-      B.row_part[2 * gx + 0] = qq;
-      B.row_part[2 * gx + 1] = yq;
+      ap[0] = qq;
+      ap[1] = yq;
+      ap[2] = ap[3] = 0.0;
     }
-    if (!FINISH) {
-      // s: threads sharing a column reduce in a fixed order
-      __syncthreads();
-      dred[tid] = acc_s;
-      __syncthreads();
-      if (tid < r32) {
-        double t = 0.0;
-        for (int k = 0; k < pstep; ++k) t += dred[tid + k * r32];
-        B.s_part[(int64_t)gx * r32 + tid] = t;
-      }
+    // s: threads sharing a column reduce in a fixed order
+    __syncthreads();
+    dred[tid] = acc_s;
+    __syncthreads();
+    if (tid < r32) {
+      double t = 0.0;
+      for (int k = 0; k < pstep; ++k) t += dred[tid + k * r32];
+      ap[4 + tid] = FINISH ? 0.0 : t;
     }
   }
 }
 
+// Loads W consecutive floats; when !ok the (valid) address is still read and the
+// values are replaced by zeros, so no branch is needed.
+template <int W>
+__device__ __forceinline__ void load_vec(float (&dst)[W], const float* src, bool ok) {
+  if constexpr (W == 4) {
+    const f32x4 t = *reinterpret_cast<const f32x4*>(src);
+    dst[0] = ok ? t.x : 0.f;
+    dst[1] = ok ? t.y : 0.f;
+    dst[2] = ok ? t.z : 0.f;
+    dst[3] = ok ? t.w : 0.f;
+  } else if constexpr (W == 2) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 t = *reinterpret_cast<const f32x2*>(src);
+    dst[0] = ok ? t.x : 0.f;
+    dst[1] = ok ? t.y : 0.f;
+  } else {
+    const float t = *src;
+    dst[0] = ok ? t : 0.f;
+  }
+}
+
 // ---------------------------------------------------------------------------
-// Theta = sum of the pass-A partials (fixed order, FP64), written in the pass-B
+// Pass A, register-resident form on the 16x16x4 fp32 matrix core (all of Theta
+// fits one wave: FV*NGF*CV <= 32 blocks of 16x16).  Grid GA; each wave owns a
+// contiguous range of 4-row steps.  Per k-step lane l works on row 4k + l/16:
+// it loads FV consecutive features for each of NGF groups (feature
+// 16*FV*g + FV*(l%16) + e) and CV consecutive columns of U (column CV*(l%16) + c);
+// MFMA (g, e, c) accumulates Theta[16*FV*g + FV*i + e][CV*j + c] at D[i][j].
+// A row's columns live in one 16-lane DPP row, so the row work (q = u.p - 1,
+// dual step, ybar, s, ||q||^2, ytilde^T q) uses a 4-step DPP butterfly whose
+// result is bitwise identical in all 16 lanes.
+// FINISH: no matrix product; writes u = fl(c_f w) back (materialises U).
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, 0xF, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+// Sum over the 16 lanes of a DPP row with involution pairings (xor 1, xor 2,
+// half-row mirror, row mirror): every step adds two equal partial sums, so all
+// lanes end with the same bits.
+__device__ __forceinline__ double row16_sum_d(double v) {
+  v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_d<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_d<0x141>(v);  // row_half_mirror
+  v += dpp_d<0x140>(v);  // row_mirror
+  return v;
+}
+
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f32x4v mfma16x16x4(float a, float b, f32x4v c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <int FV, int NGF, int CV, bool FINISH>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_pass_a_rows(
+    Geometry g, Bufs B, StepArgs S) {
+  if (FINISH ? (B.ctl->breakdown != 0) : halted(B.ctl)) return;
+  const bool stopped = FINISH && (B.ctl->stop != 0);
+  constexpr int NBLK = FV * NGF * CV;  // 16x16 blocks of Theta
+  constexpr int PF = NBLK >= 32 ? 2 : 4;  // k-steps in flight (fewer when Theta takes 128 registers)
+  __shared__ double dred[kThreads + 8];
+  __shared__ float comb[FINISH ? 4 : 2 * NBLK * 4 * 64];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int grp = lane >> 4;   // row within the k-step
+  const int li = lane & 15;    // lane within the DPP row
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r;
+  const float cf = B.ctl->c_f;
+  const bool gate = (S.end_work != 0) && (B.ctl->gate != 0) && !stopped;
+  const float gam = S.gamma_f;
+
+  float pl[CV];
+#pragma unroll
+  for (int c = 0; c < CV; ++c) {
+    const int col = CV * li + c;
+    pl[c] = (col < r) ? B.p[col] : 0.f;
+  }
+
+  // 4-row steps of this wave
+  const int64_t steps = (n + 3) >> 2;
+  const int64_t wid = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t nw = (int64_t)g.GA * 4;
+  const int64_t k0 = wid * steps / nw;
+  const int64_t k1 = (wid + 1) * steps / nw;
+
+  f32x4v acc[NBLK];
+  if (!FINISH) {
+#pragma unroll
+    for (int b = 0; b < NBLK; ++b) acc[b] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+  }
+  double s_acc[CV];
+#pragma unroll
+  for (int c = 0; c < CV; ++c) s_acc[c] = 0.0;
+  double qq = 0.0, yq = 0.0;
+
+  float xr[PF][NGF][FV];
+  float ur[PF][CV];
+  float yr[PF];
+  auto issue = [&](int slot, int64_t k) {
+    const int64_t row = 4 * k + grp;
+    const bool ok = (k < k1) && (row < n);
+    const int64_t rr = ok ? row : 0;
+    if (!FINISH) {
+#pragma unroll
+      for (int gg = 0; gg < NGF; ++gg) {
+        const int f = 16 * FV * gg + FV * li;
+        load_vec<FV>(xr[slot][gg], B.X + rr * d + (f < d ? f : 0), ok && f < d);
+      }
+    }
+    const int cu = CV * li;
+    load_vec<CV>(ur[slot], B.U + rr * r + (cu < r ? cu : 0), ok && cu < r);
+    yr[slot] = ok ? B.y[rr] : 0.f;
+  };
+#pragma unroll
+  for (int i = 0; i < PF; ++i) issue(i, k0 + i);
+
+  for (int64_t kb = k0; kb < k1; kb += PF) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int64_t k = kb + i;
+      const int64_t row = 4 * k + grp;
+      const bool valid = (k < k1) && (row < n);
+      float u[CV];
+#pragma unroll
+      for (int c = 0; c < CV; ++c) u[c] = ur[i][c] * cf;
+      if (!FINISH) {
+#pragma unroll
+        for (int gg = 0; gg < NGF; ++gg)
+#pragma unroll
+          for (int e = 0; e < FV; ++e)
+#pragma unroll
+            for (int c = 0; c < CV; ++c)
+              acc[(gg * FV + e) * CV + c] = mfma16x16x4(xr[i][gg][e], u[c], acc[(gg * FV + e) * CV + c]);
+      }
+      // q = u.p - 1 over the 16 lanes of this row (FP64)
+      double dot = 0.0;
+#pragma unroll
+      for (int c = 0; c < CV; ++c) dot += (double)u[c] * (double)pl[c];
+      dot = row16_sum_d(dot);
+      const float q = (float)(dot - 1.0);
+      float yt = yr[i];
+      if (gate) yt = fmaf(gam, q, yt);
+      const float ybar = fmaf(gam, q, yt);
+      if (valid) {
+        if (gate && li == 0) B.y[row] = yt;
+#pragma unroll
+        for (int c = 0; c < CV; ++c) s_acc[c] += (double)ybar * (double)u[c];
+        if (li == 0) {
+          qq += (double)q * (double)q;
+          yq += (double)yt * (double)q;
+        }
+        if (FINISH) {
+          const int cu = CV * li;
+          if (cu < r) {
+            if constexpr (CV == 4) {
+              f32x4 o = {u[0], u[1], u[2], u[3]};
+              *reinterpret_cast<f32x4*>(B.U + row * r + cu) = o;
+            } else if constexpr (CV == 2) {
+              typedef float f32x2 __attribute__((ext_vector_type(2)));
+              f32x2 o = {u[0], u[1]};
+              *reinterpret_cast<f32x2*>(B.U + row * r + cu) = o;
+            } else {
+              B.U[row * r + cu] = u[0];
+            }
+          }
+        }
+      }
+      issue(i, k + PF);
+    }
+  }
+
+  // ---- partials ----
+  if (!FINISH) {
+    // Theta: ((wave0 + wave2) + (wave1 + wave3)) through two LDS regions
+    constexpr int REG = NBLK * 4 * 64;
+    if (wave < 2) {
+      float* dst = comb + wave * REG;
+#pragma unroll
+      for (int b = 0; b < NBLK; ++b)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) dst[(b * 4 + v) * 64 + lane] = acc[b][v];
+    }
+    __syncthreads();
+    if (wave >= 2) {
+      float* dst = comb + (wave - 2) * REG;
+#pragma unroll
+      for (int b = 0; b < NBLK; ++b)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int idx = (b * 4 + v) * 64 + lane;
+          dst[idx] = dst[idx] + acc[b][v];
+        }
+    }
+    __syncthreads();
+    float* part = B.theta_part + (int64_t)blockIdx.x * g.d32 * g.r32;
+    const int tot = g.d32 * g.r32;
+    for (int e = tid; e < tot; e += kThreads) {
+      const int f = e / g.r32, col = e - (e / g.r32) * g.r32;
+      const int gg = f / (16 * FV), rem = f - gg * 16 * FV;
+      const int i = rem / FV, ef = rem - i * FV;
+      const int c = col % CV, j = col / CV;
+      float val = 0.f;
+      if (gg < NGF && j < 16) {
+        const int idx = (((gg * FV + ef) * CV + c) * 4 + (i & 3)) * 64 + 16 * (i >> 2) + j;
+        val = comb[idx] + comb[REG + idx];
+      }
+      part[e] = val;
+    }
+  }
+  // s: rows 0..3 of a k-step hold the same columns; waves hold disjoint rows
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < CV; ++c) {
+    double v = s_acc[c] + shfl_xor_d(s_acc[c], 16);
+    v = v + shfl_xor_d(v, 32);
+    if (grp == 0) dred[wave * 16 * CV + CV * li + c] = v;  // 4 * 16 * CV <= 256
+  }
+  __syncthreads();
+  double* ap = B.a_part + (int64_t)blockIdx.x * (4 + g.r32);
+  for (int c = tid; c < g.r32; c += kThreads) {
+    double t = 0.0;
+    if (c < 16 * CV)
+      t = ((dred[c] + dred[16 * CV + c]) + dred[32 * CV + c]) + dred[48 * CV + c];
+    ap[4 + c] = FINISH ? 0.0 : t;
+  }
+  const double tq = block_sum_d(qq, dred + kThreads);
+  const double ty = block_sum_d(yq, dred + kThreads);
+  if (tid == 0) {
+    ap[0] = tq;
+    ap[1] = ty;
+    ap[2] = ap[3] = 0.0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Segmented column sums, fixed order: out[s][c] = sum over rows of segment s of
+// P[row][c] (rows [s R/S, (s+1) R/S)).  Grid (ceil(C/64), S); thread (col, sub)
+// sums rows sub, sub+4, ... of the segment, then the four subs are added in order.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_seg_sum(const T* __restrict__ P, int64_t R, int C,
+                                                      double* __restrict__ out, int S, const DevCtl* ctl,
+                                                      int skip_if_halted) {
+  if (skip_if_halted ? halted(ctl) : (ctl->breakdown != 0)) return;
+  __shared__ double red[kThreads];
+  const int tid = threadIdx.x;
+  const int col = blockIdx.x * 64 + (tid & 63);
+  const int sub = tid >> 6;
+  const int64_t lo = (int64_t)blockIdx.y * R / S;
+  const int64_t hi = (int64_t)(blockIdx.y + 1) * R / S;
+  double acc = 0.0;
+  if (col < C)
+    for (int64_t row = lo + sub; row < hi; row += 4) acc += (double)P[row * C + col];
+  red[tid] = acc;
+  __syncthreads();
+  if (tid < 64 && col < C)
+    out[(int64_t)blockIdx.y * C + col] = ((red[tid] + red[64 + tid]) + red[128 + tid]) + red[192 + tid];
+}
+
+// ---------------------------------------------------------------------------
+// Theta = sum of the segment sums (fixed order, FP64), written in the pass-B
 // operand layout, plus per-workgroup ||Theta||_F^2 partials.
 // Layout: chunk ch of 32 features, quarter j (4 features), m-block mb, lane l,
 // element e  <->  Theta[32 ch + 16 (l/32) + 4 j + e][32 mb + l%32].
@@ -269,17 +533,7 @@ __global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B) {
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   double sum = 0.0;
   if (e < tot) {
-    const float* src = B.theta_part + e;
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    int gx = 0;
-    for (; gx + 4 <= g.GA; gx += 4) {
-      s0 += (double)src[(int64_t)(gx + 0) * tot];
-      s1 += (double)src[(int64_t)(gx + 1) * tot];
-      s2 += (double)src[(int64_t)(gx + 2) * tot];
-      s3 += (double)src[(int64_t)(gx + 3) * tot];
-    }
-    for (; gx < g.GA; ++gx) s0 += (double)src[(int64_t)gx * tot];
-    sum = (s0 + s1) + (s2 + s3);
+    for (int s = 0; s < g.SA; ++s) sum += B.seg_theta[(int64_t)s * tot + e];
     const int f = (int)(e / g.r32);
     const int c = (int)(e - (int64_t)f * g.r32);
     const int ch = f >> 5, fin = f & 31;
@@ -306,22 +560,22 @@ __global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs
   }
   __shared__ double red[8];
   const int tid = threadIdx.x;
+  const int C = 4 + g.r32;
   if (!finish) {
     for (int c = tid; c < g.r32; c += kThreads) {
       double t = 0.0;
-      for (int gx = 0; gx < g.GA; ++gx) t += B.s_part[(int64_t)gx * g.r32 + c];
+      for (int s = 0; s < g.SA; ++s) t += B.seg_a[(int64_t)s * C + 4 + c];
       B.s[c] = (c < g.r) ? (float)t : 0.f;
     }
   }
   double qq = 0.0, yq = 0.0, th2 = 0.0;
-  for (int gx = tid; gx < g.GA; gx += kThreads) {
-    qq += B.row_part[2 * gx];
-    yq += B.row_part[2 * gx + 1];
-  }
+  if (tid == 0)
+    for (int s = 0; s < g.SA; ++s) {
+      qq += B.seg_a[(int64_t)s * C + 0];
+      yq += B.seg_a[(int64_t)s * C + 1];
+    }
   if (!finish)
     for (int k = tid; k < g.RT; k += kThreads) th2 += B.th2_part[k];
-  qq = block_sum_d(qq, red);
-  yq = block_sum_d(yq, red);
   th2 = block_sum_d(th2, red);
   if (tid == 0) {
     const double rho = sqrt(qq * S.inv_n);
@@ -580,26 +834,209 @@ __global__ __launch_bounds__(kThreads) void k_pass_b(Geometry g, Bufs B, StepArg
 }
 
 // ---------------------------------------------------------------------------
+// Pass B, resident-tile form (d <= 128, r <= 128, 16-byte rows).  Same
+// arithmetic and partial layout as k_pass_b; each wave holds its tile's whole
+// Xhat slab (NCH chunks) and U slab in registers: the U loads of a tile are
+// issued before its matrix product and the next tile's Xhat before its epilogue.
+// ---------------------------------------------------------------------------
+template <int NB, int NCH>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_pass_b_res(
+    Geometry g, Bufs B, StepArgs S) {
+  if (halted(B.ctl)) return;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  float* th_s = reinterpret_cast<float*>(smem_raw);  // d32*r32
+  float* ps = th_s + g.d32 * g.r32;                   // r32
+  float* ss = ps + g.r32;                             // r32
+  double* colred = reinterpret_cast<double*>(ss + g.r32);
+  double* dred = colred + 4 * g.r32;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int h = lane >> 5;
+  const int li = lane & 31;
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r, r32 = g.r32;
+  const float cf = B.ctl->c_f;
+  const float gam = S.gamma_f;
+  const float two_alpha = S.two_alpha_f;
+  const float neg_alpha = -S.alpha_f;
+
+  {
+    const int tot4 = (g.d32 * r32) >> 2;
+    const f32x4* src = reinterpret_cast<const f32x4*>(B.theta);
+    f32x4* dst = reinterpret_cast<f32x4*>(th_s);
+    for (int v = tid; v < tot4; v += kThreads) dst[v] = src[v];
+  }
+  for (int c = tid; c < r32; c += kThreads) {
+    ps[c] = B.p[c];
+    ss[c] = B.s[c];
+  }
+  __syncthreads();
+
+  double sa = 0.0, sb = 0.0, sh = 0.0;
+  double colacc[NB];
+#pragma unroll
+  for (int m = 0; m < NB; ++m) colacc[m] = 0.0;
+  int base = 0;
+  if (li & 16) base += 8;
+  if (li & 8) base += 4;
+  if (li & 4) base += 2;
+  if (li & 2) base += 1;
+
+  const int64_t sb0 = (int64_t)blockIdx.x * g.tilesB / g.GB;
+  const int64_t sb1 = (int64_t)(blockIdx.x + 1) * g.tilesB / g.GB;
+
+  float xv[NCH][16];
+  auto load_x = [&](int64_t st, int ch) {
+    const int64_t pt = st * kTPB + wave * 32 + li;
+    const bool ok = (st < sb1) && (pt < n);
+    const float* xrow = B.X + (ok ? pt : 0) * (int64_t)d;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int f = ch * 32 + h * 16 + 4 * q;
+      const f32x4 t = *reinterpret_cast<const f32x4*>(xrow + (f < d ? f : 0));
+      const bool okf = ok && f < d;
+      xv[ch][4 * q + 0] = okf ? t.x : 0.f;
+      xv[ch][4 * q + 1] = okf ? t.y : 0.f;
+      xv[ch][4 * q + 2] = okf ? t.z : 0.f;
+      xv[ch][4 * q + 3] = okf ? t.w : 0.f;
+    }
+  };
+#pragma unroll
+  for (int ch = 0; ch < NCH; ++ch) load_x(sb0, ch);
+
+  for (int64_t st = sb0; st < sb1; ++st) {
+    const int64_t pt = st * kTPB + wave * 32 + li;
+    const bool vpt = pt < n;
+    float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
+    // epilogue operands, issued before the matrix product
+    float u[NB][16];
+#pragma unroll
+    for (int m = 0; m < NB; ++m)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int c = 32 * m + 8 * qd + 4 * h;
+        const f32x4 t = *reinterpret_cast<const f32x4*>(urow + (c < r ? c : 0));
+        const bool ok = vpt && c < r;
+        u[m][4 * qd + 0] = ok ? t.x * cf : 0.f;
+        u[m][4 * qd + 1] = ok ? t.y * cf : 0.f;
+        u[m][4 * qd + 2] = ok ? t.z * cf : 0.f;
+        u[m][4 * qd + 3] = ok ? t.w * cf : 0.f;
+      }
+    const float yt = B.y[vpt ? pt : 0];
+
+    f32x16 acc[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int m = 0; m < NB; ++m) {
+          const f32x4 a = *reinterpret_cast<const f32x4*>(th_s + (((ch * 4 + j) * NB + m) * 64 + lane) * 4);
+          acc[m] = mfma32x32x2(a.x, xv[ch][4 * j + 0], acc[m]);
+          acc[m] = mfma32x32x2(a.y, xv[ch][4 * j + 1], acc[m]);
+          acc[m] = mfma32x32x2(a.z, xv[ch][4 * j + 2], acc[m]);
+          acc[m] = mfma32x32x2(a.w, xv[ch][4 * j + 3], acc[m]);
+        }
+      load_x(st + 1, ch);  // this chunk of the next tile: a whole tile of lead time
+    }
+
+    const float* psl = ps;
+    const float* ssl = ss;
+    asm volatile("" : "+v"(psl), "+v"(ssl));
+    float dotf = 0.f;
+#pragma unroll
+    for (int m = 0; m < NB; ++m)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + 32 * m + 8 * qd + 4 * h);
+        dotf = fmaf(u[m][4 * qd + 0], pv.x, dotf);
+        dotf = fmaf(u[m][4 * qd + 1], pv.y, dotf);
+        dotf = fmaf(u[m][4 * qd + 2], pv.z, dotf);
+        dotf = fmaf(u[m][4 * qd + 3], pv.w, dotf);
+      }
+    dotf += shfl_xor_f(dotf, 32);
+    const float ybar = vpt ? fmaf(gam, dotf - 1.0f, yt) : 0.f;
+#pragma unroll
+    for (int m = 0; m < NB; ++m) {
+      float wv[16];
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int c = 32 * m + 8 * qd + 4 * h;
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+        const f32x4 sv = *reinterpret_cast<const f32x4*>(ssl + c);
+        const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+        const float se[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float uu = u[m][4 * qd + e];
+          float t = fmaf(two_alpha, acc[m][4 * qd + e], uu);
+          t = fmaf(neg_alpha, ybar * pe[e], t);
+          t = fmaf(neg_alpha, se[e], t);
+          float w = fmaxf(t, 0.f);
+          if (!vpt || c + e >= r) w = 0.f;
+          wv[4 * qd + e] = w;
+          const double wd = (double)w, ud = (double)uu;
+          sa = fma(wd, wd, sa);
+          sb = fma(ud, ud, sb);
+          sh = fma(wd, ud, sh);
+        }
+        if (vpt && c < r) {
+          f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
+          *reinterpret_cast<f32x4*>(urow + c) = o;
+        }
+      }
+      reduce_scatter<16, 16>(wv, li);
+      colacc[m] += (double)wv[0];
+    }
+  }
+
+  for (int c = tid; c < 4 * r32; c += kThreads) colred[c] = 0.0;
+  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < NB; ++m) {
+    const double v = colacc[m] + shfl_xor_d(colacc[m], 1);
+    if ((li & 1) == 0) {
+      const int col = 32 * m + 8 * (base >> 2) + 4 * h + (base & 3);
+      colred[wave * r32 + col] = v;
+    }
+  }
+  __syncthreads();
+  double* out = B.b_part + (int64_t)blockIdx.x * (4 + r32);
+  for (int c = tid; c < r32; c += kThreads)
+    out[4 + c] = ((colred[c] + colred[r32 + c]) + colred[2 * r32 + c]) + colred[3 * r32 + c];
+  const double ta = block_sum_d(sa, dred);
+  const double tb2 = block_sum_d(sb, dred);
+  const double th = block_sum_d(sh, dred);
+  if (tid == 0) {
+    out[0] = ta;
+    out[1] = tb2;
+    out[2] = th;
+    out[3] = 0.0;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Control after pass B (one workgroup): Algorithm 2 steps (d)-(f).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs S) {
   DevCtl* ctl = B.ctl;
   if (halted(ctl)) return;
-  __shared__ double red[8];
   __shared__ double cbuf[1];
   const int tid = threadIdx.x;
-  const int stride = 4 + g.r32;
-  double a = 0.0, b = 0.0, h = 0.0;
-  for (int gx = tid; gx < g.GB; gx += kThreads) {
-    const double* pp = B.b_part + (int64_t)gx * stride;
-    a += pp[0];
-    b += pp[1];
-    h += pp[2];
-  }
-  a = block_sum_d(a, red);
-  b = block_sum_d(b, red);
-  h = block_sum_d(h, red);
+  const int C = 4 + g.r32;
   if (tid == 0) {
+    double a = 0.0, b = 0.0, h = 0.0;
+    for (int s = 0; s < g.SB; ++s) {
+      a += B.seg_b[(int64_t)s * C + 0];
+      b += B.seg_b[(int64_t)s * C + 1];
+      h += B.seg_b[(int64_t)s * C + 2];
+    }
     const double nu = sqrt(a);
     const int64_t t = ctl->t_done;
     nlr_iter_stats* rec = &B.hist[t % kHistCap];
@@ -636,7 +1073,7 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
   if (c > 0.0) {
     for (int col = tid; col < g.r32; col += kThreads) {
       double t = 0.0;
-      for (int gx = 0; gx < g.GB; ++gx) t += B.b_part[(int64_t)gx * stride + 4 + col];
+      for (int s = 0; s < g.SB; ++s) t += B.seg_b[(int64_t)s * C + 4 + col];
       B.p[col] = (col < g.r) ? (float)(c * t) : 0.f;
     }
   }
@@ -694,7 +1131,38 @@ static hipError_t pass_a_nbg(const Geometry& g, const Bufs& b, const StepArgs& a
   }
 }
 
+template <int FV, int NGF, int CV>
+static hipError_t pass_a_rows_launch(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
+                                     hipStream_t st) {
+  if (finish)
+    hipLaunchKernelGGL((k_pass_a_rows<FV, NGF, CV, true>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
+  else
+    hipLaunchKernelGGL((k_pass_a_rows<FV, NGF, CV, false>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
+  return hipGetLastError();
+}
+
+static hipError_t pass_a_rows_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
+                                       hipStream_t st) {
+  const int key = g.a_fv * 100 + g.a_ngf * 10 + g.a_cv;
+  switch (key) {
+    case 111: return pass_a_rows_launch<1, 1, 1>(g, b, a, finish, st);
+    case 112: return pass_a_rows_launch<1, 1, 2>(g, b, a, finish, st);
+    case 114: return pass_a_rows_launch<1, 1, 4>(g, b, a, finish, st);
+    case 211: return pass_a_rows_launch<2, 1, 1>(g, b, a, finish, st);
+    case 212: return pass_a_rows_launch<2, 1, 2>(g, b, a, finish, st);
+    case 214: return pass_a_rows_launch<2, 1, 4>(g, b, a, finish, st);
+    case 411: return pass_a_rows_launch<4, 1, 1>(g, b, a, finish, st);
+    case 412: return pass_a_rows_launch<4, 1, 2>(g, b, a, finish, st);
+    case 414: return pass_a_rows_launch<4, 1, 4>(g, b, a, finish, st);
+    case 421: return pass_a_rows_launch<4, 2, 1>(g, b, a, finish, st);
+    case 422: return pass_a_rows_launch<4, 2, 2>(g, b, a, finish, st);
+    case 424: return pass_a_rows_launch<4, 2, 4>(g, b, a, finish, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish, hipStream_t st) {
+  if (g.a_rows) return pass_a_rows_dispatch(g, b, a, finish, st);
   if (finish) return pass_a_nbg<4, true>(g, b, a, st);
   switch (g.MBG) {
     case 1: return pass_a_nbg<1, false>(g, b, a, st);
@@ -705,9 +1173,30 @@ hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bo
 }
 
 hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int C = g.d32 * g.r32;
+  hipLaunchKernelGGL((k_seg_sum<float>), dim3((C + 63) / 64, g.SA), dim3(kThreads), 0, st,
+                     (const float*)b.theta_part, (int64_t)g.GA, C, b.seg_theta, g.SA, (const DevCtl*)b.ctl, 1);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT), dim3(kThreads), 0, st, g, b);
   return hipGetLastError();
 }
+
+hipError_t launch_seg_a(const Geometry& g, const Bufs& b, bool finish, hipStream_t st) {
+  const int C = 4 + g.r32;
+  hipLaunchKernelGGL((k_seg_sum<double>), dim3((C + 63) / 64, g.SA), dim3(kThreads), 0, st,
+                     (const double*)b.a_part, (int64_t)g.GA, C, b.seg_a, g.SA, (const DevCtl*)b.ctl,
+                     finish ? 0 : 1);
+  return hipGetLastError();
+}
+
+hipError_t launch_seg_b(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int C = 4 + g.r32;
+  hipLaunchKernelGGL((k_seg_sum<double>), dim3((C + 63) / 64, g.SB), dim3(kThreads), 0, st,
+                     (const double*)b.b_part, (int64_t)g.GB, C, b.seg_b, g.SB, (const DevCtl*)b.ctl, 1);
+  return hipGetLastError();
+}
+
 
 hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish, hipStream_t st) {
   hipLaunchKernelGGL(k_ctl_a, dim3(1), dim3(kThreads), 0, st, g, b, a, finish ? 1 : 0);
@@ -730,7 +1219,30 @@ static hipError_t pass_b_nb(const Geometry& g, const Bufs& b, const StepArgs& a,
   return hipGetLastError();
 }
 
+template <int NB, int NCH>
+static hipError_t pass_b_res_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((k_pass_b_res<NB, NCH>), dim3(g.GB), dim3(kThreads), g.ldsB_bytes, st, g, b, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  if (g.b_res) {
+    switch (g.NB * 10 + g.nch) {
+      case 11: return pass_b_res_launch<1, 1>(g, b, a, st);
+      case 12: return pass_b_res_launch<1, 2>(g, b, a, st);
+      case 13: return pass_b_res_launch<1, 3>(g, b, a, st);
+      case 14: return pass_b_res_launch<1, 4>(g, b, a, st);
+      case 21: return pass_b_res_launch<2, 1>(g, b, a, st);
+      case 22: return pass_b_res_launch<2, 2>(g, b, a, st);
+      case 23: return pass_b_res_launch<2, 3>(g, b, a, st);
+      case 24: return pass_b_res_launch<2, 4>(g, b, a, st);
+      case 41: return pass_b_res_launch<4, 1>(g, b, a, st);
+      case 42: return pass_b_res_launch<4, 2>(g, b, a, st);
+      case 43: return pass_b_res_launch<4, 3>(g, b, a, st);
+      case 44: return pass_b_res_launch<4, 4>(g, b, a, st);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (g.NB) {
     case 1: return pass_b_nb<1>(g, b, a, st);
     case 2: return pass_b_nb<2>(g, b, a, st);

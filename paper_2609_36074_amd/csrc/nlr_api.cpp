@@ -21,7 +21,7 @@ static int32_t next_pow2(int32_t x) {
 }
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K) {
+Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16) {
   Geometry g;
   std::memset(&g, 0, sizeof(g));
   g.n = n;
@@ -56,13 +56,43 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K) {
     if (comb > floats * 4) bytes = comb + (256 + 8) * 8 + 64;  // combine scratch overlaps the tiles
     g.ldsA_bytes = (int32_t)((bytes + 15) & ~15);
   }
+  // register-resident pass A (16x16x4 blocks): all of Theta in one wave, FV*NGF*CV <= 32
+  {
+    int fv = 1;
+    while (fv < 4 && 16 * fv < d) fv <<= 1;
+    if (d % fv != 0) fv = 1;
+    const int ngf = (d + 16 * fv - 1) / (16 * fv);
+    int cv = 1;
+    while (cv < 4 && 16 * cv < r) cv <<= 1;
+    const bool fits = (16 * cv >= r) && (r % cv == 0);
+    const int key = fv * 100 + ngf * 10 + cv;
+    const bool known = key == 111 || key == 112 || key == 114 || key == 211 || key == 212 || key == 214 ||
+                       key == 411 || key == 412 || key == 414 || key == 421 || key == 422 || key == 424;
+    g.a_rows = (known && fits && aligned16) ? 1 : 0;
+    g.a_fv = fv;
+    g.a_ngf = ngf;
+    g.a_cv = cv;
+    if (g.a_rows) {
+      // at least 32 four-row steps per wave, at most 1024 workgroups
+      int64_t ga = (((n + 3) / 4) + 4 * 32 - 1) / (4 * 32);
+      if (ga > 1024) ga = 1024;
+      if (ga < 1) ga = 1;
+      g.GA = (int32_t)ga;
+    }
+  }
+  g.SA = (g.GA + 31) / 32;
+  if (g.SA > 64) g.SA = 64;
   g.RT = (int32_t)(((int64_t)g.d32 * g.r32 + kThreads - 1) / kThreads);
   g.tilesB = (n + kTPB - 1) / kTPB;
   g.GB = (int32_t)(g.tilesB < 1536 ? g.tilesB : 1536);
   g.nch = g.d32 / 32;
   g.theta_lds = ((int64_t)g.d32 * g.r32 * 4 <= (64 << 10)) ? 1 : 0;
+  g.b_res = (g.nch <= 4 && g.NB <= 4 && g.NB * g.nch <= 8 && g.theta_lds && d % 4 == 0 && r % 4 == 0 &&
+             aligned16) ? 1 : 0;
   g.ldsB_bytes = (int32_t)((g.theta_lds ? (int64_t)g.d32 * g.r32 * 4 : 0) + 2 * g.r32 * 4 +
                            (4 * g.r32 + 8) * 8);
+  g.SB = (g.GB + 31) / 32;
+  if (g.SB > 64) g.SB = 64;
   // init reductions
   {
     int64_t gi = (n + 255) / 256;
@@ -77,8 +107,8 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K) {
     g.GG = (int32_t)gg;
     g.gblk = g.d32 / 32;
   }
-  g.vec_x = (d % 4 == 0) ? 1 : 0;
-  g.vec_u = (r % 4 == 0) ? 1 : 0;
+  g.vec_x = (d % 4 == 0 && aligned16) ? 1 : 0;
+  g.vec_u = (r % 4 == 0 && aligned16) ? 1 : 0;
   return g;
 }
 
@@ -99,8 +129,10 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.s = reinterpret_cast<float*>(take(r32 * 4));
   b.th2_part = reinterpret_cast<double*>(take((size_t)g.RT * 8));
   b.b_part = reinterpret_cast<double*>(take((size_t)g.GB * (4 + r32) * 8));
-  b.row_part = reinterpret_cast<double*>(take((size_t)g.GA * 2 * 8));
-  b.s_part = reinterpret_cast<double*>(take((size_t)g.GA * r32 * 8));
+  b.a_part = reinterpret_cast<double*>(take((size_t)g.GA * (4 + r32) * 8));
+  b.seg_theta = reinterpret_cast<double*>(take((size_t)g.SA * g.d32 * r32 * 8));
+  b.seg_a = reinterpret_cast<double*>(take((size_t)g.SA * (4 + r32) * 8));
+  b.seg_b = reinterpret_cast<double*>(take((size_t)g.SB * (4 + r32) * 8));
   b.i_xbar = reinterpret_cast<double*>(take(d * 8));
   // union: pass-A Theta partials | init temporaries
   const size_t u_iter = align256((size_t)g.GA * g.d32 * r32 * 4);
@@ -256,8 +288,10 @@ static nlr_status enqueue_iteration(nlr_ctx* c) {
   const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
   LAUNCH(KK_PASS_A, launch_pass_a(c->g, c->b, a, false, c->stream));
   LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, c->stream));
+  LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
   LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
   LAUNCH(KK_PASS_B, launch_pass_b(c->g, c->b, a, c->stream));
+  LAUNCH(KK_CTL_B, launch_seg_b(c->g, c->b, c->stream));
   LAUNCH(KK_CTL_B, launch_ctl_b(c->g, c->b, a, c->stream));
   c->pending = true;
   return NLR_OK;
@@ -266,6 +300,7 @@ static nlr_status enqueue_iteration(nlr_ctx* c) {
 static nlr_status enqueue_finish(nlr_ctx* c) {
   const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
   LAUNCH(KK_FINISH, launch_pass_a(c->g, c->b, a, true, c->stream));
+  LAUNCH(KK_CTL_FINISH, launch_seg_a(c->g, c->b, true, c->stream));
   LAUNCH(KK_CTL_FINISH, launch_ctl_a(c->g, c->b, a, true, c->stream));
   c->pending = false;
   return NLR_OK;
@@ -292,8 +327,10 @@ extern "C" {
 
 size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r) {
   if (!shape_ok(n, d, r) || r > kMaxR) return 0;
-  const Geometry g = make_geometry(n, d, r, 1);
-  return carve_workspace(g, nullptr, nullptr);
+  // the layout differs with the alignment of X and U (vector kernels or not): cover both
+  const size_t a = carve_workspace(make_geometry(n, d, r, 1, true), nullptr, nullptr);
+  const size_t b = carve_workspace(make_geometry(n, d, r, 1, false), nullptr, nullptr);
+  return a > b ? a : b;
 }
 
 nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, int32_t r, float* U, float* y,
@@ -306,16 +343,14 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   if (flags & ~(uint32_t)(NLR_INIT_U_IN_OMEGA | NLR_INIT_KEEP_Y | NLR_INIT_X_NORMALISED)) return NLR_EINVAL;
   if (((uintptr_t)X & 3) || ((uintptr_t)U & 3) || ((uintptr_t)y & 3)) return NLR_EINVAL;
   if (r > kMaxR) return NLR_EUNSUPPORTED;
-  const Geometry g0 = make_geometry(n, d, r, K);
+  const bool aligned16 = (((uintptr_t)X & 15) == 0) && (((uintptr_t)U & 15) == 0);
+  const Geometry g0 = make_geometry(n, d, r, K, aligned16);
   const size_t need = carve_workspace(g0, nullptr, nullptr);
   if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
 
   nlr_ctx* c = new (std::nothrow) nlr_ctx();
   if (!c) return NLR_EHIP;
   c->g = g0;
-  // vector loads need 16-byte aligned row starts
-  if (((uintptr_t)X & 15) != 0) c->g.vec_x = 0;
-  if (((uintptr_t)U & 15) != 0) c->g.vec_u = 0;
   carve_workspace(c->g, reinterpret_cast<char*>(workspace), &c->b);
   c->b.X = X;
   c->b.U = U;

@@ -69,13 +69,17 @@ struct Geometry {
   int64_t tilesA;       // ceil(n / kTPA)
   int32_t ldsA_bytes;   // dynamic LDS of pass A
   int32_t xs_stride, us_stride;
+  int32_t a_rows;       // 1: register-resident pass A (k_pass_a_rows)
+  int32_t a_fv, a_ngf, a_cv;  // its features per lane, feature groups, columns per lane
   // reduce theta
   int32_t RT;
+  int32_t SA, SB;       // segments of the two-level partial sums
   // pass B
   int32_t GB;
   int64_t tilesB;       // ceil(n / kTPB)
   int32_t nch;          // 32-feature chunks of d
   int32_t theta_lds;    // 1: Theta staged whole in LDS
+  int32_t b_res;        // 1: resident-tile pass B (k_pass_b_res)
   int32_t ldsB_bytes;
   // init
   int32_t GI;           // row-chunk workgroups of the init reductions
@@ -95,8 +99,10 @@ struct Bufs {
   float* p;            // r32
   float* s;            // r32
   float* theta_part;   // GA x d32 x r32
-  double* row_part;    // GA x 2 (||q||^2, ytilde^T q)
-  double* s_part;      // GA x r32
+  double* a_part;      // GA x (4 + r32): ||q||^2, ytilde^T q, -, -, s partials
+  double* seg_theta;   // SA x d32*r32: segment sums of theta_part
+  double* seg_a;       // SA x (4 + r32)
+  double* seg_b;       // SB x (4 + r32)
   double* th2_part;    // RT
   double* b_part;      // GB x (4 + r32): a, b, h, -, column sums
   // init temporaries (alias the pass-A partial region)
@@ -110,7 +116,8 @@ struct Bufs {
   double* i_proj;      // GI x (4 + r32)
 };
 
-Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K);
+// aligned16: X and U start on 16-byte boundaries (enables the vector-load kernels)
+Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16);
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
 
 // ---- kernel launchers (each returns the launch error) ----
@@ -126,6 +133,8 @@ hipError_t launch_zero_y(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
                          hipStream_t st);
 hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_seg_a(const Geometry& g, const Bufs& b, bool finish, hipStream_t st);
+hipError_t launch_seg_b(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
                         hipStream_t st);
 hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
