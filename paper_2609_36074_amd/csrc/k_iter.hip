@@ -359,6 +359,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
   float xr[PF][NGF][FV];
   float ur[PF][CV];
   float yr[PF];
+  // The ring holds raw loads; masks and the lazy scale are applied where the
+  // values are used, so that no instruction waits on a load right after issuing it.
+  bool fx[NGF];
+#pragma unroll
+  for (int gg = 0; gg < NGF; ++gg) fx[gg] = (16 * FV * gg + FV * li) < d;
+  const int cu = CV * li;
+  const bool cx = cu < r;
   auto issue = [&](int slot, int64_t k) {
     const int64_t row = 4 * k + grp;
     const bool ok = (k < k1) && (row < n);
@@ -367,33 +374,41 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
 #pragma unroll
       for (int gg = 0; gg < NGF; ++gg) {
         const int f = 16 * FV * gg + FV * li;
-        load_vec<FV>(xr[slot][gg], B.X + rr * d + (f < d ? f : 0), ok && f < d);
+        load_vec<FV>(xr[slot][gg], B.X + rr * d + (f < d ? f : 0), true);
       }
     }
-    const int cu = CV * li;
-    load_vec<CV>(ur[slot], B.U + rr * r + (cu < r ? cu : 0), ok && cu < r);
-    yr[slot] = ok ? B.y[rr] : 0.f;
+    load_vec<CV>(ur[slot], B.U + rr * r + (cx ? cu : 0), true);
+    yr[slot] = B.y[rr];
   };
 #pragma unroll
-  for (int i = 0; i < PF; ++i) issue(i, k0 + i);
+  for (int i = 0; i < PF; ++i) {
+    __builtin_amdgcn_sched_barrier(0);
+    issue(i, k0 + i);
+  }
+  __builtin_amdgcn_sched_barrier(0);
 
   for (int64_t kb = k0; kb < k1; kb += PF) {
 #pragma unroll
     for (int i = 0; i < PF; ++i) {
+      // keep consumption of slot i and the refill of slot i in program order, so
+      // that the loads of the other slots stay in flight
+      __builtin_amdgcn_sched_barrier(0);
       const int64_t k = kb + i;
       const int64_t row = 4 * k + grp;
       const bool valid = (k < k1) && (row < n);
       float u[CV];
 #pragma unroll
-      for (int c = 0; c < CV; ++c) u[c] = ur[i][c] * cf;
+      for (int c = 0; c < CV; ++c) u[c] = (valid && cx) ? ur[i][c] * cf : 0.f;
       if (!FINISH) {
 #pragma unroll
         for (int gg = 0; gg < NGF; ++gg)
 #pragma unroll
-          for (int e = 0; e < FV; ++e)
+          for (int e = 0; e < FV; ++e) {
+            const float x = fx[gg] ? xr[i][gg][e] : 0.f;
 #pragma unroll
             for (int c = 0; c < CV; ++c)
-              acc[(gg * FV + e) * CV + c] = mfma16x16x4(xr[i][gg][e], u[c], acc[(gg * FV + e) * CV + c]);
+              acc[(gg * FV + e) * CV + c] = mfma16x16x4(x, u[c], acc[(gg * FV + e) * CV + c]);
+          }
       }
       // q = u.p - 1 over the 16 lanes of this row (FP64)
       double dot = 0.0;
@@ -401,36 +416,34 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
       for (int c = 0; c < CV; ++c) dot += (double)u[c] * (double)pl[c];
       dot = row16_sum_d(dot);
       const float q = (float)(dot - 1.0);
-      float yt = yr[i];
+      float yt = valid ? yr[i] : 0.f;
       if (gate) yt = fmaf(gam, q, yt);
       const float ybar = fmaf(gam, q, yt);
-      if (valid) {
-        if (gate && li == 0) B.y[row] = yt;
+      // branch-free: invalid rows have u = 0; stores of invalid lanes go to the dump slot
+      if (gate) *(valid ? (B.y + row) : B.dump) = yt;  // the 16 lanes of a row store the same value
 #pragma unroll
-        for (int c = 0; c < CV; ++c) s_acc[c] += (double)ybar * (double)u[c];
-        if (li == 0) {
-          qq += (double)q * (double)q;
-          yq += (double)yt * (double)q;
-        }
-        if (FINISH) {
-          const int cu = CV * li;
-          if (cu < r) {
-            if constexpr (CV == 4) {
-              f32x4 o = {u[0], u[1], u[2], u[3]};
-              *reinterpret_cast<f32x4*>(B.U + row * r + cu) = o;
-            } else if constexpr (CV == 2) {
-              typedef float f32x2 __attribute__((ext_vector_type(2)));
-              f32x2 o = {u[0], u[1]};
-              *reinterpret_cast<f32x2*>(B.U + row * r + cu) = o;
-            } else {
-              B.U[row * r + cu] = u[0];
-            }
-          }
+      for (int c = 0; c < CV; ++c) s_acc[c] += (double)ybar * (double)u[c];
+      const bool lead = valid && li == 0;
+      qq += lead ? (double)q * (double)q : 0.0;
+      yq += lead ? (double)yt * (double)q : 0.0;
+      if (FINISH) {
+        float* dst = (valid && cx) ? (B.U + row * r + cu) : B.dump;
+        if constexpr (CV == 4) {
+          f32x4 o = {u[0], u[1], u[2], u[3]};
+          *reinterpret_cast<f32x4*>(dst) = o;
+        } else if constexpr (CV == 2) {
+          typedef float f32x2 __attribute__((ext_vector_type(2)));
+          f32x2 o = {u[0], u[1]};
+          *reinterpret_cast<f32x2*>(dst) = o;
+        } else {
+          dst[0] = u[0];
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
       issue(i, k + PF);
     }
   }
+  __builtin_amdgcn_sched_barrier(0);
 
   // ---- partials ----
   if (!FINISH) {
@@ -728,9 +741,10 @@ __global__ __launch_bounds__(kThreads) void k_pass_b(Geometry g, Bufs B, StepArg
     // lane holds row pt and columns 32 m + 8 qd + 4 h + e (m < NB, qd < 4, e < 4)
     // (the opaque copy keeps the p/s reads inside the tile loop instead of
     // hoisting 2*16*NB loop-invariant registers out of it)
-    const float* psl = ps;
-    const float* ssl = ss;
-    asm volatile("" : "+v"(psl), "+v"(ssl));
+    int lds_off = 0;  // opaque zero offset: keeps the reads in LDS address space
+    asm volatile("" : "+v"(lds_off));
+    const float* psl = ps + lds_off;
+    const float* ssl = ss + lds_off;
     float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
     auto load_u4 = [&](int c, float out[4]) {
       if (VEC) {
@@ -895,36 +909,37 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int f = ch * 32 + h * 16 + 4 * q;
+      // raw values: features >= d meet zero rows of Theta, rows >= n are masked in the epilogue
       const f32x4 t = *reinterpret_cast<const f32x4*>(xrow + (f < d ? f : 0));
-      const bool okf = ok && f < d;
-      xv[ch][4 * q + 0] = okf ? t.x : 0.f;
-      xv[ch][4 * q + 1] = okf ? t.y : 0.f;
-      xv[ch][4 * q + 2] = okf ? t.z : 0.f;
-      xv[ch][4 * q + 3] = okf ? t.w : 0.f;
+      xv[ch][4 * q + 0] = t.x;
+      xv[ch][4 * q + 1] = t.y;
+      xv[ch][4 * q + 2] = t.z;
+      xv[ch][4 * q + 3] = t.w;
     }
   };
 #pragma unroll
-  for (int ch = 0; ch < NCH; ++ch) load_x(sb0, ch);
+  for (int ch = 0; ch < NCH; ++ch) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_x(sb0, ch);
+  }
+  __builtin_amdgcn_sched_barrier(0);
 
   for (int64_t st = sb0; st < sb1; ++st) {
+    __builtin_amdgcn_sched_barrier(0);
     const int64_t pt = st * kTPB + wave * 32 + li;
     const bool vpt = pt < n;
     float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
-    // epilogue operands, issued before the matrix product
-    float u[NB][16];
+    // epilogue operands, issued before the matrix product (raw; scaled and masked at use)
+    f32x4 uraw[NB][4];
 #pragma unroll
     for (int m = 0; m < NB; ++m)
 #pragma unroll
       for (int qd = 0; qd < 4; ++qd) {
         const int c = 32 * m + 8 * qd + 4 * h;
-        const f32x4 t = *reinterpret_cast<const f32x4*>(urow + (c < r ? c : 0));
-        const bool ok = vpt && c < r;
-        u[m][4 * qd + 0] = ok ? t.x * cf : 0.f;
-        u[m][4 * qd + 1] = ok ? t.y * cf : 0.f;
-        u[m][4 * qd + 2] = ok ? t.z * cf : 0.f;
-        u[m][4 * qd + 3] = ok ? t.w * cf : 0.f;
+        uraw[m][qd] = *reinterpret_cast<const f32x4*>(urow + (c < r ? c : 0));
       }
-    const float yt = B.y[vpt ? pt : 0];
+    const float yraw = B.y[vpt ? pt : 0];
+    __builtin_amdgcn_sched_barrier(0);
 
     f32x16 acc[NB];
 #pragma unroll
@@ -943,12 +958,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
           acc[m] = mfma32x32x2(a.z, xv[ch][4 * j + 2], acc[m]);
           acc[m] = mfma32x32x2(a.w, xv[ch][4 * j + 3], acc[m]);
         }
+      __builtin_amdgcn_sched_barrier(0);
       load_x(st + 1, ch);  // this chunk of the next tile: a whole tile of lead time
+      __builtin_amdgcn_sched_barrier(0);
     }
 
-    const float* psl = ps;
-    const float* ssl = ss;
-    asm volatile("" : "+v"(psl), "+v"(ssl));
+    int lds_off = 0;  // opaque zero offset: keeps the reads in LDS address space
+    asm volatile("" : "+v"(lds_off));
+    const float* psl = ps + lds_off;
+    const float* ssl = ss + lds_off;
+    float u[NB][16];
+#pragma unroll
+    for (int m = 0; m < NB; ++m)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const bool ok = vpt && (32 * m + 8 * qd + 4 * h) < r;
+        u[m][4 * qd + 0] = ok ? uraw[m][qd].x * cf : 0.f;
+        u[m][4 * qd + 1] = ok ? uraw[m][qd].y * cf : 0.f;
+        u[m][4 * qd + 2] = ok ? uraw[m][qd].z * cf : 0.f;
+        u[m][4 * qd + 3] = ok ? uraw[m][qd].w * cf : 0.f;
+      }
     float dotf = 0.f;
 #pragma unroll
     for (int m = 0; m < NB; ++m)
@@ -961,7 +990,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
         dotf = fmaf(u[m][4 * qd + 3], pv.w, dotf);
       }
     dotf += shfl_xor_f(dotf, 32);
-    const float ybar = vpt ? fmaf(gam, dotf - 1.0f, yt) : 0.f;
+    const float ybar = vpt ? fmaf(gam, dotf - 1.0f, yraw) : 0.f;
 #pragma unroll
     for (int m = 0; m < NB; ++m) {
       float wv[16];
@@ -986,10 +1015,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
           sb = fma(ud, ud, sb);
           sh = fma(wd, ud, sh);
         }
-        if (vpt && c < r) {
-          f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
-          *reinterpret_cast<f32x4*>(urow + c) = o;
-        }
+        // unconditional store (invalid lanes write the dump slot): no branch around it
+        float* dst = (vpt && c < r) ? (urow + c) : B.dump;
+        f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
+        *reinterpret_cast<f32x4*>(dst) = o;
       }
       reduce_scatter<16, 16>(wv, li);
       colacc[m] += (double)wv[0];

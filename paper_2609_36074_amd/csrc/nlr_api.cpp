@@ -134,6 +134,7 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.seg_a = reinterpret_cast<double*>(take((size_t)g.SA * (4 + r32) * 8));
   b.seg_b = reinterpret_cast<double*>(take((size_t)g.SB * (4 + r32) * 8));
   b.i_xbar = reinterpret_cast<double*>(take(d * 8));
+  b.dump = reinterpret_cast<float*>(take(256));
   // union: pass-A Theta partials | init temporaries
   const size_t u_iter = align256((size_t)g.GA * g.d32 * r32 * 4);
   size_t u_init = 0;

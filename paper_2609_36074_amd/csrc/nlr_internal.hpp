@@ -105,6 +105,7 @@ struct Bufs {
   double* seg_b;       // SB x (4 + r32)
   double* th2_part;    // RT
   double* b_part;      // GB x (4 + r32): a, b, h, -, column sums
+  float* dump;         // 256 bytes that masked-off lanes store to (never read)
   // init temporaries (alias the pass-A partial region)
   double* i_colsum;    // GI x d
   double* i_xbar;      // d
