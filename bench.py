@@ -99,6 +99,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=2_000_000)
     ap.add_argument("--cpu-iters", type=int, default=8)
+    ap.add_argument("--pmc-calibrate", action="store_true",
+                    help="first run one elementwise copy of 1 GiB (y = x * 1), the reference kernel that scales "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE readings to bytes")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -121,6 +124,12 @@ def main():
     X, Z, _, _ = make_workload(wl)
     eprint(f"[bench] generated in {time.perf_counter() - t0:.1f} s; uploading")
     dev = torch.device("cuda:0")
+    if args.pmc_calibrate:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     Xt = torch.from_numpy(X).to(dev)
     Ut = torch.from_numpy(Z).to(dev)
     del X, Z
