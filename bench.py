@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 METRIC = "NLR points·iters/sec + achieved HBM GB/s (n=1e7,d=128,K=64, fp32)"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
+FP16_MFMA_PEAK_TFLOPS = 2500.0
 
 
 def eprint(*a):
@@ -45,7 +46,7 @@ def algorithmic_bytes(kind: str, n: int, d: int, r: int, dual_frac: float = 0.0)
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("k_iter.hip", "nlr_internal.hpp"):
+    for f in ("k_iter.hip", "k_split.hip", "k_common.hpp", "nlr_internal.hpp"):
         with open(os.path.join(ROOT, "paper_2609_36074_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -96,6 +97,9 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gmm10m")
+    ap.add_argument("--gemm", choices=("fp32", "split16"), default="fp32",
+                    help="fp32: both products on the fp32 matrix cores; split16: two-term fp16 splits of the "
+                         "operands on the fp16 matrix cores (NLR_INIT_SPLIT_F16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=2_000_000)
     ap.add_argument("--cpu-iters", type=int, default=8)
@@ -136,7 +140,9 @@ def main():
     torch.cuda.synchronize()
     alpha = 1.0 / (2.0 * (2.0 + 1.0 * (6.0 * K + 2.0)))  # half the Prop. 1 step bound at y = 0, beta = 1
     steps, warm = args.steps, args.warmup
-    ctx = nlr.Context(Xt, K, Ut, alpha=alpha, beta=1.0, eps_d=1e-4, eps_c=1e-4, T_min=1 << 30)
+    split = args.gemm == "split16"
+    ctx = nlr.Context(Xt, K, Ut, alpha=alpha, beta=1.0, eps_d=1e-4, eps_c=1e-4, T_min=1 << 30,
+                      flags=nlr.NLR_INIT_SPLIT_F16 if split else 0)
     eprint("[bench] init done; warmup")
     if warm > 0:
         ctx.run(warm)
@@ -168,12 +174,17 @@ def main():
     dom_ms = kinfo[dom]["avg_ms"]
     dom_bytes = algorithmic_bytes(dom, n, d, r, dual_frac)
     achieved = dom_bytes / (dom_ms / 1e3) / 1e9
+    dom_name = dom + ("_split16" if split else "")
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": load_traffic(dom, args.workload),
-                "kernel": dom, "avg_launch_ms": round(dom_ms, 4),
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": load_traffic(dom_name, args.workload),
+                "kernel": dom_name, "avg_launch_ms": round(dom_ms, 4),
                 "algorithmic_bytes_per_launch": dom_bytes,
                 "mfma_tflops": round(2.0 * n * d * r / (dom_ms / 1e3) / 1e12, 2),
                 "mfma_frac": round(2.0 * n * d * r / (dom_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4)}
+    if split:
+        # three fp16 products per fp32 product, against the dense fp16 peak
+        roofline["mfma_tflops"] = round(3 * 2.0 * n * d * r / (dom_ms / 1e3) / 1e12, 2)
+        roofline["mfma_frac"] = round(roofline["mfma_tflops"] / FP16_MFMA_PEAK_TFLOPS, 4)
     eprint(f"[bench] {steps} steps in {t_ms:.2f} ms -> {t_ms / steps:.3f} ms/step, {value:.3e} pts*it/s, "
            f"effective {eff_gbs:.0f} GB/s ({eff_gbs / HBM_PEAK_GBS:.1%} of HBM), "
            f"{flops * steps / (t_ms / 1e3) / 1e12:.1f} TFLOP/s")
@@ -197,9 +208,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f16x3" if split else "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "n": n, "d": d, "K": K, "r": r, "alpha": alpha, "beta": 1.0,
+                   "products": "fp16 two-term split, fp32 accumulate" if split else "fp32",
                    "eps_d": 1e-4, "eps_c": 1e-4, "dual_step_fraction": dual_frac},
         "achieved_hbm_gbs": round(eff_gbs, 1),
         "hbm_frac": round(eff_gbs / HBM_PEAK_GBS, 4),

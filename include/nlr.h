@@ -94,7 +94,17 @@ typedef struct {
 enum {
   NLR_INIT_U_IN_OMEGA = 1, /* U already lies in Omega: skip the projection (resume) */
   NLR_INIT_KEEP_Y = 2,     /* keep the caller's y instead of zeroing it (resume) */
-  NLR_INIT_X_NORMALISED = 4 /* X already holds Xhat: skip centring and spectral normalisation */
+  NLR_INIT_X_NORMALISED = 4, /* X already holds Xhat: skip centring and spectral normalisation */
+  /* Run both products of the iteration (Theta = Xhat^T U and Xhat Theta) on the
+   * fp16 matrix cores with a two-term split of every fp32 operand:
+   * v = s (hi + lo), hi = fp16(v / s), lo = fp16(v / s - hi), with s a power of
+   * two chosen from a bound on |v| so that hi and lo stay in fp16's normal
+   * range, and v w ~ s_v s_w (hi_v hi_w + hi_v lo_w + lo_v hi_w) accumulated in
+   * fp32.  The representation error is about 2^-22 relative per operand, below
+   * the TF32 products of the paper's CUTLASS kernel (Appendix C), at about a fifth of the fp32 matrix
+   * work.  Supported for d <= 128 and r <= 64 (with d % 4 == 0, r % 4 == 0 and
+   * 16-byte aligned X and U); other shapes return NLR_EUNSUPPORTED. */
+  NLR_INIT_SPLIT_F16 = 8
 };
 
 /* Bytes of device workspace nlr_init needs for an (n, d, r) problem.  Depends

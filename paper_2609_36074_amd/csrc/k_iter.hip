@@ -20,13 +20,9 @@
 // "finish" is pass A without the matrix product: it materialises U = fl(c_f w)
 // and applies the pending end-of-iteration work, so a host call always returns
 // a materialised factor.
-#include "nlr_internal.hpp"
+#include "k_common.hpp"
 
 namespace nlr {
-
-__device__ __forceinline__ bool halted(const DevCtl* ctl) {
-  return (ctl->stop | ctl->breakdown) != 0;
-}
 
 // ---------------------------------------------------------------------------
 // Tile staging: rows [row0, row0+kTPA) x cols [c0, c0+cw) of a row-major matrix
@@ -256,27 +252,6 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
   }
 }
 
-// Loads W consecutive floats; when !ok the (valid) address is still read and the
-// values are replaced by zeros, so no branch is needed.
-template <int W>
-__device__ __forceinline__ void load_vec(float (&dst)[W], const float* src, bool ok) {
-  if constexpr (W == 4) {
-    const f32x4 t = *reinterpret_cast<const f32x4*>(src);
-    dst[0] = ok ? t.x : 0.f;
-    dst[1] = ok ? t.y : 0.f;
-    dst[2] = ok ? t.z : 0.f;
-    dst[3] = ok ? t.w : 0.f;
-  } else if constexpr (W == 2) {
-    typedef float f32x2 __attribute__((ext_vector_type(2)));
-    const f32x2 t = *reinterpret_cast<const f32x2*>(src);
-    dst[0] = ok ? t.x : 0.f;
-    dst[1] = ok ? t.y : 0.f;
-  } else {
-    const float t = *src;
-    dst[0] = ok ? t : 0.f;
-  }
-}
-
 // ---------------------------------------------------------------------------
 // Pass A, register-resident form on the 16x16x4 fp32 matrix core (all of Theta
 // fits one wave: FV*NGF*CV <= 32 blocks of 16x16).  Grid GA; each wave owns a
@@ -289,28 +264,6 @@ __device__ __forceinline__ void load_vec(float (&dst)[W], const float* src, bool
 // result is bitwise identical in all 16 lanes.
 // FINISH: no matrix product; writes u = fl(c_f w) back (materialises U).
 // ---------------------------------------------------------------------------
-template <int CTRL>
-__device__ __forceinline__ double dpp_d(double v) {
-  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, 0xF, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, 0xF, 0xF, false);
-  return __hiloint2double(hi, lo);
-}
-// Sum over the 16 lanes of a DPP row with involution pairings (xor 1, xor 2,
-// half-row mirror, row mirror): every step adds two equal partial sums, so all
-// lanes end with the same bits.
-__device__ __forceinline__ double row16_sum_d(double v) {
-  v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
-  v += dpp_d<0x4E>(v);   // quad_perm [2,3,0,1]
-  v += dpp_d<0x141>(v);  // row_half_mirror
-  v += dpp_d<0x140>(v);  // row_mirror
-  return v;
-}
-
-typedef float f32x4v __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ f32x4v mfma16x16x4(float a, float b, f32x4v c) {
-  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
 template <int FV, int NGF, int CV, bool FINISH>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_pass_a_rows(
     Geometry g, Bufs B, StepArgs S) {
@@ -618,23 +571,6 @@ __global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs
       cur->breakdown = 0;
     }
     if (finish) ctl->c_f = 1.0f;
-  }
-}
-
-// Reduce-scatter of LEN per-lane values across the lanes that differ in bits
-// MASK, MASK/2, ...: afterwards a lane holds LEN >> steps sums, of the upper half
-// when its bit is set and of the lower half otherwise.
-template <int LEN, int MASK>
-__device__ __forceinline__ void reduce_scatter(float* wv, int li) {
-  if constexpr (LEN > 1 && MASK > 0) {
-    const bool up = (li & MASK) != 0;
-#pragma unroll
-    for (int k = 0; k < LEN / 2; ++k) {
-      const float send = up ? wv[k] : wv[k + LEN / 2];
-      const float keep = up ? wv[k + LEN / 2] : wv[k];
-      wv[k] = keep + shfl_xor_f(send, MASK);
-    }
-    reduce_scatter<LEN / 2, MASK / 2>(wv, li);
   }
 }
 
@@ -1255,6 +1191,7 @@ static hipError_t pass_b_res_launch(const Geometry& g, const Bufs& b, const Step
 }
 
 hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  if (g.split_b) return launch_pass_b_split(g, b, a, st);
   if (g.b_res) {
     switch (g.NB * 10 + g.nch) {
       case 11: return pass_b_res_launch<1, 1>(g, b, a, st);

@@ -21,7 +21,11 @@ static int32_t next_pow2(int32_t x) {
 }
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16) {
+bool split_supported(int32_t d, int32_t r, bool aligned16) {
+  return aligned16 && d <= 128 && r <= 64 && d % 4 == 0 && r % 4 == 0;
+}
+
+Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split) {
   Geometry g;
   std::memset(&g, 0, sizeof(g));
   g.n = n;
@@ -107,6 +111,8 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
     g.GG = (int32_t)gg;
     g.gblk = g.d32 / 32;
   }
+  g.split_b = (split && g.b_res && split_supported(d, r, aligned16)) ? 1 : 0;
+  g.split_a = 0;
   g.vec_x = (d % 4 == 0 && aligned16) ? 1 : 0;
   g.vec_u = (r % 4 == 0 && aligned16) ? 1 : 0;
   return g;
@@ -341,11 +347,14 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   *ctx = nullptr;
   if (!X || !U || !y || !params_ok(params)) return NLR_EINVAL;
   if (!shape_ok(n, d, r) || K < 1 || K > r) return NLR_EINVAL;
-  if (flags & ~(uint32_t)(NLR_INIT_U_IN_OMEGA | NLR_INIT_KEEP_Y | NLR_INIT_X_NORMALISED)) return NLR_EINVAL;
+  if (flags & ~(uint32_t)(NLR_INIT_U_IN_OMEGA | NLR_INIT_KEEP_Y | NLR_INIT_X_NORMALISED | NLR_INIT_SPLIT_F16))
+    return NLR_EINVAL;
   if (((uintptr_t)X & 3) || ((uintptr_t)U & 3) || ((uintptr_t)y & 3)) return NLR_EINVAL;
   if (r > kMaxR) return NLR_EUNSUPPORTED;
   const bool aligned16 = (((uintptr_t)X & 15) == 0) && (((uintptr_t)U & 15) == 0);
-  const Geometry g0 = make_geometry(n, d, r, K, aligned16);
+  const bool split = (flags & NLR_INIT_SPLIT_F16) != 0;
+  if (split && !split_supported(d, r, aligned16)) return NLR_EUNSUPPORTED;
+  const Geometry g0 = make_geometry(n, d, r, K, aligned16, split);
   const size_t need = carve_workspace(g0, nullptr, nullptr);
   if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
 
@@ -391,6 +400,8 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
     if (launch_spectral(g, b, st) != hipSuccess) return fail(NLR_EHIP);
     if (launch_normalise(g, b, st) != hipSuccess) return fail(NLR_EHIP);
   }
+  if (split)
+    if (launch_xscale(g, b, st) != hipSuccess) return fail(NLR_EHIP);
   if (launch_project(g, b, (double)K, (flags & NLR_INIT_U_IN_OMEGA) ? 1 : 0, st) != hipSuccess)
     return fail(NLR_EHIP);
   if (!(flags & NLR_INIT_KEEP_Y))

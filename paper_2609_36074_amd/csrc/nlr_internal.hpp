@@ -28,7 +28,7 @@ struct alignas(16) DevCtl {
   int64_t t_done;      // completed primal steps
   int64_t pad64;
   float c_f;           // lazy scale of the factor buffer (1 when materialised)
-  float pad_f;
+  float x_scale;       // power of two keeping |Xhat| x_scale < 2^15 (split-fp16 products)
   int32_t pad_i0, pad_i1;
   double a, b, h;      // fused statistics of the latest primal step
   double Delta;        // squared movement estimate
@@ -80,6 +80,7 @@ struct Geometry {
   int32_t nch;          // 32-feature chunks of d
   int32_t theta_lds;    // 1: Theta staged whole in LDS
   int32_t b_res;        // 1: resident-tile pass B (k_pass_b_res)
+  int32_t split_a, split_b;  // 1: split-fp16 products in pass A / pass B
   int32_t ldsB_bytes;
   // init
   int32_t GI;           // row-chunk workgroups of the init reductions
@@ -118,7 +119,10 @@ struct Bufs {
 };
 
 // aligned16: X and U start on 16-byte boundaries (enables the vector-load kernels)
-Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16);
+// split: split-fp16 products requested (NLR_INIT_SPLIT_F16)
+Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split = false);
+// the split-fp16 products support this shape and alignment
+bool split_supported(int32_t d, int32_t r, bool aligned16);
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
 
 // ---- kernel launchers (each returns the launch error) ----
@@ -140,6 +144,8 @@ hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, boo
                         hipStream_t st);
 hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_ctl_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_xscale(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_pass_b_split(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_labels(const Geometry& g, const Bufs& b, int32_t* labels, hipStream_t st);
 
 // ---- device helpers ----

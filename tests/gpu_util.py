@@ -54,3 +54,37 @@ def label_agreement(lab_gpu: np.ndarray, U_ref: np.ndarray, rel_gap: float = 2e-
     ref = onlr.labels(U_ref)
     bad = (lab_gpu != ref) & ~amb
     return int(bad.sum()), int(amb.sum())
+
+
+def trajectory(X, Z, K, alpha, beta, T, eps_d=1e-4, eps_c=1e-4, one_step_tol=None, flags=0):
+    """Steps the GPU T times; returns per-iteration errors vs the oracle (gate replay)
+    and per-iteration one-step errors (oracle step from the GPU's own iterate)."""
+    ctx = make_ctx(X, Z, K, alpha, beta, eps_d=eps_d, eps_c=eps_c, T_min=T, flags=flags)
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    n = X.shape[0]
+    U_gpu = [host(ctx.U)]
+    y_gpu = [host(ctx.y)]
+    stats = []
+    for t in range(T):
+        stats.append(ctx.step())
+        U_gpu.append(host(ctx.U))
+        y_gpu.append(host(ctx.y))
+    gates = [bool(s["dual_step"]) for s in stats]
+    ref = onlr.run(Xh, Z, K, alpha, beta, T=T, T_min=T, eps_d=eps_d, eps_c=eps_c, gates=gates,
+                   keep_trajectory=True)
+    traj_err = [rel_max_err(U_gpu[t + 1], ref.trajectory[t]) for t in range(T)]
+    obj_err = [obj_rel_err(stats[t]["objective"], ref.records[t].objective, 1.0) for t in range(T)]
+    # gate decisions against the oracle's own movement
+    bad_gates = [t for t in range(T)
+                 if gates[t] != (ref.records[t].delta < eps_d)
+                 and abs(ref.records[t].delta - eps_d) > 1e-3 * eps_d]
+    one = []
+    if one_step_tol is not None:
+        for t in range(T):
+            y_math = onlr.dual_from_stored(y_gpu[t])
+            r1 = onlr.run(Xh, U_gpu[t], K, alpha, beta, T=1, T_min=1, project_init=False, y0=y_math,
+                          gates=[gates[t]])
+            one.append(rel_max_err(U_gpu[t + 1], r1.U))
+            ystored = onlr.stored_dual(r1.y)
+            assert np.abs(y_gpu[t + 1] - ystored).max() <= 1e-5 * max(1e-12, np.abs(ystored).max()) + 1e-12, t
+    return ctx, ref, traj_err, obj_err, bad_gates, one, U_gpu, stats

@@ -11,7 +11,8 @@ within 1e-3 relative of eps_d).
 import numpy as np
 import pytest
 
-from gpu_util import OBJ_TOL, U_TOL, host, label_agreement, log, make_ctx, obj_rel_err, rel_max_err
+from gpu_util import (OBJ_TOL, U_TOL, host, label_agreement, log, make_ctx, obj_rel_err, rel_max_err,
+                      trajectory)
 from oracle import nlr as onlr
 from synth import gaussian_mixture, make_workload, standard_normal_factor
 
@@ -97,46 +98,12 @@ def test_one_step_tiny():
 
 
 # ---------------------------------------------------------------- trajectories
-def _trajectory(X, Z, K, alpha, beta, T, eps_d=1e-4, eps_c=1e-4, one_step_tol=None):
-    """Steps the GPU T times; returns per-iteration errors vs the oracle (gate replay)
-    and per-iteration one-step errors (oracle step from the GPU's own iterate)."""
-    ctx = make_ctx(X, Z, K, alpha, beta, eps_d=eps_d, eps_c=eps_c, T_min=T)
-    Xh, _, _ = onlr.centre_and_normalise(X)
-    n = X.shape[0]
-    U_gpu = [host(ctx.U)]
-    y_gpu = [host(ctx.y)]
-    stats = []
-    for t in range(T):
-        stats.append(ctx.step())
-        U_gpu.append(host(ctx.U))
-        y_gpu.append(host(ctx.y))
-    gates = [bool(s["dual_step"]) for s in stats]
-    ref = onlr.run(Xh, Z, K, alpha, beta, T=T, T_min=T, eps_d=eps_d, eps_c=eps_c, gates=gates,
-                   keep_trajectory=True)
-    traj_err = [rel_max_err(U_gpu[t + 1], ref.trajectory[t]) for t in range(T)]
-    obj_err = [obj_rel_err(stats[t]["objective"], ref.records[t].objective, 1.0) for t in range(T)]
-    # gate decisions against the oracle's own movement
-    bad_gates = [t for t in range(T)
-                 if gates[t] != (ref.records[t].delta < eps_d)
-                 and abs(ref.records[t].delta - eps_d) > 1e-3 * eps_d]
-    one = []
-    if one_step_tol is not None:
-        for t in range(T):
-            y_math = onlr.dual_from_stored(y_gpu[t])
-            r1 = onlr.run(Xh, U_gpu[t], K, alpha, beta, T=1, T_min=1, project_init=False, y0=y_math,
-                          gates=[gates[t]])
-            one.append(rel_max_err(U_gpu[t + 1], r1.U))
-            ystored = onlr.stored_dual(r1.y)
-            assert np.abs(y_gpu[t + 1] - ystored).max() <= 1e-5 * max(1e-12, np.abs(ystored).max()) + 1e-12, t
-    return ctx, ref, traj_err, obj_err, bad_gates, one, U_gpu, stats
-
-
 def test_trajectory_tiny_200():
     X, Z, lab, wl = _tiny()
     K = wl.K
     alpha, beta = onlr.default_step_size(K), 1.0
     log("tiny trajectory T=200")
-    ctx, ref, traj, obj, bad_gates, one, U_gpu, stats = _trajectory(X, Z, K, alpha, beta, wl.T,
+    ctx, ref, traj, obj, bad_gates, one, U_gpu, stats = trajectory(X, Z, K, alpha, beta, wl.T,
                                                                     one_step_tol=True)
     log(f"max traj err {max(traj):.3e}  max one-step err {max(one):.3e}  max obj err {max(obj):.3e}")
     assert max(traj) < U_TOL, (int(np.argmax(traj)), max(traj))
@@ -152,7 +119,7 @@ def test_trajectory_tiny_200():
 def test_trajectory_with_dual_steps():
     """Gated dual steps along a 1000-iteration trajectory."""
     X, Z, lab, K, beta, alpha = _gated()
-    ctx, ref, traj, obj, bad_gates, one, _, stats = _trajectory(X, Z, K, alpha, beta, 1000, eps_d=3e-3,
+    ctx, ref, traj, obj, bad_gates, one, _, stats = trajectory(X, Z, K, alpha, beta, 1000, eps_d=3e-3,
                                                               eps_c=1e-7, one_step_tol=True)
     ngates = sum(s["dual_step"] for s in stats)
     log(f"dual steps {ngates}; max traj err {max(traj):.3e} one-step {max(one):.3e} obj {max(obj):.3e}")
@@ -169,7 +136,7 @@ def test_ragged_shapes(n, d, r, K):
     X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 7 + d)
     Z = standard_normal_factor(n, r, seed=n + r).astype(np.float64)
     alpha = onlr.default_step_size(K)
-    _, _, traj, obj, bad_gates, one, _, _ = _trajectory(X, Z, K, alpha, 1.0, 8, one_step_tol=True)
+    _, _, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, alpha, 1.0, 8, one_step_tol=True)
     log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
     assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
     assert not bad_gates
@@ -181,7 +148,7 @@ def test_gmm1m_parity():
     K = wl.K
     alpha = onlr.default_step_size(K)
     log("gmm1m trajectory T=6")
-    ctx, ref, traj, obj, bad_gates, one, _, _ = _trajectory(X, Z, K, alpha, 1.0, 6, one_step_tol=True)
+    ctx, ref, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, alpha, 1.0, 6, one_step_tol=True)
     log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
     assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
     bad, amb = label_agreement(ctx.labels().cpu().numpy(), ref.U)
