@@ -39,14 +39,18 @@ def algorithmic_bytes(kind: str, n: int, d: int, r: int, dual_frac: float = 0.0)
         return 4.0 * (n * d + 2 * n * r + n)
     if kind == "pass_a":      # read Xhat, read U, read ytilde (+ write it on dual steps)
         return 4.0 * (n * d + n * r + n) + 4.0 * n * dual_frac
-    if kind == "step":        # whole iteration, two-pass structure
+    if kind == "pass_bf":     # fused pass B: as pass B (the Theta partials stay on chip)
+        return 4.0 * (n * d + 2 * n * r + n)
+    if kind == "pass_u":      # row pass: read U and ytilde (+ write ytilde on dual steps)
+        return 4.0 * (n * r + n) + 4.0 * n * dual_frac
+    if kind == "step":        # whole iteration of the two-pass structure: the fixed numerator
         return 4.0 * (2 * n * d + 3 * n * r + 2 * n) + 4.0 * n * dual_frac
     raise ValueError(kind)
 
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("k_iter.hip", "k_split.hip", "k_common.hpp", "nlr_internal.hpp"):
+    for f in ("k_iter.hip", "k_split.hip", "k_fused.hip", "k_common.hpp", "nlr_internal.hpp"):
         with open(os.path.join(ROOT, "paper_2609_36074_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -100,6 +104,8 @@ def main():
     ap.add_argument("--gemm", choices=("fp32", "split16"), default="fp32",
                     help="fp32: both products on the fp32 matrix cores; split16: two-term fp16 splits of the "
                          "operands on the fp16 matrix cores (NLR_INIT_SPLIT_F16)")
+    ap.add_argument("--two-pass", action="store_true",
+                    help="use the two-pass iteration (NLR_INIT_TWO_PASS) instead of the single-Xhat-pass form")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=2_000_000)
     ap.add_argument("--cpu-iters", type=int, default=8)
@@ -142,7 +148,7 @@ def main():
     steps, warm = args.steps, args.warmup
     split = args.gemm == "split16"
     ctx = nlr.Context(Xt, K, Ut, alpha=alpha, beta=1.0, eps_d=1e-4, eps_c=1e-4, T_min=1 << 30,
-                      flags=nlr.NLR_INIT_SPLIT_F16 if split else 0)
+                      flags=(nlr.NLR_INIT_SPLIT_F16 if split else 0) | (nlr.NLR_INIT_TWO_PASS if args.two_pass else 0))
     eprint("[bench] init done; warmup")
     if warm > 0:
         ctx.run(warm)
@@ -170,7 +176,7 @@ def main():
     flops = 4.0 * n * d * r
     kinfo = {k: {"total_ms": v[0], "launches": v[1], "avg_ms": (v[0] / v[1]) if v[1] else None}
              for k, v in kt.items() if v[1]}
-    dom = max(("pass_a", "pass_b"), key=lambda k: kinfo.get(k, {"total_ms": 0})["total_ms"])
+    dom = max(("pass_a", "pass_b", "pass_u", "pass_bf"), key=lambda k: kinfo.get(k, {"total_ms": 0})["total_ms"])
     dom_ms = kinfo[dom]["avg_ms"]
     dom_bytes = algorithmic_bytes(dom, n, d, r, dual_frac)
     achieved = dom_bytes / (dom_ms / 1e3) / 1e9

@@ -95,8 +95,9 @@ enum {
   NLR_INIT_U_IN_OMEGA = 1, /* U already lies in Omega: skip the projection (resume) */
   NLR_INIT_KEEP_Y = 2,     /* keep the caller's y instead of zeroing it (resume) */
   NLR_INIT_X_NORMALISED = 4, /* X already holds Xhat: skip centring and spectral normalisation */
-  /* Run both products of the iteration (Theta = Xhat^T U and Xhat Theta) on the
-   * fp16 matrix cores with a two-term split of every fp32 operand:
+  /* Run the products of the iteration on the fp16 matrix cores (both products in
+   * the single-Xhat-pass form; Xhat Theta only with NLR_INIT_TWO_PASS) with a
+   * two-term split of every fp32 operand:
    * v = s (hi + lo), hi = fp16(v / s), lo = fp16(v / s - hi), with s a power of
    * two chosen from a bound on |v| so that hi and lo stay in fp16's normal
    * range, and v w ~ s_v s_w (hi_v hi_w + hi_v lo_w + lo_v hi_w) accumulated in
@@ -104,7 +105,16 @@ enum {
    * the TF32 products of the paper's CUTLASS kernel (Appendix C), at about a fifth of the fp32 matrix
    * work.  Supported for d <= 128 and r <= 64 (with d % 4 == 0, r % 4 == 0 and
    * 16-byte aligned X and U); other shapes return NLR_EUNSUPPORTED. */
-  NLR_INIT_SPLIT_F16 = 8
+  NLR_INIT_SPLIT_F16 = 8,
+  /* Use the two-pass iteration (pass A: Theta = Xhat^T U with the row work; pass
+   * B: Xhat Theta with the fused epilogue) even where the single-Xhat-pass form
+   * is available.  By default, for d <= 128 and r <= 64 (d % 4 == 0, r % 4 == 0,
+   * 16-byte aligned X and U), each iteration reads Xhat once: pass B also forms
+   * the partials of Xhat^T W_{t+1}, and Theta_{t+1} = c_{t+1} Xhat^T W_{t+1}
+   * (U_{t+1} = c_{t+1} W_{t+1}, Algorithm 1), while a row pass over U and ytilde
+   * does the rest of pass A's work.  Both forms compute the same iteration; they
+   * differ by floating-point rounding only. */
+  NLR_INIT_TWO_PASS = 16
 };
 
 /* Bytes of device workspace nlr_init needs for an (n, d, r) problem.  Depends

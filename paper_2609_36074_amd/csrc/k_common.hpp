@@ -5,6 +5,10 @@
 
 namespace nlr {
 
+// Forms of the row-resident pass A: with the Theta product, the finish pass
+// (materialises U), and the row work alone (fused iteration).
+enum PassAMode { kPassIter = 0, kPassFinish = 1, kPassRows = 2 };
+
 __device__ __forceinline__ bool halted(const DevCtl* ctl) {
   return (ctl->stop | ctl->breakdown) != 0;
 }

@@ -262,17 +262,22 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
 // A row's columns live in one 16-lane DPP row, so the row work (q = u.p - 1,
 // dual step, ybar, s, ||q||^2, ytilde^T q) uses a 4-step DPP butterfly whose
 // result is bitwise identical in all 16 lanes.
-// FINISH: no matrix product; writes u = fl(c_f w) back (materialises U).
+// MODE kPassFinish: no matrix product; writes u = fl(c_f w) back (materialises U).
+// MODE kPassRows: no matrix product and no write of U: the row work of the fused
+// iteration, whose Theta comes from the previous pass B.
 // ---------------------------------------------------------------------------
-template <int FV, int NGF, int CV, bool FINISH>
+template <int FV, int NGF, int CV, int MODE>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_pass_a_rows(
     Geometry g, Bufs B, StepArgs S) {
+  constexpr bool FINISH = MODE == kPassFinish;
+  constexpr bool THETA = MODE == kPassIter;
   if (FINISH ? (B.ctl->breakdown != 0) : halted(B.ctl)) return;
   const bool stopped = FINISH && (B.ctl->stop != 0);
   constexpr int NBLK = FV * NGF * CV;  // 16x16 blocks of Theta
-  constexpr int PF = NBLK >= 32 ? 2 : 4;  // k-steps in flight (fewer when Theta takes 128 registers)
+  // k-steps in flight: fewer when Theta takes 128 registers, more when only U and y stream
+  constexpr int PF = THETA ? (NBLK >= 32 ? 2 : 4) : 8;
   __shared__ double dred[kThreads + 8];
-  __shared__ float comb[FINISH ? 4 : 2 * NBLK * 4 * 64];
+  __shared__ float comb[THETA ? 2 * NBLK * 4 * 64 : 4];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -300,7 +305,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
   const int64_t k1 = (wid + 1) * steps / nw;
 
   f32x4v acc[NBLK];
-  if (!FINISH) {
+  if (THETA) {
 #pragma unroll
     for (int b = 0; b < NBLK; ++b) acc[b] = (f32x4v){0.f, 0.f, 0.f, 0.f};
   }
@@ -323,7 +328,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
     const int64_t row = 4 * k + grp;
     const bool ok = (k < k1) && (row < n);
     const int64_t rr = ok ? row : 0;
-    if (!FINISH) {
+    if (THETA) {
 #pragma unroll
       for (int gg = 0; gg < NGF; ++gg) {
         const int f = 16 * FV * gg + FV * li;
@@ -352,7 +357,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
       float u[CV];
 #pragma unroll
       for (int c = 0; c < CV; ++c) u[c] = (valid && cx) ? ur[i][c] * cf : 0.f;
-      if (!FINISH) {
+      if (THETA) {
 #pragma unroll
         for (int gg = 0; gg < NGF; ++gg)
 #pragma unroll
@@ -399,7 +404,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
   __builtin_amdgcn_sched_barrier(0);
 
   // ---- partials ----
-  if (!FINISH) {
+  if (THETA) {
     // Theta: ((wave0 + wave2) + (wave1 + wave3)) through two LDS regions
     constexpr int REG = NBLK * 4 * 64;
     if (wave < 2) {
@@ -492,15 +497,18 @@ __global__ __launch_bounds__(kThreads) void k_seg_sum(const T* __restrict__ P, i
 // Layout: chunk ch of 32 features, quarter j (4 features), m-block mb, lane l,
 // element e  <->  Theta[32 ch + 16 (l/32) + 4 j + e][32 mb + l%32].
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B) {
+__global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, int nseg, int scaled) {
   if (halted(B.ctl)) return;
   __shared__ double red[8];
   const int64_t tot = (int64_t)g.d32 * g.r32;
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   double sum = 0.0;
   if (e < tot) {
-    for (int s = 0; s < g.SA; ++s) sum += B.seg_theta[(int64_t)s * tot + e];
+    for (int s = 0; s < nseg; ++s) sum += B.seg_theta[(int64_t)s * tot + e];
     const int f = (int)(e / g.r32);
+    // partials of Xhat^T W (fused pass B) carry the scale c of U = c W
+    if (scaled) sum *= (double)B.ctl->c_f;
+    if (f >= g.d) sum = 0.0;  // padded features: zero rows of Theta
     const int c = (int)(e - (int64_t)f * g.r32);
     const int ch = f >> 5, fin = f & 31;
     const int hh = fin >> 4, j = (fin & 15) >> 2, ee = fin & 3;
@@ -1097,16 +1105,18 @@ static hipError_t pass_a_nbg(const Geometry& g, const Bufs& b, const StepArgs& a
 }
 
 template <int FV, int NGF, int CV>
-static hipError_t pass_a_rows_launch(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
+static hipError_t pass_a_rows_launch(const Geometry& g, const Bufs& b, const StepArgs& a, int mode,
                                      hipStream_t st) {
-  if (finish)
-    hipLaunchKernelGGL((k_pass_a_rows<FV, NGF, CV, true>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
+  if (mode == kPassFinish)
+    hipLaunchKernelGGL((k_pass_a_rows<FV, NGF, CV, kPassFinish>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
+  else if (mode == kPassRows)
+    hipLaunchKernelGGL((k_pass_a_rows<FV, NGF, CV, kPassRows>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
   else
-    hipLaunchKernelGGL((k_pass_a_rows<FV, NGF, CV, false>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
+    hipLaunchKernelGGL((k_pass_a_rows<FV, NGF, CV, kPassIter>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
   return hipGetLastError();
 }
 
-static hipError_t pass_a_rows_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
+static hipError_t pass_a_rows_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, int finish,
                                        hipStream_t st) {
   const int key = g.a_fv * 100 + g.a_ngf * 10 + g.a_cv;
   switch (key) {
@@ -1126,8 +1136,13 @@ static hipError_t pass_a_rows_dispatch(const Geometry& g, const Bufs& b, const S
   }
 }
 
+hipError_t launch_pass_u(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  if (!g.a_rows) return hipErrorInvalidValue;
+  return pass_a_rows_dispatch(g, b, a, kPassRows, st);
+}
+
 hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish, hipStream_t st) {
-  if (g.a_rows) return pass_a_rows_dispatch(g, b, a, finish, st);
+  if (g.a_rows) return pass_a_rows_dispatch(g, b, a, finish ? kPassFinish : kPassIter, st);
   if (finish) return pass_a_nbg<4, true>(g, b, a, st);
   switch (g.MBG) {
     case 1: return pass_a_nbg<1, false>(g, b, a, st);
@@ -1137,13 +1152,15 @@ hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bo
   }
 }
 
-hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, hipStream_t st) {
+hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, bool fused_partials, hipStream_t st) {
   const int C = g.d32 * g.r32;
-  hipLaunchKernelGGL((k_seg_sum<float>), dim3((C + 63) / 64, g.SA), dim3(kThreads), 0, st,
-                     (const float*)b.theta_part, (int64_t)g.GA, C, b.seg_theta, g.SA, (const DevCtl*)b.ctl, 1);
+  const int64_t rows = fused_partials ? g.GB : g.GA;
+  const int nseg = fused_partials ? g.SAF : g.SA;
+  hipLaunchKernelGGL((k_seg_sum<float>), dim3((C + 63) / 64, nseg), dim3(kThreads), 0, st,
+                     (const float*)b.theta_part, rows, C, b.seg_theta, nseg, (const DevCtl*)b.ctl, 1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT), dim3(kThreads), 0, st, g, b);
+  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT), dim3(kThreads), 0, st, g, b, nseg, fused_partials ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -25,7 +25,7 @@ bool split_supported(int32_t d, int32_t r, bool aligned16) {
   return aligned16 && d <= 128 && r <= 64 && d % 4 == 0 && r % 4 == 0;
 }
 
-Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split) {
+Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split, bool fused) {
   Geometry g;
   std::memset(&g, 0, sizeof(g));
   g.n = n;
@@ -113,6 +113,16 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   }
   g.split_b = (split && g.b_res && split_supported(d, r, aligned16)) ? 1 : 0;
   g.split_a = 0;
+  // single-Xhat-pass iteration: the row pass and the fused pass B need the
+  // register-resident shapes; one persistent workgroup per compute unit
+  g.fused = (fused && split_supported(d, r, aligned16) && g.a_rows && g.b_res) ? 1 : 0;
+  g.SAF = g.SA;
+  if (g.fused) {
+    g.GB = (int32_t)(g.tilesB < 256 ? g.tilesB : 256);
+    g.SB = (g.GB + 31) / 32;
+    g.SAF = (g.GB + 31) / 32;
+    g.split_a = g.split_b;  // both products live in the fused pass B
+  }
   g.vec_x = (d % 4 == 0 && aligned16) ? 1 : 0;
   g.vec_u = (r % 4 == 0 && aligned16) ? 1 : 0;
   return g;
@@ -136,13 +146,15 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.th2_part = reinterpret_cast<double*>(take((size_t)g.RT * 8));
   b.b_part = reinterpret_cast<double*>(take((size_t)g.GB * (4 + r32) * 8));
   b.a_part = reinterpret_cast<double*>(take((size_t)g.GA * (4 + r32) * 8));
-  b.seg_theta = reinterpret_cast<double*>(take((size_t)g.SA * g.d32 * r32 * 8));
+  const size_t segs = (size_t)(g.SA > g.SAF ? g.SA : g.SAF);
+  b.seg_theta = reinterpret_cast<double*>(take(segs * g.d32 * r32 * 8));
   b.seg_a = reinterpret_cast<double*>(take((size_t)g.SA * (4 + r32) * 8));
   b.seg_b = reinterpret_cast<double*>(take((size_t)g.SB * (4 + r32) * 8));
   b.i_xbar = reinterpret_cast<double*>(take(d * 8));
   b.dump = reinterpret_cast<float*>(take(256));
   // union: pass-A Theta partials | init temporaries
-  const size_t u_iter = align256((size_t)g.GA * g.d32 * r32 * 4);
+  const size_t prow = (size_t)(g.GA > g.GB ? g.GA : g.GB);  // pass A or fused pass B partials
+  const size_t u_iter = align256(prow * g.d32 * r32 * 4);
   size_t u_init = 0;
   u_init += align256((size_t)g.GI * d * 8);            // colsum
   u_init += align256((size_t)g.GG * d * d * 8);         // gram partials
@@ -183,10 +195,12 @@ enum KernelKind {
   KK_CTL_B,
   KK_FINISH,
   KK_CTL_FINISH,
+  KK_PASS_U,
+  KK_PASS_BF,
   KK_COUNT
 };
-static const char* kKernelNames[KK_COUNT] = {"pass_a", "reduce_theta", "ctl_a", "pass_b",
-                                             "ctl_b",  "finish",       "ctl_finish"};
+static const char* kKernelNames[KK_COUNT] = {"pass_a", "reduce_theta", "ctl_a",  "pass_b", "ctl_b",
+                                             "finish", "ctl_finish",   "pass_u", "pass_bf"};
 
 struct nlr_ctx {
   Geometry g;
@@ -293,8 +307,21 @@ static hipError_t prof_collect(nlr_ctx* c) {
 
 static nlr_status enqueue_iteration(nlr_ctx* c) {
   const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
+  if (c->g.fused) {
+    // row pass (end of the previous iteration, s, rho, objective terms), control,
+    // fused pass B (W and the partials of Xhat^T W), control, Theta of the new factor
+    LAUNCH(KK_PASS_U, launch_pass_u(c->g, c->b, a, c->stream));
+    LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
+    LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
+    LAUNCH(KK_PASS_BF, launch_pass_bf(c->g, c->b, a, c->stream));
+    LAUNCH(KK_CTL_B, launch_seg_b(c->g, c->b, c->stream));
+    LAUNCH(KK_CTL_B, launch_ctl_b(c->g, c->b, a, c->stream));
+    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, true, c->stream));
+    c->pending = true;
+    return NLR_OK;
+  }
   LAUNCH(KK_PASS_A, launch_pass_a(c->g, c->b, a, false, c->stream));
-  LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, c->stream));
+  LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, false, c->stream));
   LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
   LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
   LAUNCH(KK_PASS_B, launch_pass_b(c->g, c->b, a, c->stream));
@@ -334,10 +361,15 @@ extern "C" {
 
 size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r) {
   if (!shape_ok(n, d, r) || r > kMaxR) return 0;
-  // the layout differs with the alignment of X and U (vector kernels or not): cover both
-  const size_t a = carve_workspace(make_geometry(n, d, r, 1, true), nullptr, nullptr);
-  const size_t b = carve_workspace(make_geometry(n, d, r, 1, false), nullptr, nullptr);
-  return a > b ? a : b;
+  // the layout differs with the alignment of X and U (vector kernels or not) and
+  // with the iteration structure (two passes or fused): cover all of them
+  size_t m = 0;
+  for (int al = 0; al < 2; ++al)
+    for (int fu = 0; fu < 2; ++fu) {
+      const size_t s = carve_workspace(make_geometry(n, d, r, 1, al != 0, false, fu != 0), nullptr, nullptr);
+      if (s > m) m = s;
+    }
+  return m;
 }
 
 nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, int32_t r, float* U, float* y,
@@ -347,14 +379,16 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   *ctx = nullptr;
   if (!X || !U || !y || !params_ok(params)) return NLR_EINVAL;
   if (!shape_ok(n, d, r) || K < 1 || K > r) return NLR_EINVAL;
-  if (flags & ~(uint32_t)(NLR_INIT_U_IN_OMEGA | NLR_INIT_KEEP_Y | NLR_INIT_X_NORMALISED | NLR_INIT_SPLIT_F16))
+  if (flags & ~(uint32_t)(NLR_INIT_U_IN_OMEGA | NLR_INIT_KEEP_Y | NLR_INIT_X_NORMALISED | NLR_INIT_SPLIT_F16 |
+                          NLR_INIT_TWO_PASS))
     return NLR_EINVAL;
   if (((uintptr_t)X & 3) || ((uintptr_t)U & 3) || ((uintptr_t)y & 3)) return NLR_EINVAL;
   if (r > kMaxR) return NLR_EUNSUPPORTED;
   const bool aligned16 = (((uintptr_t)X & 15) == 0) && (((uintptr_t)U & 15) == 0);
   const bool split = (flags & NLR_INIT_SPLIT_F16) != 0;
   if (split && !split_supported(d, r, aligned16)) return NLR_EUNSUPPORTED;
-  const Geometry g0 = make_geometry(n, d, r, K, aligned16, split);
+  const bool fused = (flags & NLR_INIT_TWO_PASS) == 0;
+  const Geometry g0 = make_geometry(n, d, r, K, aligned16, split, fused);
   const size_t need = carve_workspace(g0, nullptr, nullptr);
   if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
 
@@ -406,6 +440,12 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
     return fail(NLR_EHIP);
   if (!(flags & NLR_INIT_KEEP_Y))
     if (launch_zero_y(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+  if (g.fused) {
+    // Theta_0 = Xhat^T U_0: one pass A (its row partials are recomputed by the first row pass)
+    const StepArgs a0 = make_step_args(c, 0);
+    if (launch_pass_a(g, b, a0, false, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_reduce_theta(g, b, false, st) != hipSuccess) return fail(NLR_EHIP);
+  }
   if (read_ctl(c) != NLR_OK) return fail(NLR_EHIP);
   if (c->host_ctl->degenerate) return fail(NLR_EDEGENERATE);
   if (c->host_ctl->breakdown) return fail(NLR_EBREAKDOWN);

@@ -81,6 +81,8 @@ struct Geometry {
   int32_t theta_lds;    // 1: Theta staged whole in LDS
   int32_t b_res;        // 1: resident-tile pass B (k_pass_b_res)
   int32_t split_a, split_b;  // 1: split-fp16 products in pass A / pass B
+  int32_t fused;        // 1: single-Xhat-pass iteration (row pass + fused pass B)
+  int32_t SAF;          // segments of the fused pass B Theta partials (GB rows)
   int32_t ldsB_bytes;
   // init
   int32_t GI;           // row-chunk workgroups of the init reductions
@@ -120,7 +122,8 @@ struct Bufs {
 
 // aligned16: X and U start on 16-byte boundaries (enables the vector-load kernels)
 // split: split-fp16 products requested (NLR_INIT_SPLIT_F16)
-Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split = false);
+Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split = false,
+                       bool fused = false);
 // the split-fp16 products support this shape and alignment
 bool split_supported(int32_t d, int32_t r, bool aligned16);
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
@@ -137,7 +140,10 @@ hipError_t launch_zero_y(const Geometry& g, const Bufs& b, hipStream_t st);
 
 hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,
                          hipStream_t st);
-hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_pass_u(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+// fused_partials: the partials are Xhat^T W from the fused pass B (GB rows, scaled by c_f)
+hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, bool fused_partials, hipStream_t st);
+hipError_t launch_pass_bf(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_seg_a(const Geometry& g, const Bufs& b, bool finish, hipStream_t st);
 hipError_t launch_seg_b(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish,

@@ -74,16 +74,22 @@ def test_init_projection(n, r, K):
 
 
 # ---------------------------------------------------------------- one step
-def test_one_step_tiny():
+TWO_PASS = 16  # NLR_INIT_TWO_PASS
+
+
+@pytest.mark.parametrize("flags", [0, TWO_PASS])
+def test_one_step_tiny(flags):
     X, Z, _, wl = _tiny()
     K = wl.K
     alpha, beta = onlr.default_step_size(K), 1.0
-    ctx = make_ctx(X, Z, K, alpha, beta)
+    ctx = make_ctx(X, Z, K, alpha, beta, flags=flags)
     U0 = host(ctx.U)
     st = ctx.step()
     Xh, _, _ = onlr.centre_and_normalise(X)
     theta = ctx.inspect("theta").astype(np.float64)
-    th_ref = Xh.T @ U0
+    # two passes: Theta of the step's starting factor; single Xhat pass: Theta of the new factor,
+    # formed as c Xhat^T W inside pass B
+    th_ref = Xh.T @ (U0 if flags & TWO_PASS else host(ctx.U))
     assert rel_max_err(theta, th_ref) < 1e-5
     res = onlr.run(Xh, U0, K, alpha, beta, T=1, T_min=1, project_init=False, gates=[bool(st["dual_step"])])
     rec = res.records[0]
@@ -114,6 +120,30 @@ def test_trajectory_tiny_200():
     bad, amb = label_agreement(labels, ref.U)
     log(f"labels: {bad} mismatches, {amb} ambiguous rows")
     assert bad == 0
+
+
+def test_trajectory_tiny_two_pass():
+    """The two-pass iteration (pass A with Theta) on the same trajectory."""
+    X, Z, lab, wl = _tiny()
+    K = wl.K
+    ctx, ref, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, onlr.default_step_size(K), 1.0, wl.T,
+                                                           one_step_tol=True, flags=TWO_PASS)
+    log(f"two-pass: max traj err {max(traj):.3e}  one-step {max(one):.3e}  obj {max(obj):.3e}")
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates, bad_gates
+
+
+def test_fused_and_two_pass_agree():
+    """Both iteration structures step the same iterate; they differ by rounding only."""
+    X, Z, _, K, beta, alpha = _gated()
+    kw = dict(eps_d=3e-3, eps_c=1e-7, T_min=0)
+    a = make_ctx(X, Z, K, alpha, beta, **kw)
+    b = make_ctx(X, Z, K, alpha, beta, flags=TWO_PASS, **kw)
+    a.run(300)
+    b.run(300)
+    d = np.abs(host(a.U) - host(b.U)).max() / np.abs(host(b.U)).max()
+    log(f"fused vs two-pass after 300 steps: {d:.2e}")
+    assert d < U_TOL / 10
 
 
 def test_trajectory_with_dual_steps():

@@ -100,6 +100,18 @@ def test_split_run_equals_steps_and_deterministic():
     assert sum(h["dual_step"] for h in a.history(T)) > 50
 
 
+def test_split_two_pass_trajectory():
+    """Split products in the two-pass iteration (pass B split, pass A fp32)."""
+    X, Z, _, wl = make_workload("tiny")
+    Z = Z.astype(np.float64)
+    K = wl.K
+    _, _, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, onlr.default_step_size(K), 1.0, 100,
+                                                       one_step_tol=True, flags=SPLIT | 16)
+    log(f"  split two-pass: traj {max(traj):.3e} one {max(one):.3e} obj {max(obj):.3e}")
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates
+
+
 def test_split_matches_fp32_path_closely():
     """Both product forms step the same iterate; their difference is far inside the parity bar."""
     X, Z, _, wl = make_workload("tiny")
