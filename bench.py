@@ -1,13 +1,17 @@
 #!/usr/bin/env python3
 """Benchmark of the NLR iteration on one MI355X.
 
-A "step" is one full iteration of Algorithm 1 (pass A, Theta reduction,
-control, fused pass B, control) over the whole synthetic Gaussian-mixture
-matrix, which is resident in HBM before timing starts.  `value` is
-points*iterations per second over the timed run.  The `roofline` object
-describes the dominant kernel, timed with HIP events on the library's stream
-inside the same timed region; `cpu_baseline` times the fp64 oracle on a
-bounded sample of the same workload on the host cores.
+A "step" is one full iteration of Algorithm 1 over the whole synthetic
+Gaussian-mixture matrix, which is resident in HBM before timing starts.  By
+default the single-Xhat-pass form runs (row pass, control, fused pass B that
+also forms the next Theta's partials, control, Theta reduction) with the
+split-fp16 products; `--gemm fp32` uses the fp32 matrix cores and
+`--two-pass` the two-pass form.  A second timed run with the other product form
+is reported under "alt".  `value` is points*iterations per second over the
+timed run.  The `roofline` object describes the dominant kernel, timed with
+HIP events on the library's stream inside the same timed region;
+`cpu_baseline` times the fp64 oracle on a bounded sample of the same workload
+on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps 50] [--warmup 3] [--workload gmm10m]
 """
@@ -95,17 +99,82 @@ def cpu_baseline(workload, n_sample: int, iters: int) -> dict:
                       f"seeded {workload} mixture (d={wl.d}, K=r={wl.K}); {dt:.1f} s"}
 
 
+def kernel_flops(kind: str, n: int, d: int, r: int) -> float:
+    """fp32-equivalent matrix flops of one launch (pass_bf holds both products)."""
+    return {"pass_a": 2.0, "pass_b": 2.0, "pass_bf": 4.0}.get(kind, 0.0) * n * d * r
+
+
+def measure(nlr, torch, np, X_dev, Z_host, wl, steps, warm, split, two_pass, x_normalised=False):
+    """Init on (X_dev, fresh U_0 = Z_host), `warm` untimed iterations, then `steps` timed ones."""
+    n, d, r, K = wl.n, wl.d, wl.r, wl.K
+    Ut = torch.from_numpy(Z_host).to(X_dev.device)
+    alpha = 1.0 / (2.0 * (2.0 + 1.0 * (6.0 * K + 2.0)))  # half the Prop. 1 step bound at y = 0, beta = 1
+    flags = ((nlr.NLR_INIT_SPLIT_F16 if split else 0) | (nlr.NLR_INIT_TWO_PASS if two_pass else 0)
+             | (nlr.NLR_INIT_X_NORMALISED if x_normalised else 0))
+    torch.cuda.synchronize()
+    ctx = nlr.Context(X_dev, K, Ut, alpha=alpha, beta=1.0, eps_d=1e-4, eps_c=1e-4, T_min=1 << 30, flags=flags)
+    if warm > 0:
+        ctx.run(warm)
+    torch.cuda.synchronize()
+    ctx.set_profiling(True)
+    stream = ctx.stream
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    done, _ = ctx.run(steps)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t_ms = ev0.elapsed_time(ev1)
+    kt = ctx.kernel_times()
+    ctx.set_profiling(False)
+    assert done == steps, (done, steps)
+    hist = ctx.history(steps)
+    ctx.close()
+    del Ut
+    dual_frac = float(np.mean([h["dual_step"] for h in hist])) if hist else 0.0
+    value = n * steps / (t_ms / 1e3)
+    eff_gbs = algorithmic_bytes("step", n, d, r, dual_frac) * steps / (t_ms / 1e3) / 1e9
+    kinfo = {k: {"total_ms": v[0], "launches": v[1], "avg_ms": (v[0] / v[1]) if v[1] else None}
+             for k, v in kt.items() if v[1]}
+    dom = max(("pass_a", "pass_b", "pass_u", "pass_bf"), key=lambda k: kinfo.get(k, {"total_ms": 0})["total_ms"])
+    dom_ms = kinfo[dom]["avg_ms"]
+    dom_bytes = algorithmic_bytes(dom, n, d, r, dual_frac)
+    achieved = dom_bytes / (dom_ms / 1e3) / 1e9
+    dom_name = dom + ("_split16" if split else "")
+    fl = kernel_flops(dom, n, d, r)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": load_traffic(dom_name, wl.name),
+                "kernel": dom_name, "avg_launch_ms": round(dom_ms, 4),
+                "algorithmic_bytes_per_launch": dom_bytes}
+    if split:  # three fp16 products per fp32 product, against the dense fp16 peak
+        roofline["mfma_tflops"] = round(3.0 * fl / (dom_ms / 1e3) / 1e12, 2)
+        roofline["mfma_frac"] = round(roofline["mfma_tflops"] / FP16_MFMA_PEAK_TFLOPS, 4)
+    else:
+        roofline["mfma_tflops"] = round(fl / (dom_ms / 1e3) / 1e12, 2)
+        roofline["mfma_frac"] = round(roofline["mfma_tflops"] / FP32_MFMA_PEAK_TFLOPS, 4)
+    label = ("split-fp16" if split else "fp32") + (" two-pass" if two_pass else " single-pass")
+    eprint(f"[bench] {label}: {steps} steps in {t_ms:.2f} ms -> {t_ms / steps:.3f} ms/step, {value:.3e} pts*it/s, "
+           f"effective {eff_gbs:.0f} GB/s ({eff_gbs / HBM_PEAK_GBS:.1%} of HBM)")
+    for k, v in kinfo.items():
+        eprint(f"[bench]   {k:13s} {v['avg_ms'] * 1e3:9.1f} us x {v['launches']}")
+    return {"value": value, "t_ms": t_ms, "eff_gbs": eff_gbs, "dual_frac": dual_frac, "alpha": alpha,
+            "roofline": roofline, "kernels": kinfo}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gmm10m")
-    ap.add_argument("--gemm", choices=("fp32", "split16"), default="fp32",
-                    help="fp32: both products on the fp32 matrix cores; split16: two-term fp16 splits of the "
-                         "operands on the fp16 matrix cores (NLR_INIT_SPLIT_F16)")
+    ap.add_argument("--gemm", choices=("fp32", "split16"), default="split16",
+                    help="split16 (default): two-term fp16 splits of the operands on the fp16 matrix cores "
+                         "(NLR_INIT_SPLIT_F16); fp32: both products on the fp32 matrix cores")
     ap.add_argument("--two-pass", action="store_true",
                     help="use the two-pass iteration (NLR_INIT_TWO_PASS) instead of the single-Xhat-pass form")
+    ap.add_argument("--no-alt", action="store_true",
+                    help="skip the second timed run with the other product form (reported under 'alt')")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=2_000_000)
     ap.add_argument("--cpu-iters", type=int, default=8)
@@ -141,61 +210,19 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     Xt = torch.from_numpy(X).to(dev)
-    Ut = torch.from_numpy(Z).to(dev)
-    del X, Z
-    torch.cuda.synchronize()
-    alpha = 1.0 / (2.0 * (2.0 + 1.0 * (6.0 * K + 2.0)))  # half the Prop. 1 step bound at y = 0, beta = 1
-    steps, warm = args.steps, args.warmup
+    del X
     split = args.gemm == "split16"
-    ctx = nlr.Context(Xt, K, Ut, alpha=alpha, beta=1.0, eps_d=1e-4, eps_c=1e-4, T_min=1 << 30,
-                      flags=(nlr.NLR_INIT_SPLIT_F16 if split else 0) | (nlr.NLR_INIT_TWO_PASS if args.two_pass else 0))
-    eprint("[bench] init done; warmup")
-    if warm > 0:
-        ctx.run(warm)
-    torch.cuda.synchronize()
-
-    ctx.set_profiling(True)
-    stream = ctx.stream
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record(stream)
-    done, last = ctx.run(steps)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    t_ms = ev0.elapsed_time(ev1)
-    kt = ctx.kernel_times()
-    ctx.set_profiling(False)
-    assert done == steps, (done, steps)
-    hist = ctx.history(steps)
-    dual_frac = float(np.mean([h["dual_step"] for h in hist])) if hist else 0.0
-
-    value = n * steps / (t_ms / 1e3)
-    step_bytes = algorithmic_bytes("step", n, d, r, dual_frac)
-    eff_gbs = step_bytes * steps / (t_ms / 1e3) / 1e9
-    flops = 4.0 * n * d * r
-    kinfo = {k: {"total_ms": v[0], "launches": v[1], "avg_ms": (v[0] / v[1]) if v[1] else None}
-             for k, v in kt.items() if v[1]}
-    dom = max(("pass_a", "pass_b", "pass_u", "pass_bf"), key=lambda k: kinfo.get(k, {"total_ms": 0})["total_ms"])
-    dom_ms = kinfo[dom]["avg_ms"]
-    dom_bytes = algorithmic_bytes(dom, n, d, r, dual_frac)
-    achieved = dom_bytes / (dom_ms / 1e3) / 1e9
-    dom_name = dom + ("_split16" if split else "")
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": load_traffic(dom_name, args.workload),
-                "kernel": dom_name, "avg_launch_ms": round(dom_ms, 4),
-                "algorithmic_bytes_per_launch": dom_bytes,
-                "mfma_tflops": round(2.0 * n * d * r / (dom_ms / 1e3) / 1e12, 2),
-                "mfma_frac": round(2.0 * n * d * r / (dom_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4)}
-    if split:
-        # three fp16 products per fp32 product, against the dense fp16 peak
-        roofline["mfma_tflops"] = round(3 * 2.0 * n * d * r / (dom_ms / 1e3) / 1e12, 2)
-        roofline["mfma_frac"] = round(roofline["mfma_tflops"] / FP16_MFMA_PEAK_TFLOPS, 4)
-    eprint(f"[bench] {steps} steps in {t_ms:.2f} ms -> {t_ms / steps:.3f} ms/step, {value:.3e} pts*it/s, "
-           f"effective {eff_gbs:.0f} GB/s ({eff_gbs / HBM_PEAK_GBS:.1%} of HBM), "
-           f"{flops * steps / (t_ms / 1e3) / 1e12:.1f} TFLOP/s")
-    for k, v in kinfo.items():
-        eprint(f"[bench]   {k:13s} {v['avg_ms'] * 1e3:9.1f} us x {v['launches']}")
+    main_run = measure(nlr, torch, np, Xt, Z, wl, args.steps, args.warmup, split, args.two_pass)
+    alt = None
+    if not args.no_alt:
+        # the other product form on the same (already normalised) data and the same start
+        a = measure(nlr, torch, np, Xt, Z, wl, args.steps, args.warmup, not split, args.two_pass, x_normalised=True)
+        alt = {"products": "fp32" if split else "fp16 two-term split, fp32 accumulate",
+               "dtype": "f32" if split else "f32 (fp16x3 products)",
+               "value": a["value"], "ms_per_step": a["t_ms"] / args.steps,
+               "achieved_hbm_gbs": round(a["eff_gbs"], 1), "hbm_frac": round(a["eff_gbs"] / HBM_PEAK_GBS, 4),
+               "roofline": a["roofline"]}
+    del Z
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -203,30 +230,32 @@ def main():
         cpu = cpu_baseline(args.workload, min(args.cpu_sample, n), args.cpu_iters)
         eprint(f"[bench] cpu baseline {cpu['value']:.3e} pts*it/s on {cpu['cores']} threads")
 
+    m = main_run
     out = {
         "metric": METRIC,
-        "value": value,
+        "value": m["value"],
         "unit": "points*iters/s",
         "n_gpus": 1,
-        "steps": steps,
-        "warmup": warm,
-        "ms_per_step": t_ms / steps,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": m["t_ms"] / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16x3" if split else "f32",
+        "dtype": "f32 (fp16x3 products)" if split else "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "n": n, "d": d, "K": K, "r": r, "alpha": alpha, "beta": 1.0,
+        "config": {"workload": args.workload, "n": n, "d": d, "K": K, "r": r, "alpha": m["alpha"], "beta": 1.0,
+                   "iteration": "two-pass" if args.two_pass else "single-Xhat-pass",
                    "products": "fp16 two-term split, fp32 accumulate" if split else "fp32",
-                   "eps_d": 1e-4, "eps_c": 1e-4, "dual_step_fraction": dual_frac},
-        "achieved_hbm_gbs": round(eff_gbs, 1),
-        "hbm_frac": round(eff_gbs / HBM_PEAK_GBS, 4),
-        "roofline": roofline,
+                   "eps_d": 1e-4, "eps_c": 1e-4, "dual_step_fraction": m["dual_frac"]},
+        "achieved_hbm_gbs": round(m["eff_gbs"], 1),
+        "hbm_frac": round(m["eff_gbs"] / HBM_PEAK_GBS, 4),
+        "roofline": m["roofline"],
         "cpu_baseline": cpu,
-        "kernels": kinfo,
+        "alt": alt,
+        "kernels": m["kernels"],
     }
     print(json.dumps(out), flush=True)
-    ctx.close()
 
 
 if __name__ == "__main__":
