@@ -211,10 +211,15 @@ def main():
         del src, dst
     Xt = torch.from_numpy(X).to(dev)
     del X
-    split = args.gemm == "split16"
+    # the split products exist for d <= 128, r <= 64, d % 4 == 0 (and r % 4 == 0 in the two-pass
+    # form); other shapes run fp32 products
+    split_ok = d <= 128 and r <= 64 and d % 4 == 0 and (r % 4 == 0 or not args.two_pass)
+    split = args.gemm == "split16" and split_ok
+    if args.gemm == "split16" and not split:
+        eprint(f"[bench] split-fp16 products are not available for d={d}, r={r}: fp32 products")
     main_run = measure(nlr, torch, np, Xt, Z, wl, args.steps, args.warmup, split, args.two_pass)
     alt = None
-    if not args.no_alt:
+    if not args.no_alt and split_ok:
         # the other product form on the same (already normalised) data and the same start
         a = measure(nlr, torch, np, Xt, Z, wl, args.steps, args.warmup, not split, args.two_pass, x_normalised=True)
         alt = {"products": "fp32" if split else "fp16 two-term split, fp32 accumulate",

@@ -103,13 +103,14 @@ enum {
    * range, and v w ~ s_v s_w (hi_v hi_w + hi_v lo_w + lo_v hi_w) accumulated in
    * fp32.  The representation error is about 2^-22 relative per operand, below
    * the TF32 products of the paper's CUTLASS kernel (Appendix C), at about a fifth of the fp32 matrix
-   * work.  Supported for d <= 128 and r <= 64 (with d % 4 == 0, r % 4 == 0 and
-   * 16-byte aligned X and U); other shapes return NLR_EUNSUPPORTED. */
+   * work.  Supported for d <= 128, r <= 64, d % 4 == 0 and 16-byte aligned X and
+   * U (and r % 4 == 0 with NLR_INIT_TWO_PASS); other shapes return
+   * NLR_EUNSUPPORTED. */
   NLR_INIT_SPLIT_F16 = 8,
   /* Use the two-pass iteration (pass A: Theta = Xhat^T U with the row work; pass
    * B: Xhat Theta with the fused epilogue) even where the single-Xhat-pass form
-   * is available.  By default, for d <= 128 and r <= 64 (d % 4 == 0, r % 4 == 0,
-   * 16-byte aligned X and U), each iteration reads Xhat once: pass B also forms
+   * is available.  By default, for d <= 128 and r <= 64 (d % 4 == 0, 16-byte
+   * aligned X and U), each iteration reads Xhat once: pass B also forms
    * the partials of Xhat^T W_{t+1}, and Theta_{t+1} = c_{t+1} Xhat^T W_{t+1}
    * (U_{t+1} = c_{t+1} W_{t+1}, Algorithm 1), while a row pass over U and ytilde
    * does the rest of pass A's work.  Both forms compute the same iteration; they

@@ -66,7 +66,20 @@ __device__ __forceinline__ f16x8 tile_operand_rows(const _Float16* T, int ts, in
   return o;
 }
 
-template <int NB, int NCH, bool SPLIT>
+// Bytes of dynamic LDS the fused pass B needs.
+constexpr int fused_lds_bytes(int NB, int NCH, bool split, bool uflat) {
+  const int d32 = 32 * NCH, r32 = 32 * NB;
+  const int xs = split ? d32 + 8 : d32 + 4, ws = split ? r32 + 8 : r32 + 4, esz = split ? 2 : 4;
+  const int tile = (split ? 2 : 1) * 32 * (xs + ws) * esz + (uflat ? (32 * r32 + 4) * 4 : 0);
+  const int head = d32 * r32 * 4 + 2 * r32 * 4 + (4 * r32 + 8) * 8 + 16;
+  const int tiles = 4 * tile > 2 * d32 * r32 * 4 ? 4 * tile : 2 * d32 * r32 * 4;
+  return head + tiles;
+}
+
+// UFLAT (rows of U not 16-byte aligned, r % 4 != 0): each wave moves its 32-row
+// slab of U (32 r contiguous floats, 16-byte aligned because the slab starts at a
+// multiple of 32 rows) with whole-slab vector loads and stores through LDS.
+template <int NB, int NCH, bool SPLIT, bool UFLAT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_pass_bf(
     Geometry g, Bufs B, StepArgs S) {
   if (halted(B.ctl)) return;
@@ -75,7 +88,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   constexpr int XS = SPLIT ? D32 + 8 : D32 + 4;    // tile row strides (halves / floats)
   constexpr int WS = SPLIT ? R32 + 8 : R32 + 4;
   constexpr int ESZ = SPLIT ? 2 : 4;
-  constexpr int TILE_BYTES = (SPLIT ? 2 : 1) * 32 * (XS + WS) * ESZ;  // per wave
+  constexpr int SLAB_BYTES = (SPLIT ? 2 : 1) * 32 * (XS + WS) * ESZ;
+  constexpr int TILE_BYTES = SLAB_BYTES + (UFLAT ? (32 * R32 + 4) * 4 : 0);  // per wave
+  constexpr int NCU = UFLAT ? R32 / 8 : 1;  // 16-byte chunks of a U slab per lane (8 r <= 64 NCU)
   extern __shared__ __align__(16) unsigned char smem_raw[];
   unsigned char* th_raw = smem_raw;                                    // D32 * R32 * 4 bytes
   float* ps = reinterpret_cast<float*>(smem_raw + D32 * R32 * 4);     // R32
@@ -106,6 +121,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   _Float16* wl_t = wh_t + 32 * WS;
   float* xs_t = reinterpret_cast<float*>(mytile);
   float* ws_t = xs_t + 32 * XS;
+  float* uslab = reinterpret_cast<float*>(mytile + SLAB_BYTES);  // UFLAT: 32 r floats + 4 dump
+  float* udump = uslab + 32 * R32;
 
   // ---- Theta_t operand ----
   float two_alpha_s = two_alpha;
@@ -188,18 +205,49 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     }
   };
   f32x4 unext[NB][4];
+  f32x4 ufl[NCU];
   float ynext;
+  // valid floats of the U slab of tile st (32 r for every slab but the last)
+  auto slab_valid = [&](int64_t st) -> int {
+    const int64_t row0 = st * kTPB + wave * 32;
+    if (st >= T || row0 >= n) return 0;
+    const int64_t rows = n - row0 < 32 ? n - row0 : 32;
+    return (int)rows * r;
+  };
   auto load_u = [&](int64_t st) {
     const int64_t pt = st * kTPB + wave * 32 + li;
     const bool ok = (st < T) && (pt < n);
-    const float* ur = B.U + (ok ? pt : 0) * (int64_t)r;
+    if constexpr (UFLAT) {
+      const int nval = slab_valid(st);
+      const float* base = B.U + (nval > 0 ? (st * kTPB + wave * 32) * (int64_t)r : 0);
+      if (nval == 32 * r) {
 #pragma unroll
-    for (int m = 0; m < NB; ++m)
+        for (int i = 0; i < NCU; ++i) {
+          const int j = lane + 64 * i;
+          ufl[i] = *reinterpret_cast<const f32x4*>(base + 4 * (j < 8 * r ? j : 0));
+        }
+      } else {
 #pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        const int c = 32 * m + 8 * qd + 4 * h;
-        unext[m][qd] = *reinterpret_cast<const f32x4*>(ur + (c < r ? c : 0));
+        for (int i = 0; i < NCU; ++i) {
+          const int j = lane + 64 * i;
+          f32x4 t = {0.f, 0.f, 0.f, 0.f};
+          if (4 * j + 0 < nval) t.x = base[4 * j + 0];
+          if (4 * j + 1 < nval) t.y = base[4 * j + 1];
+          if (4 * j + 2 < nval) t.z = base[4 * j + 2];
+          if (4 * j + 3 < nval) t.w = base[4 * j + 3];
+          ufl[i] = t;
+        }
       }
+    } else {
+      const float* ur = B.U + (ok ? pt : 0) * (int64_t)r;
+#pragma unroll
+      for (int m = 0; m < NB; ++m)
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const int c = 32 * m + 8 * qd + 4 * h;
+          unext[m][qd] = *reinterpret_cast<const f32x4*>(ur + (c < r ? c : 0));
+        }
+    }
     ynext = B.y[ok ? pt : 0];
   };
   const int64_t st0 = blockIdx.x;
@@ -218,10 +266,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     const bool vpt = pt < n;
     float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
     f32x4 uraw[NB][4];
+    f32x4 ucur[NCU];
+    if constexpr (UFLAT) {
 #pragma unroll
-    for (int m = 0; m < NB; ++m)
+      for (int i = 0; i < NCU; ++i) ucur[i] = ufl[i];
+    } else {
 #pragma unroll
-      for (int qd = 0; qd < 4; ++qd) uraw[m][qd] = unext[m][qd];
+      for (int m = 0; m < NB; ++m)
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) uraw[m][qd] = unext[m][qd];
+    }
     const float yraw = ynext;
     __builtin_amdgcn_sched_barrier(0);
     load_u(st + step);  // the next tile's factor rows: a whole tile of lead time
@@ -288,16 +342,32 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     const float* psl = ps + lds_off;
     const float* ssl = ss + lds_off;
     float u[NB][16];
+    if constexpr (UFLAT) {
+      // the slab into LDS as loaded, then each lane picks its row's columns
 #pragma unroll
-    for (int m = 0; m < NB; ++m)
+      for (int i = 0; i < NCU; ++i) *reinterpret_cast<f32x4*>(uslab + 4 * (lane + 64 * i)) = ucur[i];
+      __builtin_amdgcn_wave_barrier();
 #pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        const bool ok = vpt && (32 * m + 8 * qd + 4 * h) < r;
-        u[m][4 * qd + 0] = ok ? uraw[m][qd].x * cf : 0.f;
-        u[m][4 * qd + 1] = ok ? uraw[m][qd].y * cf : 0.f;
-        u[m][4 * qd + 2] = ok ? uraw[m][qd].z * cf : 0.f;
-        u[m][4 * qd + 3] = ok ? uraw[m][qd].w * cf : 0.f;
-      }
+      for (int m = 0; m < NB; ++m)
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int c = 32 * m + 8 * (k >> 2) + 4 * h + (k & 3);
+          const float v = uslab[li * r + (c < r ? c : 0)];
+          u[m][k] = (vpt && c < r) ? v * cf : 0.f;
+        }
+      __builtin_amdgcn_wave_barrier();
+    } else {
+#pragma unroll
+      for (int m = 0; m < NB; ++m)
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const bool ok = vpt && (32 * m + 8 * qd + 4 * h) < r;
+          u[m][4 * qd + 0] = ok ? uraw[m][qd].x * cf : 0.f;
+          u[m][4 * qd + 1] = ok ? uraw[m][qd].y * cf : 0.f;
+          u[m][4 * qd + 2] = ok ? uraw[m][qd].z * cf : 0.f;
+          u[m][4 * qd + 3] = ok ? uraw[m][qd].w * cf : 0.f;
+        }
+    }
     float dotf = 0.f;
 #pragma unroll
     for (int m = 0; m < NB; ++m)
@@ -335,10 +405,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
           sb = fma(ud, ud, sb);
           sh = fma(wd, ud, sh);
         }
-        // unconditional store (invalid lanes write the dump slot): no branch around it
-        float* dst = (vpt && c < r) ? (urow + c) : B.dump;
         f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
-        *reinterpret_cast<f32x4*>(dst) = o;
+        if constexpr (UFLAT) {
+          // W over the slab's U (every lane has read its u values above); columns >= r to a dump word
+#pragma unroll
+          for (int e = 0; e < 4; ++e) *((c + e < r) ? (uslab + li * r + c + e) : udump) = wv[4 * qd + e];
+        } else {
+          // unconditional store (invalid lanes write the dump slot): no branch around it
+          float* dst = (vpt && c < r) ? (urow + c) : B.dump;
+          *reinterpret_cast<f32x4*>(dst) = o;
+        }
         // the slab of W for phase 2: row li, columns c .. c+3
         if constexpr (SPLIT) {
           f16x4 hi, lo;
@@ -357,6 +433,30 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
       }
       reduce_scatter<16, 16>(wv, li);
       colacc[m] += (double)wv[0];
+    }
+    if constexpr (UFLAT) {
+      // the slab of W back to HBM as whole 16-byte chunks
+      __builtin_amdgcn_wave_barrier();
+      const int nval = slab_valid(st);
+      float* base = B.U + (nval > 0 ? (st * kTPB + wave * 32) * (int64_t)r : 0);
+      if (nval == 32 * r) {
+#pragma unroll
+        for (int i = 0; i < NCU; ++i) {
+          const int j = lane + 64 * i;
+          const f32x4 v = *reinterpret_cast<const f32x4*>(uslab + 4 * j);
+          float* dst = (j < 8 * r) ? (base + 4 * j) : B.dump;
+          *reinterpret_cast<f32x4*>(dst) = v;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NCU; ++i) {
+          const int j = lane + 64 * i;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (4 * j + e < nval) base[4 * j + e] = uslab[4 * j + e];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
     }
 
     // ---- phase 2: partial += Xhat_slab^T W_slab (this wave's 32 rows) ----
@@ -457,43 +557,39 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   for (int e = tid; e < D32 * R32; e += kThreads) part[e] = comb[e] + comb[D32 * R32 + e];
 }
 
-template <int NB, int NCH, bool SPLIT>
+template <int NB, int NCH, bool SPLIT, bool UFLAT>
 static hipError_t pass_bf_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  constexpr int D32 = 32 * NCH, R32 = 32 * NB;
-  constexpr int XS = SPLIT ? D32 + 8 : D32 + 4;
-  constexpr int WS = SPLIT ? R32 + 8 : R32 + 4;
-  constexpr int ESZ = SPLIT ? 2 : 4;
-  constexpr int TILE_BYTES = (SPLIT ? 2 : 1) * 32 * (XS + WS) * ESZ;
-  const int head = D32 * R32 * 4 + 2 * R32 * 4 + (4 * R32 + 8) * 8 + 16;
-  const int tiles = 4 * TILE_BYTES > 2 * D32 * R32 * 4 ? 4 * TILE_BYTES : 2 * D32 * R32 * 4;
-  const int lds = head + tiles;
-  if (lds > (160 << 10)) return hipErrorInvalidValue;
+  constexpr int lds = fused_lds_bytes(NB, NCH, SPLIT, UFLAT);
+  if (lds > kMaxFusedLds) return hipErrorInvalidValue;
   if (lds > (64 << 10)) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_bf<NB, NCH, SPLIT>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_bf<NB, NCH, SPLIT, UFLAT>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((k_pass_bf<NB, NCH, SPLIT>), dim3(g.GB), dim3(kThreads), lds, st, g, b, a);
+  hipLaunchKernelGGL((k_pass_bf<NB, NCH, SPLIT, UFLAT>), dim3(g.GB), dim3(kThreads), lds, st, g, b, a);
   return hipGetLastError();
 }
 
-template <bool SPLIT>
+template <bool SPLIT, bool UFLAT>
 static hipError_t pass_bf_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   switch (g.NB * 10 + g.nch) {
-    case 11: return pass_bf_launch<1, 1, SPLIT>(g, b, a, st);
-    case 12: return pass_bf_launch<1, 2, SPLIT>(g, b, a, st);
-    case 13: return pass_bf_launch<1, 3, SPLIT>(g, b, a, st);
-    case 14: return pass_bf_launch<1, 4, SPLIT>(g, b, a, st);
-    case 21: return pass_bf_launch<2, 1, SPLIT>(g, b, a, st);
-    case 22: return pass_bf_launch<2, 2, SPLIT>(g, b, a, st);
-    case 23: return pass_bf_launch<2, 3, SPLIT>(g, b, a, st);
-    case 24: return pass_bf_launch<2, 4, SPLIT>(g, b, a, st);
+    case 11: return pass_bf_launch<1, 1, SPLIT, UFLAT>(g, b, a, st);
+    case 12: return pass_bf_launch<1, 2, SPLIT, UFLAT>(g, b, a, st);
+    case 13: return pass_bf_launch<1, 3, SPLIT, UFLAT>(g, b, a, st);
+    case 14: return pass_bf_launch<1, 4, SPLIT, UFLAT>(g, b, a, st);
+    case 21: return pass_bf_launch<2, 1, SPLIT, UFLAT>(g, b, a, st);
+    case 22: return pass_bf_launch<2, 2, SPLIT, UFLAT>(g, b, a, st);
+    case 23: return pass_bf_launch<2, 3, SPLIT, UFLAT>(g, b, a, st);
+    case 24: return pass_bf_launch<2, 4, SPLIT, UFLAT>(g, b, a, st);
     default: return hipErrorInvalidValue;
   }
 }
 
+int fused_lds_need(int NB, int nch, bool split, bool uflat) { return fused_lds_bytes(NB, nch, split, uflat); }
+
 hipError_t launch_pass_bf(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  return g.split_b ? pass_bf_dispatch<true>(g, b, a, st) : pass_bf_dispatch<false>(g, b, a, st);
+  if (g.uflat) return g.split_b ? pass_bf_dispatch<true, true>(g, b, a, st) : pass_bf_dispatch<false, true>(g, b, a, st);
+  return g.split_b ? pass_bf_dispatch<true, false>(g, b, a, st) : pass_bf_dispatch<false, false>(g, b, a, st);
 }
 
 }  // namespace nlr

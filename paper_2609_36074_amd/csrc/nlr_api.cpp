@@ -21,9 +21,6 @@ static int32_t next_pow2(int32_t x) {
 }
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-bool split_supported(int32_t d, int32_t r, bool aligned16) {
-  return aligned16 && d <= 128 && r <= 64 && d % 4 == 0 && r % 4 == 0;
-}
 
 Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split, bool fused) {
   Geometry g;
@@ -111,17 +108,24 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
     g.GG = (int32_t)gg;
     g.gblk = g.d32 / 32;
   }
-  g.split_b = (split && g.b_res && split_supported(d, r, aligned16)) ? 1 : 0;
-  g.split_a = 0;
   // single-Xhat-pass iteration: the row pass and the fused pass B need the
-  // register-resident shapes; one persistent workgroup per compute unit
-  g.fused = (fused && split_supported(d, r, aligned16) && g.a_rows && g.b_res) ? 1 : 0;
+  // register-resident shapes (d <= 128, r <= 64, 16-byte aligned X and U rows of
+  // X; U rows of any length move as whole slabs) and its LDS; one persistent
+  // workgroup per compute unit
+  const bool shape_f = aligned16 && d <= 128 && r <= 64 && d % 4 == 0 && g.a_rows;
+  const bool uflat = r % 4 != 0;
+  g.fused = (fused && shape_f && fused_lds_need(g.NB, g.nch, split, uflat) <= kMaxFusedLds) ? 1 : 0;
+  g.uflat = (g.fused && uflat) ? 1 : 0;
   g.SAF = g.SA;
   if (g.fused) {
     g.GB = (int32_t)(g.tilesB < 256 ? g.tilesB : 256);
     g.SB = (g.GB + 31) / 32;
     g.SAF = (g.GB + 31) / 32;
-    g.split_a = g.split_b;  // both products live in the fused pass B
+    g.split_a = g.split_b = split ? 1 : 0;  // both products live in the fused pass B
+  } else {
+    // two-pass form: split products in the resident pass B only
+    g.split_a = 0;
+    g.split_b = (split && g.b_res && aligned16 && d <= 128 && r <= 64 && d % 4 == 0 && r % 4 == 0) ? 1 : 0;
   }
   g.vec_x = (d % 4 == 0 && aligned16) ? 1 : 0;
   g.vec_u = (r % 4 == 0 && aligned16) ? 1 : 0;
@@ -386,9 +390,9 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   if (r > kMaxR) return NLR_EUNSUPPORTED;
   const bool aligned16 = (((uintptr_t)X & 15) == 0) && (((uintptr_t)U & 15) == 0);
   const bool split = (flags & NLR_INIT_SPLIT_F16) != 0;
-  if (split && !split_supported(d, r, aligned16)) return NLR_EUNSUPPORTED;
   const bool fused = (flags & NLR_INIT_TWO_PASS) == 0;
   const Geometry g0 = make_geometry(n, d, r, K, aligned16, split, fused);
+  if (split && !g0.split_b) return NLR_EUNSUPPORTED;
   const size_t need = carve_workspace(g0, nullptr, nullptr);
   if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
 

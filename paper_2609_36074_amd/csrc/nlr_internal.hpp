@@ -82,6 +82,7 @@ struct Geometry {
   int32_t b_res;        // 1: resident-tile pass B (k_pass_b_res)
   int32_t split_a, split_b;  // 1: split-fp16 products in pass A / pass B
   int32_t fused;        // 1: single-Xhat-pass iteration (row pass + fused pass B)
+  int32_t uflat;        // 1: the fused pass B moves U as whole 32-row slabs (r % 4 != 0)
   int32_t SAF;          // segments of the fused pass B Theta partials (GB rows)
   int32_t ldsB_bytes;
   // init
@@ -124,8 +125,9 @@ struct Bufs {
 // split: split-fp16 products requested (NLR_INIT_SPLIT_F16)
 Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split = false,
                        bool fused = false);
-// the split-fp16 products support this shape and alignment
-bool split_supported(int32_t d, int32_t r, bool aligned16);
+// dynamic LDS of the fused pass B for (NB, nch, split, U moved as whole slabs)
+int fused_lds_need(int NB, int nch, bool split, bool uflat);
+constexpr int kMaxFusedLds = 160 << 10;
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
 
 // ---- kernel launchers (each returns the launch error) ----

@@ -90,7 +90,9 @@ def test_init_argument_errors(lib):
     assert _init(lib, flags=S, d=13)[0] == nlr.NLR_EUNSUPPORTED                      # d % 4 != 0
     assert _init(lib, flags=S, d=132)[0] == nlr.NLR_EUNSUPPORTED                     # d > 128
     assert _init(lib, flags=S, r=68, K=4)[0] == nlr.NLR_EUNSUPPORTED                 # r > 64
-    assert _init(lib, flags=S, r=10, K=4)[0] == nlr.NLR_EUNSUPPORTED                 # r % 4 != 0
+    assert _init(lib, flags=S | nlr.NLR_INIT_TWO_PASS, r=10, K=4)[0] == nlr.NLR_EUNSUPPORTED  # r % 4 != 0
+    st, _ = _init(lib, flags=S, r=10, K=4, ws_bytes=1024)                            # single pass: fine
+    assert st == nlr.NLR_EWORKSPACE
     assert _init(lib, flags=S, X=FAKE + 4)[0] == nlr.NLR_EUNSUPPORTED                # X not 16-byte aligned
     assert _init(lib, flags=S, U=FAKE + 8)[0] == nlr.NLR_EUNSUPPORTED                # U not 16-byte aligned
     st, ctx = _init(lib, flags=S, ws_bytes=1024)                                      # supported: reaches the

@@ -58,7 +58,8 @@ def test_split_dual_steps():
 
 
 @pytest.mark.parametrize("n,d,r,K", [(777, 64, 16, 16), (4099, 128, 64, 64), (1000, 36, 12, 3),
-                                     (2001, 128, 60, 50), (33, 4, 4, 4), (5000, 100, 36, 9)])
+                                     (2001, 128, 60, 50), (33, 4, 4, 4), (5000, 100, 36, 9),
+                                     (1037, 16, 10, 7), (999, 32, 10, 10), (4001, 64, 30, 12), (70, 8, 1, 1)])
 def test_split_ragged(n, d, r, K):
     log(f"split: ragged n={n} d={d} r={r} K={K}")
     X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 7 + d)
