@@ -19,7 +19,9 @@ read against the paper:
 * the loop of Algorithm 1 (Section 4.3): primal step, normalisation
   breakdown test, movement, residual, gated dual ascent
   y <- y + (beta/sqrt(n)) q, stopping rule;
-* Prop. 1 (eq. L) for the fixed-dual smoothness bound.
+* Prop. 1 (eq. L) for the fixed-dual smoothness bound;
+* the data-informed starting factor of Appendix D (range finder on the Gram
+  matrix, Cholesky QR in feature space, projection onto Omega).
 
 Unlike the GPU path it forms the full n x r gradient, takes the exact fp64
 normalising multiplier c = sqrt(K / ||W||_F^2) and measures the movement
@@ -119,6 +121,31 @@ def project_omega(V: np.ndarray, K: float) -> np.ndarray:
     if not nrm > 0.0:
         raise FloatingPointError("projection of a matrix with no positive entry")
     return np.sqrt(K) * Vp / nrm
+
+
+# ----------------------------------------------------------------------------
+# Appendix D "Initialization": data-informed starting factor
+# ----------------------------------------------------------------------------
+def data_informed_start(Xhat: np.ndarray, Z: np.ndarray, K: float):
+    """(U0, Q) with V = Xhat Xhat^T Z, V = Q R, U0 = Pi_Omega(Q) (Appendix D).
+
+    The range finder is applied to the Gram matrix of the normalised data (the
+    matrix C is the one reused from the normalisation).  The QR factorisation
+    is the Cholesky QR of the appendix, taken in feature space:
+        M = Xhat^T Z,  C = Xhat^T Xhat,  V^T V = M^T C M = R^T R  (R upper
+        triangular with positive diagonal),  Q = Xhat (M R^{-1}).
+    Needs V of full column rank (r <= rank Xhat); raises LinAlgError otherwise.
+    """
+    Xhat = np.asarray(Xhat, dtype=np.float64)
+    Z = np.asarray(Z, dtype=np.float64)
+    M = Xhat.T @ Z
+    C = Xhat.T @ Xhat
+    G = M.T @ C @ M
+    L = np.linalg.cholesky(G)           # G = L L^T, R = L^T
+    # M R^{-1} = M L^{-T}: solve L Y = M^T, then (M R^{-1}) = Y^T
+    MRinv = np.linalg.solve(L, M.T).T
+    Q = Xhat @ MRinv
+    return project_omega(Q, K), Q
 
 
 def lipschitz_bound(y: np.ndarray, beta: float, K: float) -> float:

@@ -390,4 +390,40 @@ def pin_hand_kmeans():
     assert len(args) == 1 and kmeans.same_partition(args[0], np.array([0, 0, 1, 1]))
 
 
+def _data_start_instance(seed=3, n=400, d=12, K=4):
+    X, _, _ = gaussian_mixture(n, d, K, 25.0, seed=seed)
+    Xh, _, _ = nlr.centre_and_normalise(X)
+    Z = standard_normal_factor(n, K, seed=seed + 1).astype(np.float64)
+    return Xh, Z, K
+
+
+def pin_data_start_is_qr_of_range_sample():
+    """Appendix D: Q is the orthonormal factor of V = Xhat Xhat^T Z (numpy QR, signs made positive)."""
+    Xh, Z, K = _data_start_instance()
+    U0, Q = nlr.data_informed_start(Xh, Z, K)
+    V = Xh @ (Xh.T @ Z)
+    q, r = np.linalg.qr(V)
+    q = q * np.sign(np.diag(r))[None, :]
+    assert np.abs(Q - q).max() < 1e-10
+    assert np.abs(Q.T @ Q - np.eye(K)).max() < 1e-10
+    assert U0.min() >= 0.0 and abs(np.sum(U0 * U0) - K) < 1e-10
+
+
+def pin_data_start_column_scaling_invariance():
+    """The orthonormal factor of V D (D positive diagonal) is that of V: Q(Z D) = Q(Z)."""
+    Xh, Z, K = _data_start_instance(seed=5)
+    D = np.array([0.5, 3.0, 1.7, 11.0])[:K]
+    _, Q1 = nlr.data_informed_start(Xh, Z, K)
+    _, Q2 = nlr.data_informed_start(Xh, Z * D[None, :], K)
+    assert np.abs(Q1 - Q2).max() < 1e-9
+
+
+def pin_data_start_lowers_objective():
+    """Appendix D reports a lower initial augmented Lagrangian than the random start Pi(Z)."""
+    Xh, Z, K = _data_start_instance(seed=7)
+    U0, _ = nlr.data_informed_start(Xh, Z, K)
+    y = np.zeros(Xh.shape[0])
+    assert nlr.objective(Xh, U0, y, 1.0) < nlr.objective(Xh, nlr.project_omega(Z, K), y, 1.0)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

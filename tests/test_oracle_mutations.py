@@ -36,6 +36,11 @@ MUTATIONS = [
     ("Lipschitz bound without the beta term", "2.0 * np.linalg.norm(y) + beta * (6.0 * K + 2.0))", "2.0 * np.linalg.norm(y))"),
     ("argmax over columns", "np.argmax(np.asarray(U), axis=1)", "np.argmax(np.asarray(U), axis=0)"),
     ("objective sign", "return float(-np.sum(Theta * Theta) + y @ hU", "return float(np.sum(Theta * Theta) + y @ hU"),
+    ("range finder without the Gram matrix", "C = Xhat.T @ Xhat\n", "C = np.eye(Xhat.shape[1])\n"),
+    ("range finder without R^-1", "Q = Xhat @ MRinv", "Q = Xhat @ M"),
+    ("range finder with the transposed Cholesky factor", "MRinv = np.linalg.solve(L, M.T).T",
+     "MRinv = np.linalg.solve(L.T, M.T).T"),
+    ("range finder on Z instead of Xhat^T Z", "M = Xhat.T @ Z\n", "M = Z[: Xhat.shape[1]]\n"),
 ]
 
 
