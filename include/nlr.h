@@ -115,7 +115,15 @@ enum {
    * (U_{t+1} = c_{t+1} W_{t+1}, Algorithm 1), while a row pass over U and ytilde
    * does the rest of pass A's work.  Both forms compute the same iteration; they
    * differ by floating-point rounding only. */
-  NLR_INIT_TWO_PASS = 16
+  NLR_INIT_TWO_PASS = 16,
+  /* Data-informed start (Appendix D, "Initialization"): U holds Z on input (e.g.
+   * i.i.d. N(0,1) entries) and is replaced by U_0 = Pi_Omega(Q), where Q is the
+   * orthonormal factor of V = Xhat Xhat^T Z computed by Cholesky QR in feature
+   * space: M = Xhat^T Z, C = Xhat^T Xhat, M^T C M = R^T R, Q = Xhat (M R^{-1})
+   * (FP64 for the d x r and r x r algebra).  Needs V of full column rank
+   * (r <= rank Xhat); otherwise nlr_init returns NLR_EDEGENERATE.  Not combinable
+   * with NLR_INIT_U_IN_OMEGA. */
+  NLR_INIT_DATA_START = 32
 };
 
 /* Bytes of device workspace nlr_init needs for an (n, d, r) problem.  Depends

@@ -1152,6 +1152,13 @@ hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bo
   }
 }
 
+hipError_t launch_seg_theta(const Geometry& g, const Bufs& b, int64_t rows, int nseg, hipStream_t st) {
+  const int C = g.d32 * g.r32;
+  hipLaunchKernelGGL((k_seg_sum<float>), dim3((C + 63) / 64, nseg), dim3(kThreads), 0, st,
+                     (const float*)b.theta_part, rows, C, b.seg_theta, nseg, (const DevCtl*)b.ctl, 1);
+  return hipGetLastError();
+}
+
 hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, bool fused_partials, hipStream_t st) {
   const int C = g.d32 * g.r32;
   const int64_t rows = fused_partials ? g.GB : g.GA;

@@ -156,6 +156,11 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.seg_b = reinterpret_cast<double*>(take((size_t)g.SB * (4 + r32) * 8));
   b.i_xbar = reinterpret_cast<double*>(take(d * 8));
   b.dump = reinterpret_cast<float*>(take(256));
+  b.s_C = reinterpret_cast<double*>(take(d * d * 8));
+  b.s_M = reinterpret_cast<double*>(take(d * (size_t)g.r * 8));
+  b.s_CM = reinterpret_cast<double*>(take(d * (size_t)g.r * 8));
+  b.s_G = reinterpret_cast<double*>(take((size_t)g.r * g.r * 8));
+  b.s_T = reinterpret_cast<double*>(take(d * (size_t)g.r * 8));
   // union: pass-A Theta partials | init temporaries
   const size_t prow = (size_t)(g.GA > g.GB ? g.GA : g.GB);  // pass A or fused pass B partials
   const size_t u_iter = align256(prow * g.d32 * r32 * 4);
@@ -384,8 +389,9 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   if (!X || !U || !y || !params_ok(params)) return NLR_EINVAL;
   if (!shape_ok(n, d, r) || K < 1 || K > r) return NLR_EINVAL;
   if (flags & ~(uint32_t)(NLR_INIT_U_IN_OMEGA | NLR_INIT_KEEP_Y | NLR_INIT_X_NORMALISED | NLR_INIT_SPLIT_F16 |
-                          NLR_INIT_TWO_PASS))
+                          NLR_INIT_TWO_PASS | NLR_INIT_DATA_START))
     return NLR_EINVAL;
+  if ((flags & NLR_INIT_DATA_START) && (flags & NLR_INIT_U_IN_OMEGA)) return NLR_EINVAL;
   if (((uintptr_t)X & 3) || ((uintptr_t)U & 3) || ((uintptr_t)y & 3)) return NLR_EINVAL;
   if (r > kMaxR) return NLR_EUNSUPPORTED;
   const bool aligned16 = (((uintptr_t)X & 15) == 0) && (((uintptr_t)U & 15) == 0);
@@ -440,6 +446,11 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   }
   if (split)
     if (launch_xscale(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+  if (flags & NLR_INIT_DATA_START) {
+    // U holds Z: replace it by the range finder's orthonormal factor Q (Appendix D)
+    const StepArgs a0 = make_step_args(c, 0);
+    if (launch_data_start(g, b, a0, (flags & NLR_INIT_X_NORMALISED) != 0, st) != hipSuccess) return fail(NLR_EHIP);
+  }
   if (launch_project(g, b, (double)K, (flags & NLR_INIT_U_IN_OMEGA) ? 1 : 0, st) != hipSuccess)
     return fail(NLR_EHIP);
   if (!(flags & NLR_INIT_KEEP_Y))

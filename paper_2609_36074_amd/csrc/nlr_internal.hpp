@@ -119,6 +119,12 @@ struct Bufs {
   double* i_B1;        // d x d
   double* i_scal;      // 2*(kSquarings+2)
   double* i_proj;      // GI x (4 + r32)
+  // data-informed start (FP64, not aliased)
+  double* s_C;         // d x d: Xhat^T Xhat
+  double* s_M;         // d x r: Xhat^T Z
+  double* s_CM;        // d x r
+  double* s_G;         // r x r: M^T C M, then its Cholesky factor L (lower)
+  double* s_T;         // d x r: M L^{-T}
 };
 
 // aligned16: X and U start on 16-byte boundaries (enables the vector-load kernels)
@@ -154,6 +160,9 @@ hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hi
 hipError_t launch_ctl_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_xscale(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_pass_b_split(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_seg_theta(const Geometry& g, const Bufs& b, int64_t rows, int nseg, hipStream_t st);
+hipError_t launch_data_start(const Geometry& g, const Bufs& b, const StepArgs& a0, bool x_normalised,
+                             hipStream_t st);
 hipError_t launch_labels(const Geometry& g, const Bufs& b, int32_t* labels, hipStream_t st);
 
 // ---- device helpers ----

@@ -27,6 +27,7 @@ NLR_INIT_KEEP_Y = 2
 NLR_INIT_X_NORMALISED = 4
 NLR_INIT_SPLIT_F16 = 8
 NLR_INIT_TWO_PASS = 16
+NLR_INIT_DATA_START = 32
 
 NLR_MAX_KERNEL_KINDS = 16
 

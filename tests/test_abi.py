@@ -95,6 +95,7 @@ def test_init_argument_errors(lib):
     assert st == nlr.NLR_EWORKSPACE
     assert _init(lib, flags=S, X=FAKE + 4)[0] == nlr.NLR_EUNSUPPORTED                # X not 16-byte aligned
     assert _init(lib, flags=S, U=FAKE + 8)[0] == nlr.NLR_EUNSUPPORTED                # U not 16-byte aligned
+    assert _init(lib, flags=nlr.NLR_INIT_DATA_START | nlr.NLR_INIT_U_IN_OMEGA)[0] == nlr.NLR_EINVAL
     st, ctx = _init(lib, flags=S, ws_bytes=1024)                                      # supported: reaches the
     assert st == nlr.NLR_EWORKSPACE and ctx.value is None                            # workspace check
 

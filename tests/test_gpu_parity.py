@@ -301,3 +301,36 @@ def test_resume_flags():
     c.run(60)
     # p is recomputed from the stored factor on resume, so agreement is to tolerance, not bitwise
     assert rel_max_err(host(c.U), host(a.U)) < U_TOL
+
+
+# ---------------------------------------------------------------- data-informed start (Appendix D)
+DATA_START = 32  # NLR_INIT_DATA_START
+
+
+@pytest.mark.parametrize("n,d,r,K,flags", [(2000, 16, 4, 4, 0), (1037, 16, 10, 7, 0), (777, 64, 16, 16, 0),
+                                           (4099, 128, 64, 64, 0), (4099, 128, 64, 64, 8),
+                                           (1500, 768, 256, 256, 0), (3000, 32, 10, 10, 16)])
+def test_data_start(n, d, r, K, flags):
+    X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n + 3 * d)
+    Z = standard_normal_factor(n, r, seed=n + r + 1).astype(np.float64)
+    log(f"data start n={n} d={d} r={r} K={K} flags={flags}")
+    ctx = make_ctx(X, Z, K, onlr.default_step_size(K), flags=flags | DATA_START)
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    U0_ref, Q = onlr.data_informed_start(Xh, Z, K)
+    err = rel_max_err(host(ctx.U), U0_ref)
+    log(f"  U0 err {err:.2e}")
+    assert err < U_TOL / 10
+    # and the iteration from there
+    _, _, traj, obj, bad_gates, one, _, _ = trajectory(X, U0_ref, K, onlr.default_step_size(K), 1.0, 6,
+                                                       one_step_tol=True, flags=flags | 1)  # U0 in Omega
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+
+
+def test_data_start_rank_deficient_is_degenerate():
+    """r above the rank of Xhat: V = Xhat Xhat^T Z has dependent columns and Cholesky QR fails."""
+    from paper_2609_36074_amd import nlr
+    X, _, _ = gaussian_mixture(500, 8, 3, 16.0, seed=11)
+    Z = standard_normal_factor(500, 12, seed=12).astype(np.float64)
+    with pytest.raises(nlr.NlrError) as e:
+        make_ctx(X, Z, 3, 0.01, flags=DATA_START)
+    assert e.value.status == nlr.NLR_EDEGENERATE
