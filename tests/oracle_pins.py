@@ -16,7 +16,7 @@ import os
 
 import numpy as np
 
-from oracle import dense, kmeans, nlr
+from oracle import dense, kmeans, labels, nlr
 from synth import gaussian_mixture, standard_normal_factor
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
@@ -424,6 +424,83 @@ def pin_data_start_lowers_objective():
     U0, _ = nlr.data_informed_start(Xh, Z, K)
     y = np.zeros(Xh.shape[0])
     assert nlr.objective(Xh, U0, y, 1.0) < nlr.objective(Xh, nlr.project_omega(Z, K), y, 1.0)
+
+
+# ---------------------------------------------------------------- label recovery (Appendix D)
+def pin_lloyd_hand():
+    """x = 0, 1, 10, 11 from the centroids at rows 0 and 1, by hand: pass 1 labels (0, 1, 1, 1),
+    means (0, 22/3); pass 2 labels (0, 0, 1, 1), means (0.5, 10.5); pass 3 changes nothing."""
+    E = np.array([[0.0], [1.0], [10.0], [11.0]])
+    lab, passes, C = labels.lloyd(E, [0, 1])
+    assert lab.tolist() == [0, 0, 1, 1] and passes == 3
+    assert np.allclose(C[:, 0], [0.5, 10.5], rtol=0, atol=1e-15)
+
+
+def pin_lloyd_tie_lowest_index():
+    """A row equidistant from two centroids takes the lower index (x = 1 between 0 and 2)."""
+    E = np.array([[0.0], [2.0], [1.0]])
+    lab, passes, _ = labels.lloyd(E, [0, 1])
+    assert lab.tolist() == [0, 1, 0] and passes == 2
+
+
+def pin_nearest_is_euclidean():
+    """nearest() against scipy's Euclidean distances (a library route), with a point that L1 and
+    Euclidean distances assign differently: (2.1, 0) is Euclidean-nearest to (2, 2), not (0, 0)."""
+    from scipy.spatial.distance import cdist
+    C = np.array([[0.0, 0.0], [2.0, 2.0], [-3.0, 1.0]])
+    E = np.concatenate([np.array([[2.1, 0.0]]), _rng(25).standard_normal((50, 2)) * 3.0])
+    lab = labels.nearest(E, C)
+    assert lab[0] == 1
+    assert np.array_equal(lab, np.argmin(cdist(E, C), axis=1))
+
+
+def pin_lloyd_brute_force_optimum():
+    """Well-separated points: Lloyd from one seed per group ends at the exact K-means optimum."""
+    rng = _rng(21)
+    K, per = 3, 3
+    centres = np.array([[0.0, 0.0], [20.0, 0.0], [0.0, 20.0]])
+    X = np.concatenate([c + rng.standard_normal((per, 2)) for c in centres])
+    lab, passes, _ = labels.lloyd(X, [0, per, 2 * per])
+    best, args = kmeans.brute_force(X, K)
+    assert any(kmeans.same_partition(lab, a) for a in args)
+    assert abs(kmeans.within_ss(X, lab, K) - best) <= 1e-12 * best
+
+
+def pin_lloyd_fixed_point():
+    """A converged result is a fixed point: every row is nearest to the mean of its own group."""
+    rng = _rng(22)
+    E = rng.standard_normal((300, 3))
+    lab, passes, C = labels.lloyd(E, [0, 1, 2, 3], max_iter=500)
+    assert passes < 500
+    means = np.array([E[lab == k].mean(axis=0) for k in range(4)])
+    assert np.array_equal(labels.nearest(E, means), lab)
+
+
+def pin_embedding_spans_leading_singular_space():
+    """The embedding spans the leading eigenvectors of U^T U mapped by U: E E^T = P P^T with
+    P = U V_K Lambda_K^(-1/2) (eigh of the Gram matrix, a second library route)."""
+    rng = _rng(23)
+    U = np.abs(rng.standard_normal((60, 6))) * np.array([5.0, 4.0, 3.0, 1.0, 0.5, 0.1])
+    E = labels.spectral_embedding(U, 3)
+    lam, V = np.linalg.eigh(U.T @ U)
+    P = U @ V[:, ::-1][:, :3] / np.sqrt(lam[::-1][:3])[None, :]
+    assert np.abs(E @ E.T - P @ P.T).max() < 1e-10
+    assert np.abs(E.T @ E - np.eye(3)).max() < 1e-12
+
+
+def pin_spectral_labels_exact_recovery():
+    """Under exact recovery U = H (rows constant within clusters, Appendix D) the labels are the
+    partition, also with r > K extra columns carrying a small perturbation."""
+    rng = _rng(24)
+    truth = np.repeat(np.arange(4), [7, 12, 5, 9])
+    rng.shuffle(truth)
+    H = kmeans.membership(truth, 4)
+    seeds = [int(np.flatnonzero(truth == k)[0]) for k in range(4)]
+    lab, _ = labels.spectral_labels(H, 4, seeds)
+    assert kmeans.same_partition(lab, truth)
+    U = np.concatenate([H, 1e-3 * np.abs(rng.standard_normal((H.shape[0], 2)))], axis=1)
+    lab2, _ = labels.spectral_labels(U, 4, seeds)
+    assert kmeans.same_partition(lab2, truth)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

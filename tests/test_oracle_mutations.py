@@ -44,13 +44,41 @@ MUTATIONS = [
 ]
 
 
-def _load_mutant(monkeypatch, orig, new):
-    assert orig in SRC, f"mutation anchor not found: {orig!r}"
-    mod = types.ModuleType("oracle_nlr_mutant")
+LABEL_SRC = open(os.path.join(ROOT, "oracle", "labels.py")).read()
+
+# (name, original text, mutated text) planted in oracle/labels.py
+LABEL_MUTATIONS = [
+    ("trailing singular vectors", "return Uq[:, :K]", "return Uq[:, -K:]"),
+    ("farthest instead of nearest centroid", "np.argmin(D, axis=1)", "np.argmax(D, axis=1)"),
+    ("centroid as a sum", "C[k] = members.mean(axis=0)", "C[k] = members.sum(axis=0)"),
+    ("no convergence test", "if lab is not None and np.array_equal(new, lab):", "if False:"),
+    ("distance without the square", "np.sum((E - C[k][None, :]) ** 2, axis=1)", "np.sum(np.abs(E - C[k][None, :]) - 1.0, axis=1)"),
+    ("right singular vectors", "Uq, _, _ = np.linalg.svd(np.asarray(U, dtype=np.float64), full_matrices=False)\n    return Uq[:, :K]",
+     "_, _, Vt = np.linalg.svd(np.asarray(U, dtype=np.float64), full_matrices=False)\n    return Vt.T[:, :K]"),
+]
+
+
+def _load_mutant(monkeypatch, orig, new, src=SRC, name="oracle_nlr_mutant"):
+    assert orig in src, f"mutation anchor not found: {orig!r}"
+    mod = types.ModuleType(name)
     mod.__file__ = "<mutant>"
     monkeypatch.setitem(sys.modules, mod.__name__, mod)
-    exec(compile(SRC.replace(orig, new), "<mutant>", "exec"), mod.__dict__)
+    exec(compile(src.replace(orig, new), "<mutant>", "exec"), mod.__dict__)
     return mod
+
+
+@pytest.mark.parametrize("name,orig,new", LABEL_MUTATIONS, ids=[m[0] for m in LABEL_MUTATIONS])
+def test_label_mutation_is_caught(monkeypatch, name, orig, new):
+    mutant = _load_mutant(monkeypatch, orig, new, LABEL_SRC, "oracle_labels_mutant")
+    monkeypatch.setattr(oracle_pins, "labels", mutant)
+    caught = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin()
+        except Exception:
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin catches the planted mistake: {name}"
 
 
 @pytest.mark.parametrize("name,orig,new", MUTATIONS, ids=[m[0] for m in MUTATIONS])
