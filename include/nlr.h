@@ -126,6 +126,23 @@ enum {
   NLR_INIT_DATA_START = 32
 };
 
+/* Cluster labels by spectral embedding and K-means (Appendix D, "Recover
+ * cluster labels from U"): the rows of the leading K left singular vectors of
+ * the current U embed the n points (computed as U V_K Lambda_K^(-1/2) from the
+ * FP64 eigendecomposition of U^T U); Lloyd's iteration starts from the embedded
+ * rows seed_rows[0..K-1] (host array of row indices, e.g. drawn at random by the
+ * caller), assigns every row to its nearest centroid (squared Euclidean distance
+ * in FP64, lowest centroid index on ties), stops after the first pass that
+ * changes no label or after max_iter passes, and moves each centroid to the
+ * mean of its rows in between (a centroid without rows stays in place).
+ * labels: device int32[n] (written every pass).  passes_done: host, nullable.
+ * Needs 1 <= K <= r (K <= 128, else NLR_EUNSUPPORTED), seed rows in [0, n);
+ * NLR_EDEGENERATE if the K-th eigenvalue of U^T U is not above 1e-14 of the
+ * largest.  Call between iterations (it uses the context's workspace) on the
+ * context's stream; synchronises once per pass. */
+nlr_status nlr_labels_spectral(nlr_ctx* ctx, int32_t K, const int64_t* seed_rows, int32_t max_iter,
+                               int32_t* labels, int32_t* passes_done);
+
 /* Bytes of device workspace nlr_init needs for an (n, d, r) problem.  Depends
  * only on (n, d, r).  Returns 0 when the shape is invalid or unsupported. */
 size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r);

@@ -132,6 +132,47 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   return g;
 }
 
+static int32_t lab_gu(int64_t n, int32_t r) {
+  int64_t gu = (n + 4095) / 4096;
+  const int64_t cap = ((int64_t)16 << 20) / ((int64_t)r * r * 8);  // partials within 16 MiB
+  if (gu > cap) gu = cap;
+  if (gu > 64) gu = 64;
+  return (int32_t)(gu < 1 ? 1 : gu);
+}
+static int32_t lab_ga2(int64_t n) {
+  int64_t ga = (n + 63) / 64;
+  return (int32_t)(ga > 256 ? 256 : (ga < 1 ? 1 : ga));
+}
+
+size_t lab_scratch_bytes(int64_t n, int32_t r, int32_t K) {
+  const size_t rr = (size_t)r * r * 8;
+  return align256((size_t)lab_gu(n, r) * rr) + 2 * align256(rr) + align256((size_t)r * K * 8) +
+         align256((size_t)K * K * 8) + align256((size_t)lab_ga2(n) * ((size_t)K * K + K + 1) * 8) +
+         align256((size_t)K * 8) + align256(64);
+}
+
+LabScratch carve_lab_scratch(int64_t n, int32_t r, int32_t K, char* base) {
+  LabScratch L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> char* {
+    char* p = base + off;
+    off += align256(bytes);
+    return p;
+  };
+  const size_t rr = (size_t)r * r * 8;
+  L.GU = lab_gu(n, r);
+  L.GA2 = lab_ga2(n);
+  L.gpart = reinterpret_cast<double*>(take((size_t)L.GU * rr));
+  L.A = reinterpret_cast<double*>(take(rr));
+  L.V = reinterpret_cast<double*>(take(rr));
+  L.P = reinterpret_cast<double*>(take((size_t)r * K * 8));
+  L.cent = reinterpret_cast<double*>(take((size_t)K * K * 8));
+  L.apart = reinterpret_cast<double*>(take((size_t)L.GA2 * ((size_t)K * K + K + 1) * 8));
+  L.seeds = reinterpret_cast<int64_t*>(take((size_t)K * 8));
+  L.flag = reinterpret_cast<int32_t*>(take(64));
+  return L;
+}
+
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   size_t off = 0;
   auto take = [&](size_t bytes) -> char* {
@@ -170,7 +211,11 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   u_init += 3 * align256(d * d * 8);                    // C, B0, B1
   u_init += align256(2 * (kSquarings + 2) * 8);         // scal
   u_init += align256((size_t)g.GI * (4 + r32) * 8);     // projection partials
-  const size_t ubytes = u_iter > u_init ? u_iter : u_init;
+  // the spectral label recovery (between host calls) uses the same region
+  const int32_t kmax = g.r < kLabMaxK ? g.r : kLabMaxK;
+  const size_t u_lab = lab_scratch_bytes(g.n, g.r, kmax);
+  size_t ubytes = u_iter > u_init ? u_iter : u_init;
+  if (u_lab > ubytes) ubytes = u_lab;
   char* ub = take(ubytes);
   b.theta_part = reinterpret_cast<float*>(ub);
   if (base) {
@@ -539,6 +584,38 @@ nlr_status nlr_labels(nlr_ctx* c, int32_t* labels) {
   if (!c || !labels || ((uintptr_t)labels & 3)) return NLR_EINVAL;
   if (c->failed) return NLR_ESTATE;
   if (launch_labels(c->g, c->b, labels, c->stream) != hipSuccess) return hip_fail(c);
+  return NLR_OK;
+}
+
+nlr_status nlr_labels_spectral(nlr_ctx* c, int32_t K, const int64_t* seed_rows, int32_t max_iter,
+                               int32_t* labels, int32_t* passes_done) {
+  if (!c || !labels || !seed_rows || ((uintptr_t)labels & 3) || max_iter < 1) return NLR_EINVAL;
+  if (K < 1 || K > c->g.r) return NLR_EINVAL;
+  if (K > kLabMaxK) return NLR_EUNSUPPORTED;
+  for (int32_t k = 0; k < K; ++k)
+    if (seed_rows[k] < 0 || seed_rows[k] >= c->g.n) return NLR_EINVAL;
+  if (c->failed) return NLR_ESTATE;
+  const Geometry& g = c->g;
+  LabScratch L = carve_lab_scratch(g.n, g.r, K, reinterpret_cast<char*>(c->b.theta_part));
+  int32_t flags[2] = {0, 0};
+  if (hipMemcpyAsync(L.seeds, seed_rows, (size_t)K * sizeof(int64_t), hipMemcpyHostToDevice, c->stream) !=
+      hipSuccess)
+    return hip_fail(c);
+  if (launch_lab_embed(g, c->b, L, K, c->stream) != hipSuccess) return hip_fail(c);
+  if (hipMemcpyAsync(flags, L.flag, sizeof(flags), hipMemcpyDeviceToHost, c->stream) != hipSuccess)
+    return hip_fail(c);
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+  if (flags[0]) return NLR_EDEGENERATE;
+  int32_t pass = 0;
+  while (pass < max_iter) {
+    ++pass;
+    if (launch_lab_pass(g, c->b, L, K, labels, pass == 1 ? 1 : 0, c->stream) != hipSuccess) return hip_fail(c);
+    if (hipMemcpyAsync(flags, L.flag, sizeof(flags), hipMemcpyDeviceToHost, c->stream) != hipSuccess)
+      return hip_fail(c);
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+    if (pass > 1 && flags[1] == 0) break;
+  }
+  if (passes_done) *passes_done = pass;
   return NLR_OK;
 }
 

@@ -127,6 +127,24 @@ struct Bufs {
   double* s_T;         // d x r: M L^{-T}
 };
 
+// Scratch of the spectral label recovery (carved from the Theta-partial region,
+// which is free between host calls).
+struct LabScratch {
+  int32_t GU;          // row chunks of the U^T U partials
+  int32_t GA2;         // row chunks of the assignment pass
+  double* gpart;       // GU x r x r
+  double* A;           // r x r: U^T U, diagonalised in place
+  double* V;           // r x r: eigenvectors
+  double* P;           // r x K: V_K Lambda_K^(-1/2)
+  double* cent;        // K x K centroids
+  double* apart;       // GA2 x (K*K + K + 1): cluster sums, counts, changed labels
+  int64_t* seeds;      // K seed rows
+  int32_t* flag;       // [0] degenerate spectrum, [1] changed labels of the last pass
+};
+constexpr int kLabMaxK = 128;
+size_t lab_scratch_bytes(int64_t n, int32_t r, int32_t K);
+LabScratch carve_lab_scratch(int64_t n, int32_t r, int32_t K, char* base);
+
 // aligned16: X and U start on 16-byte boundaries (enables the vector-load kernels)
 // split: split-fp16 products requested (NLR_INIT_SPLIT_F16)
 Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned16, bool split = false,
@@ -163,6 +181,9 @@ hipError_t launch_pass_b_split(const Geometry& g, const Bufs& b, const StepArgs&
 hipError_t launch_seg_theta(const Geometry& g, const Bufs& b, int64_t rows, int nseg, hipStream_t st);
 hipError_t launch_data_start(const Geometry& g, const Bufs& b, const StepArgs& a0, bool x_normalised,
                              hipStream_t st);
+hipError_t launch_lab_embed(const Geometry& g, const Bufs& b, const LabScratch& L, int K, hipStream_t st);
+hipError_t launch_lab_pass(const Geometry& g, const Bufs& b, const LabScratch& L, int K, int32_t* labels,
+                           int first, hipStream_t st);
 hipError_t launch_labels(const Geometry& g, const Bufs& b, int32_t* labels, hipStream_t st);
 
 // ---- device helpers ----

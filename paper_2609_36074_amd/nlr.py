@@ -32,6 +32,7 @@ NLR_INIT_DATA_START = 32
 NLR_MAX_KERNEL_KINDS = 16
 
 EXPORTED = ["nlr_workspace_bytes", "nlr_init", "nlr_set_params", "nlr_step", "nlr_run", "nlr_labels",
+            "nlr_labels_spectral",
             "nlr_history", "nlr_normaliser", "nlr_inspect", "nlr_set_profiling", "nlr_kernel_times",
             "nlr_destroy", "nlr_status_string", "nlr_version"]
 
@@ -86,6 +87,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nlr_run.restype = ctypes.c_int
     lib.nlr_labels.argtypes = [P, P]
     lib.nlr_labels.restype = ctypes.c_int
+    lib.nlr_labels_spectral.argtypes = [P, i32, ctypes.POINTER(i64), i32, P, ctypes.POINTER(i32)]
+    lib.nlr_labels_spectral.restype = ctypes.c_int
     lib.nlr_history.argtypes = [P, ctypes.POINTER(NlrIterStats), i32, ctypes.POINTER(i32)]
     lib.nlr_history.restype = ctypes.c_int
     lib.nlr_normaliser.argtypes = [P, ctypes.POINTER(dbl), P]
@@ -216,6 +219,17 @@ class Context:
             out = torch.empty(self.n, dtype=torch.int32, device=self.X.device)
         _check(nlr_labels(self._ctx, out.data_ptr()), "nlr_labels")
         return out
+
+    def labels_spectral(self, K: int, seed_rows, max_iter: int = 100, out=None):
+        """(labels tensor, assignment passes): spectral embedding + K-means (Appendix D)."""
+        import torch
+        if out is None:
+            out = torch.empty(self.n, dtype=torch.int32, device=self.X.device)
+        seeds = (ctypes.c_int64 * len(seed_rows))(*[int(s) for s in seed_rows])
+        passes = ctypes.c_int32(0)
+        _check(load_library().nlr_labels_spectral(self._ctx, int(K), seeds, int(max_iter), out.data_ptr(),
+                                                  ctypes.byref(passes)), "nlr_labels_spectral")
+        return out, passes.value
 
     # -- read-back --
     def history(self, max_records: int = 4096):
