@@ -104,13 +104,14 @@ def kernel_flops(kind: str, n: int, d: int, r: int) -> float:
     return {"pass_a": 2.0, "pass_b": 2.0, "pass_bf": 4.0}.get(kind, 0.0) * n * d * r
 
 
-def measure(nlr, torch, np, X_dev, Z_host, wl, steps, warm, split, two_pass, x_normalised=False):
-    """Init on (X_dev, fresh U_0 = Z_host), `warm` untimed iterations, then `steps` timed ones."""
+def measure(nlr, torch, np, X_host, Z_host, wl, steps, warm, split, two_pass):
+    """Init on fresh device copies of (X_host, U_0 = Z_host), `warm` untimed iterations, then `steps`
+    timed ones.  (nlr_init normalises X in place, and the split form also stores it split.)"""
     n, d, r, K = wl.n, wl.d, wl.r, wl.K
+    X_dev = torch.from_numpy(X_host).to("cuda:0")
     Ut = torch.from_numpy(Z_host).to(X_dev.device)
     alpha = 1.0 / (2.0 * (2.0 + 1.0 * (6.0 * K + 2.0)))  # half the Prop. 1 step bound at y = 0, beta = 1
-    flags = ((nlr.NLR_INIT_SPLIT_F16 if split else 0) | (nlr.NLR_INIT_TWO_PASS if two_pass else 0)
-             | (nlr.NLR_INIT_X_NORMALISED if x_normalised else 0))
+    flags = (nlr.NLR_INIT_SPLIT_F16 if split else 0) | (nlr.NLR_INIT_TWO_PASS if two_pass else 0)
     torch.cuda.synchronize()
     ctx = nlr.Context(X_dev, K, Ut, alpha=alpha, beta=1.0, eps_d=1e-4, eps_c=1e-4, T_min=1 << 30, flags=flags)
     if warm > 0:
@@ -131,7 +132,8 @@ def measure(nlr, torch, np, X_dev, Z_host, wl, steps, warm, split, two_pass, x_n
     assert done == steps, (done, steps)
     hist = ctx.history(steps)
     ctx.close()
-    del Ut
+    del Ut, X_dev
+    torch.cuda.empty_cache()
     dual_frac = float(np.mean([h["dual_step"] for h in hist])) if hist else 0.0
     value = n * steps / (t_ms / 1e3)
     eff_gbs = algorithmic_bytes("step", n, d, r, dual_frac) * steps / (t_ms / 1e3) / 1e9
@@ -209,25 +211,23 @@ def main():
         torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         del src, dst
-    Xt = torch.from_numpy(X).to(dev)
-    del X
     # the split products exist for d <= 128, r <= 64, d % 4 == 0 (and r % 4 == 0 in the two-pass
     # form); other shapes run fp32 products
     split_ok = d <= 128 and r <= 64 and d % 4 == 0 and (r % 4 == 0 or not args.two_pass)
     split = args.gemm == "split16" and split_ok
     if args.gemm == "split16" and not split:
         eprint(f"[bench] split-fp16 products are not available for d={d}, r={r}: fp32 products")
-    main_run = measure(nlr, torch, np, Xt, Z, wl, args.steps, args.warmup, split, args.two_pass)
+    main_run = measure(nlr, torch, np, X, Z, wl, args.steps, args.warmup, split, args.two_pass)
     alt = None
     if not args.no_alt and split_ok:
-        # the other product form on the same (already normalised) data and the same start
-        a = measure(nlr, torch, np, Xt, Z, wl, args.steps, args.warmup, not split, args.two_pass, x_normalised=True)
+        # the other product form on the same data and the same start
+        a = measure(nlr, torch, np, X, Z, wl, args.steps, args.warmup, not split, args.two_pass)
         alt = {"products": "fp32" if split else "fp16 two-term split, fp32 accumulate",
                "dtype": "f32" if split else "f32 (fp16x3 products)",
                "value": a["value"], "ms_per_step": a["t_ms"] / args.steps,
                "achieved_hbm_gbs": round(a["eff_gbs"], 1), "hbm_frac": round(a["eff_gbs"] / HBM_PEAK_GBS, 4),
                "roofline": a["roofline"]}
-    del Z
+    del X, Z
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -105,7 +105,11 @@ enum {
    * the TF32 products of the paper's CUTLASS kernel (Appendix C), at about a fifth of the fp32 matrix
    * work.  Supported for d <= 128, r <= 64, d % 4 == 0 and 16-byte aligned X and
    * U (and r % 4 == 0 with NLR_INIT_TWO_PASS); other shapes return
-   * NLR_EUNSUPPORTED. */
+   * NLR_EUNSUPPORTED.  In the single-Xhat-pass form X is left holding Xhat in
+   * split form after nlr_init: each 16 bytes that held 4 consecutive features
+   * hold their 4 fp16 hi halves then their 4 fp16 lo halves of x * s (s a power
+   * of two), so X no longer reads as fp32 (do not pass it to nlr_init again with
+   * NLR_INIT_X_NORMALISED). */
   NLR_INIT_SPLIT_F16 = 8,
   /* Use the two-pass iteration (pass A: Theta = Xhat^T U with the row work; pass
    * B: Xhat Theta with the fused epilogue) even where the single-Xhat-pass form

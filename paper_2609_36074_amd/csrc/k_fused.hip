@@ -53,6 +53,16 @@ __device__ __forceinline__ f16x4 lds_read_tr16(const _Float16* p) {
   return o;
 }
 
+// Two stored 4-feature units of split Xhat (8 dwords: hi, hi, lo, lo, hi, hi, lo, lo)
+// as the hi and lo operands of 8 features.
+__device__ __forceinline__ void unpack_split(const float* v, f16x8& hi, f16x8& lo) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 h = {__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[4]), __float_as_uint(v[5])};
+  const u32x4 l = {__float_as_uint(v[2]), __float_as_uint(v[3]), __float_as_uint(v[6]), __float_as_uint(v[7])};
+  hi = __builtin_bit_cast(f16x8, h);
+  lo = __builtin_bit_cast(f16x8, l);
+}
+
 // 32x32x16 operand with k = row from a row-major fp16 tile T (row stride ts):
 // lane l gets T[r0 + 8 (l/32) + e][c0 + l%32], e = 0..7.
 __device__ __forceinline__ f16x8 tile_operand_rows(const _Float16* T, int ts, int r0, int c0, int lane) {
@@ -292,9 +302,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
       if constexpr (SPLIT) {
         const f16x8* th_h = reinterpret_cast<const f16x8*>(th_raw);
         const f16x8* th_l = th_h + KS * NB * 64;
+        // Xhat is stored split since initialisation: the 16 bytes of features 4q..4q+3 hold
+        // their four hi halves, then their four lo halves
         f16x8 xh[2], xl[2];
-        split_f16(&xv[ch][0], sx, xh[0], xl[0]);
-        split_f16(&xv[ch][8], sx, xh[1], xl[1]);
+        unpack_split(&xv[ch][0], xh[0], xl[0]);
+        unpack_split(&xv[ch][8], xh[1], xl[1]);
         // the slab for phase 2: row li, features 32 ch + 16 h + [0, 16)
         _Float16* xrh = xh_t + li * XS + 32 * ch + 16 * h;
         _Float16* xrl = xl_t + li * XS + 32 * ch + 16 * h;

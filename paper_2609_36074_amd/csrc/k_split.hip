@@ -297,6 +297,38 @@ hipError_t launch_pass_b_split(const Geometry& g, const Bufs& b, const StepArgs&
   }
 }
 
+// Xhat in place into split form (the single-pass iteration's only reader of X):
+// each 16-byte unit of 4 features becomes their 4 hi halves then their 4 lo halves
+// of x * x_scale, the same split the products would otherwise form every iteration.
+__global__ __launch_bounds__(kThreads) void k_split_x(Bufs B, int64_t units) {
+  const float s = B.ctl->x_scale;
+  for (int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x; u < units; u += (int64_t)gridDim.x * kThreads) {
+    f32x4* p = reinterpret_cast<f32x4*>(B.X) + u;
+    const f32x4 v = *p;
+    const float x[4] = {v.x, v.y, v.z, v.w};
+    typedef _Float16 f16x4s __attribute__((ext_vector_type(4)));
+    f16x4s hi, lo;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float t = x[e] * s;
+      const _Float16 h = (_Float16)t;
+      hi[e] = h;
+      lo[e] = (_Float16)(t - (float)h);
+    }
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 hb = __builtin_bit_cast(f32x2, hi);
+    const f32x2 lb = __builtin_bit_cast(f32x2, lo);
+    const f32x4 o = {hb.x, hb.y, lb.x, lb.y};
+    *p = o;
+  }
+}
+
+hipError_t launch_split_x(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int64_t units = g.n * (int64_t)g.d / 4;  // d % 4 == 0
+  hipLaunchKernelGGL(k_split_x, dim3(4096), dim3(kThreads), 0, st, b, units);
+  return hipGetLastError();
+}
+
 hipError_t launch_xscale(const Geometry& g, const Bufs& b, hipStream_t st) {
   hipLaunchKernelGGL(k_xmax_partial, dim3(g.GI), dim3(kThreads), 0, st, g, b);
   hipError_t e = hipGetLastError();

@@ -505,6 +505,9 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
     const StepArgs a0 = make_step_args(c, 0);
     if (launch_pass_a(g, b, a0, false, st) != hipSuccess) return fail(NLR_EHIP);
     if (launch_reduce_theta(g, b, false, st) != hipSuccess) return fail(NLR_EHIP);
+    // split products: the fused pass B is then the only reader of X; store Xhat split once
+    if (g.split_b)
+      if (launch_split_x(g, b, st) != hipSuccess) return fail(NLR_EHIP);
   }
   if (read_ctl(c) != NLR_OK) return fail(NLR_EHIP);
   if (c->host_ctl->degenerate) return fail(NLR_EDEGENERATE);

@@ -177,6 +177,7 @@ hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, boo
 hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_ctl_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_xscale(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_split_x(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_pass_b_split(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_seg_theta(const Geometry& g, const Bufs& b, int64_t rows, int nseg, hipStream_t st);
 hipError_t launch_data_start(const Geometry& g, const Bufs& b, const StepArgs& a0, bool x_normalised,
