@@ -89,8 +89,15 @@ constexpr int fused_lds_bytes(int NB, int NCH, bool split, bool uflat) {
 // UFLAT (rows of U not 16-byte aligned, r % 4 != 0): each wave moves its 32-row
 // slab of U (32 r contiguous floats, 16-byte aligned because the slab starts at a
 // multiple of 32 rows) with whole-slab vector loads and stores through LDS.
+// Waves per SIMD: two for the small shapes (registers allow it, and a second
+// wave is what hides a tile's memory latency), one when the d x r partial takes
+// 128 accumulator registers.
+template <int NB, int NCH>
+constexpr int fused_waves_per_simd() { return (NB == 1 && NCH <= 2) ? 2 : 1; }
+
 template <int NB, int NCH, bool SPLIT, bool UFLAT>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_pass_bf(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_waves_per_simd<NB, NCH>(),
+                                                                            fused_waves_per_simd<NB, NCH>()))) void k_pass_bf(
     Geometry g, Bufs B, StepArgs S) {
   if (halted(B.ctl)) return;
   constexpr int KS = 2 * NCH;                      // 16-feature k-steps (split phase 1)

@@ -118,7 +118,9 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   g.uflat = (g.fused && uflat) ? 1 : 0;
   g.SAF = g.SA;
   if (g.fused) {
-    g.GB = (int32_t)(g.tilesB < 256 ? g.tilesB : 256);
+    // persistent grid: one (two for the shapes with two waves per SIMD) workgroup per CU
+    const int64_t gmax = (g.NB == 1 && g.nch <= 2) ? 512 : 256;
+    g.GB = (int32_t)(g.tilesB < gmax ? g.tilesB : gmax);
     g.SB = (g.GB + 31) / 32;
     g.SAF = (g.GB + 31) / 32;
     g.split_a = g.split_b = split ? 1 : 0;  // both products live in the fused pass B
@@ -723,7 +725,7 @@ const char* nlr_status_string(nlr_status s) {
     case NLR_EINVAL: return "invalid argument";
     case NLR_EWORKSPACE: return "workspace missing, misaligned or too small";
     case NLR_EBREAKDOWN: return "normalisation breakdown (||W_+||_F <= 1e-20)";
-    case NLR_EDEGENERATE: return "degenerate data (centred matrix is zero)";
+    case NLR_EDEGENERATE: return "degenerate input (zero centred data, or a rank-deficient sample or spectrum)";
     case NLR_EHIP: return "HIP runtime error";
     case NLR_ESTATE: return "context failed earlier or used out of order";
     case NLR_EUNSUPPORTED: return "shape outside the compiled kernel family";
