@@ -54,7 +54,7 @@ def algorithmic_bytes(kind: str, n: int, d: int, r: int, dual_frac: float = 0.0)
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("k_iter.hip", "k_split.hip", "k_fused.hip", "k_common.hpp", "nlr_internal.hpp"):
+    for f in ("k_iter.hip", "k_split.hip", "k_fused.hip", "k_panel.hip", "k_common.hpp", "nlr_internal.hpp"):
         with open(os.path.join(ROOT, "paper_2609_36074_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -212,8 +212,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     # the split products exist for d <= 128, r <= 64, d % 4 == 0 (and r % 4 == 0 in the two-pass
-    # form); other shapes run fp32 products
-    split_ok = d <= 128 and r <= 64 and d % 4 == 0 and (r % 4 == 0 or not args.two_pass)
+    # form), and in the two-pass panel form for d % 8 == 0, r % 4 == 0, r <= 256; other shapes run
+    # fp32 products
+    split_ok = (d <= 128 and r <= 64 and d % 4 == 0 and (r % 4 == 0 or not args.two_pass)) or \
+        (d % 8 == 0 and r % 4 == 0 and r <= 256)
     split = args.gemm == "split16" and split_ok
     if args.gemm == "split16" and not split:
         eprint(f"[bench] split-fp16 products are not available for d={d}, r={r}: fp32 products")

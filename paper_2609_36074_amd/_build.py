@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libnlr.so")
-SOURCES = ["nlr_api.cpp", "k_iter.hip", "k_init.hip", "k_split.hip", "k_fused.hip", "k_start.hip", "k_labels.hip"]
+SOURCES = ["nlr_api.cpp", "k_iter.hip", "k_init.hip", "k_split.hip", "k_fused.hip", "k_start.hip", "k_labels.hip", "k_panel.hip"]
 ARCH = "gfx950"
 
 

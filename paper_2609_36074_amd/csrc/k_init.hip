@@ -24,7 +24,8 @@ __global__ void k_ctl_init(Bufs B, float gamma_f) {
     c->pad64 = 0;
     c->c_f = 1.0f;
     c->x_scale = 1.0f;
-    c->pad_i0 = c->pad_i1 = 0;
+    c->th_scale = 1.0f;
+    c->pad_i1 = 0;
     c->a = c->b = c->h = 0.0;
     c->Delta = c->delta = 0.0;
     c->rho = c->objective = c->theta_fro2 = 0.0;

@@ -102,8 +102,9 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
   const bool gate = (S.end_work != 0) && (B.ctl->gate != 0) && !stopped;
   const float gam = S.gamma_f;
 
-  const int64_t tb = (int64_t)gx * g.tilesA / g.GA;
-  const int64_t te = (int64_t)(gx + 1) * g.tilesA / g.GA;
+  // the grid is GA (Theta product) or GAF (finish pass)
+  const int64_t tb = (int64_t)gx * g.tilesA / gridDim.x;
+  const int64_t te = (int64_t)(gx + 1) * g.tilesA / gridDim.x;
 
   if (do_rows)
     for (int c = tid; c < r32; c += kThreads) p_s[c] = (c < r) ? B.p[c] : 0.f;
@@ -500,6 +501,7 @@ __global__ __launch_bounds__(kThreads) void k_seg_sum(const T* __restrict__ P, i
 __global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, int nseg, int scaled) {
   if (halted(B.ctl)) return;
   __shared__ double red[8];
+  __shared__ float mred[4];
   const int64_t tot = (int64_t)g.d32 * g.r32;
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   double sum = 0.0;
@@ -518,6 +520,12 @@ __global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, i
   }
   const double t2 = block_sum_d(sum * sum, red);
   if (threadIdx.x == 0) B.th2_part[blockIdx.x] = t2;
+  // max |Theta| of the block (the panel form scales its split Theta operand by it)
+  float m = fabsf((float)sum);
+  for (int k = 32; k >= 1; k >>= 1) m = fmaxf(m, shfl_xor_f(m, k));
+  if ((threadIdx.x & 63) == 0) mred[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) B.thmax_part[blockIdx.x] = fmaxf(fmaxf(mred[0], mred[1]), fmaxf(mred[2], mred[3]));
 }
 
 // ---------------------------------------------------------------------------
@@ -1086,7 +1094,8 @@ static hipError_t allow_lds(F* kern, size_t lds) {
 
 template <int MBG, int NBG, bool FIN>
 static hipError_t pass_a_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  const dim3 grid(g.GA, FIN ? 1 : g.mgroups * g.ngroups);
+  // the finish pass writes no Theta partials: its grid is sized for the rows alone
+  const dim3 grid(FIN ? g.GAF : g.GA, FIN ? 1 : g.mgroups * g.ngroups);
   const size_t lds = g.ldsA_bytes;
   hipError_t e = allow_lds(k_pass_a<MBG, NBG, FIN>, lds);
   if (e != hipSuccess) return e;
@@ -1159,24 +1168,34 @@ hipError_t launch_seg_theta(const Geometry& g, const Bufs& b, int64_t rows, int 
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, bool fused_partials, hipStream_t st) {
+hipError_t launch_reduce_theta_rows(const Geometry& g, const Bufs& b, int64_t rows, int nseg, bool scaled,
+                                    hipStream_t st) {
   const int C = g.d32 * g.r32;
-  const int64_t rows = fused_partials ? g.GB : g.GA;
-  const int nseg = fused_partials ? g.SAF : g.SA;
   hipLaunchKernelGGL((k_seg_sum<float>), dim3((C + 63) / 64, nseg), dim3(kThreads), 0, st,
                      (const float*)b.theta_part, rows, C, b.seg_theta, nseg, (const DevCtl*)b.ctl, 1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT), dim3(kThreads), 0, st, g, b, nseg, fused_partials ? 1 : 0);
+  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT), dim3(kThreads), 0, st, g, b, nseg, scaled ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, bool fused_partials, hipStream_t st) {
+  return fused_partials ? launch_reduce_theta_rows(g, b, g.GB, g.SAF, true, st)
+                        : launch_reduce_theta_rows(g, b, g.GA, g.SA, false, st);
+}
+
+// a_part rows -> g.SA segment sums (the segment count k_ctl_a reads)
+hipError_t launch_seg_a_rows(const Geometry& g, const Bufs& b, int64_t rows, bool finish, hipStream_t st) {
+  const int C = 4 + g.r32;
+  hipLaunchKernelGGL((k_seg_sum<double>), dim3((C + 63) / 64, g.SA), dim3(kThreads), 0, st,
+                     (const double*)b.a_part, rows, C, b.seg_a, g.SA, (const DevCtl*)b.ctl, finish ? 0 : 1);
   return hipGetLastError();
 }
 
 hipError_t launch_seg_a(const Geometry& g, const Bufs& b, bool finish, hipStream_t st) {
-  const int C = 4 + g.r32;
-  hipLaunchKernelGGL((k_seg_sum<double>), dim3((C + 63) / 64, g.SA), dim3(kThreads), 0, st,
-                     (const double*)b.a_part, (int64_t)g.GA, C, b.seg_a, g.SA, (const DevCtl*)b.ctl,
-                     finish ? 0 : 1);
-  return hipGetLastError();
+  // the register-resident finish runs on the pass-A grid; the generic one on GAF
+  const int64_t rows = (finish && !g.a_rows) ? g.GAF : g.GA;
+  return launch_seg_a_rows(g, b, rows, finish, st);
 }
 
 hipError_t launch_seg_b(const Geometry& g, const Bufs& b, hipStream_t st) {

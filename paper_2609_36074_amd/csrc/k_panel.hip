@@ -1,0 +1,710 @@
+// Panel kernels of the split-fp16 two-pass iteration for large d x r (gfx950).
+//
+// When Theta (d x r) is too large for one workgroup to hold -- the
+// single-Xhat-pass form keeps all of Xhat^T W in registers and the resident pass
+// B all of Theta in LDS -- the two products of an iteration (Algorithm 1;
+// Theta = Xhat^T U, then Xhat Theta with the epilogue of eq. (entrywise-fusion))
+// run as LDS-tiled panel products on the 32x32x16 fp16 matrix cores with the
+// two-term split of both operands (v s = hi + lo, three products hi*lo, lo*hi,
+// hi*hi accumulated in fp32).
+//
+// Operands reach LDS by direct global-to-LDS loads (global_load_lds_dwordx4:
+// each lane moves 16 bytes, a wave instruction fills 1 KiB of LDS), several
+// stages ahead of the matrix cores, so no registers are spent on staging.  The
+// waits are explicit: before a stage is read, each wave waits until its own
+// loads of that stage have landed (vmcnt, loads complete in issue order) and a
+// workgroup barrier makes the other waves' loads visible.  The LDS images are
+// swizzled at 16-byte granularity so that the operand reads are free of bank
+// conflicts; the swizzle is chosen by the global addresses each lane loads from.
+//
+// Pass A (k_pass_a_panel): workgroup (split s, feature block j) of 8 waves
+// accumulates Theta[256 j .. 256 j + 255][all columns] over the rows of split s,
+// 16 rows per stage.  Xhat arrives split (stored so since initialisation: every 32
+// bytes that held 8 features hold their 8 fp16 hi halves, then their 8 lo
+// halves); U arrives as fp32 and is scaled (u = fl(c_f w), the lazy
+// normalisation), split and written as fp16 hi/lo slabs; both are read with the
+// transposing ds_read_b64_tr_b16.  The workgroups of feature block 0 also do the
+// row work that ends the previous iteration and starts this one (q = u.p - 1,
+// the gated dual step, ybar, s = U^T ybar, ||q||^2, ytilde^T q) and store ybar
+// for pass B.  The feature blocks of one split are launched on the same XCD
+// (workgroup ids congruent mod 8) and stream the same U rows at the same time,
+// so U is fetched from HBM about once.
+//
+// Pass B (k_pass_b_panel): workgroup of 4 waves (two per compute unit) over
+// 128-row tiles, 16 features per stage: Theta^T chunks (split and laid out once
+// per iteration by k_theta_split_panel) and Xhat row chunks in LDS, then the
+// epilogue on the accumulators: w = max(u + 2 alpha G - alpha ybar p - alpha s, 0),
+// FP64 a = ||W||^2, b = ||U||^2, h = <W, U>, column sums of W, W stored over U.
+#include "k_common.hpp"
+
+namespace nlr {
+
+typedef _Float16 pf16x4 __attribute__((ext_vector_type(4)));
+typedef __fp16 ph16x4 __attribute__((__vector_size__(4 * sizeof(__fp16))));
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// 16 bytes per lane from global memory to LDS: lane l writes lds_wave_base + 16 l.
+__device__ __forceinline__ void dma16(const void* src, unsigned char* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void_t*)lds_wave_base, 16, 0, 0);
+}
+
+// Wait until at most N vector memory operations of this wave are outstanding and
+// its LDS operations are done, then a workgroup barrier.  Written as one asm
+// block so that no memory access is moved across it.
+template <int N>
+__device__ __forceinline__ void wait_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ pf16x4 lds_tr16(const _Float16* p) {
+  ph16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4f16((__attribute__((address_space(3))) ph16x4*)(p));
+  pf16x4 o;
+  o[0] = (_Float16)v[0];
+  o[1] = (_Float16)v[1];
+  o[2] = (_Float16)v[2];
+  o[3] = (_Float16)v[3];
+  return o;
+}
+
+// Fixed-order sum over a 512-thread workgroup; result valid in thread 0.
+__device__ __forceinline__ double block_sum8_d(double v, double* red) {
+  for (int m = 32; m >= 1; m >>= 1) v += shfl_xor_d(v, m);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  double r = 0.0;
+  if (threadIdx.x == 0) r = (((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7])));
+  __syncthreads();
+  return r;
+}
+
+// ===========================================================================
+// Pass A
+// ===========================================================================
+constexpr int kPAStages = 4;    // stages in the LDS ring
+constexpr int kPAPts = 16;      // rows (points) per stage = one k-step of the 32x32x16 product
+constexpr int kPAFeat = 256;    // features per workgroup block
+constexpr int kPAThreads = 512;
+
+template <int NBW>
+struct PanelA {
+  static constexpr int RC = 64 * NBW;                 // columns: two column waves x 32 NBW
+  static constexpr int XB = kPAPts * kPAFeat * 4;     // Xhat rows of a stage (split, 1 KiB per row)
+  static constexpr int UB = kPAPts * RC * 4;          // U rows of a stage (fp32)
+  static constexpr int STAGE = XB + UB;
+  static constexpr int INSTR = STAGE / 1024;          // 1 KiB load instructions per stage
+  static constexpr int OPS = INSTR / 8;               // per wave, at least
+  static constexpr int WS = RC + 16;                  // split slab row stride (halves)
+  static constexpr int SLAB = 2 * kPAPts * WS * 2;    // hi and lo slabs (bytes)
+  static constexpr int LPP = RC / 8;                  // threads per row in the conversion
+  static constexpr int LDS = kPAStages * STAGE + SLAB + 16 * 8;
+  static_assert(INSTR * 1024 == STAGE, "whole instructions");
+  static_assert(kPAPts * RC * 4 / 1024 * 1024 == UB, "U stage in whole KiB");
+  static_assert(kPAPts * RC / 8 <= kPAThreads, "one conversion unit per thread");
+  static_assert(kPAPts * RC * 8 <= kPAStages * STAGE, "s combine fits the ring");
+};
+
+// 16-byte piece P (= 2 * unit + hi/lo) of row R of a pass-A Xhat stage sits in slot P ^ pa_swz(R).
+__device__ __forceinline__ int pa_swz(int R) { return (R & 1) | ((R & 2) << 1); }
+
+template <int NBW>
+__global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_a_panel(
+    Geometry g, Bufs B, StepArgs S) {
+  using P = PanelA<NBW>;
+  if (halted(B.ctl)) return;
+  // workgroup -> (split, feature block): the blocks of a split share blockIdx.x mod 8 (one XCD)
+  const int per = 8 * g.pfb;
+  const int grp = blockIdx.x / per;
+  const int rem = blockIdx.x - grp * per;
+  const int fb = rem >> 3;
+  const int sp = grp * 8 + (rem & 7);
+  if (sp >= g.PS) return;
+
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  unsigned char* ring = smem_raw;
+  _Float16* slab_h = reinterpret_cast<_Float16*>(smem_raw + kPAStages * P::STAGE);
+  _Float16* slab_l = slab_h + kPAPts * P::WS;
+  double* dred = reinterpret_cast<double*>(smem_raw + kPAStages * P::STAGE + P::SLAB);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int fw = wave & 3;   // 64-feature group of the block
+  const int cw = wave >> 2;  // column half
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r;
+  const float cf = B.ctl->c_f;
+  const float su = g.su;
+  const bool rows_work = (fb == 0);
+  const bool gate = (S.end_work != 0) && (B.ctl->gate != 0);
+  const float gam = S.gamma_f;
+
+  const int64_t p0 = (int64_t)sp * n / g.PS;
+  const int64_t p1 = (int64_t)(sp + 1) * n / g.PS;
+  const int nst = (int)((p1 - p0 + kPAPts - 1) / kPAPts);
+
+  // conversion unit of this thread: row cr of the stage, columns cc .. cc + 7
+  const bool conv = tid < kPAPts * P::LPP;
+  const int cr = tid / P::LPP;
+  const int cc = 8 * (tid - cr * P::LPP);
+  float pr[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) pr[e] = (conv && cc + e < g.r32) ? B.p[cc + e] : 0.f;
+  double s_acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s_acc[e] = 0.0;
+  double qq = 0.0, yq = 0.0;
+
+  f32x16 acc[2][NBW];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < NBW; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  auto issue = [&](int st) {
+    unsigned char* slot = ring + (st % kPAStages) * P::STAGE;
+    const int64_t rbase = p0 + (int64_t)st * kPAPts;
+#pragma unroll
+    for (int q = 0; q < (P::INSTR + 7) / 8; ++q) {
+      const int i = wave + 8 * q;
+      if (i < P::INSTR) {
+        const void* src;
+        if (i < kPAPts) {
+          // Xhat row i of the stage: slot `lane` takes piece lane ^ swz(i)
+          int64_t row = rbase + i;
+          if (row >= p1) row = p1 - 1;
+          const int pc = lane ^ pa_swz(i);
+          int unit = fb * (kPAFeat / 8) + (pc >> 1);
+          if (8 * unit >= d) unit = 0;  // features >= d: any finite data of the row
+          src = B.X + row * (int64_t)d + 8 * unit + 4 * (pc & 1);
+        } else {
+          // U: fp32 rows of RC floats, 16 bytes per lane
+          const int q4 = 64 * (i - kPAPts) + lane;
+          const int rr = q4 / (P::RC / 4);
+          const int col = 4 * (q4 - rr * (P::RC / 4));
+          int64_t row = rbase + rr;
+          if (row >= p1) row = p1 - 1;
+          src = B.U + row * (int64_t)r + (col < r ? col : 0);
+        }
+        dma16(src, slot + i * 1024);
+      }
+    }
+  };
+
+  for (int st = 0; st < kPAStages - 1 && st < nst; ++st) issue(st);
+
+  for (int st = 0; st < nst; ++st) {
+    // this wave's loads of stage st have landed (the later ones may be in flight)
+    const int newer = (nst - 1 - st) < (kPAStages - 2) ? (nst - 1 - st) : (kPAStages - 2);
+    if (newer >= 2) wait_barrier<2 * P::OPS>();
+    else if (newer == 1) wait_barrier<P::OPS>();
+    else wait_barrier<0>();
+    if (st + kPAStages - 1 < nst) issue(st + kPAStages - 1);
+    int slot_off = (st % kPAStages) * P::STAGE;  // opaque: addresses formed per stage
+    asm volatile("" : "+s"(slot_off));
+    const unsigned char* slot = ring + slot_off;
+
+    // ---- U: lazy scale, split into the hi/lo slabs; row work ----
+    if (conv) {
+      const float* ub = reinterpret_cast<const float*>(slot + P::XB) + cr * P::RC + cc;
+      const f32x4 a0 = *reinterpret_cast<const f32x4*>(ub);
+      const f32x4 a1 = *reinterpret_cast<const f32x4*>(ub + 4);
+      const float raw[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      const int64_t row = p0 + (int64_t)st * kPAPts + cr;
+      const bool vrow = row < p1;
+      float u[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) u[e] = (vrow && cc + e < r) ? raw[e] * cf : 0.f;
+      f16x8 hi, lo;
+      split_f16(u, su, hi, lo);
+      *reinterpret_cast<f16x8*>(slab_h + cr * P::WS + cc) = hi;
+      *reinterpret_cast<f16x8*>(slab_l + cr * P::WS + cc) = lo;
+      if (rows_work) {
+        double dot = 0.0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dot += (double)u[e] * (double)pr[e];
+#pragma unroll
+        for (int m = 1; m < P::LPP; m <<= 1) dot += shfl_xor_d(dot, m);
+        if (vrow) {
+          const float q = (float)(dot - 1.0);
+          float yt = B.y[row];
+          const bool lead = (tid - cr * P::LPP) == 0;
+          if (gate) {
+            yt = fmaf(gam, q, yt);
+            if (lead) B.y[row] = yt;
+          }
+          const float ybar = fmaf(gam, q, yt);
+          if (lead) {
+            B.ybar[row] = ybar;
+            qq += (double)q * (double)q;
+            yq += (double)yt * (double)q;
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) s_acc[e] = fma((double)ybar, (double)u[e], s_acc[e]);
+        }
+      }
+    }
+    wait_barrier<63>();  // slabs written (lgkmcnt(0)); vmcnt left as it is
+
+    // ---- Theta block += Xhat_stage^T U_stage ----
+    const _Float16* xs = reinterpret_cast<const _Float16*>(slot);
+    f16x8 ah[2], al[2];
+    {
+      const int gq = lane >> 4, s16 = lane & 15;
+      const int R = 8 * (gq >> 1) + (s16 >> 2);  // and R + 4 (same swizzle)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int fc = 64 * fw + 32 * i + 16 * (gq & 1) + 4 * (s16 & 3);
+        const int u8 = fc >> 3, qd = (fc >> 2) & 1;
+        const int sh = (2 * u8) ^ pa_swz(R), sl = (2 * u8 + 1) ^ pa_swz(R);
+        const _Float16* ph = xs + R * (kPAFeat * 2) + sh * 8 + qd * 4;
+        const _Float16* pl = xs + R * (kPAFeat * 2) + sl * 8 + qd * 4;
+        const pf16x4 h0 = lds_tr16(ph), h1 = lds_tr16(ph + 4 * kPAFeat * 2);
+        const pf16x4 l0 = lds_tr16(pl), l1 = lds_tr16(pl + 4 * kPAFeat * 2);
+        ah[i] = (f16x8){h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
+        al[i] = (f16x8){l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
+      }
+    }
+#pragma unroll
+    for (int cb = 0; cb < NBW; ++cb) {
+      const int c0 = (P::RC / 2) * cw + 32 * cb;
+      const int gq = lane >> 4, s16 = lane & 15;
+      const int R = 8 * (gq >> 1) + (s16 >> 2);
+      const int c = c0 + 16 * (gq & 1) + 4 * (s16 & 3);
+      const _Float16* ph = slab_h + R * P::WS + c;
+      const _Float16* pl = slab_l + R * P::WS + c;
+      const pf16x4 h0 = lds_tr16(ph), h1 = lds_tr16(ph + 4 * P::WS);
+      const pf16x4 l0 = lds_tr16(pl), l1 = lds_tr16(pl + 4 * P::WS);
+      const f16x8 bh = (f16x8){h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
+      const f16x8 bl = (f16x8){l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        acc[i][cb] = mfma32x32x16h(ah[i], bl, acc[i][cb]);
+        acc[i][cb] = mfma32x32x16h(al[i], bh, acc[i][cb]);
+        acc[i][cb] = mfma32x32x16h(ah[i], bh, acc[i][cb]);
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- Theta partial of this split: rows of this feature block ----
+  {
+    const float unscale = (1.0f / B.ctl->x_scale) * (1.0f / su);
+    float* part = B.theta_part + (int64_t)sp * g.d32 * g.r32;
+    const int h = lane >> 5, li = lane & 31;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int cb = 0; cb < NBW; ++cb) {
+        const int c = (P::RC / 2) * cw + 32 * cb + li;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int f = kPAFeat * fb + 64 * fw + 32 * i + 8 * (v >> 2) + 4 * h + (v & 3);
+          if (f < g.d32 && c < g.r32) part[(int64_t)f * g.r32 + c] = acc[i][cb][v] * unscale;
+        }
+      }
+  }
+
+  // ---- row partials: ||q||^2, ytilde^T q, s (fixed order over the rows of a stage) ----
+  if (rows_work) {
+    double* ap = B.a_part + (int64_t)sp * (4 + g.r32);
+    double* sred = reinterpret_cast<double*>(ring);  // kPAPts x RC (the ring is free now)
+    if (conv)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sred[cr * P::RC + cc + e] = s_acc[e];
+    const double tq = block_sum8_d(qq, dred);  // its barriers also publish sred
+    const double ty = block_sum8_d(yq, dred);
+    if (tid == 0) {
+      ap[0] = tq;
+      ap[1] = ty;
+      ap[2] = ap[3] = 0.0;
+    }
+    for (int c = tid; c < g.r32; c += kPAThreads) {
+      double t = 0.0;
+      for (int k = 0; k < kPAPts; ++k) t += sred[k * P::RC + c];
+      ap[4 + c] = t;
+    }
+  }
+}
+
+// ===========================================================================
+// Theta for pass B: split hi/lo of Theta * s_theta in the pass-B LDS image
+// ===========================================================================
+constexpr int kPBRows = 128;    // rows per pass-B tile (two row waves x 64)
+constexpr int kPBStages = 3;
+constexpr int kPBThreads = 256;
+
+template <int NBW>
+struct PanelB {
+  static constexpr int RC = 64 * NBW;             // columns of the two column waves
+  static constexpr int TH = RC * 64;              // Theta^T chunk: per column 16 features hi + lo
+  static constexpr int XB = kPBRows * 64;         // Xhat chunk: per row 16 features split
+  static constexpr int STAGE = TH + XB;
+  static constexpr int INSTR = STAGE / 1024;
+  static constexpr int OPS = INSTR / 4;           // per wave
+  static constexpr int LDS = kPBStages * STAGE + 2 * RC * 4 + (2 * RC + 8) * 8;
+  static_assert(INSTR % 4 == 0, "equal share of the loads per wave");
+};
+
+// Stage k of the Theta image: column c owns 64 bytes = four 16-byte pieces
+// P = 2 hl + j (features 16k + 8j .. 16k + 8j + 7, hl = 0 hi / 1 lo), piece P in
+// slot P ^ ((c >> 1) & 3).
+__global__ __launch_bounds__(kThreads) void k_theta_split_panel(Geometry g, Bufs B, int RC) {
+  if (halted(B.ctl)) return;
+  __shared__ float red[4];
+  float m = 0.f;
+  for (int k = threadIdx.x; k < g.RT; k += kThreads) m = fmaxf(m, B.thmax_part[k]);
+  for (int k = 32; k >= 1; k >>= 1) m = fmaxf(m, shfl_xor_f(m, k));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  const float sth = f16_range_scale(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));
+  if (blockIdx.x == 0 && threadIdx.x == 0) B.ctl->th_scale = sth;
+  const int nk = (g.d + 15) >> 4;
+  const int64_t rec = (int64_t)blockIdx.x * kThreads + threadIdx.x;  // (stage, column)
+  if (rec >= (int64_t)nk * RC) return;
+  const int k = (int)(rec / RC);
+  const int c = (int)(rec - (int64_t)k * RC);
+  float v[16];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    const int f = 16 * k + t;
+    float x = 0.f;
+    if (f < g.d && c < g.r32) {
+      const int ch = f >> 5, fin = f & 31;
+      const int hh = fin >> 4, j = (fin & 15) >> 2, ee = fin & 3;
+      const int mbk = c >> 5, l = hh * 32 + (c & 31);
+      x = B.theta[((((int64_t)ch * 4 + j) * g.NB + mbk) * 64 + l) * 4 + ee];
+    }
+    v[t] = x;
+  }
+  f16x8 h0, l0, h1, l1;
+  split_f16(v, sth, h0, l0);
+  split_f16(v + 8, sth, h1, l1);
+  f16x8* out = reinterpret_cast<f16x8*>(reinterpret_cast<unsigned char*>(B.theta_split) + rec * 64);
+  const int sw = (c >> 1) & 3;
+  out[0 ^ sw] = h0;  // P = 0: hi, features 0..7
+  out[1 ^ sw] = h1;  // P = 1: hi, features 8..15
+  out[2 ^ sw] = l0;  // P = 2: lo, features 0..7
+  out[3 ^ sw] = l1;  // P = 3: lo, features 8..15
+}
+
+// ===========================================================================
+// Pass B
+// ===========================================================================
+// Row R of a pass-B Xhat chunk: piece P = 2 unit + hl in slot P ^ ((R >> 1) & 3).
+template <int NBW>
+__global__ __launch_bounds__(kPBThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_b_panel(
+    Geometry g, Bufs B, StepArgs S) {
+  using P = PanelB<NBW>;
+  if (halted(B.ctl)) return;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  unsigned char* ring = smem_raw;
+  float* ps = reinterpret_cast<float*>(smem_raw + kPBStages * P::STAGE);
+  float* ss = ps + P::RC;
+  double* colred = reinterpret_cast<double*>(ss + P::RC);  // 2 x RC
+  double* dred = colred + 2 * P::RC;                       // 8
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int wr = wave >> 1;  // 64-row half of the tile
+  const int cw = wave & 1;   // column half
+  const int h = lane >> 5;
+  const int li = lane & 31;
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r;
+  const int nk = (d + 15) >> 4;
+  const float cf = B.ctl->c_f;
+  const float two_alpha_s = S.two_alpha_f * (1.0f / B.ctl->x_scale) * (1.0f / B.ctl->th_scale);
+  const float neg_alpha = -S.alpha_f;
+
+  for (int c = tid; c < P::RC; c += kPBThreads) {
+    ps[c] = (c < g.r32) ? B.p[c] : 0.f;
+    ss[c] = (c < g.r32) ? B.s[c] : 0.f;
+  }
+
+  const int64_t T = g.tilesP;
+  const int G = gridDim.x;
+  const int my_tiles = ((int64_t)blockIdx.x < T) ? (int)((T - 1 - blockIdx.x) / G + 1) : 0;
+  const int total = my_tiles * nk;  // stages of this workgroup, over all its tiles
+
+  // issue cursor: next stage to load (feature chunk ik of the tile at row ir0) and its ring slot
+  int ik = 0, islot = 0, issued = 0;
+  int64_t ir0 = (int64_t)blockIdx.x * kPBRows;
+  auto issue_next = [&]() {
+    unsigned char* slot = ring + islot * P::STAGE;
+    // uniform bases plus 32-bit per-lane offsets (no 64-bit per-lane addresses to keep)
+    const unsigned char* tb = reinterpret_cast<const unsigned char*>(B.theta_split) + (int64_t)ik * P::TH;
+    const float* xb = B.X + ir0 * (int64_t)d;
+    const int rmax = (n - 1 - ir0) < (kPBRows - 1) ? (int)(n - 1 - ir0) : (kPBRows - 1);
+    int ln = lane;  // opaque: per-lane offsets are formed here, not kept across the loop
+    asm volatile("" : "+v"(ln));
+#pragma unroll
+    for (int q = 0; q < P::OPS; ++q) {
+      const int i = wave + 4 * q;
+      const void* src;
+      if (i < P::TH / 1024) {
+        src = tb + (i * 1024 + ln * 16);
+      } else {
+        const int R = 16 * (i - P::TH / 1024) + (ln >> 2);
+        const int pc = (ln & 3) ^ ((R >> 1) & 3);
+        const int Rc = R < rmax ? R : rmax;  // rows >= n: the last row (masked later)
+        int unit = 2 * ik + (pc >> 1);
+        if (8 * unit >= d) unit = 0;  // features >= d meet zero rows of Theta
+        src = xb + (Rc * d + 8 * unit + 4 * (pc & 1));
+      }
+      dma16(src, slot + i * 1024);
+    }
+    ++issued;
+    if (++ik == nk) {
+      ik = 0;
+      ir0 += (int64_t)G * kPBRows;
+    }
+    if (++islot == kPBStages) islot = 0;
+  };
+
+  for (int q = 0; q < kPBStages - 1 && q < total; ++q) issue_next();
+
+  double sa = 0.0, sb = 0.0, sh = 0.0;
+  double colacc[NBW];
+#pragma unroll
+  for (int m = 0; m < NBW; ++m) colacc[m] = 0.0;
+  int base = 0;
+  if (li & 16) base += 8;
+  if (li & 8) base += 4;
+  if (li & 4) base += 2;
+  if (li & 2) base += 1;
+
+  int gs = 0, rslot = 0;  // stage being consumed and its ring slot
+  for (int ti = 0; ti < my_tiles; ++ti) {
+    const int64_t row0 = ((int64_t)blockIdx.x + (int64_t)ti * G) * kPBRows;
+    f32x16 acc[2][NBW];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < NBW; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    for (int k = 0; k < nk; ++k, ++gs) {
+      // this wave's loads of stage gs have landed once at most those of stage gs + 1 are pending
+      if (issued > gs + 1) wait_barrier<P::OPS>();
+      else wait_barrier<0>();
+      if (issued < total) issue_next();
+      // opaque slot offset: the operand addresses are formed per stage instead of
+      // being precomputed for every ring slot (which would not fit in registers)
+      int slot_off = rslot * P::STAGE;
+      asm volatile("" : "+s"(slot_off));
+      if (++rslot == kPBStages) rslot = 0;
+      const unsigned char* slot = ring + slot_off;
+      f16x8 ah[NBW], al[NBW];
+#pragma unroll
+      for (int cb = 0; cb < NBW; ++cb) {
+        const int c = (P::RC / 2) * cw + 32 * cb + li;
+        const int sw = (c >> 1) & 3;
+        ah[cb] = *reinterpret_cast<const f16x8*>(slot + c * 64 + ((h ^ sw) << 4));
+        al[cb] = *reinterpret_cast<const f16x8*>(slot + c * 64 + (((2 + h) ^ sw) << 4));
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int R = 64 * wr + 32 * i + li;
+        const int sw = (R >> 1) & 3;
+        const unsigned char* xb = slot + P::TH + R * 64;
+        const f16x8 bh = *reinterpret_cast<const f16x8*>(xb + (((2 * h) ^ sw) << 4));
+        const f16x8 bl = *reinterpret_cast<const f16x8*>(xb + (((2 * h + 1) ^ sw) << 4));
+#pragma unroll
+        for (int cb = 0; cb < NBW; ++cb) {
+          acc[i][cb] = mfma32x32x16h(ah[cb], bl, acc[i][cb]);
+          acc[i][cb] = mfma32x32x16h(al[cb], bh, acc[i][cb]);
+          acc[i][cb] = mfma32x32x16h(ah[cb], bh, acc[i][cb]);
+        }
+      }
+    }
+
+    // ---- epilogue (eq. entrywise-fusion) on rows row0 + 64 wr + 32 i + li ----
+    // blocks (i, cb) in order; the U loads of the next block are issued before
+    // the arithmetic of the current one (scheduling barriers keep it that way)
+    f32x4 ubuf[2][4];
+    auto load_u = [&](int bi, f32x4 (&dst)[4]) {
+      const int i = bi / NBW, cb = bi - (bi / NBW) * NBW;
+      const int64_t pt = row0 + 64 * wr + 32 * i + li;
+      const float* urow = B.U + (pt < n ? pt : 0) * (int64_t)r;
+      const int cbase = (P::RC / 2) * cw + 32 * cb;
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int c = cbase + 8 * qd + 4 * h;
+        dst[qd] = *reinterpret_cast<const f32x4*>(urow + (c < r ? c : 0));
+      }
+    };
+    // opaque zero offset: the p and s addresses are formed per tile rather than
+    // held in registers across the loop
+    int lds_off = 0;
+    asm volatile("" : "+v"(lds_off));
+    const float* psl = ps + lds_off;
+    const float* ssl = ss + lds_off;
+    // per-lane column offsets and masks are likewise formed per tile (an opaque lane id)
+    int lane_o = lane;
+    asm volatile("" : "+v"(lane_o));
+    const int h = lane_o >> 5, li = lane_o & 31;
+    __builtin_amdgcn_sched_barrier(0);
+    load_u(0, ubuf[0]);
+    float yb2[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int64_t pt = row0 + 64 * wr + 32 * i + li;
+      yb2[i] = pt < n ? B.ybar[pt] : 0.f;
+    }
+#pragma unroll
+    for (int bi = 0; bi < 2 * NBW; ++bi) {
+      const int i = bi / NBW, cb = bi - (bi / NBW) * NBW;
+      __builtin_amdgcn_sched_barrier(0);
+      if (bi + 1 < 2 * NBW) load_u(bi + 1, ubuf[(bi + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+      const int64_t pt = row0 + 64 * wr + 32 * i + li;
+      const bool vpt = pt < n;
+      float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
+      const float yb = yb2[i];
+      const int cbase = (P::RC / 2) * cw + 32 * cb;
+      float wv[16];
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int c = cbase + 8 * qd + 4 * h;
+        const bool ok = vpt && c < r;  // r % 4 == 0: four columns valid together
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+        const f32x4 sv = *reinterpret_cast<const f32x4*>(ssl + c);
+        const f32x4 uv = ubuf[bi & 1][qd];
+        const float ue[4] = {uv.x, uv.y, uv.z, uv.w};
+        const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+        const float se[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float uu = ok ? ue[e] * cf : 0.f;
+          float t = fmaf(two_alpha_s, acc[i][cb][4 * qd + e], uu);
+          t = fmaf(neg_alpha, yb * pe[e], t);
+          t = fmaf(neg_alpha, se[e], t);
+          float w = fmaxf(t, 0.f);
+          if (!ok) w = 0.f;
+          wv[4 * qd + e] = w;
+          const double wd = (double)w, ud = (double)uu;
+          sa = fma(wd, wd, sa);
+          sb = fma(ud, ud, sb);
+          sh = fma(wd, ud, sh);
+        }
+        const f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
+        *reinterpret_cast<f32x4*>(ok ? (urow + c) : B.dump) = o;
+      }
+      reduce_scatter<16, 16>(wv, li);
+      colacc[cb] += (double)wv[0];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // ---- statistics of this workgroup ----
+  __syncthreads();
+  for (int c = tid; c < 2 * P::RC; c += kPBThreads) colred[c] = 0.0;
+  __syncthreads();
+#pragma unroll
+  for (int cb = 0; cb < NBW; ++cb) {
+    const double v = colacc[cb] + shfl_xor_d(colacc[cb], 1);
+    if ((li & 1) == 0) {
+      const int col = (P::RC / 2) * cw + 32 * cb + 8 * (base >> 2) + 4 * h + (base & 3);
+      colred[wr * P::RC + col] = v;
+    }
+  }
+  __syncthreads();
+  double* out = B.b_part + (int64_t)blockIdx.x * (4 + g.r32);
+  for (int c = tid; c < g.r32; c += kPBThreads) out[4 + c] = colred[c] + colred[P::RC + c];
+  const double ta = block_sum_d(sa, dred);
+  const double tb2 = block_sum_d(sb, dred);
+  const double th = block_sum_d(sh, dred);
+  if (tid == 0) {
+    out[0] = ta;
+    out[1] = tb2;
+    out[2] = th;
+    out[3] = 0.0;
+  }
+}
+
+// ===========================================================================
+// Split storage of Xhat for the panel kernels: every 32 bytes (8 features) hold
+// the 8 fp16 hi halves, then the 8 lo halves, of x * x_scale.
+// ===========================================================================
+__global__ __launch_bounds__(kThreads) void k_split_x8(Bufs B, int64_t units) {
+  const float s = B.ctl->x_scale;
+  for (int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x; u < units; u += (int64_t)gridDim.x * kThreads) {
+    f32x4* p = reinterpret_cast<f32x4*>(B.X) + 2 * u;
+    const f32x4 a = p[0], b = p[1];
+    const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    f16x8 hi, lo;
+    split_f16(x, s, hi, lo);
+    p[0] = __builtin_bit_cast(f32x4, hi);
+    p[1] = __builtin_bit_cast(f32x4, lo);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+template <int NBW>
+static hipError_t pass_a_panel_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  constexpr int lds = PanelA<NBW>::LDS;
+  static_assert(lds <= (160 << 10), "LDS");
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_a_panel<NBW>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pass_a_panel<NBW>, dim3(g.GPA), dim3(kPAThreads), lds, st, g, b, a);
+  return hipGetLastError();
+}
+
+template <int NBW>
+static hipError_t pass_b_panel_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  constexpr int lds = PanelB<NBW>::LDS;
+  static_assert(lds <= (80 << 10), "two workgroups per compute unit");
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_b_panel<NBW>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pass_b_panel<NBW>, dim3(g.GB), dim3(kPBThreads), lds, st, g, b, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_pass_a_panel(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  switch (g.pnbw) {
+    case 1: return pass_a_panel_launch<1>(g, b, a, st);
+    case 2: return pass_a_panel_launch<2>(g, b, a, st);
+    case 4: return pass_a_panel_launch<4>(g, b, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_theta_split_panel(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int RC = 64 * g.pnbw;
+  const int64_t recs = (int64_t)((g.d + 15) / 16) * RC;
+  hipLaunchKernelGGL(k_theta_split_panel, dim3((unsigned)((recs + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                     st, g, b, RC);
+  return hipGetLastError();
+}
+
+hipError_t launch_pass_b_panel(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  switch (g.pnbw) {
+    case 1: return pass_b_panel_launch<1>(g, b, a, st);
+    case 2: return pass_b_panel_launch<2>(g, b, a, st);
+    case 4: return pass_b_panel_launch<4>(g, b, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_split_x8(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int64_t units = g.n * (int64_t)g.d / 8;  // d % 8 == 0
+  hipLaunchKernelGGL(k_split_x8, dim3(4096), dim3(kThreads), 0, st, b, units);
+  return hipGetLastError();
+}
+
+int panel_lds_a(int nbw) {
+  return nbw == 1 ? PanelA<1>::LDS : nbw == 2 ? PanelA<2>::LDS : PanelA<4>::LDS;
+}
+
+}  // namespace nlr

@@ -131,6 +131,29 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   }
   g.vec_x = (d % 4 == 0 && aligned16) ? 1 : 0;
   g.vec_u = (r % 4 == 0 && aligned16) ? 1 : 0;
+  // finish pass of the generic form: no Theta partials, so a grid for the rows alone
+  g.GAF = g.a_rows ? g.GA : (int32_t)(g.tilesA < 1024 ? g.tilesA : 1024);
+  // split-fp16 panel form: the shapes the single-pass and resident kernels do not take
+  g.panel = 0;
+  if (split && !g.fused && !g.split_b && aligned16 && d % 8 == 0 && r % 4 == 0 && r <= kMaxR) {
+    g.panel = 1;
+    g.pnbw = g.NB >= 2 ? g.NB / 2 : 1;
+    g.pfb = (d + 255) / 256;
+    // one 8-wave workgroup per compute unit; the feature blocks of a split on one XCD
+    int64_t ps = 8 * (256 / (8 * g.pfb));
+    const int64_t cap = n / 64 > 1 ? n / 64 : 1;  // at least four 16-row stages per split
+    if (ps > cap) ps = cap;
+    if (ps < 1) ps = 1;
+    g.PS = (int32_t)ps;
+    g.GPA = 8 * g.pfb * ((g.PS + 7) / 8);
+    g.tilesP = (n + 127) / 128;
+    g.GB = (int32_t)(g.tilesP < 512 ? g.tilesP : 512);  // two 4-wave workgroups per compute unit
+    g.SB = (g.GB + 31) / 32;
+    // |u| <= sqrt(K) for U in Omega (||U||_F^2 = K); 1% margin for rounding
+    int e2;
+    (void)std::frexp(1.01 * std::sqrt((double)K), &e2);
+    g.su = (float)std::ldexp(1.0, 15 - e2);
+  }
   return g;
 }
 
@@ -192,20 +215,28 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.s = reinterpret_cast<float*>(take(r32 * 4));
   b.th2_part = reinterpret_cast<double*>(take((size_t)g.RT * 8));
   b.b_part = reinterpret_cast<double*>(take((size_t)g.GB * (4 + r32) * 8));
-  b.a_part = reinterpret_cast<double*>(take((size_t)g.GA * (4 + r32) * 8));
+  int64_t arows = g.GA > g.GAF ? g.GA : g.GAF;
+  if (g.panel && g.PS > arows) arows = g.PS;
+  b.a_part = reinterpret_cast<double*>(take((size_t)arows * (4 + r32) * 8));
   const size_t segs = (size_t)(g.SA > g.SAF ? g.SA : g.SAF);
   b.seg_theta = reinterpret_cast<double*>(take(segs * g.d32 * r32 * 8));
   b.seg_a = reinterpret_cast<double*>(take((size_t)g.SA * (4 + r32) * 8));
   b.seg_b = reinterpret_cast<double*>(take((size_t)g.SB * (4 + r32) * 8));
   b.i_xbar = reinterpret_cast<double*>(take(d * 8));
   b.dump = reinterpret_cast<float*>(take(256));
+  b.thmax_part = reinterpret_cast<float*>(take((size_t)g.RT * 4));
+  if (g.panel) {
+    b.ybar = reinterpret_cast<float*>(take((size_t)g.n * 4));
+    b.theta_split = take((size_t)((g.d + 15) / 16) * 64 * g.pnbw * 64);
+  }
   b.s_C = reinterpret_cast<double*>(take(d * d * 8));
   b.s_M = reinterpret_cast<double*>(take(d * (size_t)g.r * 8));
   b.s_CM = reinterpret_cast<double*>(take(d * (size_t)g.r * 8));
   b.s_G = reinterpret_cast<double*>(take((size_t)g.r * g.r * 8));
   b.s_T = reinterpret_cast<double*>(take(d * (size_t)g.r * 8));
   // union: pass-A Theta partials | init temporaries
-  const size_t prow = (size_t)(g.GA > g.GB ? g.GA : g.GB);  // pass A or fused pass B partials
+  size_t prow = (size_t)(g.GA > g.GB ? g.GA : g.GB);  // pass A or fused pass B partials
+  if (g.panel && (size_t)g.PS > prow) prow = (size_t)g.PS;
   const size_t u_iter = align256(prow * g.d32 * r32 * 4);
   size_t u_init = 0;
   u_init += align256((size_t)g.GI * d * 8);            // colsum
@@ -376,6 +407,20 @@ static nlr_status enqueue_iteration(nlr_ctx* c) {
     c->pending = true;
     return NLR_OK;
   }
+  if (c->g.panel) {
+    // split-fp16 panel products (large d x r): pass A (with the row work, ybar
+    // stored), Theta and its split operand, control, pass B, control
+    LAUNCH(KK_PASS_A, launch_pass_a_panel(c->g, c->b, a, c->stream));
+    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta_rows(c->g, c->b, c->g.PS, c->g.SA, false, c->stream));
+    LAUNCH(KK_REDUCE_THETA, launch_theta_split_panel(c->g, c->b, c->stream));
+    LAUNCH(KK_CTL_A, launch_seg_a_rows(c->g, c->b, c->g.PS, false, c->stream));
+    LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
+    LAUNCH(KK_PASS_B, launch_pass_b_panel(c->g, c->b, a, c->stream));
+    LAUNCH(KK_CTL_B, launch_seg_b(c->g, c->b, c->stream));
+    LAUNCH(KK_CTL_B, launch_ctl_b(c->g, c->b, a, c->stream));
+    c->pending = true;
+    return NLR_OK;
+  }
   LAUNCH(KK_PASS_A, launch_pass_a(c->g, c->b, a, false, c->stream));
   LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, false, c->stream));
   LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
@@ -421,10 +466,12 @@ size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r) {
   // with the iteration structure (two passes or fused): cover all of them
   size_t m = 0;
   for (int al = 0; al < 2; ++al)
-    for (int fu = 0; fu < 2; ++fu) {
-      const size_t s = carve_workspace(make_geometry(n, d, r, 1, al != 0, false, fu != 0), nullptr, nullptr);
-      if (s > m) m = s;
-    }
+    for (int fu = 0; fu < 2; ++fu)
+      for (int sp = 0; sp < 2; ++sp) {
+        const size_t s =
+            carve_workspace(make_geometry(n, d, r, 1, al != 0, sp != 0, fu != 0), nullptr, nullptr);
+        if (s > m) m = s;
+      }
   return m;
 }
 
@@ -445,7 +492,7 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   const bool split = (flags & NLR_INIT_SPLIT_F16) != 0;
   const bool fused = (flags & NLR_INIT_TWO_PASS) == 0;
   const Geometry g0 = make_geometry(n, d, r, K, aligned16, split, fused);
-  if (split && !g0.split_b) return NLR_EUNSUPPORTED;
+  if (split && !g0.split_b && !g0.panel) return NLR_EUNSUPPORTED;
   const size_t need = carve_workspace(g0, nullptr, nullptr);
   if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
 
@@ -511,6 +558,9 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
     if (g.split_b)
       if (launch_split_x(g, b, st) != hipSuccess) return fail(NLR_EHIP);
   }
+  // panel form: both passes read Xhat only as split operands; store it so once
+  if (g.panel)
+    if (launch_split_x8(g, b, st) != hipSuccess) return fail(NLR_EHIP);
   if (read_ctl(c) != NLR_OK) return fail(NLR_EHIP);
   if (c->host_ctl->degenerate) return fail(NLR_EDEGENERATE);
   if (c->host_ctl->breakdown) return fail(NLR_EBREAKDOWN);

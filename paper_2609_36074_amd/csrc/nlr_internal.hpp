@@ -29,7 +29,8 @@ struct alignas(16) DevCtl {
   int64_t pad64;
   float c_f;           // lazy scale of the factor buffer (1 when materialised)
   float x_scale;       // power of two keeping |Xhat| x_scale < 2^15 (split-fp16 products)
-  int32_t pad_i0, pad_i1;
+  float th_scale;      // power of two keeping |Theta| th_scale < 2^15 (panel pass B operand)
+  int32_t pad_i1;
   double a, b, h;      // fused statistics of the latest primal step
   double Delta;        // squared movement estimate
   double delta;        // movement estimate
@@ -90,6 +91,15 @@ struct Geometry {
   int32_t GG;           // row-chunk workgroups of the Gram partials
   int32_t gblk;         // 32-wide blocks of d for the Gram
   int32_t vec_x, vec_u; // 16-byte vector loads allowed on X / U rows
+  int32_t GAF;          // workgroups of the finish pass (generic pass A form)
+  // split-fp16 panel form (large d x r, two passes)
+  int32_t panel;        // 1: k_pass_a_panel / k_pass_b_panel iteration
+  int32_t pnbw;         // 32-column blocks per column wave (1, 2 or 4): 64 pnbw columns
+  int32_t pfb;          // 256-feature blocks of pass A
+  int32_t PS;           // row splits of pass A
+  int32_t GPA;          // pass A workgroups (8 pfb ceil(PS / 8), same XCD per split)
+  int64_t tilesP;       // 128-row tiles of pass B
+  float su;             // power-of-two scale of U in the split (|u| <= sqrt(K))
 };
 
 // Pointers into caller memory and the workspace.
@@ -110,6 +120,9 @@ struct Bufs {
   double* th2_part;    // RT
   double* b_part;      // GB x (4 + r32): a, b, h, -, column sums
   float* dump;         // 256 bytes that masked-off lanes store to (never read)
+  float* thmax_part;   // RT: per-workgroup max |Theta| of the reduction
+  float* ybar;         // n: ybar of the current iteration (panel form: pass A -> pass B)
+  void* theta_split;   // panel form: split Theta^T chunks, 64 bytes per (16 features, column)
   // init temporaries (alias the pass-A partial region)
   double* i_colsum;    // GI x d
   double* i_xbar;      // d
@@ -186,6 +199,14 @@ hipError_t launch_lab_embed(const Geometry& g, const Bufs& b, const LabScratch& 
 hipError_t launch_lab_pass(const Geometry& g, const Bufs& b, const LabScratch& L, int K, int32_t* labels,
                            int first, hipStream_t st);
 hipError_t launch_labels(const Geometry& g, const Bufs& b, int32_t* labels, hipStream_t st);
+hipError_t launch_pass_a_panel(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_theta_split_panel(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_pass_b_panel(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_split_x8(const Geometry& g, const Bufs& b, hipStream_t st);
+// a_part rows written by the latest producer (pass A grid, finish grid or panel splits)
+hipError_t launch_seg_a_rows(const Geometry& g, const Bufs& b, int64_t rows, bool finish, hipStream_t st);
+hipError_t launch_reduce_theta_rows(const Geometry& g, const Bufs& b, int64_t rows, int nseg, bool scaled,
+                                    hipStream_t st);
 
 // ---- device helpers ----
 typedef float f32x4 __attribute__((ext_vector_type(4)));

@@ -88,9 +88,14 @@ def test_init_argument_errors(lib):
     # split-fp16 products: shapes and alignments outside the supported set
     S = nlr.NLR_INIT_SPLIT_F16
     assert _init(lib, flags=S, d=13)[0] == nlr.NLR_EUNSUPPORTED                      # d % 4 != 0
-    assert _init(lib, flags=S, d=132)[0] == nlr.NLR_EUNSUPPORTED                     # d > 128
-    assert _init(lib, flags=S, r=68, K=4)[0] == nlr.NLR_EUNSUPPORTED                 # r > 64
+    assert _init(lib, flags=S, d=132)[0] == nlr.NLR_EUNSUPPORTED                     # d > 128, d % 8 != 0
+    assert _init(lib, flags=S, d=136, r=10, K=4)[0] == nlr.NLR_EUNSUPPORTED          # d > 128, r % 4 != 0
+    assert _init(lib, flags=S, r=66, K=4)[0] == nlr.NLR_EUNSUPPORTED                 # r > 64, r % 4 != 0
     assert _init(lib, flags=S | nlr.NLR_INIT_TWO_PASS, r=10, K=4)[0] == nlr.NLR_EUNSUPPORTED  # r % 4 != 0
+    # panel form (d > 128 or r > 64 with d % 8 == 0, r % 4 == 0): supported, reaches the workspace check
+    for kw in (dict(d=136), dict(r=68, K=4), dict(d=768, r=256, K=256, n=3000)):
+        st, ctx = _init(lib, flags=S, ws_bytes=1024, **kw)
+        assert st == nlr.NLR_EWORKSPACE and ctx.value is None, kw
     st, _ = _init(lib, flags=S, r=10, K=4, ws_bytes=1024)                            # single pass: fine
     assert st == nlr.NLR_EWORKSPACE
     assert _init(lib, flags=S, X=FAKE + 4)[0] == nlr.NLR_EUNSUPPORTED                # X not 16-byte aligned

@@ -126,3 +126,55 @@ def test_split_matches_fp32_path_closely():
     d = np.abs(Ua - Ub).max() / np.abs(Ua).max()
     log(f"  split vs fp32 after 40 steps: {d:.2e}")
     assert d < U_TOL / 10
+
+
+# ---- panel form: the split products for d > 128 or r > 64 (d % 8 == 0, r % 4 == 0) ----
+@pytest.mark.parametrize("n,d,r,K", [(3001, 136, 8, 4), (2049, 256, 68, 10), (4000, 64, 128, 32),
+                                     (1500, 768, 256, 256), (777, 200, 100, 20), (5000, 520, 36, 9),
+                                     (70, 136, 8, 2), (1200, 8, 96, 5)])
+def test_split_panel_ragged(n, d, r, K):
+    log(f"split panel: n={n} d={d} r={r} K={K}")
+    X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 5 + d)
+    Z = standard_normal_factor(n, r, seed=n + 3 * r).astype(np.float64)
+    _, _, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, onlr.default_step_size(K), 1.0, 6,
+                                                       one_step_tol=True, flags=SPLIT)
+    log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates
+
+
+def _gated_wide():
+    X, _, _ = gaussian_mixture(2000, 136, 4, 25.0, seed=21)
+    Z = standard_normal_factor(2000, 4, seed=22).astype(np.float64)
+    K, beta = 4, 2.0
+    return X, Z, K, beta, 1.8 * onlr.default_step_size(K, beta)
+
+
+def test_split_panel_dual_steps():
+    X, Z, K, beta, alpha = _gated_wide()
+    log("split panel: gated trajectory T=1000 (d = 136)")
+    _, _, traj, obj, bad_gates, one, _, stats = trajectory(X, Z, K, alpha, beta, 1000, eps_d=3e-3, eps_c=1e-7,
+                                                           one_step_tol=True, flags=SPLIT)
+    ngates = sum(s["dual_step"] for s in stats)
+    log(f"  dual steps {ngates}; traj {max(traj):.3e} one {max(one):.3e} obj {max(obj):.3e}")
+    assert ngates > 200
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates, bad_gates
+
+
+def test_split_panel_run_equals_steps_and_deterministic():
+    X, Z, K, beta, alpha = _gated_wide()
+    kw = dict(eps_d=3e-3, eps_c=1e-7, T_min=0, flags=SPLIT)
+    a = make_ctx(X, Z, K, alpha, beta, **kw)
+    b = make_ctx(X, Z, K, alpha, beta, **kw)
+    c = make_ctx(X, Z, K, alpha, beta, **kw)
+    T = 600
+    done, _ = a.run(T)
+    assert done == T
+    for _ in range(T):
+        b.step(with_stats=False)
+    c.run(T)
+    Ua, Ub, Uc = host(a.U), host(b.U), host(c.U)
+    assert np.array_equal(Ua, Ub) and np.array_equal(host(a.y), host(b.y))
+    assert np.array_equal(Ua, Uc) and np.array_equal(host(a.y), host(c.y))
+    assert sum(h["dual_step"] for h in a.history(T)) > 50

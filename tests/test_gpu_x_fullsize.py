@@ -32,7 +32,7 @@ def _need_gpu():
 
 
 # (workload, flags): the bench's product form for each shape (split where supported)
-CASES = [("gmm10m", SPLIT), ("gmm10m", 0), ("gmm50m", 0), ("embed2m", 0)]
+CASES = [("gmm10m", SPLIT), ("gmm10m", 0), ("gmm50m", 0), ("embed2m", SPLIT), ("embed2m", 0)]
 
 
 @pytest.mark.parametrize("workload,flags", CASES)
