@@ -83,7 +83,10 @@ __device__ __forceinline__ double block_sum8_d(double v, double* red) {
 // ===========================================================================
 // Pass A
 // ===========================================================================
-constexpr int kPAStages = 4;    // stages in the LDS ring
+// LDS banks: 64 banks of 4 bytes.  A ds_read_b128 is served 16 lanes at a time
+// and a ds_read_b64_tr_b16 32 lanes at a time (256 bytes each); the swizzles
+// below give every such group 256 distinct bytes.
+constexpr int kPAStages = 3;    // stages in the LDS rings
 constexpr int kPAPts = 16;      // rows (points) per stage = one k-step of the 32x32x16 product
 constexpr int kPAFeat = 256;    // features per workgroup block
 constexpr int kPAThreads = 512;
@@ -93,28 +96,36 @@ struct PanelA {
   static constexpr int RC = 64 * NBW;                 // columns: two column waves x 32 NBW
   static constexpr int XB = kPAPts * kPAFeat * 4;     // Xhat rows of a stage (split, 1 KiB per row)
   static constexpr int UB = kPAPts * RC * 4;          // U rows of a stage (fp32)
-  static constexpr int STAGE = XB + UB;
-  static constexpr int INSTR = STAGE / 1024;          // 1 KiB load instructions per stage
-  static constexpr int OPS = INSTR / 8;               // per wave, at least
-  static constexpr int WS = RC + 16;                  // split slab row stride (halves)
-  static constexpr int SLAB = 2 * kPAPts * WS * 2;    // hi and lo slabs (bytes)
+  static constexpr int XI = XB / 1024;                // 1 KiB load instructions per stage: Xhat
+  static constexpr int UI = UB / 1024;                //                                    U
+  static constexpr int OPS_X = XI / 8;                // Xhat loads per wave and stage (exact)
+  static constexpr int WS = RC + 32;                  // split slab row stride (halves)
+  static constexpr int SLAB = kPAPts * WS * 2;        // one slab (bytes)
   static constexpr int LPP = RC / 8;                  // threads per row in the conversion
-  static constexpr int LDS = kPAStages * STAGE + SLAB + 16 * 8;
-  static_assert(INSTR * 1024 == STAGE, "whole instructions");
-  static_assert(kPAPts * RC * 4 / 1024 * 1024 == UB, "U stage in whole KiB");
+  static constexpr int XR = kPAStages * XB;           // Xhat ring
+  static constexpr int UR = kPAStages * UB;           // U ring
+  static constexpr int LDS = XR + UR + 4 * SLAB + 16 * 8;  // rings, two (hi, lo) slab pairs, reduction
+  static_assert(XI % 8 == 0, "equal Xhat loads per wave");
+  static_assert(UI * 1024 == UB, "U stage in whole KiB");
   static_assert(kPAPts * RC / 8 <= kPAThreads, "one conversion unit per thread");
-  static_assert(kPAPts * RC * 8 <= kPAStages * STAGE, "s combine fits the ring");
+  static_assert(kPAPts * RC * 8 <= XR + UR, "s combine fits the rings");
 };
 
-// 16-byte piece P (= 2 * unit + hi/lo) of row R of a pass-A Xhat stage sits in slot P ^ pa_swz(R).
-__device__ __forceinline__ int pa_swz(int R) { return (R & 1) | ((R & 2) << 1); }
+// 16-byte piece P (= 2 unit + hi/lo) of row R of a pass-A Xhat stage sits in slot P ^ pa_swz(R).
+__device__ __forceinline__ int pa_swz(int R) { return (R & 1) | ((R & 2) << 2); }
 
+// Workgroup (split s, feature block j), 8 waves: wave w holds features 64 (w % 4) .. + 63
+// of the block and column half w / 4.  Stage t covers rows p0 + 16 t ..; its loads
+// (Xhat of stage t, U of stage t + 1) are issued two stages ahead, and the U of
+// stage t + 1 is scaled and split while the matrix cores work on stage t.  The
+// row work of stage t is done by the workgroup with j = t mod (number of blocks),
+// so the feature blocks of a split do equal work and stream the same U rows at
+// about the same time (they share an XCD: workgroup ids congruent mod 8).
 template <int NBW>
 __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_a_panel(
     Geometry g, Bufs B, StepArgs S) {
   using P = PanelA<NBW>;
   if (halted(B.ctl)) return;
-  // workgroup -> (split, feature block): the blocks of a split share blockIdx.x mod 8 (one XCD)
   const int per = 8 * g.pfb;
   const int grp = blockIdx.x / per;
   const int rem = blockIdx.x - grp * per;
@@ -123,21 +134,21 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
   if (sp >= g.PS) return;
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  unsigned char* ring = smem_raw;
-  _Float16* slab_h = reinterpret_cast<_Float16*>(smem_raw + kPAStages * P::STAGE);
-  _Float16* slab_l = slab_h + kPAPts * P::WS;
-  double* dred = reinterpret_cast<double*>(smem_raw + kPAStages * P::STAGE + P::SLAB);
+  unsigned char* xring = smem_raw;
+  unsigned char* uring = smem_raw + P::XR;
+  _Float16* slabs = reinterpret_cast<_Float16*>(smem_raw + P::XR + P::UR);  // [2][hi, lo][16][WS]
+  double* dred = reinterpret_cast<double*>(smem_raw + P::XR + P::UR + 4 * P::SLAB);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
-  const int fw = wave & 3;   // 64-feature group of the block
-  const int cw = wave >> 2;  // column half
+  const int fw = wave & 3;
+  const int cw = wave >> 2;
   const int64_t n = g.n;
   const int d = g.d, r = g.r;
+  const int nfb = g.pfb;
   const float cf = B.ctl->c_f;
   const float su = g.su;
-  const bool rows_work = (fb == 0);
   const bool gate = (S.end_work != 0) && (B.ctl->gate != 0);
   const float gam = S.gamma_f;
 
@@ -145,7 +156,7 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
   const int64_t p1 = (int64_t)(sp + 1) * n / g.PS;
   const int nst = (int)((p1 - p0 + kPAPts - 1) / kPAPts);
 
-  // conversion unit of this thread: row cr of the stage, columns cc .. cc + 7
+  // conversion unit of this thread: row cr of a stage, columns cc .. cc + 7
   const bool conv = tid < kPAPts * P::LPP;
   const int cr = tid / P::LPP;
   const int cc = 8 * (tid - cr * P::LPP);
@@ -165,116 +176,129 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  auto issue = [&](int st) {
-    unsigned char* slot = ring + (st % kPAStages) * P::STAGE;
-    const int64_t rbase = p0 + (int64_t)st * kPAPts;
+  // loads of group t: Xhat of stage t (if t >= 0) and U of stage t + 1 (if it exists)
+  auto issue_group = [&](int t) {
+    int ln = lane;  // opaque: per-lane offsets are formed here, not kept across the loop
+    asm volatile("" : "+v"(ln));
+    if (t >= 0) {
+      unsigned char* xs = xring + (t % kPAStages) * P::XB;
+      const float* xb = B.X + (p0 + (int64_t)t * kPAPts) * (int64_t)d;
+      const int rmax = (int)((p1 - 1) - (p0 + (int64_t)t * kPAPts));
 #pragma unroll
-    for (int q = 0; q < (P::INSTR + 7) / 8; ++q) {
-      const int i = wave + 8 * q;
-      if (i < P::INSTR) {
-        const void* src;
-        if (i < kPAPts) {
-          // Xhat row i of the stage: slot `lane` takes piece lane ^ swz(i)
-          int64_t row = rbase + i;
-          if (row >= p1) row = p1 - 1;
-          const int pc = lane ^ pa_swz(i);
-          int unit = fb * (kPAFeat / 8) + (pc >> 1);
-          if (8 * unit >= d) unit = 0;  // features >= d: any finite data of the row
-          src = B.X + row * (int64_t)d + 8 * unit + 4 * (pc & 1);
-        } else {
-          // U: fp32 rows of RC floats, 16 bytes per lane
-          const int q4 = 64 * (i - kPAPts) + lane;
+      for (int q = 0; q < P::OPS_X; ++q) {
+        const int i = wave + 8 * q;  // Xhat row i of the stage
+        const int R = i < rmax ? i : rmax;
+        const int pc = ln ^ pa_swz(i);
+        int unit = fb * (kPAFeat / 8) + (pc >> 1);
+        if (8 * unit >= d) unit = 0;  // features >= d: any finite data of the row
+        dma16(xb + (R * d + 8 * unit + 4 * (pc & 1)), xs + i * 1024);
+      }
+    }
+    const int tu = t + 1;
+    if (tu < nst) {
+      unsigned char* us = uring + (tu % kPAStages) * P::UB;
+      const float* ub = B.U + (p0 + (int64_t)tu * kPAPts) * (int64_t)r;
+      const int rmax = (int)((p1 - 1) - (p0 + (int64_t)tu * kPAPts));
+#pragma unroll
+      for (int q = 0; q < (P::UI + 7) / 8; ++q) {
+        const int i = wave + 8 * q;
+        if (i < P::UI) {
+          const int q4 = 64 * i + ln;
           const int rr = q4 / (P::RC / 4);
           const int col = 4 * (q4 - rr * (P::RC / 4));
-          int64_t row = rbase + rr;
-          if (row >= p1) row = p1 - 1;
-          src = B.U + row * (int64_t)r + (col < r ? col : 0);
+          const int R = rr < rmax ? rr : rmax;
+          dma16(ub + (R * r + (col < r ? col : 0)), us + i * 1024);
         }
-        dma16(src, slot + i * 1024);
       }
     }
   };
 
-  for (int st = 0; st < kPAStages - 1 && st < nst; ++st) issue(st);
-
-  for (int st = 0; st < nst; ++st) {
-    // this wave's loads of stage st have landed (the later ones may be in flight)
-    const int newer = (nst - 1 - st) < (kPAStages - 2) ? (nst - 1 - st) : (kPAStages - 2);
-    if (newer >= 2) wait_barrier<2 * P::OPS>();
-    else if (newer == 1) wait_barrier<P::OPS>();
-    else wait_barrier<0>();
-    if (st + kPAStages - 1 < nst) issue(st + kPAStages - 1);
-    int slot_off = (st % kPAStages) * P::STAGE;  // opaque: addresses formed per stage
-    asm volatile("" : "+s"(slot_off));
-    const unsigned char* slot = ring + slot_off;
-
-    // ---- U: lazy scale, split into the hi/lo slabs; row work ----
-    if (conv) {
-      const float* ub = reinterpret_cast<const float*>(slot + P::XB) + cr * P::RC + cc;
-      const f32x4 a0 = *reinterpret_cast<const f32x4*>(ub);
-      const f32x4 a1 = *reinterpret_cast<const f32x4*>(ub + 4);
-      const float raw[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      const int64_t row = p0 + (int64_t)st * kPAPts + cr;
-      const bool vrow = row < p1;
-      float u[8];
+  // scale, split and (for this block's share) the row work of stage t's U
+  auto convert = [&](int t) {
+    if (!conv) return;
+    const float* ub = reinterpret_cast<const float*>(uring + (t % kPAStages) * P::UB) + cr * P::RC + cc;
+    const f32x4 a0 = *reinterpret_cast<const f32x4*>(ub);
+    const f32x4 a1 = *reinterpret_cast<const f32x4*>(ub + 4);
+    const float raw[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+    const int64_t row = p0 + (int64_t)t * kPAPts + cr;
+    const bool vrow = row < p1;
+    float u[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) u[e] = (vrow && cc + e < r) ? raw[e] * cf : 0.f;
-      f16x8 hi, lo;
-      split_f16(u, su, hi, lo);
-      *reinterpret_cast<f16x8*>(slab_h + cr * P::WS + cc) = hi;
-      *reinterpret_cast<f16x8*>(slab_l + cr * P::WS + cc) = lo;
-      if (rows_work) {
-        double dot = 0.0;
+    for (int e = 0; e < 8; ++e) u[e] = (vrow && cc + e < r) ? raw[e] * cf : 0.f;
+    f16x8 hi, lo;
+    split_f16(u, su, hi, lo);
+    _Float16* sh = slabs + (t & 1) * 2 * kPAPts * P::WS;
+    *reinterpret_cast<f16x8*>(sh + cr * P::WS + cc) = hi;
+    *reinterpret_cast<f16x8*>(sh + kPAPts * P::WS + cr * P::WS + cc) = lo;
+    if (t % nfb == fb) {
+      double dot = 0.0;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dot += (double)u[e] * (double)pr[e];
+      for (int e = 0; e < 8; ++e) dot += (double)u[e] * (double)pr[e];
 #pragma unroll
-        for (int m = 1; m < P::LPP; m <<= 1) dot += shfl_xor_d(dot, m);
-        if (vrow) {
-          const float q = (float)(dot - 1.0);
-          float yt = B.y[row];
-          const bool lead = (tid - cr * P::LPP) == 0;
-          if (gate) {
-            yt = fmaf(gam, q, yt);
-            if (lead) B.y[row] = yt;
-          }
-          const float ybar = fmaf(gam, q, yt);
-          if (lead) {
-            B.ybar[row] = ybar;
-            qq += (double)q * (double)q;
-            yq += (double)yt * (double)q;
-          }
-#pragma unroll
-          for (int e = 0; e < 8; ++e) s_acc[e] = fma((double)ybar, (double)u[e], s_acc[e]);
+      for (int m = 1; m < P::LPP; m <<= 1) dot += shfl_xor_d(dot, m);
+      if (vrow) {
+        const float q = (float)(dot - 1.0);
+        float yt = B.y[row];
+        const bool lead = (tid - cr * P::LPP) == 0;
+        if (gate) {
+          yt = fmaf(gam, q, yt);
+          if (lead) B.y[row] = yt;
         }
+        const float ybar = fmaf(gam, q, yt);
+        if (lead) {
+          B.ybar[row] = ybar;
+          qq += (double)q * (double)q;
+          yq += (double)yt * (double)q;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s_acc[e] = fma((double)ybar, (double)u[e], s_acc[e]);
       }
     }
-    wait_barrier<63>();  // slabs written (lgkmcnt(0)); vmcnt left as it is
+  };
+
+  // prologue: groups -1 (U of stage 0), 0 and 1; wait for group -1, split U of stage 0
+  constexpr int G = P::OPS_X;  // loads per wave of a group, at least
+  issue_group(-1);
+  if (nst > 0) issue_group(0);
+  if (nst > 1) issue_group(1);
+  if (nst > 1) wait_barrier<2 * G>();
+  else if (nst > 0) wait_barrier<G>();
+  else wait_barrier<0>();
+  convert(0);
+
+  for (int st = 0; st < nst; ++st) {
+    // group st (Xhat of stage st, U of stage st + 1) has landed; slab st & 1 is complete
+    if (st + 1 < nst) wait_barrier<G>();
+    else wait_barrier<0>();
+    if (st + 2 < nst) issue_group(st + 2);
+    if (st + 1 < nst) convert(st + 1);
 
     // ---- Theta block += Xhat_stage^T U_stage ----
-    const _Float16* xs = reinterpret_cast<const _Float16*>(slot);
+    int x_off = (st % kPAStages) * P::XB;  // opaque: addresses formed per stage
+    asm volatile("" : "+s"(x_off));
+    int s_off = (st & 1) * 2 * kPAPts * P::WS;
+    asm volatile("" : "+s"(s_off));
+    const _Float16* xs = reinterpret_cast<const _Float16*>(xring + x_off);
+    const _Float16* slab_h = slabs + s_off;
+    const _Float16* slab_l = slab_h + kPAPts * P::WS;
+    const int gq = lane >> 4, s16 = lane & 15;
+    const int R = 8 * (gq >> 1) + (s16 >> 2);  // and R + 4 (same swizzle)
     f16x8 ah[2], al[2];
-    {
-      const int gq = lane >> 4, s16 = lane & 15;
-      const int R = 8 * (gq >> 1) + (s16 >> 2);  // and R + 4 (same swizzle)
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int fc = 64 * fw + 32 * i + 16 * (gq & 1) + 4 * (s16 & 3);
-        const int u8 = fc >> 3, qd = (fc >> 2) & 1;
-        const int sh = (2 * u8) ^ pa_swz(R), sl = (2 * u8 + 1) ^ pa_swz(R);
-        const _Float16* ph = xs + R * (kPAFeat * 2) + sh * 8 + qd * 4;
-        const _Float16* pl = xs + R * (kPAFeat * 2) + sl * 8 + qd * 4;
-        const pf16x4 h0 = lds_tr16(ph), h1 = lds_tr16(ph + 4 * kPAFeat * 2);
-        const pf16x4 l0 = lds_tr16(pl), l1 = lds_tr16(pl + 4 * kPAFeat * 2);
-        ah[i] = (f16x8){h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
-        al[i] = (f16x8){l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
-      }
+    for (int i = 0; i < 2; ++i) {
+      const int fc = 64 * fw + 32 * i + 16 * (gq & 1) + 4 * (s16 & 3);
+      const int u8 = fc >> 3, qd = (fc >> 2) & 1;
+      const int sh = (2 * u8) ^ pa_swz(R), sl = (2 * u8 + 1) ^ pa_swz(R);
+      const _Float16* ph = xs + R * (kPAFeat * 2) + sh * 8 + qd * 4;
+      const _Float16* pl = xs + R * (kPAFeat * 2) + sl * 8 + qd * 4;
+      const pf16x4 h0 = lds_tr16(ph), h1 = lds_tr16(ph + 4 * kPAFeat * 2);
+      const pf16x4 l0 = lds_tr16(pl), l1 = lds_tr16(pl + 4 * kPAFeat * 2);
+      ah[i] = (f16x8){h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
+      al[i] = (f16x8){l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
     }
 #pragma unroll
     for (int cb = 0; cb < NBW; ++cb) {
-      const int c0 = (P::RC / 2) * cw + 32 * cb;
-      const int gq = lane >> 4, s16 = lane & 15;
-      const int R = 8 * (gq >> 1) + (s16 >> 2);
-      const int c = c0 + 16 * (gq & 1) + 4 * (s16 & 3);
+      const int c = (P::RC / 2) * cw + 32 * cb + 16 * (gq & 1) + 4 * (s16 & 3);
       const _Float16* ph = slab_h + R * P::WS + c;
       const _Float16* pl = slab_l + R * P::WS + c;
       const pf16x4 h0 = lds_tr16(ph), h1 = lds_tr16(ph + 4 * P::WS);
@@ -309,10 +333,10 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
       }
   }
 
-  // ---- row partials: ||q||^2, ytilde^T q, s (fixed order over the rows of a stage) ----
-  if (rows_work) {
-    double* ap = B.a_part + (int64_t)sp * (4 + g.r32);
-    double* sred = reinterpret_cast<double*>(ring);  // kPAPts x RC (the ring is free now)
+  // ---- row partials of this workgroup's share: ||q||^2, ytilde^T q, s ----
+  {
+    double* ap = B.a_part + ((int64_t)sp * nfb + fb) * (4 + g.r32);
+    double* sred = reinterpret_cast<double*>(smem_raw);  // kPAPts x RC (the rings are free now)
     if (conv)
 #pragma unroll
       for (int e = 0; e < 8; ++e) sred[cr * P::RC + cc + e] = s_acc[e];
@@ -352,7 +376,7 @@ struct PanelB {
 
 // Stage k of the Theta image: column c owns 64 bytes = four 16-byte pieces
 // P = 2 hl + j (features 16k + 8j .. 16k + 8j + 7, hl = 0 hi / 1 lo), piece P in
-// slot P ^ ((c >> 1) & 3).
+// slot P ^ ((c >> 2) & 3).
 __global__ __launch_bounds__(kThreads) void k_theta_split_panel(Geometry g, Bufs B, int RC) {
   if (halted(B.ctl)) return;
   __shared__ float red[4];
@@ -385,7 +409,7 @@ __global__ __launch_bounds__(kThreads) void k_theta_split_panel(Geometry g, Bufs
   split_f16(v, sth, h0, l0);
   split_f16(v + 8, sth, h1, l1);
   f16x8* out = reinterpret_cast<f16x8*>(reinterpret_cast<unsigned char*>(B.theta_split) + rec * 64);
-  const int sw = (c >> 1) & 3;
+  const int sw = (c >> 2) & 3;
   out[0 ^ sw] = h0;  // P = 0: hi, features 0..7
   out[1 ^ sw] = h1;  // P = 1: hi, features 8..15
   out[2 ^ sw] = l0;  // P = 2: lo, features 0..7
@@ -395,7 +419,7 @@ __global__ __launch_bounds__(kThreads) void k_theta_split_panel(Geometry g, Bufs
 // ===========================================================================
 // Pass B
 // ===========================================================================
-// Row R of a pass-B Xhat chunk: piece P = 2 unit + hl in slot P ^ ((R >> 1) & 3).
+// Row R of a pass-B Xhat chunk: piece P = 2 unit + hl in slot P ^ ((R >> 2) & 3).
 template <int NBW>
 __global__ __launch_bounds__(kPBThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_b_panel(
     Geometry g, Bufs B, StepArgs S) {
@@ -451,7 +475,7 @@ __global__ __launch_bounds__(kPBThreads) __attribute__((amdgpu_waves_per_eu(2, 2
         src = tb + (i * 1024 + ln * 16);
       } else {
         const int R = 16 * (i - P::TH / 1024) + (ln >> 2);
-        const int pc = (ln & 3) ^ ((R >> 1) & 3);
+        const int pc = (ln & 3) ^ ((R >> 2) & 3);
         const int Rc = R < rmax ? R : rmax;  // rows >= n: the last row (masked later)
         int unit = 2 * ik + (pc >> 1);
         if (8 * unit >= d) unit = 0;  // features >= d meet zero rows of Theta
@@ -505,14 +529,14 @@ __global__ __launch_bounds__(kPBThreads) __attribute__((amdgpu_waves_per_eu(2, 2
 #pragma unroll
       for (int cb = 0; cb < NBW; ++cb) {
         const int c = (P::RC / 2) * cw + 32 * cb + li;
-        const int sw = (c >> 1) & 3;
+        const int sw = (c >> 2) & 3;
         ah[cb] = *reinterpret_cast<const f16x8*>(slot + c * 64 + ((h ^ sw) << 4));
         al[cb] = *reinterpret_cast<const f16x8*>(slot + c * 64 + (((2 + h) ^ sw) << 4));
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int R = 64 * wr + 32 * i + li;
-        const int sw = (R >> 1) & 3;
+        const int sw = (R >> 2) & 3;
         const unsigned char* xb = slot + P::TH + R * 64;
         const f16x8 bh = *reinterpret_cast<const f16x8*>(xb + (((2 * h) ^ sw) << 4));
         const f16x8 bl = *reinterpret_cast<const f16x8*>(xb + (((2 * h + 1) ^ sw) << 4));

@@ -216,7 +216,7 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.th2_part = reinterpret_cast<double*>(take((size_t)g.RT * 8));
   b.b_part = reinterpret_cast<double*>(take((size_t)g.GB * (4 + r32) * 8));
   int64_t arows = g.GA > g.GAF ? g.GA : g.GAF;
-  if (g.panel && g.PS > arows) arows = g.PS;
+  if (g.panel && (int64_t)g.PS * g.pfb > arows) arows = (int64_t)g.PS * g.pfb;  // one row per pass-A workgroup
   b.a_part = reinterpret_cast<double*>(take((size_t)arows * (4 + r32) * 8));
   const size_t segs = (size_t)(g.SA > g.SAF ? g.SA : g.SAF);
   b.seg_theta = reinterpret_cast<double*>(take(segs * g.d32 * r32 * 8));
@@ -413,7 +413,7 @@ static nlr_status enqueue_iteration(nlr_ctx* c) {
     LAUNCH(KK_PASS_A, launch_pass_a_panel(c->g, c->b, a, c->stream));
     LAUNCH(KK_REDUCE_THETA, launch_reduce_theta_rows(c->g, c->b, c->g.PS, c->g.SA, false, c->stream));
     LAUNCH(KK_REDUCE_THETA, launch_theta_split_panel(c->g, c->b, c->stream));
-    LAUNCH(KK_CTL_A, launch_seg_a_rows(c->g, c->b, c->g.PS, false, c->stream));
+    LAUNCH(KK_CTL_A, launch_seg_a_rows(c->g, c->b, (int64_t)c->g.PS * c->g.pfb, false, c->stream));
     LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
     LAUNCH(KK_PASS_B, launch_pass_b_panel(c->g, c->b, a, c->stream));
     LAUNCH(KK_CTL_B, launch_seg_b(c->g, c->b, c->stream));
