@@ -52,9 +52,16 @@ def algorithmic_bytes(kind: str, n: int, d: int, r: int, dual_frac: float = 0.0)
     raise ValueError(kind)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(kernel: str) -> str:
+    """Hash of the sources that define `kernel` (a traffic record is void once they change)."""
+    if kernel.startswith("pass_bf"):
+        files = ("k_fused.hip",)
+    elif kernel.startswith("pass_u"):
+        files = ("k_iter.hip",)
+    else:  # pass_a / pass_b: generic, resident, split and panel forms
+        files = ("k_iter.hip", "k_split.hip", "k_panel.hip")
     h = hashlib.sha256()
-    for f in ("k_iter.hip", "k_split.hip", "k_fused.hip", "k_panel.hip", "k_common.hpp", "nlr_internal.hpp"):
+    for f in files + ("k_common.hpp", "nlr_internal.hpp"):
         with open(os.path.join(ROOT, "paper_2609_36074_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -69,7 +76,7 @@ def load_traffic(kernel: str, workload: str):
     try:
         with open(path) as f:
             t = json.load(f)
-        if t.get("kernel_source_hash") != kernel_source_hash():
+        if t.get("kernel_source_hash") != kernel_source_hash(kernel):
             return None
         return float(t["bytes_per_launch"])
     except Exception:

@@ -103,13 +103,18 @@ enum {
    * range, and v w ~ s_v s_w (hi_v hi_w + hi_v lo_w + lo_v hi_w) accumulated in
    * fp32.  The representation error is about 2^-22 relative per operand, below
    * the TF32 products of the paper's CUTLASS kernel (Appendix C), at about a fifth of the fp32 matrix
-   * work.  Supported for d <= 128, r <= 64, d % 4 == 0 and 16-byte aligned X and
-   * U (and r % 4 == 0 with NLR_INIT_TWO_PASS); other shapes return
-   * NLR_EUNSUPPORTED.  In the single-Xhat-pass form X is left holding Xhat in
-   * split form after nlr_init: each 16 bytes that held 4 consecutive features
-   * hold their 4 fp16 hi halves then their 4 fp16 lo halves of x * s (s a power
-   * of two), so X no longer reads as fp32 (do not pass it to nlr_init again with
-   * NLR_INIT_X_NORMALISED). */
+   * work.  X and U must be 16-byte aligned.  Supported shapes: d <= 128, r <= 64,
+   * d % 4 == 0 (and r % 4 == 0 with NLR_INIT_TWO_PASS), run in the
+   * single-Xhat-pass form; and, for every other shape with d % 8 == 0,
+   * r % 4 == 0 and r <= 256, the two-pass panel form (LDS-tiled products, both
+   * split; ybar is kept in the workspace between the passes).  Other shapes
+   * return NLR_EUNSUPPORTED.  X is left holding Xhat in split form after
+   * nlr_init, so it no longer reads as fp32 (do not pass it to nlr_init again
+   * with NLR_INIT_X_NORMALISED): in the single-Xhat-pass form each 16 bytes that
+   * held 4 consecutive features hold their 4 fp16 hi halves then their 4 fp16 lo
+   * halves of x * s (s a power of two); in the panel form each 32 bytes that held
+   * 8 features hold their 8 hi halves then their 8 lo halves.  U_0 must lie in
+   * Omega (|u| <= sqrt(K)); nlr_init projects it unless NLR_INIT_U_IN_OMEGA. */
   NLR_INIT_SPLIT_F16 = 8,
   /* Use the two-pass iteration (pass A: Theta = Xhat^T U with the row work; pass
    * B: Xhat Theta with the fused epilogue) even where the single-Xhat-pass form
