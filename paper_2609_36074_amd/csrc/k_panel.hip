@@ -47,6 +47,10 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 __device__ __forceinline__ void dma16(const void* src, unsigned char* lds_wave_base) {
   __builtin_amdgcn_global_load_lds(src, (lds_void_t*)lds_wave_base, 16, 0, 0);
 }
+// 4 bytes per lane: lane l writes lds_wave_base + 4 l.
+__device__ __forceinline__ void dma4(const void* src, unsigned char* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void_t*)lds_wave_base, 4, 0, 0);
+}
 
 // Wait until at most N vector memory operations of this wave are outstanding and
 // its LDS operations are done, then a workgroup barrier.  Written as one asm
@@ -86,7 +90,8 @@ __device__ __forceinline__ double block_sum8_d(double v, double* red) {
 // LDS banks: 64 banks of 4 bytes.  A ds_read_b128 is served 16 lanes at a time
 // and a ds_read_b64_tr_b16 32 lanes at a time (256 bytes each); the swizzles
 // below give every such group 256 distinct bytes.
-constexpr int kPAStages = 3;    // stages in the LDS rings
+constexpr int kPAXStages = 4;   // Xhat ring: loads three stages ahead
+constexpr int kPAUStages = 5;   // U ring: a slot also holds its stage's split U until it is read
 constexpr int kPAPts = 16;      // rows (points) per stage = one k-step of the 32x32x16 product
 constexpr int kPAFeat = 256;    // features per workgroup block
 constexpr int kPAThreads = 512;
@@ -95,32 +100,125 @@ template <int NBW>
 struct PanelA {
   static constexpr int RC = 64 * NBW;                 // columns: two column waves x 32 NBW
   static constexpr int XB = kPAPts * kPAFeat * 4;     // Xhat rows of a stage (split, 1 KiB per row)
-  static constexpr int UB = kPAPts * RC * 4;          // U rows of a stage (fp32)
+  static constexpr int UB = kPAPts * RC * 4;          // U rows of a stage (fp32, then split in place)
+  static constexpr int UBP = UB + kPAPts * 4;         // U slot: the U rows, then ytilde of the rows
   static constexpr int XI = XB / 1024;                // 1 KiB load instructions per stage: Xhat
   static constexpr int UI = UB / 1024;                //                                    U
   static constexpr int OPS_X = XI / 8;                // Xhat loads per wave and stage (exact)
-  static constexpr int WS = RC + 32;                  // split slab row stride (halves)
-  static constexpr int SLAB = kPAPts * WS * 2;        // one slab (bytes)
   static constexpr int LPP = RC / 8;                  // threads per row in the conversion
-  static constexpr int XR = kPAStages * XB;           // Xhat ring
-  static constexpr int UR = kPAStages * UB;           // U ring
-  static constexpr int LDS = XR + UR + 4 * SLAB + 16 * 8;  // rings, two (hi, lo) slab pairs, reduction
+  static constexpr int XR = kPAXStages * XB;          // Xhat ring
+  static constexpr int UR = kPAUStages * UBP;         // U ring
+  static constexpr int LDS = XR + UR + 16 * 8;        // rings, reduction
   static_assert(XI % 8 == 0, "equal Xhat loads per wave");
   static_assert(UI * 1024 == UB, "U stage in whole KiB");
+  static_assert(RC / 4 >= 16, "a U row spans at least 16 pieces (swizzle)");
   static_assert(kPAPts * RC / 8 <= kPAThreads, "one conversion unit per thread");
   static_assert(kPAPts * RC * 8 <= XR + UR, "s combine fits the rings");
 };
 
-// 16-byte piece P (= 2 unit + hi/lo) of row R of a pass-A Xhat stage sits in slot P ^ pa_swz(R).
+// 16-byte piece P of row R of a pass-A stage sits in slot P ^ pa_swz(R).  Xhat rows:
+// P = 2 unit + (0 hi, 1 lo) of 8 features.  U rows: first P = fp32 columns 4P .. 4P + 3,
+// then, split in place, P = 2 unit + (0 hi, 1 lo) of columns 8 unit .. 8 unit + 7 (the
+// two pieces of a unit stay in the two slots that held its fp32 values).
 __device__ __forceinline__ int pa_swz(int R) { return (R & 1) | ((R & 2) << 2); }
+
+// LDS byte address of this lane's first transposing read of a 32x32x16 operand with
+// k = row, from a pass-A stage image at byte offset `base` (rows of `row_bytes`, pieces
+// swizzled as above); the second read is 4 rows further.  Together they give lane l
+// T[8 (l/32) + e][c0 + l%32] (hi or lo), e = 0..7.
+__device__ __forceinline__ uint32_t pa_operand_addr(uint32_t base, int row_bytes, int c0, int hl, int lane) {
+  const int gq = lane >> 4, s16 = lane & 15;
+  const int R = 8 * (gq >> 1) + (s16 >> 2);  // and R + 4 (same swizzle)
+  const int c = c0 + 16 * (gq & 1) + 4 * (s16 & 3);
+  const int slot = (2 * (c >> 3) + hl) ^ pa_swz(R);
+  return base + (uint32_t)(R * row_bytes + slot * 16 + ((c >> 2) & 1) * 8);
+}
+
+__device__ __forceinline__ f16x8 pa_join(pf16x4 a, pf16x4 b) {
+  return (f16x8){a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+// The transposing reads of one pass-A stage, written as assembly: the compiler treats
+// the ds_read_b64_tr_b16 builtin as a possible reader of every global-to-LDS load in
+// flight and waits for all of them first, which would empty the load ring every stage.
+// One statement issues the reads and waits for their data (lgkmcnt(0)), so its outputs
+// are defined only when they hold the data.  X: xa[i][hl] (8 reads, rows 4 apart = XO
+// bytes); U: ua[cb][hl] (4 NBW reads, UO bytes).
+#define PA_TR(o, a) "ds_read_b64_tr_b16 %" #o ", %" #a "\n\t"
+#define PA_TRO(o, a, f) "ds_read_b64_tr_b16 %" #o ", %" #a " offset:%" #f "\n\t"
+template <int NBW, int XO, int UO>
+__device__ __forceinline__ void pa_stage_reads(const uint32_t (&xa)[2][2], const uint32_t (&ua)[NBW][2],
+                                               f16x8 (&ah)[2], f16x8 (&al)[2], f16x8 (&bh)[NBW],
+                                               f16x8 (&bl)[NBW]) {
+  pf16x4 x0, x1, x2, x3, x4, x5, x6, x7;
+  if constexpr (NBW == 1) {
+    pf16x4 u0, u1, u2, u3;
+    asm volatile(PA_TR(0, 12) PA_TRO(1, 12, 18) PA_TR(2, 13) PA_TRO(3, 13, 18)
+                 PA_TR(4, 14) PA_TRO(5, 14, 18) PA_TR(6, 15) PA_TRO(7, 15, 18)
+                 PA_TR(8, 16) PA_TRO(9, 16, 19) PA_TR(10, 17) PA_TRO(11, 17, 19)
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3), "=&v"(x4), "=&v"(x5), "=&v"(x6), "=&v"(x7),
+                   "=&v"(u0), "=&v"(u1), "=&v"(u2), "=&v"(u3)
+                 : "v"(xa[0][0]), "v"(xa[0][1]), "v"(xa[1][0]), "v"(xa[1][1]), "v"(ua[0][0]), "v"(ua[0][1]),
+                   "n"(XO), "n"(UO)
+                 : "memory");
+    bh[0] = pa_join(u0, u1);
+    bl[0] = pa_join(u2, u3);
+  } else {
+    // the Xhat reads are issued first and complete with the U reads' wait below
+    asm volatile(PA_TR(0, 8) PA_TRO(1, 8, 12) PA_TR(2, 9) PA_TRO(3, 9, 12)
+                 PA_TR(4, 10) PA_TRO(5, 10, 12) PA_TR(6, 11) PA_TRO(7, 11, 12)
+                 : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3), "=&v"(x4), "=&v"(x5), "=&v"(x6), "=&v"(x7)
+                 : "v"(xa[0][0]), "v"(xa[0][1]), "v"(xa[1][0]), "v"(xa[1][1]), "n"(XO)
+                 : "memory");
+    if constexpr (NBW == 2) {
+      pf16x4 u0, u1, u2, u3, u4, u5, u6, u7;
+      asm volatile(PA_TR(0, 16) PA_TRO(1, 16, 20) PA_TR(2, 17) PA_TRO(3, 17, 20)
+                   PA_TR(4, 18) PA_TRO(5, 18, 20) PA_TR(6, 19) PA_TRO(7, 19, 20)
+                   "s_waitcnt lgkmcnt(0)"
+                   : "=&v"(u0), "=&v"(u1), "=&v"(u2), "=&v"(u3), "=&v"(u4), "=&v"(u5), "=&v"(u6), "=&v"(u7),
+                     "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3), "+v"(x4), "+v"(x5), "+v"(x6), "+v"(x7)
+                   : "v"(ua[0][0]), "v"(ua[0][1]), "v"(ua[1][0]), "v"(ua[1][1]), "n"(UO)
+                   : "memory");
+      bh[0] = pa_join(u0, u1);
+      bl[0] = pa_join(u2, u3);
+      bh[1] = pa_join(u4, u5);
+      bl[1] = pa_join(u6, u7);
+    } else {
+      static_assert(NBW == 4, "NBW");
+      pf16x4 u[16];
+      asm volatile(PA_TR(0, 24) PA_TRO(1, 24, 32) PA_TR(2, 25) PA_TRO(3, 25, 32)
+                   PA_TR(4, 26) PA_TRO(5, 26, 32) PA_TR(6, 27) PA_TRO(7, 27, 32)
+                   PA_TR(8, 28) PA_TRO(9, 28, 32) PA_TR(10, 29) PA_TRO(11, 29, 32)
+                   PA_TR(12, 30) PA_TRO(13, 30, 32) PA_TR(14, 31) PA_TRO(15, 31, 32)
+                   "s_waitcnt lgkmcnt(0)"
+                   : "=&v"(u[0]), "=&v"(u[1]), "=&v"(u[2]), "=&v"(u[3]), "=&v"(u[4]), "=&v"(u[5]),
+                     "=&v"(u[6]), "=&v"(u[7]), "=&v"(u[8]), "=&v"(u[9]), "=&v"(u[10]), "=&v"(u[11]),
+                     "=&v"(u[12]), "=&v"(u[13]), "=&v"(u[14]), "=&v"(u[15]),
+                     "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3), "+v"(x4), "+v"(x5), "+v"(x6), "+v"(x7)
+                   : "v"(ua[0][0]), "v"(ua[0][1]), "v"(ua[1][0]), "v"(ua[1][1]), "v"(ua[2][0]),
+                     "v"(ua[2][1]), "v"(ua[3][0]), "v"(ua[3][1]), "n"(UO)
+                   : "memory");
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        bh[cb] = pa_join(u[4 * cb + 0], u[4 * cb + 1]);
+        bl[cb] = pa_join(u[4 * cb + 2], u[4 * cb + 3]);
+      }
+    }
+  }
+  ah[0] = pa_join(x0, x1);
+  al[0] = pa_join(x2, x3);
+  ah[1] = pa_join(x4, x5);
+  al[1] = pa_join(x6, x7);
+}
 
 // Workgroup (split s, feature block j), 8 waves: wave w holds features 64 (w % 4) .. + 63
 // of the block and column half w / 4.  Stage t covers rows p0 + 16 t ..; its loads
-// (Xhat of stage t, U of stage t + 1) are issued two stages ahead, and the U of
-// stage t + 1 is scaled and split while the matrix cores work on stage t.  The
-// row work of stage t is done by the workgroup with j = t mod (number of blocks),
-// so the feature blocks of a split do equal work and stream the same U rows at
-// about the same time (they share an XCD: workgroup ids congruent mod 8).
+// (Xhat of stage t, U of stage t + 1) are issued three stages ahead, and the U of
+// stage t + 1 is scaled and split (in its ring slot) while the matrix cores work on
+// stage t.  The row work of stage t is done by the workgroup with j = t mod (number
+// of blocks), so the feature blocks of a split do equal work and stream the same U
+// rows at about the same time (they share an XCD: workgroup ids congruent mod 8).
 template <int NBW>
 __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_a_panel(
     Geometry g, Bufs B, StepArgs S) {
@@ -136,8 +234,10 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
   extern __shared__ __align__(16) unsigned char smem_raw[];
   unsigned char* xring = smem_raw;
   unsigned char* uring = smem_raw + P::XR;
-  _Float16* slabs = reinterpret_cast<_Float16*>(smem_raw + P::XR + P::UR);  // [2][hi, lo][16][WS]
-  double* dred = reinterpret_cast<double*>(smem_raw + P::XR + P::UR + 4 * P::SLAB);
+  double* dred = reinterpret_cast<double*>(smem_raw + P::XR + P::UR);
+  // LDS byte address of the dynamic area (operand of the assembly reads)
+  const uint32_t lds_base =
+      (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem_raw);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -156,10 +256,11 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
   const int64_t p1 = (int64_t)(sp + 1) * n / g.PS;
   const int nst = (int)((p1 - p0 + kPAPts - 1) / kPAPts);
 
-  // conversion unit of this thread: row cr of a stage, columns cc .. cc + 7
+  // conversion unit of this thread: row cr of a stage, columns 8 cu .. 8 cu + 7
   const bool conv = tid < kPAPts * P::LPP;
   const int cr = tid / P::LPP;
-  const int cc = 8 * (tid - cr * P::LPP);
+  const int cu = tid - cr * P::LPP;
+  const int cc = 8 * cu;
   float pr[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) pr[e] = (conv && cc + e < g.r32) ? B.p[cc + e] : 0.f;
@@ -181,7 +282,7 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
     int ln = lane;  // opaque: per-lane offsets are formed here, not kept across the loop
     asm volatile("" : "+v"(ln));
     if (t >= 0) {
-      unsigned char* xs = xring + (t % kPAStages) * P::XB;
+      unsigned char* xs = xring + (t % kPAXStages) * P::XB;
       const float* xb = B.X + (p0 + (int64_t)t * kPAPts) * (int64_t)d;
       const int rmax = (int)((p1 - 1) - (p0 + (int64_t)t * kPAPts));
 #pragma unroll
@@ -196,29 +297,38 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
     }
     const int tu = t + 1;
     if (tu < nst) {
-      unsigned char* us = uring + (tu % kPAStages) * P::UB;
+      unsigned char* us = uring + (tu % kPAUStages) * P::UBP;
       const float* ub = B.U + (p0 + (int64_t)tu * kPAPts) * (int64_t)r;
       const int rmax = (int)((p1 - 1) - (p0 + (int64_t)tu * kPAPts));
 #pragma unroll
       for (int q = 0; q < (P::UI + 7) / 8; ++q) {
         const int i = wave + 8 * q;
         if (i < P::UI) {
-          const int q4 = 64 * i + ln;
+          const int q4 = 64 * i + ln;               // 16-byte slot of the stage
           const int rr = q4 / (P::RC / 4);
-          const int col = 4 * (q4 - rr * (P::RC / 4));
+          const int col = 4 * ((q4 - rr * (P::RC / 4)) ^ pa_swz(rr));  // its piece's columns
           const int R = rr < rmax ? rr : rmax;
           dma16(ub + (R * r + (col < r ? col : 0)), us + i * 1024);
         }
       }
+      // ytilde of the stage's rows (the row work reads it from LDS: a global load there
+      // would have to wait for every ring load issued before it)
+      if (wave == 0 && ln < kPAPts) {
+        const int R = ln < rmax ? ln : rmax;
+        dma4(B.y + (p0 + (int64_t)tu * kPAPts + R), us + P::UB);
+      }
     }
   };
 
-  // scale, split and (for this block's share) the row work of stage t's U
+  // scale and split stage t's U in place; this block's share of the row work
   auto convert = [&](int t) {
     if (!conv) return;
-    const float* ub = reinterpret_cast<const float*>(uring + (t % kPAStages) * P::UB) + cr * P::RC + cc;
-    const f32x4 a0 = *reinterpret_cast<const f32x4*>(ub);
-    const f32x4 a1 = *reinterpret_cast<const f32x4*>(ub + 4);
+    unsigned char* uslot = uring + (t % kPAUStages) * P::UBP;
+    float* urow = reinterpret_cast<float*>(uslot) + cr * P::RC;
+    f32x4* s0 = reinterpret_cast<f32x4*>(urow) + ((2 * cu) ^ pa_swz(cr));
+    f32x4* s1 = reinterpret_cast<f32x4*>(urow) + ((2 * cu + 1) ^ pa_swz(cr));
+    const f32x4 a0 = *s0;
+    const f32x4 a1 = *s1;
     const float raw[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
     const int64_t row = p0 + (int64_t)t * kPAPts + cr;
     const bool vrow = row < p1;
@@ -227,9 +337,8 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
     for (int e = 0; e < 8; ++e) u[e] = (vrow && cc + e < r) ? raw[e] * cf : 0.f;
     f16x8 hi, lo;
     split_f16(u, su, hi, lo);
-    _Float16* sh = slabs + (t & 1) * 2 * kPAPts * P::WS;
-    *reinterpret_cast<f16x8*>(sh + cr * P::WS + cc) = hi;
-    *reinterpret_cast<f16x8*>(sh + kPAPts * P::WS + cr * P::WS + cc) = lo;
+    *s0 = __builtin_bit_cast(f32x4, hi);
+    *s1 = __builtin_bit_cast(f32x4, lo);
     if (t % nfb == fb) {
       double dot = 0.0;
 #pragma unroll
@@ -238,8 +347,8 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
       for (int m = 1; m < P::LPP; m <<= 1) dot += shfl_xor_d(dot, m);
       if (vrow) {
         const float q = (float)(dot - 1.0);
-        float yt = B.y[row];
-        const bool lead = (tid - cr * P::LPP) == 0;
+        float yt = reinterpret_cast<const float*>(uslot + P::UB)[cr];
+        const bool lead = cu == 0;
         if (gate) {
           yt = fmaf(gam, q, yt);
           if (lead) B.y[row] = yt;
@@ -256,62 +365,56 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
     }
   };
 
-  // prologue: groups -1 (U of stage 0), 0 and 1; wait for group -1, split U of stage 0
+  // prologue: groups -1 (U of stage 0) .. 2; wait for group -1, split U of stage 0
   constexpr int G = P::OPS_X;  // loads per wave of a group, at least
   issue_group(-1);
-  if (nst > 0) issue_group(0);
-  if (nst > 1) issue_group(1);
-  if (nst > 1) wait_barrier<2 * G>();
-  else if (nst > 0) wait_barrier<G>();
-  else wait_barrier<0>();
+  for (int t = 0; t < 3 && t < nst; ++t) issue_group(t);
+  {
+    const int newer = nst < 3 ? nst : 3;  // groups 0 .. newer - 1 issued after group -1
+    if (newer >= 3) wait_barrier<3 * G>();
+    else if (newer == 2) wait_barrier<2 * G>();
+    else if (newer == 1) wait_barrier<G>();
+    else wait_barrier<0>();
+  }
   convert(0);
 
   for (int st = 0; st < nst; ++st) {
-    // group st (Xhat of stage st, U of stage st + 1) has landed; slab st & 1 is complete
-    if (st + 1 < nst) wait_barrier<G>();
+    // group st (Xhat of stage st, U of stage st + 1) has landed; U of stage st is split
+    const int newer = (nst - 1 - st) < 2 ? (nst - 1 - st) : 2;
+    if (newer >= 2) wait_barrier<2 * G>();
+    else if (newer == 1) wait_barrier<G>();
     else wait_barrier<0>();
-    if (st + 2 < nst) issue_group(st + 2);
+    // split the next stage's U (its y/ybar stores then precede the new ring loads, so
+    // the next waits need not wait for them)
     if (st + 1 < nst) convert(st + 1);
+    if (st + 3 < nst) issue_group(st + 3);
 
     // ---- Theta block += Xhat_stage^T U_stage ----
-    int x_off = (st % kPAStages) * P::XB;  // opaque: addresses formed per stage
+    int x_off = (st % kPAXStages) * P::XB;  // opaque: addresses formed per stage
     asm volatile("" : "+s"(x_off));
-    int s_off = (st & 1) * 2 * kPAPts * P::WS;
-    asm volatile("" : "+s"(s_off));
-    const _Float16* xs = reinterpret_cast<const _Float16*>(xring + x_off);
-    const _Float16* slab_h = slabs + s_off;
-    const _Float16* slab_l = slab_h + kPAPts * P::WS;
-    const int gq = lane >> 4, s16 = lane & 15;
-    const int R = 8 * (gq >> 1) + (s16 >> 2);  // and R + 4 (same swizzle)
-    f16x8 ah[2], al[2];
+    int u_off = (st % kPAUStages) * P::UBP;
+    asm volatile("" : "+s"(u_off));
+    const uint32_t xbase = lds_base + (uint32_t)x_off;
+    const uint32_t ubase = lds_base + (uint32_t)(P::XR + u_off);
+    uint32_t xa[2][2], ua[NBW][2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int fc = 64 * fw + 32 * i + 16 * (gq & 1) + 4 * (s16 & 3);
-      const int u8 = fc >> 3, qd = (fc >> 2) & 1;
-      const int sh = (2 * u8) ^ pa_swz(R), sl = (2 * u8 + 1) ^ pa_swz(R);
-      const _Float16* ph = xs + R * (kPAFeat * 2) + sh * 8 + qd * 4;
-      const _Float16* pl = xs + R * (kPAFeat * 2) + sl * 8 + qd * 4;
-      const pf16x4 h0 = lds_tr16(ph), h1 = lds_tr16(ph + 4 * kPAFeat * 2);
-      const pf16x4 l0 = lds_tr16(pl), l1 = lds_tr16(pl + 4 * kPAFeat * 2);
-      ah[i] = (f16x8){h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
-      al[i] = (f16x8){l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
-    }
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int cb = 0; cb < NBW; ++cb) {
-      const int c = (P::RC / 2) * cw + 32 * cb + 16 * (gq & 1) + 4 * (s16 & 3);
-      const _Float16* ph = slab_h + R * P::WS + c;
-      const _Float16* pl = slab_l + R * P::WS + c;
-      const pf16x4 h0 = lds_tr16(ph), h1 = lds_tr16(ph + 4 * P::WS);
-      const pf16x4 l0 = lds_tr16(pl), l1 = lds_tr16(pl + 4 * P::WS);
-      const f16x8 bh = (f16x8){h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
-      const f16x8 bl = (f16x8){l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
+      for (int hl = 0; hl < 2; ++hl) xa[i][hl] = pa_operand_addr(xbase, kPAFeat * 4, 64 * fw + 32 * i, hl, lane);
+#pragma unroll
+    for (int cb = 0; cb < NBW; ++cb)
+#pragma unroll
+      for (int hl = 0; hl < 2; ++hl) ua[cb][hl] = pa_operand_addr(ubase, P::RC * 4, (P::RC / 2) * cw + 32 * cb, hl, lane);
+    f16x8 ah[2], al[2], bh[NBW], bl[NBW];
+    pa_stage_reads<NBW, 4 * kPAFeat * 4, 4 * P::RC * 4>(xa, ua, ah, al, bh, bl);
+#pragma unroll
+    for (int cb = 0; cb < NBW; ++cb)
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        acc[i][cb] = mfma32x32x16h(ah[i], bl, acc[i][cb]);
-        acc[i][cb] = mfma32x32x16h(al[i], bh, acc[i][cb]);
-        acc[i][cb] = mfma32x32x16h(ah[i], bh, acc[i][cb]);
+        acc[i][cb] = mfma32x32x16h(ah[i], bl[cb], acc[i][cb]);
+        acc[i][cb] = mfma32x32x16h(al[i], bh[cb], acc[i][cb]);
+        acc[i][cb] = mfma32x32x16h(ah[i], bh[cb], acc[i][cb]);
       }
-    }
   }
   __syncthreads();
 
