@@ -47,6 +47,8 @@ def algorithmic_bytes(kind: str, n: int, d: int, r: int, dual_frac: float = 0.0)
         return 4.0 * (n * d + 2 * n * r + n)
     if kind == "pass_u":      # row pass: read U and ytilde (+ write ytilde on dual steps)
         return 4.0 * (n * r + n) + 4.0 * n * dual_frac
+    if kind == "finish":      # read W, write U = c W, read ytilde (+ write it on a pending dual step)
+        return 4.0 * (2 * n * r + n) + 4.0 * n * dual_frac
     if kind == "step":        # whole iteration of the two-pass structure: the fixed numerator
         return 4.0 * (2 * n * d + 3 * n * r + 2 * n) + 4.0 * n * dual_frac
     raise ValueError(kind)

@@ -309,7 +309,8 @@ DATA_START = 32  # NLR_INIT_DATA_START
 
 @pytest.mark.parametrize("n,d,r,K,flags", [(2000, 16, 4, 4, 0), (1037, 16, 10, 7, 0), (777, 64, 16, 16, 0),
                                            (4099, 128, 64, 64, 0), (4099, 128, 64, 64, 8),
-                                           (1500, 768, 256, 256, 0), (3000, 32, 10, 10, 16)])
+                                           (1500, 768, 256, 256, 0), (3000, 32, 10, 10, 16),
+                                           (1500, 768, 256, 256, 8), (2049, 256, 68, 10, 8)])
 def test_data_start(n, d, r, K, flags):
     X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n + 3 * d)
     Z = standard_normal_factor(n, r, seed=n + r + 1).astype(np.float64)
