@@ -61,6 +61,19 @@ __device__ __forceinline__ void wait_barrier() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
+// wait_barrier<n> for a run-time n (values above 31 wait for more than needed: still correct)
+__device__ __forceinline__ void wait_barrier_n(int n) {
+  switch (n < 31 ? (n < 0 ? 0 : n) : 31) {
+#define NLR_WB(k) case k: wait_barrier<k>(); break;
+    NLR_WB(0) NLR_WB(1) NLR_WB(2) NLR_WB(3) NLR_WB(4) NLR_WB(5) NLR_WB(6) NLR_WB(7)
+    NLR_WB(8) NLR_WB(9) NLR_WB(10) NLR_WB(11) NLR_WB(12) NLR_WB(13) NLR_WB(14) NLR_WB(15)
+    NLR_WB(16) NLR_WB(17) NLR_WB(18) NLR_WB(19) NLR_WB(20) NLR_WB(21) NLR_WB(22) NLR_WB(23)
+    NLR_WB(24) NLR_WB(25) NLR_WB(26) NLR_WB(27) NLR_WB(28) NLR_WB(29) NLR_WB(30)
+#undef NLR_WB
+    default: wait_barrier<31>(); break;
+  }
+}
+
 __device__ __forceinline__ pf16x4 lds_tr16(const _Float16* p) {
   ph16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4f16((__attribute__((address_space(3))) ph16x4*)(p));
   pf16x4 o;
@@ -108,7 +121,7 @@ struct PanelA {
   static constexpr int LPP = RC / 8;                  // threads per row in the conversion
   static constexpr int XR = kPAXStages * XB;          // Xhat ring
   static constexpr int UR = kPAUStages * UBP;         // U ring
-  static constexpr int LDS = XR + UR + 16 * 8;        // rings, reduction
+  static constexpr int LDS = XR + UR + 16 * 8 + RC * 4 + 32;  // rings, reduction, p, dump
   static_assert(XI % 8 == 0, "equal Xhat loads per wave");
   static_assert(UI * 1024 == UB, "U stage in whole KiB");
   static_assert(RC / 4 >= 16, "a U row spans at least 16 pieces (swizzle)");
@@ -235,6 +248,8 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
   unsigned char* xring = smem_raw;
   unsigned char* uring = smem_raw + P::XR;
   double* dred = reinterpret_cast<double*>(smem_raw + P::XR + P::UR);
+  float* ps = reinterpret_cast<float*>(smem_raw + P::XR + P::UR + 16 * 8);  // p (RC)
+  f32x4* ldump = reinterpret_cast<f32x4*>(ps + P::RC);                     // 32 bytes never read
   // LDS byte address of the dynamic area (operand of the assembly reads)
   const uint32_t lds_base =
       (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem_raw);
@@ -258,12 +273,11 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
 
   // conversion unit of this thread: row cr of a stage, columns 8 cu .. 8 cu + 7
   const bool conv = tid < kPAPts * P::LPP;
-  const int cr = tid / P::LPP;
-  const int cu = tid - cr * P::LPP;
+  const int ct = tid % (kPAPts * P::LPP);  // threads beyond the units repeat one (split only)
+  const int cr = ct / P::LPP;
+  const int cu = ct - cr * P::LPP;
   const int cc = 8 * cu;
-  float pr[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) pr[e] = (conv && cc + e < g.r32) ? B.p[cc + e] : 0.f;
+  for (int c = tid; c < P::RC; c += kPAThreads) ps[c] = (c < g.r32) ? B.p[c] : 0.f;  // published by the prologue barrier
   double s_acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) s_acc[e] = 0.0;
@@ -320,73 +334,87 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
     }
   };
 
-  // scale and split stage t's U in place; this block's share of the row work
-  auto convert = [&](int t) {
-    if (!conv) return;
-    unsigned char* uslot = uring + (t % kPAUStages) * P::UBP;
-    float* urow = reinterpret_cast<float*>(uslot) + cr * P::RC;
-    f32x4* s0 = reinterpret_cast<f32x4*>(urow) + ((2 * cu) ^ pa_swz(cr));
-    f32x4* s1 = reinterpret_cast<f32x4*>(urow) + ((2 * cu + 1) ^ pa_swz(cr));
-    const f32x4 a0 = *s0;
-    const f32x4 a1 = *s1;
+  // this thread's 8 values of stage t's U (scaled by c_f, the lazy normalisation)
+  auto load_u8 = [&](int t, float (&u)[8], bool& vrow) {
+    const float* urow = reinterpret_cast<const float*>(uring + (t % kPAUStages) * P::UBP) + cr * P::RC;
+    const f32x4 a0 = reinterpret_cast<const f32x4*>(urow)[(2 * cu) ^ pa_swz(cr)];
+    const f32x4 a1 = reinterpret_cast<const f32x4*>(urow)[(2 * cu + 1) ^ pa_swz(cr)];
     const float raw[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
     const int64_t row = p0 + (int64_t)t * kPAPts + cr;
-    const bool vrow = row < p1;
-    float u[8];
+    vrow = row < p1;
 #pragma unroll
     for (int e = 0; e < 8; ++e) u[e] = (vrow && cc + e < r) ? raw[e] * cf : 0.f;
+  };
+  // split stage t's U in place; branch-free, so it can share a block with the products
+  // (threads beyond the conversion units repeat one's arithmetic and store to a dump slot:
+  // the split is not idempotent, so only the unit's own thread may rewrite it)
+  auto split_u = [&](int t) {
+    float u[8];
+    bool vrow;
+    load_u8(t, u, vrow);
     f16x8 hi, lo;
     split_f16(u, su, hi, lo);
-    *s0 = __builtin_bit_cast(f32x4, hi);
-    *s1 = __builtin_bit_cast(f32x4, lo);
-    if (t % nfb == fb) {
-      double dot = 0.0;
+    f32x4* urow = reinterpret_cast<f32x4*>(uring + (t % kPAUStages) * P::UBP + cr * P::RC * 4);
+    *(conv ? urow + ((2 * cu) ^ pa_swz(cr)) : ldump) = __builtin_bit_cast(f32x4, hi);
+    *(conv ? urow + ((2 * cu + 1) ^ pa_swz(cr)) : ldump + 1) = __builtin_bit_cast(f32x4, lo);
+  };
+  // the row work of stage t (this block's share): reads the fp32 U before it is split
+  auto row_work = [&](int t) {
+    if (!conv) return;
+    float u[8];
+    bool vrow;
+    load_u8(t, u, vrow);
+    const f32x4 p0v = *reinterpret_cast<const f32x4*>(ps + cc);
+    const f32x4 p1v = *reinterpret_cast<const f32x4*>(ps + cc + 4);
+    const float pr[8] = {p0v.x, p0v.y, p0v.z, p0v.w, p1v.x, p1v.y, p1v.z, p1v.w};
+    double dot = 0.0;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) dot += (double)u[e] * (double)pr[e];
+    for (int e = 0; e < 8; ++e) dot += (double)u[e] * (double)pr[e];
 #pragma unroll
-      for (int m = 1; m < P::LPP; m <<= 1) dot += shfl_xor_d(dot, m);
-      if (vrow) {
-        const float q = (float)(dot - 1.0);
-        float yt = reinterpret_cast<const float*>(uslot + P::UB)[cr];
-        const bool lead = cu == 0;
-        if (gate) {
-          yt = fmaf(gam, q, yt);
-          if (lead) B.y[row] = yt;
-        }
-        const float ybar = fmaf(gam, q, yt);
-        if (lead) {
-          B.ybar[row] = ybar;
-          qq += (double)q * (double)q;
-          yq += (double)yt * (double)q;
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s_acc[e] = fma((double)ybar, (double)u[e], s_acc[e]);
+    for (int m = 1; m < P::LPP; m <<= 1) dot += shfl_xor_d(dot, m);
+    if (vrow) {
+      const int64_t row = p0 + (int64_t)t * kPAPts + cr;
+      const float q = (float)(dot - 1.0);
+      float yt = reinterpret_cast<const float*>(uring + (t % kPAUStages) * P::UBP + P::UB)[cr];
+      const bool lead = cu == 0;
+      if (gate) {
+        yt = fmaf(gam, q, yt);
+        if (lead) B.y[row] = yt;
       }
+      const float ybar = fmaf(gam, q, yt);
+      if (lead) {
+        B.ybar[row] = ybar;
+        qq += (double)q * (double)q;
+        yq += (double)yt * (double)q;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_acc[e] = fma((double)ybar, (double)u[e], s_acc[e]);
     }
   };
 
+  // loads this wave issues for group t (t < nst): its Xhat rows, and if stage t + 1
+  // exists its U rows and (wave 0) the ytilde of those rows
+  const int ops_u = P::UI / 8 + (wave < P::UI % 8 ? 1 : 0) + (wave == 0 ? 1 : 0);
+  auto group_ops = [&](int t) { return P::OPS_X + (t + 1 < nst ? ops_u : 0); };
+
   // prologue: groups -1 (U of stage 0) .. 2; wait for group -1, split U of stage 0
-  constexpr int G = P::OPS_X;  // loads per wave of a group, at least
   issue_group(-1);
   for (int t = 0; t < 3 && t < nst; ++t) issue_group(t);
   {
-    const int newer = nst < 3 ? nst : 3;  // groups 0 .. newer - 1 issued after group -1
-    if (newer >= 3) wait_barrier<3 * G>();
-    else if (newer == 2) wait_barrier<2 * G>();
-    else if (newer == 1) wait_barrier<G>();
-    else wait_barrier<0>();
+    int newer = 0;  // loads of groups 0 .. 2, issued after group -1
+    for (int t = 0; t < 3 && t < nst; ++t) newer += group_ops(t);
+    wait_barrier_n(newer);
   }
-  convert(0);
+  if (0 % nfb == fb) row_work(0);
+  split_u(0);
 
   for (int st = 0; st < nst; ++st) {
-    // group st (Xhat of stage st, U of stage st + 1) has landed; U of stage st is split
-    const int newer = (nst - 1 - st) < 2 ? (nst - 1 - st) : 2;
-    if (newer >= 2) wait_barrier<2 * G>();
-    else if (newer == 1) wait_barrier<G>();
-    else wait_barrier<0>();
-    // split the next stage's U (its y/ybar stores then precede the new ring loads, so
-    // the next waits need not wait for them)
-    if (st + 1 < nst) convert(st + 1);
+    // group st (Xhat of stage st, U of stage st + 1) has landed once at most the loads
+    // of groups st + 1 and st + 2 (issued after it) are pending; U of stage st is split
+    int newer = 0;
+    if (st + 1 < nst) newer += group_ops(st + 1);
+    if (st + 2 < nst) newer += group_ops(st + 2);
+    wait_barrier_n(newer);
     if (st + 3 < nst) issue_group(st + 3);
 
     // ---- Theta block += Xhat_stage^T U_stage ----
@@ -407,6 +435,10 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
       for (int hl = 0; hl < 2; ++hl) ua[cb][hl] = pa_operand_addr(ubase, P::RC * 4, (P::RC / 2) * cw + 32 * cb, hl, lane);
     f16x8 ah[2], al[2], bh[NBW], bl[NBW];
     pa_stage_reads<NBW, 4 * kPAFeat * 4, 4 * P::RC * 4>(xa, ua, ah, al, bh, bl);
+    // the next stage's row work (reads its fp32 U), then its split, which shares this
+    // block with the products (on the last stage it rewrites a slot no one reads)
+    if (st + 1 < nst && (st + 1) % nfb == fb) row_work(st + 1);
+    split_u(st + 1);
 #pragma unroll
     for (int cb = 0; cb < NBW; ++cb)
 #pragma unroll
@@ -442,7 +474,7 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
     double* sred = reinterpret_cast<double*>(smem_raw);  // kPAPts x RC (the rings are free now)
     if (conv)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sred[cr * P::RC + cc + e] = s_acc[e];
+      for (int e = 0; e < 8; ++e) sred[cr * P::RC + cc + e] = s_acc[e];  // (conv: cr, cc are the thread's own)
     const double tq = block_sum8_d(qq, dred);  // its barriers also publish sred
     const double ty = block_sum8_d(yq, dred);
     if (tid == 0) {
