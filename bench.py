@@ -126,7 +126,7 @@ def measure(nlr, torch, np, X_host, Z_host, wl, steps, warm, split, two_pass):
     if warm > 0:
         ctx.run(warm)
     torch.cuda.synchronize()
-    ctx.set_profiling(True)
+    ctx.set_profiling(2)  # events around the row and pass kernels only (the roofline's candidates)
     stream = ctx.stream
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)

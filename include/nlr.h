@@ -210,8 +210,10 @@ nlr_status nlr_normaliser(nlr_ctx* ctx, double* a, double* xbar_host);
 nlr_status nlr_inspect(nlr_ctx* ctx, int32_t what, void* host_dst, size_t bytes);
 
 /* Per-kernel timing with HIP events recorded on the context's stream around
- * every launch made by nlr_step / nlr_run (off by default).  enable = 0 turns
- * it off and clears the totals. */
+ * the launches made by nlr_step / nlr_run (off by default): enable = 1 around
+ * every launch, 2 around the row and pass kernels only (pass_a, pass_b, pass_u,
+ * pass_bf, finish: fewer events in the stream); 0 turns it off and clears the
+ * totals; other values return NLR_EINVAL. */
 nlr_status nlr_set_profiling(nlr_ctx* ctx, int32_t enable);
 
 /* Kernel timing totals since profiling was enabled (synchronises).  For kernel

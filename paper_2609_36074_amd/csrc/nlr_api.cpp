@@ -303,6 +303,7 @@ struct nlr_ctx {
   DevCtl* host_ctl;   // pinned mirror of the control block
   // profiling
   bool prof;
+  int prof_level;     // 1: every launch; 2: the row and pass kernels only
   std::vector<hipEvent_t> ev_pool;
   std::vector<std::pair<int, int>> ev_pairs;  // (kind, index of start event)
   size_t ev_used;
@@ -346,9 +347,22 @@ static StepArgs make_step_args(const nlr_ctx* c, int end_work) {
 }
 
 // ---- profiling helpers ----
+static bool pass_kernel(int kind) {
+  return kind == KK_PASS_A || kind == KK_PASS_B || kind == KK_PASS_U || kind == KK_PASS_BF || kind == KK_FINISH;
+}
+static hipError_t grow_events(nlr_ctx* c, size_t want) {
+  while (c->ev_pool.size() < want) {
+    hipEvent_t e;
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) return err;
+    c->ev_pool.push_back(e);
+  }
+  return hipSuccess;
+}
 static hipError_t prof_begin(nlr_ctx* c, int kind, int* slot) {
   *slot = -1;
   if (!c->prof) return hipSuccess;
+  if (c->prof_level == 2 && !pass_kernel(kind)) return hipSuccess;
   if (c->ev_used + 2 > c->ev_pool.size()) {
     for (int k = 0; k < 64; ++k) {
       hipEvent_t e;
@@ -511,6 +525,7 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   c->t_host = 0;
   c->t_host_valid = true;
   c->prof = false;
+  c->prof_level = 0;
   c->ev_used = 0;
   for (int k = 0; k < KK_COUNT; ++k) {
     c->prof_ms[k] = 0.0;
@@ -735,11 +750,14 @@ nlr_status nlr_inspect(nlr_ctx* c, int32_t what, void* host_dst, size_t bytes) {
 }
 
 nlr_status nlr_set_profiling(nlr_ctx* c, int32_t enable) {
-  if (!c) return NLR_EINVAL;
+  if (!c || enable < 0 || enable > 2) return NLR_EINVAL;
   if (c->prof && !enable) {
     if (prof_collect(c) != hipSuccess) return hip_fail(c);
   }
   c->prof = enable != 0;
+  c->prof_level = enable;
+  // events for a few hundred launches exist before timing starts
+  if (c->prof && grow_events(c, 1024) != hipSuccess) return hip_fail(c);
   for (int k = 0; k < KK_COUNT; ++k) {
     c->prof_ms[k] = 0.0;
     c->prof_n[k] = 0;

@@ -258,8 +258,10 @@ class Context:
         _check(load_library().nlr_inspect(self._ctx, code, out.ctypes.data, out.nbytes), "nlr_inspect")
         return out
 
-    def set_profiling(self, enable: bool):
-        _check(load_library().nlr_set_profiling(self._ctx, 1 if enable else 0), "nlr_set_profiling")
+    def set_profiling(self, enable):
+        """False/0 off, True/1 every launch, 2 the row and pass kernels only."""
+        level = int(enable) if not isinstance(enable, bool) else (1 if enable else 0)
+        _check(load_library().nlr_set_profiling(self._ctx, level), "nlr_set_profiling")
 
     def kernel_times(self):
         names = (ctypes.c_char_p * NLR_MAX_KERNEL_KINDS)()

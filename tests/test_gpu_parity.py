@@ -335,3 +335,24 @@ def test_data_start_rank_deficient_is_degenerate():
     with pytest.raises(nlr.NlrError) as e:
         make_ctx(X, Z, 3, 0.01, flags=DATA_START)
     assert e.value.status == nlr.NLR_EDEGENERATE
+
+
+def test_profiling_levels():
+    """nlr_set_profiling: 1 times every launch, 2 only the row and pass kernels, others are rejected."""
+    from paper_2609_36074_amd import nlr
+    X, Z, _, wl = make_workload("tiny")
+    ctx = make_ctx(X, Z.astype(np.float64), wl.K, onlr.default_step_size(wl.K), T_min=10)
+    lib = nlr.load_library()
+    assert lib.nlr_set_profiling(ctx._ctx, 3) == nlr.NLR_EINVAL
+    assert lib.nlr_set_profiling(ctx._ctx, -1) == nlr.NLR_EINVAL
+    ctx.set_profiling(1)
+    ctx.run(4)
+    every = {k: v for k, v in ctx.kernel_times().items() if v[1]}
+    ctx.set_profiling(2)
+    ctx.run(4)
+    passes = {k: v for k, v in ctx.kernel_times().items() if v[1]}
+    ctx.set_profiling(0)
+    log(f"  level 1: {sorted(every)}; level 2: {sorted(passes)}")
+    assert {"ctl_a", "ctl_b", "reduce_theta"} <= set(every)
+    assert set(passes) <= {"pass_a", "pass_b", "pass_u", "pass_bf", "finish"} and passes
+    assert all(v[0] > 0 for v in passes.values())
