@@ -106,4 +106,17 @@ __device__ __forceinline__ float f16_range_scale(float vmax) {
   return ldexpf(1.0f, k);
 }
 
+// Fixed-order sum over a 512-thread workgroup; result valid in thread 0.
+__device__ __forceinline__ double block_sum8_d(double v, double* red) {
+  for (int m = 32; m >= 1; m >>= 1) v += shfl_xor_d(v, m);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  double r = 0.0;
+  if (threadIdx.x == 0) r = (((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7])));
+  __syncthreads();
+  return r;
+}
+
 }  // namespace nlr

@@ -23,7 +23,8 @@
 //            accumulators holding all of the d x r partial.
 // At the end the four waves' partials are added in a fixed order and written as
 // this workgroup's partial; a fixed-order reduction and the scale c_{t+1} give
-// Theta_{t+1}.
+// Theta_{t+1}.  Split shapes with 97..128 features and 33..64 columns run the
+// eight-wave form k_pass_bf8 further below instead.
 // SPLIT: both products use the two-term fp16 split of k_split.hip; otherwise
 // fp32 matrix cores (32x32x2 for phase 1, 16x16x4 for phase 2).
 #include <type_traits>
@@ -572,8 +573,630 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_
     }
     __syncthreads();
   }
-  float* part = B.theta_part + (int64_t)blockIdx.x * D32 * R32;
+  float* part = B.theta_part + (int64_t)blockIdx.x * g.theta_cols;
   for (int e = tid; e < D32 * R32; e += kThreads) part[e] = comb[e] + comb[D32 * R32 + e];
+}
+
+// ===========================================================================
+// Eight-wave form of the split fused pass B (written for 32-feature chunks NCH in
+// {1, 2, 4} and 32-column blocks NB in {1, 2}; dispatched for NCH = 4, NB = 2, with
+// 16-byte aligned rows and r % 4 == 0).
+//
+// The form above keeps the whole d x r partial of Xhat^T W in every wave, which
+// leaves room for one wave per SIMD only, and its prefetched rows then wait in
+// spare registers.  Here one 512-thread workgroup per compute unit walks
+// 128-row tiles; wave w owns the 16-row slab 16w .. 16w + 15 of a tile for the
+// first product (16x16x32 fp16 matrix cores: lane l holds row l % 16 and, of
+// each 16-column block, the columns 4 (l / 16) .. + 3) and the epilogue, and the
+// second product is shared out by blocks of the result: wave w owns the 32
+// features 32 (w % NCH) .. + 31 of the partial, all columns, over the 16-row
+// steps NCH (w / NCH) .. NCH (w / NCH + 1) - 1 of each tile, reading the split
+// Xhat and W tiles that the slab owners wrote to LDS (one workgroup barrier
+// before, one after).  A wave then holds 16 accumulators of the partial and two
+// tiles of prefetched rows (split Xhat, U, ytilde) in registers: the rows of tile
+// t + 2 step are requested as soon as tile t has consumed its own.  W leaves
+// through LDS: each wave stages its slab's rows, packed as in U, in its own rows
+// of the W tile and stores them as whole contiguous 1 KiB pieces before the
+// same rows take the split of W.
+// ===========================================================================
+namespace bf8 {
+
+constexpr int kThreads8 = 512;
+constexpr int kRows = 128;  // rows per tile: 8 waves x 16
+static_assert(kRows == kTPB, "the fused pass B tiles are kTPB rows");
+
+// Tiles in LDS: row R of a tile is a run of 16-byte units (four features or four
+// columns: their fp16 hi halves, then their lo halves, as Xhat is stored).  Unit u
+// of row R sits in slot u ^ swz(R), and on odd rows its two 8-byte halves are
+// exchanged.  A unit write (16 lanes: 16 consecutive rows, one unit) and a
+// transposing read (32 lanes: rows R0 .. R0 + 3, eight consecutive units, one
+// half) then each touch 64 distinct 4-byte banks.
+__device__ __forceinline__ int swz(int R) { return (R ^ ((R & 2) << 2)) & 15; }
+
+template <int NB, int NCH>
+struct Shape {
+  static constexpr int CB16 = 2 * NB;                     // 16-column blocks
+  static constexpr int R32 = 32 * NB, D32 = 32 * NCH;
+  static constexpr int XU = 8 * NCH > 16 ? 8 * NCH : 16;  // units per Xhat tile row
+  static constexpr int WU = 8 * NB > 16 ? 8 * NB : 16;    // units per W tile row
+  static constexpr int XRS = 16 * XU, WRS = 16 * WU;      // tile row bytes
+  static constexpr int RS2 = 8 / (NCH * NB);              // row splits of the second product
+  static constexpr int KPW = 8 / RS2;                     // its 16-row steps per wave
+  static constexpr int TH = NCH * CB16 * 64 * 16;         // bytes of one plane of the Theta operand
+  static constexpr int OFF_X = 2 * TH;
+  static constexpr int OFF_W = OFF_X + kRows * XRS;
+  static constexpr int OFF_P = OFF_W + kRows * WRS;
+  static constexpr int OFF_S = OFF_P + R32 * 4;
+  static constexpr int OFF_COL = OFF_S + R32 * 4;         // 8 x R32 doubles: column sums of W
+  static constexpr int OFF_COLY = OFF_COL + 8 * R32 * 8;  // 8 x R32 doubles: W^T ytilde
+  static constexpr int OFF_D = OFF_COLY + 8 * R32 * 8;    // 8 x 8 doubles
+  static constexpr int OFF_F = OFF_D + 8 * 8 * 8;         // 8 floats
+  static constexpr int LDS = OFF_F + 8 * 4;
+  static_assert(RS2 * NCH * NB == 8, "eight waves share the second product");
+  static_assert(RS2 * D32 * R32 * 4 <= kRows * XRS, "the partial combine fits the Xhat tile");
+  static_assert(2 * R32 * R32 * 4 <= kRows * WRS, "the Gram combine fits the W tile");
+};
+
+// Byte offset within a tile (rows of RS bytes) of this lane's transposing read
+// for k-rows 8 (l / 32) + 4 half + (l % 16) / 4 and the units u0 + 4 ((l / 16) % 2)
+// + l % 4 (u0 a multiple of 8), half hl (0 hi, 1 lo): the two reads (half 0, 1)
+// of a 16-row step give lane l the 8 k-rows 8 (l / 32) + e of column 4 u0 + l % 32.
+__device__ __forceinline__ uint32_t tr_off(int RS, int u0, int hl, int half, int lane) {
+  const int gq = lane >> 4, s = lane & 15;
+  const int R = 8 * (gq >> 1) + 4 * half + (s >> 2);
+  const int u = u0 + 4 * (gq & 1) + (s & 3);
+  return (uint32_t)(R * RS + 16 * (u ^ swz(R)) + 8 * (hl ^ (R & 1)));
+}
+
+// Index of Theta[f][c] in the pass-B operand layout written by the Theta reduction.
+template <int NB>
+__device__ __forceinline__ int theta_index(int f, int c) {
+  const int ch = f >> 5, fin = f & 31;
+  const int hh = fin >> 4, jq = (fin & 15) >> 2, ee = fin & 3;
+  const int mb = c >> 5, l = hh * 32 + (c & 31);
+  return ((((ch * 4 + jq) * NB + mb) * 64 + l) * 4) + ee;
+}
+
+__device__ __forceinline__ f16x8 join4(f16x4 a, f16x4 b) {
+  return (f16x8){a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+// The transposing reads of one 16-row step of the second product, as assembly:
+// the compiler orders the ds_read_b64_tr_b16 builtin after every global store in
+// flight (it waits for the vector memory counter first), which would drain the
+// prefetched rows each tile.  One statement issues the reads and waits for their
+// data, so its outputs are defined only when they hold it.  xa[half][hl],
+// wa[half][hl]: LDS byte addresses; OX / OW: the step's byte offset.
+#define BF8_TR(o, a, f) "ds_read_b64_tr_b16 %" #o ", %" #a " offset:%" #f "\n\t"
+template <int OX, int OW>
+__device__ __forceinline__ void step_reads(const uint32_t (&xa)[2][2], const uint32_t (&wa)[2][2], f16x8& xh,
+                                           f16x8& xl, f16x8& wh, f16x8& wl) {
+  f16x4 x0, x1, x2, x3, w0, w1, w2, w3;
+  asm volatile(BF8_TR(0, 8, 16) BF8_TR(1, 9, 16) BF8_TR(2, 10, 16) BF8_TR(3, 11, 16)
+               BF8_TR(4, 12, 17) BF8_TR(5, 13, 17) BF8_TR(6, 14, 17) BF8_TR(7, 15, 17)
+               "s_waitcnt lgkmcnt(0)"
+               : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3), "=&v"(w0), "=&v"(w1), "=&v"(w2), "=&v"(w3)
+               : "v"(xa[0][0]), "v"(xa[1][0]), "v"(xa[0][1]), "v"(xa[1][1]),
+                 "v"(wa[0][0]), "v"(wa[1][0]), "v"(wa[0][1]), "v"(wa[1][1]), "n"(OX), "n"(OW)
+               : "memory");
+  xh = join4(x0, x1);
+  xl = join4(x2, x3);
+  wh = join4(w0, w1);
+  wl = join4(w2, w3);
+}
+// The W operand of a column block for the Gram product (4 reads).
+template <int OW>
+__device__ __forceinline__ void gram_reads(const uint32_t (&ga)[2][2], f16x8& gh, f16x8& gl) {
+  f16x4 w0, w1, w2, w3;
+  asm volatile(BF8_TR(0, 4, 8) BF8_TR(1, 5, 8) BF8_TR(2, 6, 8) BF8_TR(3, 7, 8)
+               "s_waitcnt lgkmcnt(0)"
+               : "=&v"(w0), "=&v"(w1), "=&v"(w2), "=&v"(w3)
+               : "v"(ga[0][0]), "v"(ga[1][0]), "v"(ga[0][1]), "v"(ga[1][1]), "n"(OW)
+               : "memory");
+  gh = join4(w0, w1);
+  gl = join4(w2, w3);
+}
+#undef BF8_TR
+
+// Slot of unit q of a wave's staged fp32 slab: the low four bits exchanged with the
+// 16-unit block index, so a store of 16 rows' unit u and a read of 16 consecutive
+// units each meet 64 distinct banks (rows of 16 units).
+__device__ __forceinline__ int stage_slot(int q) { return q ^ ((q >> 4) & 15); }
+
+__device__ __forceinline__ f32x4 mfma16x16x32h(f16x8 a, f16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// Reduce-scatter of 16 values over the 16 lanes of a DPP row: afterwards lane li
+// holds the sum over the row of element li.  The four exchanges pair lane li with
+// 15 - li, then 7 - li within each half row, then li ^ 2 and li ^ 1 (DPP, no LDS);
+// the lane whose index has the exchange's bit set keeps the upper half.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int LEN, int BIT, int CTRL>
+__device__ __forceinline__ void rs_step(float* v, int li) {
+  const bool up = (li & BIT) != 0;
+#pragma unroll
+  for (int k = 0; k < LEN / 2; ++k) {
+    const float send = up ? v[k] : v[k + LEN / 2];
+    const float keep = up ? v[k + LEN / 2] : v[k];
+    v[k] = keep + dpp_f<CTRL>(send);
+  }
+}
+__device__ __forceinline__ void reduce_scatter16_row(float* v, int li) {
+  rs_step<16, 8, 0x140>(v, li);  // row_mirror
+  rs_step<8, 4, 0x141>(v, li);   // row_half_mirror
+  rs_step<4, 2, 0x4E>(v, li);    // quad_perm [2, 3, 0, 1]
+  rs_step<2, 1, 0xB1>(v, li);    // quad_perm [1, 0, 3, 2]
+}
+
+// a 16-byte unit with its 8-byte halves exchanged when `odd`
+__device__ __forceinline__ f32x4 unit_swap(f32x4 v, bool odd) {
+  f32x4 o;
+  o.x = odd ? v.z : v.x;
+  o.y = odd ? v.w : v.y;
+  o.z = odd ? v.x : v.z;
+  o.w = odd ? v.y : v.w;
+  return o;
+}
+
+}  // namespace bf8
+
+template <int NB, int NCH>
+__global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_bf8(
+    Geometry g, Bufs B, StepArgs S) {
+  using P = bf8::Shape<NB, NCH>;
+  constexpr int CB16 = P::CB16, R32 = P::R32, D32 = P::D32;
+  constexpr int KPW = P::KPW;
+  // the row work's dot and the Gram blocks are laid out for 64 columns, 128 features
+  static_assert(NB == 2 && NCH == 4, "one-pass form: 33..64 columns, 97..128 features");
+  if (halted(B.ctl)) return;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  f16x8* th_h = reinterpret_cast<f16x8*>(smem_raw);
+  f16x8* th_l = reinterpret_cast<f16x8*>(smem_raw + P::TH);
+  unsigned char* xt = smem_raw + P::OFF_X;
+  unsigned char* wt = smem_raw + P::OFF_W;
+  float* ps = reinterpret_cast<float*>(smem_raw + P::OFF_P);
+  float* ss = reinterpret_cast<float*>(smem_raw + P::OFF_S);
+  double* colred = reinterpret_cast<double*>(smem_raw + P::OFF_COL);
+  double* colyred = reinterpret_cast<double*>(smem_raw + P::OFF_COLY);
+  double* dred = reinterpret_cast<double*>(smem_raw + P::OFF_D);
+  float* fred = reinterpret_cast<float*>(smem_raw + P::OFF_F);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int j = lane & 15, gq = lane >> 4;
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r;
+  const float cf = B.ctl->c_f;
+  const float gam = S.gamma_f;
+  const float neg_alpha = -S.alpha_f;
+  const float sx = B.ctl->x_scale;
+  // the factor of this iteration is read from one buffer, W_{t+1} written to the other
+  const int ubsel = B.ctl->ubuf;
+  const float* Usrc = ubsel ? B.U2 : B.U;
+  float* Udst = ubsel ? B.U : B.U2;
+  // the pending gated dual step (the end of the previous iteration)
+  const bool gate = (S.end_work != 0) && (B.ctl->gate != 0);
+
+  // ---- Theta_t as the A operand of the first product: lane l of block (ks, cb)
+  // holds column 16 cb + l % 16 and, for q = l / 16, features 32 ks + 4 q + e and
+  // 32 ks + 16 + 4 q + e (e = 0..3), the features of the two Xhat units that lane
+  // q of a row loads ----
+  float tmax = 0.f;
+  for (int e = tid; e < D32 * R32; e += bf8::kThreads8) tmax = fmaxf(tmax, fabsf(B.theta[e]));
+  for (int m = 32; m >= 1; m >>= 1) tmax = fmaxf(tmax, shfl_xor_f(tmax, m));
+  if (lane == 0) fred[wave] = tmax;
+  __syncthreads();
+  tmax = fred[0];
+#pragma unroll
+  for (int w = 1; w < 8; ++w) tmax = fmaxf(tmax, fred[w]);
+  const float sth = f16_range_scale(tmax);
+  const float two_alpha_s = S.two_alpha_f * (1.0f / sx) * (1.0f / sth);
+  for (int idx = tid; idx < NCH * CB16 * 64; idx += bf8::kThreads8) {
+    const int l = idx & 63;
+    const int cb = (idx >> 6) % CB16;
+    const int ks = (idx >> 6) / CB16;
+    const int c = 16 * cb + (l & 15), q = l >> 4;
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int f = 32 * ks + 4 * q + (e < 4 ? e : 12 + e);
+      v[e] = B.theta[bf8::theta_index<NB>(f, c)];
+    }
+    f16x8 hi, lo;
+    split_f16(v, sth, hi, lo);
+    th_h[idx] = hi;
+    th_l[idx] = lo;
+  }
+  for (int c = tid; c < R32; c += bf8::kThreads8) {
+    ps[c] = B.p[c];
+    ss[c] = B.s[c];
+  }
+  __syncthreads();
+
+  // ---- per-lane constants ----
+  // second product: wave w owns the 32 x 32 block (fb, cb2) of the partial over the
+  // 16-row steps KPW rsp .. KPW (rsp + 1) - 1 of each tile; and the block (ga, cb2)
+  // of the Gram partial W^T W over the steps 4 gh .. 4 gh + 3
+  const int fb = wave % NCH, cb2 = (wave / NCH) % NB, rsp = wave / (NCH * NB);
+  const int ga = fb & 1, gh = fb >> 1;
+  const uint32_t lds0 =
+      (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem_raw);
+  uint32_t xa[2][2], wa[2][2], wg[2][2];
+#pragma unroll
+  for (int half = 0; half < 2; ++half)
+#pragma unroll
+    for (int hl = 0; hl < 2; ++hl) {
+      xa[half][hl] = lds0 + P::OFF_X + (uint32_t)(16 * KPW * rsp * P::XRS) + (uint32_t)(256 * (fb >> 1)) +
+                     bf8::tr_off(P::XRS, 8 * (fb & 1), hl, half, lane);
+      wa[half][hl] = lds0 + P::OFF_W + (uint32_t)(16 * KPW * rsp * P::WRS) + bf8::tr_off(P::WRS, 8 * cb2, hl, half, lane);
+      wg[half][hl] = lds0 + P::OFF_W + (uint32_t)(64 * gh * P::WRS) + bf8::tr_off(P::WRS, 8 * ga, hl, half, lane);
+    }
+
+  double sa = 0.0, sb = 0.0, sh = 0.0, colacc = 0.0, colyacc = 0.0, qq = 0.0, yq = 0.0;
+  f32x16 acc2, accg;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc2[v] = accg[v] = 0.f;
+
+  const int64_t T = g.tilesB;
+  const int64_t step = gridDim.x;
+
+  // the next tile's rows are requested as soon as this tile has consumed its own
+  struct Buf {
+    f32x4 x[NCH][2];
+  };
+  struct UBuf {
+    f32x4 u[CB16];
+    float y;
+  };
+  // lane-derived offsets are recomputed where used (from an opaque copy of the lane
+  // id), not kept live across the tile loop
+  auto opaque_lane = [&]() -> int {
+    int lo = lane;
+    asm volatile("" : "+v"(lo));
+    return lo;
+  };
+  // row of this lane within tile st (row 0 of the tile for rows >= n; a tile >= T
+  // reads tile 0, whose values are never used)
+  auto lane_row = [&](int64_t st, int jj, int64_t& tile_base) -> uint32_t {
+    const int64_t stc = st < T ? st : 0;
+    tile_base = stc * bf8::kRows;
+    const int rr = 16 * wave + jj;
+    return (tile_base + rr < n) ? (uint32_t)rr : 0u;
+  };
+  // uniform tile base + 32-bit lane byte offset (the scalar-base form of the loads)
+  auto load_x = [&](Buf& b, int64_t st) {
+    const int lo = opaque_lane(), gq = lo >> 4;
+    int64_t tb;
+    const uint32_t rr = lane_row(st, lo & 15, tb);
+    const char* base = reinterpret_cast<const char*>(B.X + tb * (int64_t)d);
+#pragma unroll
+    for (int ks = 0; ks < NCH; ++ks)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int f = 32 * ks + 16 * hh + 4 * gq;  // features >= d meet zero rows of Theta_t
+        const uint32_t off = 4u * (rr * (uint32_t)d + (uint32_t)(f < d ? f : 0));
+        b.x[ks][hh] = *reinterpret_cast<const f32x4*>(base + off);
+      }
+  };
+  auto load_u = [&](UBuf& b, int64_t st) {
+    const int lo = opaque_lane(), gq = lo >> 4;
+    int64_t tb;
+    const uint32_t rr = lane_row(st, lo & 15, tb);
+    const char* base = reinterpret_cast<const char*>(Usrc + tb * (int64_t)r);
+#pragma unroll
+    for (int cb = 0; cb < CB16; ++cb) {
+      const int c = 16 * cb + 4 * gq;
+      const uint32_t off = 4u * (rr * (uint32_t)r + (uint32_t)(c < r ? c : 0));
+      b.u[cb] = *reinterpret_cast<const f32x4*>(base + off);
+    }
+    b.y = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(B.y + tb) + 4u * rr);
+  };
+
+  UBuf ub;
+  auto tile = [&](Buf& bx, int64_t st, int64_t nst) {
+    __builtin_amdgcn_sched_barrier(0);
+    const int lane = opaque_lane();
+    const int j = lane & 15, gq = lane >> 4;
+    const int sj = bf8::swz(j);
+    const bool oddj = (j & 1) != 0;
+    const int gs = gq ^ sj;
+    const uint32_t xrow = (uint32_t)((16 * wave + j) * P::XRS);
+    const uint32_t wrow = (uint32_t)((16 * wave + j) * P::WRS);
+    const int64_t pt = st * bf8::kRows + 16 * wave + j;
+    const bool vpt = pt < n;
+    // ---- first product: G = Xhat_slab Theta_t ----
+    f32x4 acc1[CB16];
+#pragma unroll
+    for (int cb = 0; cb < CB16; ++cb) acc1[cb] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < NCH; ++ks) {
+      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+      const f32x4 xa0 = bx.x[ks][0], xa1 = bx.x[ks][1];
+      const u32x4 hb = {__float_as_uint(xa0.x), __float_as_uint(xa0.y), __float_as_uint(xa1.x), __float_as_uint(xa1.y)};
+      const u32x4 lb = {__float_as_uint(xa0.z), __float_as_uint(xa0.w), __float_as_uint(xa1.z), __float_as_uint(xa1.w)};
+      const f16x8 xh = __builtin_bit_cast(f16x8, hb);
+      const f16x8 xl = __builtin_bit_cast(f16x8, lb);
+      // the slab's units into the Xhat tile of the second product
+      *reinterpret_cast<f32x4*>(xt + xrow + 16 * ((8 * ks) ^ gs)) = bf8::unit_swap(xa0, oddj);
+      *reinterpret_cast<f32x4*>(xt + xrow + 16 * ((8 * ks + 4) ^ gs)) = bf8::unit_swap(xa1, oddj);
+#pragma unroll
+      for (int cb = 0; cb < CB16; ++cb) {
+        const f16x8 ah = th_h[(ks * CB16 + cb) * 64 + lane];
+        const f16x8 al = th_l[(ks * CB16 + cb) * 64 + lane];
+        acc1[cb] = bf8::mfma16x16x32h(ah, xl, acc1[cb]);
+        acc1[cb] = bf8::mfma16x16x32h(al, xh, acc1[cb]);
+        acc1[cb] = bf8::mfma16x16x32h(ah, xh, acc1[cb]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    load_x(bx, nst);  // Xhat rows of the next tile
+    __builtin_amdgcn_sched_barrier(0);
+
+    // ---- row work on row pt, columns 16 cb + 4 gq + v ----
+    int lds_off = 0;  // opaque zero offset: p and s are read from LDS here, not kept in registers
+    asm volatile("" : "+v"(lds_off));
+    const float* psl = ps + lds_off;
+    const float* ssl = ss + lds_off;
+    // okf: 1 for a valid row and column, else 0 (masked lanes compute on finite
+    // values and their results are multiplied away: no branches)
+    float okf[CB16];
+    float u[CB16][4];
+#pragma unroll
+    for (int cb = 0; cb < CB16; ++cb) {
+      okf[cb] = (vpt && (16 * cb + 4 * gq) < r) ? 1.0f : 0.0f;
+      const float sc = cf * okf[cb];
+      u[cb][0] = ub.u[cb].x * sc;
+      u[cb][1] = ub.u[cb].y * sc;
+      u[cb][2] = ub.u[cb].z * sc;
+      u[cb][3] = ub.u[cb].w * sc;
+    }
+    // q = u.p - 1 (FP64): the partial of each group of four columns, then the pairs
+    // (columns 4k.. with 4(k^1).., then 4(k^2)..), then the groups of 16 and 32 --
+    // the order of the row pass and the finish pass, so that q, the stored dual and
+    // ybar are bitwise the same whichever kernel does the row work
+    double pd[CB16];
+#pragma unroll
+    for (int cb = 0; cb < CB16; ++cb) {
+      const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + 16 * cb + 4 * gq);
+      const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+      double dd = 0.0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dd += (double)u[cb][e] * (double)pe[e];
+      pd[cb] = dd;
+    }
+#pragma unroll
+    for (int cb = 0; cb < CB16; ++cb) pd[cb] += shfl_xor_d(pd[cb], 16);
+#pragma unroll
+    for (int cb = 0; cb < CB16; ++cb) pd[cb] += shfl_xor_d(pd[cb], 32);
+    const double dot = (pd[0] + pd[1]) + (pd[2] + pd[3]);
+    const float q = (float)(dot - 1.0);
+    float yt = vpt ? ub.y : 0.f;
+    if (gate) yt = fmaf(gam, q, yt);
+    const float ybar = fmaf(gam, q, yt);
+    if (gate) *(vpt ? (B.y + pt) : B.dump) = yt;  // the four lanes of a row store the same value
+    {
+      const bool lead = vpt && gq == 0;
+      qq += lead ? (double)q * (double)q : 0.0;
+      yq += lead ? (double)yt * (double)q : 0.0;
+    }
+
+    // ---- epilogue (eq. entrywise-fusion).  W of the slab: kept in registers, staged
+    // fp32 in this wave's rows of the W tile (private to the wave until the barrier
+    // below) as the packed rows of U, so that it goes to HBM in whole, contiguous
+    // 1 KiB stores; then the same rows take its split for the second product ----
+    unsigned char* wst = wt + 16 * wave * P::WRS;
+    const int ru = r >> 2;  // 16-byte units per row of U
+    float wv[4 * CB16];
+#pragma unroll
+    for (int cb = 0; cb < CB16; ++cb) {
+      const int c = 16 * cb + 4 * gq;
+      const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+      const f32x4 sv = *reinterpret_cast<const f32x4*>(ssl + c);
+      const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+      const float se[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float uu = u[cb][e];
+        float t = fmaf(two_alpha_s, acc1[cb][e], uu);
+        t = fmaf(neg_alpha, ybar * pe[e], t);
+        t = fmaf(neg_alpha, se[e], t);
+        const float w = fmaxf(t, 0.f) * okf[cb];
+        wv[4 * cb + e] = w;
+        const double wd = (double)w, ud = (double)uu;
+        sa = fma(wd, wd, sa);
+        sb = fma(ud, ud, sb);
+        sh = fma(wd, ud, sh);
+      }
+      const f32x4 o = {wv[4 * cb + 0], wv[4 * cb + 1], wv[4 * cb + 2], wv[4 * cb + 3]};
+      // unit j ru + c / 4 of the packed slab (columns >= r to the last unit, never stored)
+      const int uq = (c < r) ? (j * ru + 4 * cb + gq) : (16 * P::WU - 1);
+      *reinterpret_cast<f32x4*>(wst + 16 * bf8::stage_slot(uq)) = o;
+    }
+    __builtin_amdgcn_wave_barrier();
+    {
+      const int64_t row0 = st * bf8::kRows + 16 * wave;
+      const int64_t rows = n - row0 < 16 ? n - row0 : 16;
+      const int nvalid = rows > 0 ? (int)rows * ru : 0;  // 16-byte units of the slab in U
+      char* sbase = reinterpret_cast<char*>(Udst + (rows > 0 ? row0 : 0) * (int64_t)r);
+#pragma unroll
+      for (int i = 0; i < 2 * NB; ++i) {  // 16 rows x R32 floats = 128 NB units
+        const int q = lane + 64 * i;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(wst + 16 * bf8::stage_slot(q));
+        if (q < nvalid) *reinterpret_cast<f32x4*>(sbase + 16u * (uint32_t)q) = v;
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int cb = 0; cb < CB16; ++cb) {
+      f16x4 hi, lo;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float ts = wv[4 * cb + e] * kWScale;
+        const _Float16 hh = (_Float16)ts;
+        hi[e] = hh;
+        lo[e] = (_Float16)(ts - (float)hh);
+      }
+      typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+      const u32x2 hu = __builtin_bit_cast(u32x2, hi);
+      const u32x2 lu = __builtin_bit_cast(u32x2, lo);
+      const f32x4 unit = {__uint_as_float(hu.x), __uint_as_float(hu.y), __uint_as_float(lu.x), __uint_as_float(lu.y)};
+      *reinterpret_cast<f32x4*>(wt + wrow + 16 * ((4 * cb + gq) ^ sj)) = bf8::unit_swap(unit, oddj);
+    }
+    // column sums of the slab, of W and of W ytilde_t (ytilde after this pass's dual
+    // step: the Gram terms of the next iteration's s): lane (j, gq) keeps the
+    // column of element j of its 16 values
+    {
+      float wy[4 * CB16];
+#pragma unroll
+      for (int k = 0; k < 4 * CB16; ++k) wy[k] = wv[k] * yt;
+      bf8::reduce_scatter16_row(wv, j);
+      bf8::reduce_scatter16_row(wy, j);
+      colacc += (double)wv[0];
+      colyacc += (double)wy[0];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    load_u(ub, st + step);  // factor rows and ytilde of the next tile
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+
+    // ---- second product: partial += Xhat_tile^T W_tile (this wave's block and
+    // steps), and the Gram block W_ga^T W_cb2 over this wave's four steps ----
+    // the wave's four Gram steps first: steps k = 0..3 are the tile's 16-row steps
+    // 4 gh + k, where the Gram block W_ga^T W_cb2 takes the W operand just read as
+    // its B operand; steps k = 4..7 are the tile's steps k - 4 gh
+    uint32_t xr[2][2], wr[2][2];
+    auto rebase = [&](int sign) {
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+#pragma unroll
+        for (int hl = 0; hl < 2; ++hl) {
+          xr[half][hl] = xa[half][hl] + (uint32_t)(sign * 64 * gh * P::XRS);
+          wr[half][hl] = wa[half][hl] + (uint32_t)(sign * 64 * gh * P::WRS);
+        }
+    };
+    auto p2 = [&](auto kc) {
+      constexpr int K = decltype(kc)::value;
+      f16x8 xh, xl, wh, wl;
+      bf8::step_reads<16 * K * P::XRS, 16 * K * P::WRS>(xr, wr, xh, xl, wh, wl);
+      acc2 = mfma32x32x16h(xh, wl, acc2);
+      acc2 = mfma32x32x16h(xl, wh, acc2);
+      acc2 = mfma32x32x16h(xh, wh, acc2);
+      if constexpr (K < 4) {
+        f16x8 gah, gal;
+        bf8::gram_reads<16 * K * P::WRS>(wg, gah, gal);
+        accg = mfma32x32x16h(gah, wl, accg);
+        accg = mfma32x32x16h(gal, wh, accg);
+        accg = mfma32x32x16h(gah, wh, accg);
+      }
+    };
+    rebase(1);
+    p2(std::integral_constant<int, 0>{});
+    p2(std::integral_constant<int, 1>{});
+    p2(std::integral_constant<int, 2>{});
+    p2(std::integral_constant<int, 3>{});
+    rebase(-1);
+    p2(std::integral_constant<int, 4>{});
+    p2(std::integral_constant<int, 5>{});
+    p2(std::integral_constant<int, 6>{});
+    p2(std::integral_constant<int, 7>{});
+    __syncthreads();
+  };
+
+  Buf A;
+  load_x(A, blockIdx.x);
+  load_u(ub, blockIdx.x);
+  for (int64_t st = blockIdx.x; st < T; st += step) tile(A, st, st + step);
+
+  // ---- statistics of this workgroup ----
+  {
+    const int col = 16 * (j >> 2) + 4 * gq + (j & 3);
+    colred[wave * R32 + col] = colacc;
+    colyred[wave * R32 + col] = colyacc;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    sa += shfl_xor_d(sa, m);
+    sb += shfl_xor_d(sb, m);
+    sh += shfl_xor_d(sh, m);
+    qq += shfl_xor_d(qq, m);
+    yq += shfl_xor_d(yq, m);
+  }
+  if (lane == 0) {
+    dred[8 * wave + 0] = sa;
+    dred[8 * wave + 1] = sb;
+    dred[8 * wave + 2] = sh;
+    dred[8 * wave + 3] = qq;
+    dred[8 * wave + 4] = yq;
+  }
+  // ---- partials of Xhat^T W_{t+1} (row splits in order, [f][c] order) and of
+  // W^T W (the two halves of each block in order, [k][l] order) ----
+  float* comb = reinterpret_cast<float*>(xt);   // RS2 x D32 x R32 (the tiles are no longer read)
+  float* gcomb = reinterpret_cast<float*>(wt);  // 2 x R32 x R32
+  const float unscale = (1.0f / sx) * (1.0f / kWScale);
+  {
+    const int h = lane >> 5, li = lane & 31;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int f = 32 * fb + 8 * (v >> 2) + 4 * h + (v & 3);
+      comb[(rsp * D32 + f) * R32 + 32 * cb2 + li] = acc2[v] * unscale;
+      const int k = 32 * ga + 8 * (v >> 2) + 4 * h + (v & 3);
+      gcomb[(gh * R32 + k) * R32 + 32 * cb2 + li] = accg[v] * (1.0f / (kWScale * kWScale));
+    }
+  }
+  __syncthreads();
+  double* out = B.b_part + (int64_t)blockIdx.x * (4 + R32);
+  double* aout = B.a_part + (int64_t)blockIdx.x * (4 + R32);
+  for (int c = tid; c < R32; c += bf8::kThreads8) {
+    const double* q = colred + c;
+    out[4 + c] = (((q[0] + q[R32]) + (q[2 * R32] + q[3 * R32])) + ((q[4 * R32] + q[5 * R32]) + (q[6 * R32] + q[7 * R32])));
+    const double* qy = colyred + c;
+    aout[4 + c] =
+        (((qy[0] + qy[R32]) + (qy[2 * R32] + qy[3 * R32])) + ((qy[4 * R32] + qy[5 * R32]) + (qy[6 * R32] + qy[7 * R32])));
+  }
+  if (tid < 5) {
+    const double* q = dred + tid;
+    const double v = (((q[0] + q[8]) + (q[16] + q[24])) + ((q[32] + q[40]) + (q[48] + q[56])));
+    if (tid < 3) out[tid] = v;
+    else aout[tid - 3] = v;  // ||q||^2, ytilde^T q
+  }
+  if (tid == 5) out[3] = 0.0;
+  if (tid == 6) aout[2] = 0.0;
+  if (tid == 7) aout[3] = 0.0;
+  float* part = B.theta_part + (int64_t)blockIdx.x * g.theta_cols;
+  for (int e = tid; e < D32 * R32; e += bf8::kThreads8) {
+    float acc = comb[e];
+#pragma unroll
+    for (int s2 = 1; s2 < P::RS2; ++s2) acc += comb[s2 * D32 * R32 + e];
+    part[e] = acc;
+  }
+  float* gpart = part + D32 * R32;  // W^T W follows Theta in the row
+  for (int e = tid; e < R32 * R32; e += bf8::kThreads8) gpart[e] = gcomb[e] + gcomb[R32 * R32 + e];
+}
+
+template <int NB, int NCH>
+static hipError_t pass_bf8_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  constexpr int lds = bf8::Shape<NB, NCH>::LDS;
+  static_assert(lds <= kMaxFusedLds, "LDS");
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_bf8<NB, NCH>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_pass_bf8<NB, NCH>), dim3(g.GB), dim3(bf8::kThreads8), lds, st, g, b, a);
+  return hipGetLastError();
+}
+
+// shapes of the eight-wave form
+bool fused8_shape(int NB, int nch) { return (NB == 2 && nch == 4); }
+
+static hipError_t pass_bf8_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  switch (g.NB * 10 + g.nch) {
+    case 24: return pass_bf8_launch<2, 4>(g, b, a, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <int NB, int NCH, bool SPLIT, bool UFLAT>
@@ -607,6 +1230,7 @@ static hipError_t pass_bf_dispatch(const Geometry& g, const Bufs& b, const StepA
 int fused_lds_need(int NB, int nch, bool split, bool uflat) { return fused_lds_bytes(NB, nch, split, uflat); }
 
 hipError_t launch_pass_bf(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  if (g.fused8) return pass_bf8_dispatch(g, b, a, st);
   if (g.uflat) return g.split_b ? pass_bf_dispatch<true, true>(g, b, a, st) : pass_bf_dispatch<false, true>(g, b, a, st);
   return g.split_b ? pass_bf_dispatch<true, false>(g, b, a, st) : pass_bf_dispatch<false, false>(g, b, a, st);
 }

@@ -25,11 +25,12 @@ __global__ void k_ctl_init(Bufs B, float gamma_f) {
     c->c_f = 1.0f;
     c->x_scale = 1.0f;
     c->th_scale = 1.0f;
-    c->pad_i1 = 0;
+    c->ubuf = 0;
     c->a = c->b = c->h = 0.0;
     c->Delta = c->delta = 0.0;
     c->rho = c->objective = c->theta_fro2 = 0.0;
     c->spectral_a = 1.0;
+    c->c_gram = 1.0;
   }
 }
 

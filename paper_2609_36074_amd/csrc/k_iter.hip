@@ -219,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
       __syncthreads();
     }
     if (ks == 0) {
-      float* part = B.theta_part + (int64_t)gx * g.d32 * r32;
+      float* part = B.theta_part + (int64_t)gx * g.theta_cols;
       const int lr = lane >> 5, lc = lane & 31;
 #pragma unroll
       for (int j = 0; j < NBG; ++j) {
@@ -272,7 +272,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
     Geometry g, Bufs B, StepArgs S) {
   constexpr bool FINISH = MODE == kPassFinish;
   constexpr bool THETA = MODE == kPassIter;
-  if (FINISH ? (B.ctl->breakdown != 0) : halted(B.ctl)) return;
+  // the iterate is in the workspace factor buffer after an odd number of one-pass
+  // iterations; the finish pass moves it to U
+  const float* Usrc = B.ctl->ubuf ? B.U2 : B.U;
+  if (FINISH && B.ctl->breakdown != 0) {
+    // the unnormalised update replaces the factor
+    if (B.ctl->ubuf) {
+      const int64_t tot = g.n * (int64_t)g.r;
+      for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < tot; e += (int64_t)gridDim.x * kThreads)
+        B.U[e] = B.U2[e];
+    }
+    return;
+  }
+  if (!FINISH && halted(B.ctl)) return;
   const bool stopped = FINISH && (B.ctl->stop != 0);
   constexpr int NBLK = FV * NGF * CV;  // 16x16 blocks of Theta
   // k-steps in flight: fewer when Theta takes 128 registers, more when only U and y stream
@@ -336,7 +348,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
         load_vec<FV>(xr[slot][gg], B.X + rr * d + (f < d ? f : 0), true);
       }
     }
-    load_vec<CV>(ur[slot], B.U + rr * r + (cx ? cu : 0), true);
+    load_vec<CV>(ur[slot], Usrc + rr * r + (cx ? cu : 0), true);
     yr[slot] = B.y[rr];
   };
 #pragma unroll
@@ -427,7 +439,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
         }
     }
     __syncthreads();
-    float* part = B.theta_part + (int64_t)blockIdx.x * g.d32 * g.r32;
+    float* part = B.theta_part + (int64_t)blockIdx.x * g.theta_cols;
     const int tot = g.d32 * g.r32;
     for (int e = tid; e < tot; e += kThreads) {
       const int f = e / g.r32, col = e - (e / g.r32) * g.r32;
@@ -500,13 +512,30 @@ __global__ __launch_bounds__(kThreads) void k_seg_sum(const T* __restrict__ P, i
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, int nseg, int scaled) {
   if (halted(B.ctl)) return;
-  __shared__ double red[8];
+  __shared__ double red[kThreads];
   __shared__ float mred[4];
+  if (blockIdx.x >= g.RT) {
+    // one-pass iteration: the W^T W columns of the partial rows, times P (the column
+    // sums of W, already reduced): (W^T W P)_k, each row's products added in a tree
+    const int r32 = g.r32;
+    const int e = (blockIdx.x - g.RT) * kThreads + threadIdx.x;  // entry k r32 + l
+    const int k = e / r32, l = e - k * r32;
+    double G = 0.0;
+    for (int s = 0; s < nseg; ++s) G += B.seg_theta[(int64_t)s * g.theta_cols + (int64_t)g.d32 * r32 + e];
+    red[threadIdx.x] = G * B.gram_vec[l];
+    __syncthreads();
+    for (int w = r32 >> 1; w >= 1; w >>= 1) {
+      if (l < w) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + w];
+      __syncthreads();
+    }
+    if (l == 0) B.gram_vec[2 * r32 + k] = red[threadIdx.x];
+    return;
+  }
   const int64_t tot = (int64_t)g.d32 * g.r32;
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   double sum = 0.0;
   if (e < tot) {
-    for (int s = 0; s < nseg; ++s) sum += B.seg_theta[(int64_t)s * tot + e];
+    for (int s = 0; s < nseg; ++s) sum += B.seg_theta[(int64_t)s * g.theta_cols + e];
     const int f = (int)(e / g.r32);
     // partials of Xhat^T W (fused pass B) carry the scale c of U = c W
     if (scaled) sum *= (double)B.ctl->c_f;
@@ -537,7 +566,10 @@ __global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs
   if (ctl->breakdown) return;
   if (ctl->stop) {
     // stopped earlier in this call: the finish pass only materialised U
-    if (finish && threadIdx.x == 0) ctl->c_f = 1.0f;
+    if (finish && threadIdx.x == 0) {
+      ctl->c_f = 1.0f;
+      ctl->ubuf = 0;
+    }
     return;
   }
   __shared__ double red[8];
@@ -586,7 +618,10 @@ __global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs
       cur->stop = 0;
       cur->breakdown = 0;
     }
-    if (finish) ctl->c_f = 1.0f;
+    if (finish) {
+      ctl->c_f = 1.0f;
+      ctl->ubuf = 0;
+    }
   }
 }
 
@@ -1061,6 +1096,162 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
 }
 
 // ---------------------------------------------------------------------------
+// One-pass iteration (the eight-wave fused pass B does the row work too), control
+// after the pass (one workgroup).  The pass did the row work of this iteration --
+// the end of the previous one: its gated dual step, q and the objective terms --
+// before the primal step, so the stopping rule of the previous iteration is decided
+// here, after the fact: when it fires, this iteration's W (written to the other
+// factor buffer) and partials are discarded and the iterate stays the previous
+// one.  Otherwise as k_ctl_b, then the column sums P of W and W^T ytilde for the
+// next iteration's s (k_s_gram).  S.row_pass: the row pass did this iteration's
+// row work (k_ctl_a has already decided the stopping rule and the record).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_ctl_one(Geometry g, Bufs B, StepArgs S) {
+  DevCtl* ctl = B.ctl;
+  if (halted(ctl)) return;
+  __shared__ double red[8];
+  __shared__ double cbuf[1];
+  __shared__ int sflag[1];
+  const int tid = threadIdx.x;
+  double th2 = 0.0;
+  for (int k = tid; k < g.RT; k += kThreads) th2 += B.th2_part[k];
+  th2 = block_sum_d(th2, red);
+  if (tid == 0) {
+    int stopped = 0;
+    const int64_t t = ctl->t_done;
+    if (!S.row_pass) {
+      const double qq = B.seg_a[0], yq = B.seg_a[1];
+      const double rho = sqrt(qq * S.inv_n);
+      ctl->rho = rho;
+      if (S.end_work && t > 0) {
+        nlr_iter_stats* prev = &B.hist[(t - 1) % kHistCap];
+        const int stop = (ctl->Delta < S.eps_d * S.eps_d * S.K) && (ctl->delta < S.eps_c) &&
+                         (rho < S.eps_c) && (t >= S.T_min);
+        prev->rho = rho;
+        prev->stop = stop;
+        if (stop) {
+          ctl->stop = 1;
+          stopped = 1;
+        }
+      }
+      if (!stopped) {
+        const double obj = -th2 + yq + 0.5 * S.beta * S.inv_n * qq;
+        ctl->objective = obj;
+        ctl->theta_fro2 = th2;
+        nlr_iter_stats* cur = &B.hist[t % kHistCap];
+        cur->t = t;
+        cur->objective = obj;
+        cur->theta_fro2 = th2;
+        cur->rho = 0.0;
+        cur->stop = 0;
+      }
+    }
+    sflag[0] = stopped;
+    cbuf[0] = 0.0;
+    if (!stopped) {
+      const double a = B.seg_b[0], b = B.seg_b[1], h = B.seg_b[2];
+      const double nu = sqrt(a);
+      nlr_iter_stats* rec = &B.hist[t % kHistCap];
+      rec->a = a;
+      rec->b = b;
+      rec->h = h;
+      rec->dual_step = 0;
+      rec->breakdown = 0;
+      // W_{t+1} is in the other buffer from here on (on breakdown it replaces the factor)
+      ctl->ubuf ^= 1;
+      if (!(nu > 1e-20) || !isfinite(a)) {
+        ctl->breakdown = 1;
+        rec->breakdown = 1;
+        rec->c = 0.f;
+        rec->delta = 0.0;
+      } else {
+        const float cf = (float)(sqrt(S.K) / nu);
+        const double c = (double)cf;
+        double D = c * c * a + b - 2.0 * c * h;
+        if (D < 0.0) D = 0.0;
+        const double delta = sqrt(D) / sqrt(S.K);
+        const int gate = D < S.eps_d * S.eps_d * S.K;
+        ctl->a = a;
+        ctl->b = b;
+        ctl->h = h;
+        ctl->Delta = D;
+        ctl->delta = delta;
+        ctl->gate = gate;
+        ctl->c_f = cf;
+        ctl->c_gram = c;
+        ctl->t_done = t + 1;
+        rec->c = cf;
+        rec->delta = delta;
+        rec->dual_step = gate;
+        cbuf[0] = c;
+      }
+    }
+  }
+  __syncthreads();
+  if (sflag[0]) return;
+  const double c = cbuf[0];
+  if (c > 0.0) {
+    for (int col = tid; col < g.r32; col += kThreads) {
+      const double P = B.seg_b[4 + col], wy = B.seg_a[4 + col];
+      B.p[col] = (col < g.r) ? (float)(c * P) : 0.f;
+      B.gram_vec[col] = P;
+      B.gram_vec[g.r32 + col] = wy;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fixed-order sums over the GB rows of the one-pass iteration's per-workgroup
+// statistics, one segment each: blockIdx.y 0 a_part -> seg_a, 1 b_part -> seg_b.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_seg_ab(Geometry g, Bufs B) {
+  if (halted(B.ctl)) return;
+  __shared__ double red[kThreads];
+  const double* P = blockIdx.y ? B.b_part : B.a_part;
+  double* out = blockIdx.y ? B.seg_b : B.seg_a;
+  const int C = 4 + g.r32;
+  const int tid = threadIdx.x;
+  // 8 columns x 32 row phases per block; the phases are added in a fixed tree
+  const int col = blockIdx.x * 8 + (tid & 7);
+  const int sub = tid >> 3;
+  double acc = 0.0;
+  if (col < C)
+    for (int64_t row = sub; row < g.GB; row += 32) acc += P[row * C + col];
+  red[tid] = acc;
+  __syncthreads();
+  for (int w = 16; w >= 1; w >>= 1) {
+    if (sub < w) red[tid] = red[tid] + red[tid + 8 * w];
+    __syncthreads();
+  }
+  if (tid < 8 && col < C) out[col] = red[tid];
+}
+
+// ---------------------------------------------------------------------------
+// s = U^T ybar of the one-pass iteration from the Gram terms of the pass that
+// produced U = c W (one workgroup).  Per row q = u.p - 1 = c^2 w.P - 1 and
+// ybar = ytilde_prev + (1 + gate) gamma q (the pending gated dual step, then the
+// penalty term; gamma = beta / n), so
+//   s = c W^T ytilde_prev + (1 + gate) gamma c (c^2 (W^T W) P - P)
+// with W^T W (the columns after Theta in the Theta partial rows, reduced with them
+// and multiplied by P in k_reduce_theta), P and W^T ytilde_prev summed in a fixed
+// order (FP64).  The last term
+// is U^T q: small near feasibility and weighted by gamma, so the fp32-accumulated
+// Gram partials carry it well below the iteration's rounding.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_s_gram(Geometry g, Bufs B, StepArgs S) {
+  const DevCtl* ctl = B.ctl;
+  if (halted(ctl)) return;
+  const int r32 = g.r32;
+  const int k = threadIdx.x;
+  if (k >= r32) return;
+  const double c = ctl->c_gram;
+  const double gmul = (1.0 + (ctl->gate ? 1.0 : 0.0)) * (double)S.gamma_f;
+  const double P = B.gram_vec[k], wy = B.gram_vec[r32 + k], gp = B.gram_vec[2 * r32 + k];
+  const double sk = c * wy + gmul * c * (c * c * gp - P);
+  B.s[k] = (k < g.r) ? (float)sk : 0.f;
+}
+
+// ---------------------------------------------------------------------------
 // Row-argmax labels, lowest index on ties.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_labels(Geometry g, const float* __restrict__ U,
@@ -1162,7 +1353,7 @@ hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bo
 }
 
 hipError_t launch_seg_theta(const Geometry& g, const Bufs& b, int64_t rows, int nseg, hipStream_t st) {
-  const int C = g.d32 * g.r32;
+  const int C = g.theta_cols;
   hipLaunchKernelGGL((k_seg_sum<float>), dim3((C + 63) / 64, nseg), dim3(kThreads), 0, st,
                      (const float*)b.theta_part, rows, C, b.seg_theta, nseg, (const DevCtl*)b.ctl, 1);
   return hipGetLastError();
@@ -1170,12 +1361,15 @@ hipError_t launch_seg_theta(const Geometry& g, const Bufs& b, int64_t rows, int 
 
 hipError_t launch_reduce_theta_rows(const Geometry& g, const Bufs& b, int64_t rows, int nseg, bool scaled,
                                     hipStream_t st) {
-  const int C = g.d32 * g.r32;
+  const int C = g.theta_cols;
   hipLaunchKernelGGL((k_seg_sum<float>), dim3((C + 63) / 64, nseg), dim3(kThreads), 0, st,
                      (const float*)b.theta_part, rows, C, b.seg_theta, nseg, (const DevCtl*)b.ctl, 1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT), dim3(kThreads), 0, st, g, b, nseg, scaled ? 1 : 0);
+  // one-pass iteration (partials of its pass): blocks after the RT Theta blocks form
+  // (W^T W) P from the r32 r32 Gram entries
+  const int gb = (g.fused8 && scaled) ? (g.r32 * g.r32) / kThreads : 0;
+  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT + gb), dim3(kThreads), 0, st, g, b, nseg, scaled ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -1263,6 +1457,22 @@ hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hi
 
 hipError_t launch_ctl_b(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(k_ctl_b, dim3(1), dim3(kThreads), 0, st, g, b, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ctl_one(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_ctl_one, dim3(1), dim3(kThreads), 0, st, g, b, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_s_gram(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_s_gram, dim3(1), dim3(64), 0, st, g, b, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_seg_ab(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int C = 4 + g.r32;
+  hipLaunchKernelGGL(k_seg_ab, dim3((C + 7) / 8, 2), dim3(kThreads), 0, st, g, b);
   return hipGetLastError();
 }
 

@@ -84,19 +84,6 @@ __device__ __forceinline__ pf16x4 lds_tr16(const _Float16* p) {
   return o;
 }
 
-// Fixed-order sum over a 512-thread workgroup; result valid in thread 0.
-__device__ __forceinline__ double block_sum8_d(double v, double* red) {
-  for (int m = 32; m >= 1; m >>= 1) v += shfl_xor_d(v, m);
-  const int w = threadIdx.x >> 6;
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) red[w] = v;
-  __syncthreads();
-  double r = 0.0;
-  if (threadIdx.x == 0) r = (((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7])));
-  __syncthreads();
-  return r;
-}
-
 // ===========================================================================
 // Pass A
 // ===========================================================================
@@ -453,7 +440,7 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
   // ---- Theta partial of this split: rows of this feature block ----
   {
     const float unscale = (1.0f / B.ctl->x_scale) * (1.0f / su);
-    float* part = B.theta_part + (int64_t)sp * g.d32 * g.r32;
+    float* part = B.theta_part + (int64_t)sp * g.theta_cols;
     const int h = lane >> 5, li = lane & 31;
 #pragma unroll
     for (int i = 0; i < 2; ++i)

@@ -38,7 +38,7 @@ __global__ __launch_bounds__(kThreads) void k_start_m(Geometry g, Bufs B) {
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (e >= tot) return;
   double sum = 0.0;
-  for (int s = 0; s < g.SA; ++s) sum += B.seg_theta[(int64_t)s * tot + e];
+  for (int s = 0; s < g.SA; ++s) sum += B.seg_theta[(int64_t)s * g.theta_cols + e];
   const int f = (int)(e / g.r32), c = (int)(e % g.r32);
   if (f < g.d && c < g.r) B.s_M[(int64_t)f * g.r + c] = sum;
 }

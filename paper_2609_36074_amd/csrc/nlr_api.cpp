@@ -116,10 +116,13 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   const bool uflat = r % 4 != 0;
   g.fused = (fused && shape_f && fused_lds_need(g.NB, g.nch, split, uflat) <= kMaxFusedLds) ? 1 : 0;
   g.uflat = (g.fused && uflat) ? 1 : 0;
+  g.fused8 = (g.fused && split && !uflat && fused8_shape(g.NB, g.nch)) ? 1 : 0;
+  // the one-pass iteration's W^T W partials follow its Theta partials in one row
+  g.theta_cols = g.d32 * g.r32 + (g.fused8 ? g.r32 * g.r32 : 0);
   g.SAF = g.SA;
   if (g.fused) {
     // persistent grid: one (two for the shapes with two waves per SIMD) workgroup per CU
-    const int64_t gmax = (g.NB == 1 && g.nch <= 2) ? 512 : 256;
+    const int64_t gmax = (!g.fused8 && g.NB == 1 && g.nch <= 2) ? 512 : 256;
     g.GB = (int32_t)(g.tilesB < gmax ? g.tilesB : gmax);
     g.SB = (g.GB + 31) / 32;
     g.SAF = (g.GB + 31) / 32;
@@ -217,14 +220,19 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.b_part = reinterpret_cast<double*>(take((size_t)g.GB * (4 + r32) * 8));
   int64_t arows = g.GA > g.GAF ? g.GA : g.GAF;
   if (g.panel && (int64_t)g.PS * g.pfb > arows) arows = (int64_t)g.PS * g.pfb;  // one row per pass-A workgroup
+  if (g.fused8 && (int64_t)g.GB > arows) arows = g.GB;  // the one-pass iteration's row statistics
   b.a_part = reinterpret_cast<double*>(take((size_t)arows * (4 + r32) * 8));
   const size_t segs = (size_t)(g.SA > g.SAF ? g.SA : g.SAF);
-  b.seg_theta = reinterpret_cast<double*>(take(segs * g.d32 * r32 * 8));
+  b.seg_theta = reinterpret_cast<double*>(take(segs * (size_t)g.theta_cols * 8));
   b.seg_a = reinterpret_cast<double*>(take((size_t)g.SA * (4 + r32) * 8));
   b.seg_b = reinterpret_cast<double*>(take((size_t)g.SB * (4 + r32) * 8));
   b.i_xbar = reinterpret_cast<double*>(take(d * 8));
   b.dump = reinterpret_cast<float*>(take(256));
   b.thmax_part = reinterpret_cast<float*>(take((size_t)g.RT * 4));
+  if (g.fused8) {
+    b.U2 = reinterpret_cast<float*>(take((size_t)g.n * (size_t)g.r * 4));
+    b.gram_vec = reinterpret_cast<double*>(take(3 * r32 * 8));
+  }
   if (g.panel) {
     b.ybar = reinterpret_cast<float*>(take((size_t)g.n * 4));
     b.theta_split = take((size_t)((g.d + 15) / 16) * 64 * g.pnbw * 64);
@@ -237,7 +245,7 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   // union: pass-A Theta partials | init temporaries
   size_t prow = (size_t)(g.GA > g.GB ? g.GA : g.GB);  // pass A or fused pass B partials
   if (g.panel && (size_t)g.PS > prow) prow = (size_t)g.PS;
-  const size_t u_iter = align256(prow * g.d32 * r32 * 4);
+  const size_t u_iter = align256(prow * (size_t)g.theta_cols * 4);
   size_t u_init = 0;
   u_init += align256((size_t)g.GI * d * 8);            // colsum
   u_init += align256((size_t)g.GG * d * d * 8);         // gram partials
@@ -296,6 +304,7 @@ struct nlr_ctx {
   int device;
   nlr_params prm;
   bool pending;       // end-of-iteration work of the latest pass B not yet applied
+  bool gram_valid;    // one-pass iteration: the Gram terms of the latest pass give the next s
   bool failed;        // sticky failure
   bool breakdown;
   int64_t t_host;     // last known iteration counter
@@ -408,6 +417,30 @@ static hipError_t prof_collect(nlr_ctx* c) {
 
 static nlr_status enqueue_iteration(nlr_ctx* c) {
   const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
+  if (c->g.fused8) {
+    // one pass over the rows per iteration: the pass does the row work of the
+    // iteration (the end of the previous one) as well as the primal step, reading
+    // the factor from one buffer and writing W to the other; s comes from the Gram
+    // terms of the previous pass (k_s_gram), or, when there is no previous pass
+    // (after init or a stop), from the row pass
+    StepArgs ap = a;
+    if (!c->gram_valid) {
+      LAUNCH(KK_PASS_U, launch_pass_u(c->g, c->b, a, c->stream));
+      LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
+      LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
+      ap.end_work = 0;
+      ap.row_pass = 1;
+    } else {
+      LAUNCH(KK_CTL_A, launch_s_gram(c->g, c->b, a, c->stream));
+    }
+    LAUNCH(KK_PASS_BF, launch_pass_bf(c->g, c->b, ap, c->stream));
+    LAUNCH(KK_CTL_B, launch_seg_ab(c->g, c->b, c->stream));
+    LAUNCH(KK_CTL_B, launch_ctl_one(c->g, c->b, ap, c->stream));
+    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, true, c->stream));
+    c->gram_valid = true;
+    c->pending = true;
+    return NLR_OK;
+  }
   if (c->g.fused) {
     // row pass (end of the previous iteration, s, rho, objective terms), control,
     // fused pass B (W and the partials of Xhat^T W), control, Theta of the new factor
@@ -520,6 +553,7 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   c->stream = reinterpret_cast<hipStream_t>(stream);
   c->prm = *params;
   c->pending = false;
+  c->gram_valid = false;
   c->failed = false;
   c->breakdown = false;
   c->t_host = 0;
@@ -634,6 +668,9 @@ nlr_status nlr_run(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* l
   if (prof_collect(c) != hipSuccess) return hip_fail(c);
   const int64_t t1 = c->host_ctl->t_done;
   if (iters_done) *iters_done = (int32_t)(t1 - t0);
+  // a stop may have discarded the latest pass of the one-pass iteration: the next
+  // iteration forms s from the rows again
+  if (c->host_ctl->stop || c->host_ctl->breakdown) c->gram_valid = false;
   if (c->host_ctl->breakdown) {
     c->failed = true;
     c->breakdown = true;

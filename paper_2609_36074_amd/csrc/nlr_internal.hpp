@@ -30,7 +30,7 @@ struct alignas(16) DevCtl {
   float c_f;           // lazy scale of the factor buffer (1 when materialised)
   float x_scale;       // power of two keeping |Xhat| x_scale < 2^15 (split-fp16 products)
   float th_scale;      // power of two keeping |Theta| th_scale < 2^15 (panel pass B operand)
-  int32_t pad_i1;
+  int32_t ubuf;        // factor buffer of the current iterate: 0 the caller's U, 1 the workspace copy
   double a, b, h;      // fused statistics of the latest primal step
   double Delta;        // squared movement estimate
   double delta;        // movement estimate
@@ -38,6 +38,7 @@ struct alignas(16) DevCtl {
   double objective;    // fhat at the start of the latest iteration
   double theta_fro2;
   double spectral_a;   // ||X_c||_2
+  double c_gram;       // scale c of the factor whose Gram terms are stored (one-pass iteration)
 };
 
 // Scalars of one iteration, passed by value.
@@ -53,7 +54,7 @@ struct StepArgs {
   double inv_n;
   int64_t T_min;
   int32_t end_work;    // apply the pending end-of-iteration vector work (dual step, rho, stop test)
-  int32_t pad2;
+  int32_t row_pass;    // one-pass iteration: the row pass already did this iteration's row work
 };
 
 // Launch geometry; a pure function of (n, d, r) so that reduction orders,
@@ -84,6 +85,8 @@ struct Geometry {
   int32_t split_a, split_b;  // 1: split-fp16 products in pass A / pass B
   int32_t fused;        // 1: single-Xhat-pass iteration (row pass + fused pass B)
   int32_t uflat;        // 1: the fused pass B moves U as whole 32-row slabs (r % 4 != 0)
+  int32_t fused8;       // 1: the fused pass B in its eight-wave form (k_pass_bf8), one-pass iteration
+  int32_t theta_cols;   // floats per row of the Theta partials: d32 r32 (+ r32 r32 of W^T W, one-pass)
   int32_t SAF;          // segments of the fused pass B Theta partials (GB rows)
   int32_t ldsB_bytes;
   // init
@@ -112,7 +115,7 @@ struct Bufs {
   float* theta;        // d32*r32, pass-B operand layout
   float* p;            // r32
   float* s;            // r32
-  float* theta_part;   // GA x d32 x r32
+  float* theta_part;   // rows of theta_cols floats (GA, GB or PS rows)
   double* a_part;      // GA x (4 + r32): ||q||^2, ytilde^T q, -, -, s partials
   double* seg_theta;   // SA x d32*r32: segment sums of theta_part
   double* seg_a;       // SA x (4 + r32)
@@ -123,6 +126,9 @@ struct Bufs {
   float* thmax_part;   // RT: per-workgroup max |Theta| of the reduction
   float* ybar;         // n: ybar of the current iteration (panel form: pass A -> pass B)
   void* theta_split;   // panel form: split Theta^T chunks, 64 bytes per (16 features, column)
+  // one-pass iteration (eight-wave fused pass B)
+  float* U2;           // n x r: second factor buffer (pass reads one, writes the other)
+  double* gram_vec;    // 3 r32: column sums P of W, W^T ytilde, (W^T W) P (fixed-order sums)
   // init temporaries (alias the pass-A partial region)
   double* i_colsum;    // GI x d
   double* i_xbar;      // d
@@ -164,6 +170,7 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
                        bool fused = false);
 // dynamic LDS of the fused pass B for (NB, nch, split, U moved as whole slabs)
 int fused_lds_need(int NB, int nch, bool split, bool uflat);
+bool fused8_shape(int NB, int nch);
 constexpr int kMaxFusedLds = 160 << 10;
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
 
@@ -205,6 +212,9 @@ hipError_t launch_pass_b_panel(const Geometry& g, const Bufs& b, const StepArgs&
 hipError_t launch_split_x8(const Geometry& g, const Bufs& b, hipStream_t st);
 // a_part rows written by the latest producer (pass A grid, finish grid or panel splits)
 hipError_t launch_seg_a_rows(const Geometry& g, const Bufs& b, int64_t rows, bool finish, hipStream_t st);
+hipError_t launch_ctl_one(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_s_gram(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_seg_ab(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_reduce_theta_rows(const Geometry& g, const Bufs& b, int64_t rows, int nseg, bool scaled,
                                     hipStream_t st);
 

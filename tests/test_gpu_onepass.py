@@ -1,0 +1,129 @@
+"""The one-pass iteration (97..128 features, 33..64 columns, split products): one
+pass over the rows per iteration does the row work of the iteration (the end of
+the previous one) and the primal step, reading the factor from one buffer and
+writing W to the other; s comes from the Gram terms of the previous pass, and
+the stopping rule of an iteration is decided after the next pass, which is then
+discarded.  Checked against the fp64 oracle as the other forms: trajectories
+with gated dual steps, bitwise equality of nlr_run and nlr_step, the stopping
+rule, and breakdown (the unnormalised update, written to the workspace buffer,
+replaces the factor).
+"""
+import numpy as np
+import pytest
+
+from gpu_util import OBJ_TOL, U_TOL, host, log, make_ctx, rel_max_err, trajectory
+from oracle import nlr as onlr
+from synth import gaussian_mixture, standard_normal_factor
+
+pytestmark = pytest.mark.gpu
+
+SPLIT = 8  # NLR_INIT_SPLIT_F16
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_36074_amd import nlr
+    nlr.load_library()
+
+
+def _gated(d, r):
+    """A 3000-row mixture (seed 1) on which, with alpha = 1.8/(2 L0), beta = 2, eps_d = 3e-3 and
+    eps_c = 1e-3, the oracle stops after 432 iterations with 144 dual steps at d = 100, r = 36, and
+    after 564 with 244 at d = 128, r = 64 (first dual steps near iteration 25)."""
+    K, beta = 4, 2.0
+    X, lab, _ = gaussian_mixture(3000, d, K, 25.0, seed=1)
+    Z = standard_normal_factor(3000, r, seed=2).astype(np.float64)
+    return X, Z, K, beta, 1.8 * onlr.default_step_size(K, beta)
+
+
+# the oracle takes 162 dual steps in 450 iterations (d = 100) and 280 in 600 (d = 128)
+@pytest.mark.parametrize("d,r,T", [(100, 36, 450), (128, 64, 600)])
+def test_onepass_gated_trajectory(d, r, T):
+    X, Z, K, beta, alpha = _gated(d, r)
+    log(f"one-pass gated trajectory d={d} r={r} T={T}")
+    _, _, traj, obj, bad_gates, one, _, stats = trajectory(X, Z, K, alpha, beta, T, eps_d=3e-3, eps_c=1e-7,
+                                                           one_step_tol=True, flags=SPLIT)
+    ngates = sum(s["dual_step"] for s in stats)
+    log(f"  dual steps {ngates}; traj {max(traj):.3e} one {max(one):.3e} obj {max(obj):.3e}")
+    assert ngates > 100
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates, bad_gates
+
+
+def test_onepass_run_equals_steps_bitwise():
+    X, Z, K, beta, alpha = _gated(100, 36)
+    kw = dict(eps_d=3e-3, eps_c=1e-7, T_min=0, flags=SPLIT)
+    a = make_ctx(X, Z, K, alpha, beta, **kw)
+    b = make_ctx(X, Z, K, alpha, beta, **kw)
+    c = make_ctx(X, Z, K, alpha, beta, **kw)
+    T = 451  # odd: the last pass writes the workspace buffer; 162 dual steps in the first 450
+    done, _ = a.run(T)
+    assert done == T
+    done_c, _ = c.run(T)
+    for _ in range(T):
+        b.step(with_stats=False)
+    for name in ("U", "y"):
+        ua, ub, uc = host(getattr(a, name)), host(getattr(b, name)), host(getattr(c, name))
+        assert np.array_equal(ua, ub), name
+        assert np.array_equal(ua, uc), name
+    assert sum(h["dual_step"] for h in a.history(T)) > 50
+    # two runs continue as one
+    d = make_ctx(X, Z, K, alpha, beta, **kw)
+    d.run(200)
+    d.run(251)
+    assert np.array_equal(host(d.U), host(a.U)) and np.array_equal(host(d.y), host(a.y))
+
+
+@pytest.mark.parametrize("d,r,expect", [(100, 36, 432), (128, 64, 564)])
+def test_onepass_stop_rule(d, r, expect):
+    X, Z, K, beta, alpha = _gated(d, r)
+    eps_d, eps_c = 3e-3, 1e-3
+    ctx = make_ctx(X, Z, K, alpha, beta, eps_d=eps_d, eps_c=eps_c, T_min=5, flags=SPLIT)
+    done, last = ctx.run(3000)
+    log(f"one-pass d={d} r={r}: stopped after {done} iterations (oracle {expect}): {last}")
+    assert done < 3000 and last["stop"] == 1
+    assert last["delta"] < min(eps_d, eps_c) and last["rho"] < eps_c and done >= 5
+    hist = ctx.history(4096)
+    assert len(hist) == done
+    for h in hist[:-1]:
+        assert not (h["delta"] < min(eps_d, eps_c) and h["rho"] < eps_c and h["t"] + 1 >= 5), h
+    gates = [bool(h["dual_step"]) for h in hist]
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    ref = onlr.run(Xh, Z, K, alpha, beta, T=done, T_min=5, eps_d=eps_d, eps_c=eps_c, gates=gates)
+    rec = ref.records[-1]
+    band = 1e-3
+    assert rec.delta < min(eps_d, eps_c) * (1 + band) and rec.rho < eps_c * (1 + band)
+    assert rel_max_err(host(ctx.U), ref.U) < U_TOL
+    ys = onlr.stored_dual(ref.y)
+    assert np.abs(host(ctx.y) - ys).max() <= 1e-4 * np.abs(ys).max()
+    # a second run continues from the stopped iterate
+    more, _ = ctx.run(5)
+    assert more >= 1
+
+
+@pytest.mark.parametrize("steps_first", [0, 1])
+def test_onepass_breakdown(steps_first):
+    """A step that leaves no positive entry: the unnormalised update (zero) replaces the factor,
+    on the first iteration after init (s from the row pass) and after a run (s from the Gram terms)."""
+    from paper_2609_36074_amd import nlr
+    n, K = 200, 3
+    X, _, _ = gaussian_mixture(n, 100, 2, 9.0, seed=10)
+    Z = np.ones((n, 36))
+    alpha_bad = 1.0 / (2 * 1.0 * (K - 1)) * 1.5
+    if steps_first:
+        # one good iteration first, then a step size that leaves every entry below -0.4
+        ctx = make_ctx(X, np.abs(standard_normal_factor(n, 36, seed=3)), K, 1e-3, 1.0, flags=SPLIT)
+        ctx.run(1)
+        ctx.set_params(alpha=100.0 / (2 * 1.0 * (K - 1)))
+    else:
+        ctx = make_ctx(X, Z, K, alpha_bad, 1.0, flags=SPLIT)
+    with pytest.raises(nlr.NlrError) as e:
+        ctx.run(1)
+    assert e.value.status == nlr.NLR_EBREAKDOWN
+    assert np.all(host(ctx.U) == 0.0)
+    with pytest.raises(nlr.NlrError) as e:
+        ctx.run(3)
+    assert e.value.status == nlr.NLR_ESTATE

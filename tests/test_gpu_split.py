@@ -71,6 +71,42 @@ def test_split_ragged(n, d, r, K):
     assert not bad_gates
 
 
+# The eight-wave fused pass B (d in 97..128, r in 33..64, r % 4 == 0): one tile per
+# workgroup (tail only), 2-3 and 3-4 tiles per workgroup (loop and tail), padded
+# features (d < 128) and masked columns (r < 64).
+@pytest.mark.parametrize("n,d,r,K", [(130, 128, 64, 64), (70001, 104, 40, 20), (98381, 128, 64, 30),
+                                     (5000, 100, 44, 11), (131072, 128, 64, 64)])
+def test_split_fused8(n, d, r, K):
+    log(f"split fused8: n={n} d={d} r={r} K={K}")
+    X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 5 + d)
+    Z = standard_normal_factor(n, r, seed=n + 3 * r).astype(np.float64)
+    _, _, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, onlr.default_step_size(K), 1.0, 6,
+                                                       one_step_tol=True, flags=SPLIT)
+    log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates
+
+
+def test_split_fused8_run_equals_steps_and_deterministic():
+    X, _, _ = gaussian_mixture(70001, 104, 20, 16.0, seed=11)
+    Z = standard_normal_factor(70001, 40, seed=12).astype(np.float64)
+    K = 20
+    kw = dict(eps_d=1e-9, eps_c=1e-12, T_min=0, flags=SPLIT)
+    alpha = onlr.default_step_size(K)
+    a = make_ctx(X, Z, K, alpha, 1.0, **kw)
+    b = make_ctx(X, Z, K, alpha, 1.0, **kw)
+    c = make_ctx(X, Z, K, alpha, 1.0, **kw)
+    T = 25
+    done, _ = a.run(T)
+    assert done == T
+    for _ in range(T):
+        b.step(with_stats=False)
+    c.run(T)
+    Ua, Ub, Uc = host(a.U), host(b.U), host(c.U)
+    assert np.array_equal(Ua, Ub) and np.array_equal(host(a.y), host(b.y))
+    assert np.array_equal(Ua, Uc) and np.array_equal(host(a.y), host(c.y))
+
+
 def test_split_gmm1m():
     X, Z, _, wl = make_workload("gmm1m")
     Z = Z.astype(np.float64)
