@@ -24,7 +24,7 @@
 // At the end the four waves' partials are added in a fixed order and written as
 // this workgroup's partial; a fixed-order reduction and the scale c_{t+1} give
 // Theta_{t+1}.  Split shapes with 97..128 features and 33..64 columns run the
-// eight-wave form k_pass_bf8 further below instead.
+// one-pass iteration kernel k_pass_bf8 further below instead.
 // SPLIT: both products use the two-term fp16 split of k_split.hip; otherwise
 // fp32 matrix cores (32x32x2 for phase 1, 16x16x4 for phase 2).
 #include <type_traits>
@@ -578,26 +578,34 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_
 }
 
 // ===========================================================================
-// Eight-wave form of the split fused pass B (written for 32-feature chunks NCH in
-// {1, 2, 4} and 32-column blocks NB in {1, 2}; dispatched for NCH = 4, NB = 2, with
-// 16-byte aligned rows and r % 4 == 0).
+// One-pass iteration kernel: the eight-wave form of the split fused pass B, which
+// also does the iteration's row work (97..128 features, 33..64 columns, 16-byte
+// aligned rows, r % 4 == 0).
 //
 // The form above keeps the whole d x r partial of Xhat^T W in every wave, which
-// leaves room for one wave per SIMD only, and its prefetched rows then wait in
-// spare registers.  Here one 512-thread workgroup per compute unit walks
-// 128-row tiles; wave w owns the 16-row slab 16w .. 16w + 15 of a tile for the
-// first product (16x16x32 fp16 matrix cores: lane l holds row l % 16 and, of
-// each 16-column block, the columns 4 (l / 16) .. + 3) and the epilogue, and the
-// second product is shared out by blocks of the result: wave w owns the 32
-// features 32 (w % NCH) .. + 31 of the partial, all columns, over the 16-row
-// steps NCH (w / NCH) .. NCH (w / NCH + 1) - 1 of each tile, reading the split
-// Xhat and W tiles that the slab owners wrote to LDS (one workgroup barrier
-// before, one after).  A wave then holds 16 accumulators of the partial and two
-// tiles of prefetched rows (split Xhat, U, ytilde) in registers: the rows of tile
-// t + 2 step are requested as soon as tile t has consumed its own.  W leaves
-// through LDS: each wave stages its slab's rows, packed as in U, in its own rows
-// of the W tile and stores them as whole contiguous 1 KiB pieces before the
-// same rows take the split of W.
+// leaves room for one wave per SIMD only.  Here one 512-thread workgroup per
+// compute unit walks 128-row tiles; wave w owns the 16-row slab 16w .. 16w + 15
+// of a tile for the first product (16x16x32 fp16 matrix cores: lane l holds row
+// l % 16 and, of each 16-column block, the columns 4 (l / 16) .. + 3), the row
+// work and the epilogue, and the second product is shared out by 32 x 32 blocks
+// of the result: wave w owns the features 32 (w % 4) .. + 31 and the columns
+// 32 (w / 4) .. + 31 of the partial over all 128 rows of the tile, reading the
+// split Xhat and W tiles that the slab owners wrote to LDS (one workgroup
+// barrier before, one after).  The rows of the next tile are requested as soon
+// as a tile has consumed its own.
+//
+// Row work (the end of the previous iteration): q = u.p - 1 in FP64, the pending
+// gated dual step (ytilde stored), ybar, ||q||^2 and ytilde^T q -- as the row
+// pass does, so that the row pass is not needed.  Its s = U^T ybar is instead
+// formed by k_s_gram from terms this kernel accumulates while W is on chip: the
+// column sums of W and of W ytilde (FP64 across tiles) and the Gram W^T W (a
+// third product on the matrix cores, from the W tile; wave w adds the block
+// (rows 32 (w % 2) .., columns 32 (w / 4) ..) of the tile's row half w / 2 % 2).
+// The factor is read from one buffer and W written to the other (B.ctl->ubuf):
+// the stopping rule of the previous iteration is decided after this kernel, which
+// is then discarded if the rule fires.  W leaves through LDS: each wave stages its
+// slab's rows, packed as in U, in its own rows of the W tile and stores them as
+// whole contiguous 1 KiB pieces before the same rows take the split of W.
 // ===========================================================================
 namespace bf8 {
 
@@ -625,9 +633,9 @@ struct Shape {
   static constexpr int TH = NCH * CB16 * 64 * 16;         // bytes of one plane of the Theta operand
   static constexpr int OFF_X = 2 * TH;
   static constexpr int OFF_W = OFF_X + kRows * XRS;
-  static constexpr int OFF_P = OFF_W + kRows * WRS;
-  static constexpr int OFF_S = OFF_P + R32 * 4;
-  static constexpr int OFF_COL = OFF_S + R32 * 4;         // 8 x R32 doubles: column sums of W
+  static constexpr int OFF_P = OFF_W + kRows * WRS;      // R32 doubles: p (the row work's FP64 dot)
+  static constexpr int OFF_S = OFF_P + R32 * 8;           // 2 x R32 floats: -alpha p, -alpha s
+  static constexpr int OFF_COL = OFF_S + 2 * R32 * 4;     // 8 x R32 doubles: column sums of W
   static constexpr int OFF_COLY = OFF_COL + 8 * R32 * 8;  // 8 x R32 doubles: W^T ytilde
   static constexpr int OFF_D = OFF_COLY + 8 * R32 * 8;    // 8 x 8 doubles
   static constexpr int OFF_F = OFF_D + 8 * 8 * 8;         // 8 floats
@@ -732,14 +740,13 @@ __device__ __forceinline__ void reduce_scatter16_row(float* v, int li) {
   rs_step<2, 1, 0xB1>(v, li);    // quad_perm [1, 0, 3, 2]
 }
 
-// a 16-byte unit with its 8-byte halves exchanged when `odd`
-__device__ __forceinline__ f32x4 unit_swap(f32x4 v, bool odd) {
-  f32x4 o;
-  o.x = odd ? v.z : v.x;
-  o.y = odd ? v.w : v.y;
-  o.z = odd ? v.x : v.z;
-  o.w = odd ? v.y : v.w;
-  return o;
+// A 16-byte unit (hi halves, lo halves) into its LDS slot, its two 8-byte halves
+// exchanged when `odd` (by address: two 8-byte writes, no data movement).
+__device__ __forceinline__ void put_unit(unsigned char* slot, f32x4 v, bool odd) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  const int o = odd ? 8 : 0;
+  *reinterpret_cast<f32x2*>(slot + o) = (f32x2){v.x, v.y};
+  *reinterpret_cast<f32x2*>(slot + (o ^ 8)) = (f32x2){v.z, v.w};
 }
 
 }  // namespace bf8
@@ -758,8 +765,9 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
   f16x8* th_l = reinterpret_cast<f16x8*>(smem_raw + P::TH);
   unsigned char* xt = smem_raw + P::OFF_X;
   unsigned char* wt = smem_raw + P::OFF_W;
-  float* ps = reinterpret_cast<float*>(smem_raw + P::OFF_P);
-  float* ss = reinterpret_cast<float*>(smem_raw + P::OFF_S);
+  double* pds = reinterpret_cast<double*>(smem_raw + P::OFF_P);
+  float* naps = reinterpret_cast<float*>(smem_raw + P::OFF_S);  // -alpha p
+  float* nass = naps + R32;                                      // -alpha s
   double* colred = reinterpret_cast<double*>(smem_raw + P::OFF_COL);
   double* colyred = reinterpret_cast<double*>(smem_raw + P::OFF_COLY);
   double* dred = reinterpret_cast<double*>(smem_raw + P::OFF_D);
@@ -813,8 +821,9 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     th_l[idx] = lo;
   }
   for (int c = tid; c < R32; c += bf8::kThreads8) {
-    ps[c] = B.p[c];
-    ss[c] = B.s[c];
+    pds[c] = (double)B.p[c];
+    naps[c] = neg_alpha * B.p[c];
+    nass[c] = neg_alpha * B.s[c];
   }
   __syncthreads();
 
@@ -922,8 +931,8 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
       const f16x8 xh = __builtin_bit_cast(f16x8, hb);
       const f16x8 xl = __builtin_bit_cast(f16x8, lb);
       // the slab's units into the Xhat tile of the second product
-      *reinterpret_cast<f32x4*>(xt + xrow + 16 * ((8 * ks) ^ gs)) = bf8::unit_swap(xa0, oddj);
-      *reinterpret_cast<f32x4*>(xt + xrow + 16 * ((8 * ks + 4) ^ gs)) = bf8::unit_swap(xa1, oddj);
+      bf8::put_unit(xt + xrow + 16 * ((8 * ks) ^ gs), xa0, oddj);
+      bf8::put_unit(xt + xrow + 16 * ((8 * ks + 4) ^ gs), xa1, oddj);
 #pragma unroll
       for (int cb = 0; cb < CB16; ++cb) {
         const f16x8 ah = th_h[(ks * CB16 + cb) * 64 + lane];
@@ -940,8 +949,9 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     // ---- row work on row pt, columns 16 cb + 4 gq + v ----
     int lds_off = 0;  // opaque zero offset: p and s are read from LDS here, not kept in registers
     asm volatile("" : "+v"(lds_off));
-    const float* psl = ps + lds_off;
-    const float* ssl = ss + lds_off;
+    const double* pdl = pds + lds_off;
+    const float* napl = naps + lds_off;
+    const float* nasl = nass + lds_off;
     // okf: 1 for a valid row and column, else 0 (masked lanes compute on finite
     // values and their results are multiplied away: no branches)
     float okf[CB16];
@@ -962,11 +972,13 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     double pd[CB16];
 #pragma unroll
     for (int cb = 0; cb < CB16; ++cb) {
-      const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + 16 * cb + 4 * gq);
-      const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+      typedef double f64x2 __attribute__((ext_vector_type(2)));
+      const f64x2 p01 = *reinterpret_cast<const f64x2*>(pdl + 16 * cb + 4 * gq);
+      const f64x2 p23 = *reinterpret_cast<const f64x2*>(pdl + 16 * cb + 4 * gq + 2);
+      const double pe[4] = {p01.x, p01.y, p23.x, p23.y};
       double dd = 0.0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) dd += (double)u[cb][e] * (double)pe[e];
+      for (int e = 0; e < 4; ++e) dd += (double)u[cb][e] * pe[e];
       pd[cb] = dd;
     }
 #pragma unroll
@@ -995,16 +1007,16 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
 #pragma unroll
     for (int cb = 0; cb < CB16; ++cb) {
       const int c = 16 * cb + 4 * gq;
-      const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
-      const f32x4 sv = *reinterpret_cast<const f32x4*>(ssl + c);
-      const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
-      const float se[4] = {sv.x, sv.y, sv.z, sv.w};
+      const f32x4 pv = *reinterpret_cast<const f32x4*>(napl + c);
+      const f32x4 sv = *reinterpret_cast<const f32x4*>(nasl + c);
+      const float pe[4] = {pv.x, pv.y, pv.z, pv.w};  // -alpha p
+      const float se[4] = {sv.x, sv.y, sv.z, sv.w};  // -alpha s
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float uu = u[cb][e];
         float t = fmaf(two_alpha_s, acc1[cb][e], uu);
-        t = fmaf(neg_alpha, ybar * pe[e], t);
-        t = fmaf(neg_alpha, se[e], t);
+        t = fmaf(ybar, pe[e], t);
+        t = t + se[e];
         const float w = fmaxf(t, 0.f) * okf[cb];
         wv[4 * cb + e] = w;
         const double wd = (double)w, ud = (double)uu;
@@ -1045,7 +1057,7 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
       const u32x2 hu = __builtin_bit_cast(u32x2, hi);
       const u32x2 lu = __builtin_bit_cast(u32x2, lo);
       const f32x4 unit = {__uint_as_float(hu.x), __uint_as_float(hu.y), __uint_as_float(lu.x), __uint_as_float(lu.y)};
-      *reinterpret_cast<f32x4*>(wt + wrow + 16 * ((4 * cb + gq) ^ sj)) = bf8::unit_swap(unit, oddj);
+      bf8::put_unit(wt + wrow + 16 * ((4 * cb + gq) ^ sj), unit, oddj);
     }
     // column sums of the slab, of W and of W ytilde_t (ytilde after this pass's dual
     // step: the Gram terms of the next iteration's s): lane (j, gq) keeps the
