@@ -878,18 +878,21 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     return (tile_base + rr < n) ? (uint32_t)rr : 0u;
   };
   // uniform tile base + 32-bit lane byte offset (the scalar-base form of the loads)
-  auto load_x = [&](Buf& b, int64_t st) {
+  // the two units of 32-feature step ks (all of them for ks < 0)
+  auto load_x = [&](Buf& b, int64_t st, int kso) {
     const int lo = opaque_lane(), gq = lo >> 4;
     int64_t tb;
     const uint32_t rr = lane_row(st, lo & 15, tb);
     const char* base = reinterpret_cast<const char*>(B.X + tb * (int64_t)d);
 #pragma unroll
     for (int ks = 0; ks < NCH; ++ks)
+      if (kso < 0 || ks == kso) {
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int f = 32 * ks + 16 * hh + 4 * gq;  // features >= d meet zero rows of Theta_t
-        const uint32_t off = 4u * (rr * (uint32_t)d + (uint32_t)(f < d ? f : 0));
-        b.x[ks][hh] = *reinterpret_cast<const f32x4*>(base + off);
+        for (int hh = 0; hh < 2; ++hh) {
+          const int f = 32 * ks + 16 * hh + 4 * gq;  // features >= d meet zero rows of Theta_t
+          const uint32_t off = 4u * (rr * (uint32_t)d + (uint32_t)(f < d ? f : 0));
+          b.x[ks][hh] = *reinterpret_cast<const f32x4*>(base + off);
+        }
       }
   };
   auto load_u = [&](UBuf& b, int64_t st) {
@@ -941,10 +944,10 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
         acc1[cb] = bf8::mfma16x16x32h(al, xh, acc1[cb]);
         acc1[cb] = bf8::mfma16x16x32h(ah, xh, acc1[cb]);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      load_x(bx, nst, ks);  // this step's Xhat units of the next tile
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);
-    load_x(bx, nst);  // Xhat rows of the next tile
-    __builtin_amdgcn_sched_barrier(0);
 
     // ---- row work on row pt, columns 16 cb + 4 gq + v ----
     int lds_off = 0;  // opaque zero offset: p and s are read from LDS here, not kept in registers
@@ -990,6 +993,10 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     float yt = vpt ? ub.y : 0.f;
     if (gate) yt = fmaf(gam, q, yt);
     const float ybar = fmaf(gam, q, yt);
+    // the factor rows and ytilde of this tile are consumed: request the next tile's
+    __builtin_amdgcn_sched_barrier(0);
+    load_u(ub, st + step);
+    __builtin_amdgcn_sched_barrier(0);
     if (gate) *(vpt ? (B.y + pt) : B.dump) = yt;  // the four lanes of a row store the same value
     {
       const bool lead = vpt && gq == 0;
@@ -1071,9 +1078,6 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
       colacc += (double)wv[0];
       colyacc += (double)wy[0];
     }
-    __builtin_amdgcn_sched_barrier(0);
-    load_u(ub, st + step);  // factor rows and ytilde of the next tile
-    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
 
     // ---- second product: partial += Xhat_tile^T W_tile (this wave's block and
@@ -1120,7 +1124,7 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
   };
 
   Buf A;
-  load_x(A, blockIdx.x);
+  load_x(A, blockIdx.x, -1);
   load_u(ub, blockIdx.x);
   for (int64_t st = blockIdx.x; st < T; st += step) tile(A, st, st + step);
 
