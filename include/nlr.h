@@ -110,7 +110,7 @@ enum {
    * split; ybar is kept in the workspace between the passes).  Other shapes
    * return NLR_EUNSUPPORTED.  X is left holding Xhat in split form after
    * nlr_init, so it no longer reads as fp32 (do not pass it to nlr_init again
-   * with NLR_INIT_X_NORMALISED): in the single-Xhat-pass form each 16 bytes that
+   * with NLR_INIT_X_NORMALISED): in the single-Xhat-pass and one-pass forms each 16 bytes that
    * held 4 consecutive features hold their 4 fp16 hi halves then their 4 fp16 lo
    * halves of x * s (s a power of two); in the panel form each 32 bytes that held
    * 8 features hold their 8 hi halves then their 8 lo halves.  U_0 must lie in
@@ -122,8 +122,15 @@ enum {
    * aligned X and U), each iteration reads Xhat once: pass B also forms
    * the partials of Xhat^T W_{t+1}, and Theta_{t+1} = c_{t+1} Xhat^T W_{t+1}
    * (U_{t+1} = c_{t+1} W_{t+1}, Algorithm 1), while a row pass over U and ytilde
-   * does the rest of pass A's work.  Both forms compute the same iteration; they
-   * differ by floating-point rounding only. */
+   * does the rest of pass A's work.  With NLR_INIT_SPLIT_F16 and 97..128
+   * features, 33..64 columns (d % 4 == 0, r % 4 == 0) the default is the
+   * one-pass form: the same kernel also does the row work (q, the gated dual
+   * step, ybar), s = U^T ybar is formed from W^T W, W^T ytilde and the column sums
+   * of the previous pass's W, and the stopping rule of an iteration is decided
+   * after the next pass, which reads the factor from one buffer and writes W to a
+   * second n x r buffer in the workspace (discarded when the rule fires).  All
+   * forms compute the same iteration; they differ by floating-point rounding
+   * only. */
   NLR_INIT_TWO_PASS = 16,
   /* Data-informed start (Appendix D, "Initialization"): U holds Z on input (e.g.
    * i.i.d. N(0,1) entries) and is replaced by U_0 = Pi_Omega(Q), where Q is the

@@ -11,7 +11,7 @@ replaces the factor).
 import numpy as np
 import pytest
 
-from gpu_util import OBJ_TOL, U_TOL, host, log, make_ctx, rel_max_err, trajectory
+from gpu_util import OBJ_TOL, U_TOL, host, log, make_ctx, rel_max_err, to_dev, trajectory
 from oracle import nlr as onlr
 from synth import gaussian_mixture, standard_normal_factor
 
@@ -127,3 +127,44 @@ def test_onepass_breakdown(steps_first):
     with pytest.raises(nlr.NlrError) as e:
         ctx.run(3)
     assert e.value.status == nlr.NLR_ESTATE
+
+
+def test_onepass_beta_change_between_runs():
+    """s of the first iteration after nlr_set_params comes from the stored Gram terms with the
+    new beta; the trajectory still follows the oracle across the change."""
+    X, Z, K, beta, alpha = _gated(100, 36)
+    ctx = make_ctx(X, Z, K, alpha, beta, eps_d=3e-3, eps_c=1e-7, T_min=0, flags=SPLIT)
+    T1, T2, beta2 = 150, 150, 0.5
+    done1, _ = ctx.run(T1)
+    ctx.set_params(beta=beta2)
+    done2, _ = ctx.run(T2)
+    assert done1 == T1 and done2 == T2
+    hist = ctx.history(4096)
+    gates = [bool(h["dual_step"]) for h in hist]
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    r1 = onlr.run(Xh, Z, K, alpha, beta, T=T1, T_min=T1, eps_d=3e-3, eps_c=1e-7, gates=gates[:T1])
+    r2 = onlr.run(Xh, r1.U, K, alpha, beta2, T=T2, T_min=T2, eps_d=3e-3, eps_c=1e-7, gates=gates[T1:],
+                  project_init=False, y0=r1.y, t0=T1)
+    err = rel_max_err(host(ctx.U), r2.U)
+    log(f"one-pass beta change: {sum(gates)} dual steps, U err {err:.2e}")
+    assert sum(gates) > 20
+    assert err < U_TOL
+    ys = onlr.stored_dual(r2.y)
+    assert np.abs(host(ctx.y) - ys).max() <= 1e-4 * np.abs(ys).max()
+
+
+def test_onepass_resume_flags():
+    """Resuming from (U, y) with U_IN_OMEGA | KEEP_Y | X_NORMALISED continues the iteration."""
+    from paper_2609_36074_amd import nlr
+    X, Z, K, beta, alpha = _gated(128, 64)
+    kw = dict(eps_d=3e-3, eps_c=1e-7, T_min=0)
+    a = make_ctx(X, Z, K, alpha, beta, flags=SPLIT, **kw)
+    a.run(120)
+    b = make_ctx(X, Z, K, alpha, beta, flags=SPLIT, **kw)
+    b.run(61)
+    # X holds the split Xhat after a split init, so the resumed context gets Xhat (fp32) anew
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    flags = nlr.NLR_INIT_U_IN_OMEGA | nlr.NLR_INIT_KEEP_Y | nlr.NLR_INIT_X_NORMALISED | SPLIT
+    c = nlr.Context(to_dev(Xh.astype(np.float32)), K, b.U, b.y, alpha=alpha, beta=beta, flags=flags, **kw)
+    c.run(59)
+    assert rel_max_err(host(c.U), host(a.U)) < U_TOL
