@@ -597,7 +597,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_
 // Row work (the end of the previous iteration): q = u.p - 1 in FP64, the pending
 // gated dual step (ytilde stored), ybar, ||q||^2 and ytilde^T q -- as the row
 // pass does, so that the row pass is not needed.  Its s = U^T ybar is instead
-// formed by k_s_gram from terms this kernel accumulates while W is on chip: the
+// formed (by k_reduce_theta after the pass, or by k_s_gram at the start of a host
+// call) from terms this kernel accumulates while W is on chip: the
 // column sums of W and of W ytilde (FP64 across tiles) and the Gram W^T W (a
 // third product on the matrix cores, from the W tile; wave w adds the block
 // (rows 32 (w % 2) .., columns 32 (w / 4) ..) of the tile's row half w / 2 % 2).
@@ -616,9 +617,12 @@ static_assert(kRows == kTPB, "the fused pass B tiles are kTPB rows");
 // Tiles in LDS: row R of a tile is a run of 16-byte units (four features or four
 // columns: their fp16 hi halves, then their lo halves, as Xhat is stored).  Unit u
 // of row R sits in slot u ^ swz(R), and on odd rows its two 8-byte halves are
-// exchanged.  A unit write (16 lanes: 16 consecutive rows, one unit) and a
-// transposing read (32 lanes: rows R0 .. R0 + 3, eight consecutive units, one
-// half) then each touch 64 distinct 4-byte banks.
+// exchanged.  A transposing read (32 lanes: rows R0 .. R0 + 3, eight consecutive
+// units, one half) then touches 64 distinct 4-byte banks.  The unit writes (two
+// 8-byte writes; gfx950 serves those with conflicts whenever lanes whose indices
+// differ modulo 16 share a bank) are not conflict-free, but are off the critical
+// path: one 16-byte write per unit with the halves exchanged in registers is not
+// faster.
 __device__ __forceinline__ int swz(int R) { return (R ^ ((R & 2) << 2)) & 15; }
 
 template <int NB, int NCH>

@@ -485,23 +485,29 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
 // sums rows sub, sub+4, ... of the segment, then the four subs are added in order.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(kThreads) void k_seg_sum(const T* __restrict__ P, int64_t R, int C,
-                                                      double* __restrict__ out, int S, const DevCtl* ctl,
-                                                      int skip_if_halted) {
-  if (skip_if_halted ? halted(ctl) : (ctl->breakdown != 0)) return;
-  __shared__ double red[kThreads];
+__device__ __forceinline__ void seg_sum_block(const T* __restrict__ P, int64_t R, int C, double* __restrict__ out,
+                                              int S, int bx, int by, double* red) {
   const int tid = threadIdx.x;
-  const int col = blockIdx.x * 64 + (tid & 63);
+  const int col = bx * 64 + (tid & 63);
   const int sub = tid >> 6;
-  const int64_t lo = (int64_t)blockIdx.y * R / S;
-  const int64_t hi = (int64_t)(blockIdx.y + 1) * R / S;
+  const int64_t lo = (int64_t)by * R / S;
+  const int64_t hi = (int64_t)(by + 1) * R / S;
   double acc = 0.0;
   if (col < C)
     for (int64_t row = lo + sub; row < hi; row += 4) acc += (double)P[row * C + col];
   red[tid] = acc;
   __syncthreads();
   if (tid < 64 && col < C)
-    out[(int64_t)blockIdx.y * C + col] = ((red[tid] + red[64 + tid]) + red[128 + tid]) + red[192 + tid];
+    out[(int64_t)by * C + col] = ((red[tid] + red[64 + tid]) + red[128 + tid]) + red[192 + tid];
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_seg_sum(const T* __restrict__ P, int64_t R, int C,
+                                                      double* __restrict__ out, int S, const DevCtl* ctl,
+                                                      int skip_if_halted) {
+  if (skip_if_halted ? halted(ctl) : (ctl->breakdown != 0)) return;
+  __shared__ double red[kThreads];
+  seg_sum_block<T>(P, R, C, out, S, blockIdx.x, blockIdx.y, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -510,7 +516,10 @@ __global__ __launch_bounds__(kThreads) void k_seg_sum(const T* __restrict__ P, i
 // Layout: chunk ch of 32 features, quarter j (4 features), m-block mb, lane l,
 // element e  <->  Theta[32 ch + 16 (l/32) + 4 j + e][32 mb + l%32].
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, int nseg, int scaled) {
+__device__ __forceinline__ float s_from_gram(const Bufs& B, int r32, int k, double gp, float gamma_f);
+
+// gamma_f >= 0 (one-pass iteration): the extra blocks also form s for the next pass.
+__global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, int nseg, int scaled, float gamma_f) {
   if (halted(B.ctl)) return;
   __shared__ double red[kThreads];
   __shared__ float mred[4];
@@ -528,7 +537,14 @@ __global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, i
       if (l < w) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + w];
       __syncthreads();
     }
-    if (l == 0) B.gram_vec[2 * r32 + k] = red[threadIdx.x];
+    if (l == 0) {
+      const double gp = red[threadIdx.x];
+      B.gram_vec[2 * r32 + k] = gp;
+      if (gamma_f >= 0.f) {
+        const float sk = s_from_gram(B, r32, k, gp, gamma_f);
+        B.s[k] = (k < g.r) ? sk : 0.f;
+      }
+    }
     return;
   }
   const int64_t tot = (int64_t)g.d32 * g.r32;
@@ -1103,7 +1119,7 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
 // here, after the fact: when it fires, this iteration's W (written to the other
 // factor buffer) and partials are discarded and the iterate stays the previous
 // one.  Otherwise as k_ctl_b, then the column sums P of W and W^T ytilde for the
-// next iteration's s (k_s_gram).  S.row_pass: the row pass did this iteration's
+// next iteration's s (formed by the next one-pass kernel).  S.row_pass: the row pass did this iteration's
 // row work (k_ctl_a has already decided the stopping rule and the record).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_ctl_one(Geometry g, Bufs B, StepArgs S) {
@@ -1202,17 +1218,15 @@ __global__ __launch_bounds__(kThreads) void k_ctl_one(Geometry g, Bufs B, StepAr
 
 // ---------------------------------------------------------------------------
 // Fixed-order sums over the GB rows of the one-pass iteration's per-workgroup
-// statistics, one segment each: blockIdx.y 0 a_part -> seg_a, 1 b_part -> seg_b.
+// statistics, one segment each: by 0 a_part -> seg_a, 1 b_part -> seg_b.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_seg_ab(Geometry g, Bufs B) {
-  if (halted(B.ctl)) return;
-  __shared__ double red[kThreads];
-  const double* P = blockIdx.y ? B.b_part : B.a_part;
-  double* out = blockIdx.y ? B.seg_b : B.seg_a;
+__device__ __forceinline__ void seg_ab_block(const Geometry& g, const Bufs& B, int bx, int by, double* red) {
+  const double* P = by ? B.b_part : B.a_part;
+  double* out = by ? B.seg_b : B.seg_a;
   const int C = 4 + g.r32;
   const int tid = threadIdx.x;
   // 8 columns x 32 row phases per block; the phases are added in a fixed tree
-  const int col = blockIdx.x * 8 + (tid & 7);
+  const int col = bx * 8 + (tid & 7);
   const int sub = tid >> 3;
   double acc = 0.0;
   if (col < C)
@@ -1226,29 +1240,48 @@ __global__ __launch_bounds__(kThreads) void k_seg_ab(Geometry g, Bufs B) {
   if (tid < 8 && col < C) out[col] = red[tid];
 }
 
+// The segment sums after a one-pass kernel in one launch: blockIdx.y < nseg the
+// segments of the Theta and W^T W partial rows, nseg and nseg + 1 the statistics
+// (a_part, b_part; the first (4 + r32 + 7) / 8 blocks of those rows).
+__global__ __launch_bounds__(kThreads) void k_seg_onepass(Geometry g, Bufs B, int nseg) {
+  if (halted(B.ctl)) return;
+  __shared__ double red[kThreads];
+  const int by = blockIdx.y;
+  if (by < nseg) {
+    seg_sum_block<float>(B.theta_part, g.GB, g.theta_cols, B.seg_theta, nseg, blockIdx.x, by, red);
+  } else if ((int)blockIdx.x < (4 + g.r32 + 7) / 8) {
+    seg_ab_block(g, B, blockIdx.x, by - nseg, red);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // s = U^T ybar of the one-pass iteration from the Gram terms of the pass that
-// produced U = c W (one workgroup).  Per row q = u.p - 1 = c^2 w.P - 1 and
-// ybar = ytilde_prev + (1 + gate) gamma q (the pending gated dual step, then the
-// penalty term; gamma = beta / n), so
+// produced U = c W.  Per row q = u.p - 1 = c^2 w.P - 1 and ybar = ytilde_prev +
+// (1 + gate) gamma q (the pending gated dual step, then the penalty term; gamma =
+// beta / n), so
 //   s = c W^T ytilde_prev + (1 + gate) gamma c (c^2 (W^T W) P - P)
 // with W^T W (the columns after Theta in the Theta partial rows, reduced with them
 // and multiplied by P in k_reduce_theta), P and W^T ytilde_prev summed in a fixed
-// order (FP64).  The last term
-// is U^T q: small near feasibility and weighted by gamma, so the fp32-accumulated
-// Gram partials carry it well below the iteration's rounding.
+// order (FP64).  The last term is U^T q: small near feasibility and weighted by
+// gamma, so the fp32-accumulated Gram partials carry it well below the iteration's
+// rounding.  k_reduce_theta forms s right after the pass with the step arguments of
+// the call; k_s_gram (one workgroup) forms it again at the start of a host call,
+// whose step arguments (beta) may differ.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ float s_from_gram(const Bufs& B, int r32, int k, double gp, float gamma_f) {
+  const double c = B.ctl->c_gram;
+  const double gmul = (1.0 + (B.ctl->gate ? 1.0 : 0.0)) * (double)gamma_f;
+  const double P = B.gram_vec[k], wy = B.gram_vec[r32 + k];
+  return (float)(c * wy + gmul * c * (c * c * gp - P));
+}
+
 __global__ __launch_bounds__(64) void k_s_gram(Geometry g, Bufs B, StepArgs S) {
-  const DevCtl* ctl = B.ctl;
-  if (halted(ctl)) return;
+  if (halted(B.ctl)) return;
   const int r32 = g.r32;
   const int k = threadIdx.x;
   if (k >= r32) return;
-  const double c = ctl->c_gram;
-  const double gmul = (1.0 + (ctl->gate ? 1.0 : 0.0)) * (double)S.gamma_f;
-  const double P = B.gram_vec[k], wy = B.gram_vec[r32 + k], gp = B.gram_vec[2 * r32 + k];
-  const double sk = c * wy + gmul * c * (c * c * gp - P);
-  B.s[k] = (k < g.r) ? (float)sk : 0.f;
+  const float sk = s_from_gram(B, r32, k, B.gram_vec[2 * r32 + k], S.gamma_f);
+  B.s[k] = (k < g.r) ? sk : 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -1369,7 +1402,7 @@ hipError_t launch_reduce_theta_rows(const Geometry& g, const Bufs& b, int64_t ro
   // one-pass iteration (partials of its pass): blocks after the RT Theta blocks form
   // (W^T W) P from the r32 r32 Gram entries
   const int gb = (g.fused8 && scaled) ? (g.r32 * g.r32) / kThreads : 0;
-  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT + gb), dim3(kThreads), 0, st, g, b, nseg, scaled ? 1 : 0);
+  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT + gb), dim3(kThreads), 0, st, g, b, nseg, scaled ? 1 : 0, -1.0f);
   return hipGetLastError();
 }
 
@@ -1465,14 +1498,21 @@ hipError_t launch_ctl_one(const Geometry& g, const Bufs& b, const StepArgs& a, h
   return hipGetLastError();
 }
 
-hipError_t launch_s_gram(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_s_gram, dim3(1), dim3(64), 0, st, g, b, a);
+hipError_t launch_seg_onepass(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int cx = (g.theta_cols + 63) / 64, ax = (4 + g.r32 + 7) / 8;
+  hipLaunchKernelGGL(k_seg_onepass, dim3(cx > ax ? cx : ax, g.SAF + 2), dim3(kThreads), 0, st, g, b, g.SAF);
   return hipGetLastError();
 }
 
-hipError_t launch_seg_ab(const Geometry& g, const Bufs& b, hipStream_t st) {
-  const int C = 4 + g.r32;
-  hipLaunchKernelGGL(k_seg_ab, dim3((C + 7) / 8, 2), dim3(kThreads), 0, st, g, b);
+hipError_t launch_reduce_theta_onepass(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  // blocks after the RT Theta blocks form (W^T W) P from the r32 r32 Gram entries, and s
+  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT + (g.r32 * g.r32) / kThreads), dim3(kThreads), 0, st, g, b, g.SAF, 1,
+                     a.gamma_f);
+  return hipGetLastError();
+}
+
+hipError_t launch_s_gram(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_s_gram, dim3(1), dim3(64), 0, st, g, b, a);
   return hipGetLastError();
 }
 

@@ -415,14 +415,19 @@ static hipError_t prof_collect(nlr_ctx* c) {
       return hip_fail(c);                               \
   } while (0)
 
-static nlr_status enqueue_iteration(nlr_ctx* c) {
+// first: the first iteration of a host call (nlr_step, nlr_run), whose step
+// arguments may differ from those of the pass before it
+static nlr_status enqueue_iteration(nlr_ctx* c, bool first) {
   const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
   if (c->g.fused8) {
     // one pass over the rows per iteration: the pass does the row work of the
     // iteration (the end of the previous one) as well as the primal step, reading
     // the factor from one buffer and writing W to the other; s comes from the Gram
-    // terms of the previous pass (k_s_gram), or, when there is no previous pass
-    // (after init or a stop), from the row pass
+    // terms of the previous pass (formed after that pass with this call's step
+    // arguments, or anew at the start of a call), or, when there is no previous
+    // pass (after init or a stop), from the row pass.  Then one launch of segment
+    // sums (Theta and W^T W partials, the row statistics), the control, and Theta
+    // with (W^T W) P and the next s.
     StepArgs ap = a;
     if (!c->gram_valid) {
       LAUNCH(KK_PASS_U, launch_pass_u(c->g, c->b, a, c->stream));
@@ -430,13 +435,13 @@ static nlr_status enqueue_iteration(nlr_ctx* c) {
       LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
       ap.end_work = 0;
       ap.row_pass = 1;
-    } else {
+    } else if (first) {
       LAUNCH(KK_CTL_A, launch_s_gram(c->g, c->b, a, c->stream));
     }
     LAUNCH(KK_PASS_BF, launch_pass_bf(c->g, c->b, ap, c->stream));
-    LAUNCH(KK_CTL_B, launch_seg_ab(c->g, c->b, c->stream));
+    LAUNCH(KK_CTL_B, launch_seg_onepass(c->g, c->b, c->stream));
     LAUNCH(KK_CTL_B, launch_ctl_one(c->g, c->b, ap, c->stream));
-    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, true, c->stream));
+    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta_onepass(c->g, c->b, ap, c->stream));
     c->gram_valid = true;
     c->pending = true;
     return NLR_OK;
@@ -628,7 +633,7 @@ nlr_status nlr_step(nlr_ctx* c, nlr_iter_stats* stats) {
   if (!c) return NLR_EINVAL;
   if (c->failed) return NLR_ESTATE;
   if (launch_clear_stop(c->b, c->stream) != hipSuccess) return hip_fail(c);
-  nlr_status s = enqueue_iteration(c);
+  nlr_status s = enqueue_iteration(c, true);
   if (s != NLR_OK) return s;
   s = enqueue_finish(c);
   if (s != NLR_OK) return s;
@@ -659,7 +664,7 @@ nlr_status nlr_run(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* l
       if (read_ctl(c) != NLR_OK) return NLR_EHIP;
       if (c->host_ctl->stop || c->host_ctl->breakdown) break;
     }
-    nlr_status s = enqueue_iteration(c);
+    nlr_status s = enqueue_iteration(c, k == 0);
     if (s != NLR_OK) return s;
   }
   nlr_status s = enqueue_finish(c);

@@ -213,8 +213,9 @@ hipError_t launch_split_x8(const Geometry& g, const Bufs& b, hipStream_t st);
 // a_part rows written by the latest producer (pass A grid, finish grid or panel splits)
 hipError_t launch_seg_a_rows(const Geometry& g, const Bufs& b, int64_t rows, bool finish, hipStream_t st);
 hipError_t launch_ctl_one(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+hipError_t launch_seg_onepass(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_reduce_theta_onepass(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_s_gram(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
-hipError_t launch_seg_ab(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_reduce_theta_rows(const Geometry& g, const Bufs& b, int64_t rows, int nseg, bool scaled,
                                     hipStream_t st);
 
