@@ -52,8 +52,18 @@ __global__ __launch_bounds__(kThreads) void k_colsum(Geometry g, Bufs B) {
     const int col = tid % d;
     const int rsub = tid / d;
     double acc = 0.0;
-    if (rsub < rstep)
-      for (int64_t i = r0 + rsub; i < r1; i += rstep) acc += (double)B.X[i * d + col];
+    if (rsub < rstep) {
+      // sixteen rows' loads in flight, added in row order
+      int64_t i = r0 + rsub;
+      for (; i + 15 * rstep < r1; i += 16 * rstep) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = B.X[(i + u * rstep) * d + col];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc += (double)v[u];
+      }
+      for (; i < r1; i += rstep) acc += (double)B.X[i * d + col];
+    }
     red[tid] = acc;
     __syncthreads();
     if (tid < d) {
@@ -78,57 +88,90 @@ __global__ __launch_bounds__(kThreads) void k_colmean(Geometry g, Bufs B) {
   B.i_xbar[j] = t / (double)g.n;
 }
 
-// Partial centred Gram blocks: block (bi, bj) of sum over the chunk's rows of
-// (x - xbar)(x - xbar)^T, FP64.  Thread (ta, tb) owns entries (32 bi + ta, 32 bj + 4 tb + e).
+// Partial centred Gram blocks on the fp64 matrix cores (v_mfma_f64_16x16x4f64):
+// workgroup (chunk gx, block pair bp) adds the 64 x 64 block (bi, bj), bi <= bj, of
+// the sum over the chunk's rows of (x - xbar)(x - xbar)^T.  Wave w owns the block
+// rows 16 w .. 16 w + 15 and all 64 columns (four 16 x 16 tiles).  A product step
+// takes 4 rows: lane l supplies row l / 16 of the step and feature l % 16 of its
+// tile (the A operand from the block's rows, the B operands from its columns), and
+// holds result element (4 v + l / 16, l % 16) of a tile in entry v.  The blocks
+// below the diagonal are not formed (the sum is symmetric; k_gram_reduce reads
+// their mirror).
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(kThreads) void k_gram(Geometry g, Bufs B) {
-  __shared__ double xa[64][33];
-  __shared__ double xb[64][33];
   const int tid = threadIdx.x;
   const int d = g.d;
-  const int bi = blockIdx.y / g.gblk;
-  const int bj = blockIdx.y - bi * g.gblk;
+  const int nb = (d + 63) / 64;
+  int bp = blockIdx.y, bi = 0;
+  while (bp >= nb - bi) {
+    bp -= nb - bi;
+    ++bi;
+  }
+  const int bj = bi + bp;
   const int64_t n = g.n;
   const int64_t r0 = (int64_t)blockIdx.x * n / g.GG;
   const int64_t r1 = (int64_t)(blockIdx.x + 1) * n / g.GG;
-  const int ta = tid >> 3, tb = tid & 7;
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  for (int64_t t0 = r0; t0 < r1; t0 += 64) {
-    __syncthreads();
-    for (int v = tid; v < 64 * 32; v += kThreads) {
-      const int rr = v >> 5, cc = v & 31;
-      const int64_t i = t0 + rr;
-      const int ca = bi * 32 + cc, cb = bj * 32 + cc;
-      double va = 0.0, vb = 0.0;
-      if (i < r1) {
-        if (ca < d) va = (double)B.X[i * d + ca] - B.i_xbar[ca];
-        if (cb < d) vb = (double)B.X[i * d + cb] - B.i_xbar[cb];
-      }
-      xa[rr][cc] = va;
-      xb[rr][cc] = vb;
-    }
-    __syncthreads();
-#pragma unroll 4
-    for (int rr = 0; rr < 64; ++rr) {
-      const double a = xa[rr][ta];
+  const int lane = tid & 63, w = tid >> 6;
+  const int kq = lane >> 4, cl = lane & 15;
+  const int fa = 64 * bi + 16 * w + cl;
+  const bool oka = fa < d;
+  const double ma = oka ? B.i_xbar[fa] : 0.0;
+  int fbj[4];
+  bool okb[4];
+  double mb[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] += a * xb[rr][4 * tb + e];
+  for (int J = 0; J < 4; ++J) {
+    fbj[J] = 64 * bj + 16 * J + cl;
+    okb[J] = fbj[J] < d;
+    mb[J] = okb[J] ? B.i_xbar[fbj[J]] : 0.0;
+  }
+  f64x4_t acc[4];
+#pragma unroll
+  for (int J = 0; J < 4; ++J) acc[J] = (f64x4_t){0.0, 0.0, 0.0, 0.0};
+  // rounds of 8 steps (32 rows): the round's loads are issued together
+  for (int64_t t0 = r0; t0 < r1; t0 += 32) {
+    float va[8], vb[8][4];
+    bool okr[8];
+#pragma unroll
+    for (int st = 0; st < 8; ++st) {
+      const int64_t row = t0 + 4 * st + kq;
+      okr[st] = row < r1;
+      const int64_t rb = (okr[st] ? row : r0) * (int64_t)d;
+      va[st] = B.X[rb + (oka ? fa : 0)];
+#pragma unroll
+      for (int J = 0; J < 4; ++J) vb[st][J] = B.X[rb + (okb[J] ? fbj[J] : 0)];
+    }
+#pragma unroll
+    for (int st = 0; st < 8; ++st) {
+      const double a = (okr[st] && oka) ? (double)va[st] - ma : 0.0;
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        const double b = (okr[st] && okb[J]) ? (double)vb[st][J] - mb[J] : 0.0;
+        acc[J] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc[J], 0, 0, 0);
+      }
     }
   }
   double* out = B.i_gram + (int64_t)blockIdx.x * d * d;
-  const int ia = bi * 32 + ta;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int jb = bj * 32 + 4 * tb + e;
-    if (ia < d && jb < d) out[(int64_t)ia * d + jb] = acc[e];
-  }
+  for (int J = 0; J < 4; ++J)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int ia = 64 * bi + 16 * w + 4 * v + kq;
+      const int jb = fbj[J];
+      if (ia < d && jb < d) out[(int64_t)ia * d + jb] = acc[J][v];
+    }
 }
 
+// C = the sum of the chunks' partials in chunk order; entries below the block
+// diagonal from the mirrored entry.
 __global__ __launch_bounds__(kThreads) void k_gram_reduce(Geometry g, Bufs B) {
   const int64_t dd = (int64_t)g.d * g.d;
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (e >= dd) return;
+  const int i = (int)(e / g.d), j = (int)(e - (int64_t)i * g.d);
+  const int64_t src = (i / 64 > j / 64) ? (int64_t)j * g.d + i : e;
   double t = 0.0;
-  for (int gx = 0; gx < g.GG; ++gx) t += B.i_gram[(int64_t)gx * dd + e];
+  for (int gx = 0; gx < g.GG; ++gx) t += B.i_gram[(int64_t)gx * dd + src];
   B.i_C[e] = t;
 }
 
@@ -251,17 +294,38 @@ __global__ __launch_bounds__(kThreads) void k_power(Geometry g, Bufs B, const do
 }
 
 // X <- (X - 1 xbar^T) / a in place; 256 rows per workgroup.
+// Threads map to (column, row offset) as in k_colsum, eight rows' loads in flight.
 __global__ __launch_bounds__(kThreads) void k_normalise(Geometry g, Bufs B) {
   if (B.ctl->degenerate) return;
   const double a = B.ctl->spectral_a;
   const int d = g.d;
+  const int tid = threadIdx.x;
   const int64_t row0 = (int64_t)blockIdx.x * 256;
-  const int64_t rows = (g.n - row0) < 256 ? (g.n - row0) : 256;
-  const int tot = (int)rows * d;
-  float* base = B.X + row0 * d;
-  for (int e = threadIdx.x; e < tot; e += kThreads) {
-    const int col = e % d;
-    base[e] = (float)(((double)base[e] - B.i_xbar[col]) / a);
+  const int64_t row1 = (g.n - row0) < 256 ? g.n : row0 + 256;
+  auto one = [&](int64_t i, int col, double xb) {
+    float* p = B.X + i * d + col;
+    *p = (float)(((double)*p - xb) / a);
+  };
+  if (d <= kThreads) {
+    const int rstep = kThreads / d;
+    const int col = tid % d;
+    const int rsub = tid / d;
+    if (rsub >= rstep) return;
+    const double xb = B.i_xbar[col];
+    int64_t i = row0 + rsub;
+    for (; i + 7 * rstep < row1; i += 8 * rstep) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = B.X[(i + u * rstep) * d + col];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) B.X[(i + u * rstep) * d + col] = (float)(((double)v[u] - xb) / a);
+    }
+    for (; i < row1; i += rstep) one(i, col, xb);
+  } else {
+    for (int col = tid; col < d; col += kThreads) {
+      const double xb = B.i_xbar[col];
+      for (int64_t i = row0; i < row1; ++i) one(i, col, xb);
+    }
   }
 }
 
@@ -279,12 +343,26 @@ __global__ __launch_bounds__(kThreads) void k_proj_partial(Geometry g, Bufs B) {
   const int col = tid % r;
   const int rsub = tid / r;
   double cs = 0.0, sq = 0.0;
-  if (rsub < rstep)
-    for (int64_t i = r0 + rsub; i < r1; i += rstep) {
+  if (rsub < rstep) {
+    // sixteen rows' loads in flight, added in row order
+    int64_t i = r0 + rsub;
+    for (; i + 15 * rstep < r1; i += 16 * rstep) {
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = B.U[(i + u * rstep) * r + col];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const float uu = fmaxf(v[u], 0.f);
+        cs += (double)uu;
+        sq += (double)uu * (double)uu;
+      }
+    }
+    for (; i < r1; i += rstep) {
       const float u = fmaxf(B.U[i * r + col], 0.f);
       cs += (double)u;
       sq += (double)u * (double)u;
     }
+  }
   red[tid] = cs;
   __syncthreads();
   if (tid < r) {
@@ -365,7 +443,8 @@ hipError_t launch_colsum(const Geometry& g, const Bufs& b, hipStream_t st) {
 }
 
 hipError_t launch_gram(const Geometry& g, const Bufs& b, hipStream_t st) {
-  hipLaunchKernelGGL(k_gram, dim3(g.GG, g.gblk * g.gblk), dim3(kThreads), 0, st, g, b);
+  const int nb = (g.d + 63) / 64;
+  hipLaunchKernelGGL(k_gram, dim3(g.GG, nb * (nb + 1) / 2), dim3(kThreads), 0, st, g, b);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t dd = (int64_t)g.d * g.d;

@@ -24,7 +24,15 @@ __global__ __launch_bounds__(kThreads) void k_xmax_partial(Geometry g, Bufs B) {
   const int64_t e0 = (int64_t)blockIdx.x * g.n / g.GI * g.d;
   const int64_t e1 = (int64_t)(blockIdx.x + 1) * g.n / g.GI * g.d;
   float m = 0.f;
-  for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) m = fmaxf(m, fabsf(B.X[e]));
+  int64_t e = e0 + threadIdx.x;
+  for (; e + 15 * kThreads < e1; e += 16 * kThreads) {  // sixteen loads in flight
+    float v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = B.X[e + u * kThreads];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) m = fmaxf(m, fabsf(v[u]));
+  }
+  for (; e < e1; e += kThreads) m = fmaxf(m, fabsf(B.X[e]));
   for (int k = 32; k >= 1; k >>= 1) m = fmaxf(m, shfl_xor_f(m, k));
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
   __syncthreads();
