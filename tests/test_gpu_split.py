@@ -73,9 +73,10 @@ def test_split_ragged(n, d, r, K):
 
 # The eight-wave fused pass B (d in 97..128, r in 33..64, r % 4 == 0): one tile per
 # workgroup (tail only), 2-3 and 3-4 tiles per workgroup (loop and tail), padded
-# features (d < 128) and masked columns (r < 64).
+# features (d < 128) and masked columns (r < 64), and fewer rows than one tile.
 @pytest.mark.parametrize("n,d,r,K", [(130, 128, 64, 64), (70001, 104, 40, 20), (98381, 128, 64, 30),
-                                     (5000, 100, 44, 11), (131072, 128, 64, 64)])
+                                     (5000, 100, 44, 11), (131072, 128, 64, 64), (100, 128, 64, 8),
+                                     (64, 104, 36, 36)])
 def test_split_fused8(n, d, r, K):
     log(f"split fused8: n={n} d={d} r={r} K={K}")
     X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 5 + d)
