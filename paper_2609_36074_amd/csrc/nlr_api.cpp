@@ -830,7 +830,11 @@ void nlr_destroy(nlr_ctx* c) {
 }
 
 const char* nlr_status_string(nlr_status s) {
-  switch (s) {
+  // a C caller may pass any int; reading it through the enum type would be
+  // undefined in C++ for values outside the enumerators' range
+  int v;
+  std::memcpy(&v, &s, sizeof v);
+  switch (v) {
     case NLR_OK: return "ok";
     case NLR_EINVAL: return "invalid argument";
     case NLR_EWORKSPACE: return "workspace missing, misaligned or too small";
