@@ -115,9 +115,20 @@ def cpu_baseline(workload, n_sample: int, iters: int) -> dict:
     t0 = time.perf_counter()
     onlr.run(Xh, U0, wl.K, alpha, 1.0, T=iters, T_min=iters, project_init=False)
     dt = time.perf_counter() - t0
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), cpu)
+    except OSError:
+        pass
+    try:
+        visible = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        visible = os.cpu_count() or 1
     return {"value": n_sample * iters / dt, "unit": "points*iters/s", "cores": int(threads), "kind": "oracle",
             "sample": f"fp64 oracle loop, {iters} iterations on the first {n_sample} rows of the same "
-                      f"seeded {workload} mixture (d={wl.d}, K=r={wl.K}); {dt:.1f} s"}
+                      f"seeded {workload} mixture (d={wl.d}, K=r={wl.K}); {dt:.1f} s",
+            "cpu": cpu, "cores_visible": int(visible)}
 
 
 def kernel_flops(kind: str, n: int, d: int, r: int) -> float:
