@@ -74,7 +74,15 @@ __global__ __launch_bounds__(kThreads) void k_colsum(Geometry g, Bufs B) {
   } else {
     for (int col = tid; col < d; col += kThreads) {
       double acc = 0.0;
-      for (int64_t i = r0; i < r1; ++i) acc += (double)B.X[i * d + col];
+      int64_t i = r0;
+      for (; i + 7 < r1; i += 8) {  // eight rows' loads in flight, added in row order
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = B.X[(i + u) * d + col];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc += (double)v[u];
+      }
+      for (; i < r1; ++i) acc += (double)B.X[i * d + col];
       out[col] = acc;
     }
   }
@@ -260,12 +268,23 @@ __global__ __launch_bounds__(kThreads) void k_power(Geometry g, Bufs B, const do
   __syncthreads();
   double lam = 0.0;
   for (int it = 0; it <= kPowerIters; ++it) {
-    // w = C v, one wave per row, lanes stride the columns
-    for (int i = wave; i < d; i += 4) {
-      double t = 0.0;
-      for (int j = lane; j < d; j += 64) t += C[(int64_t)i * d + j] * v[j];
-      for (int m = 32; m >= 1; m >>= 1) t += shfl_xor_d(t, m);
-      if (lane == 0) w[i] = t;
+    // w = C v, one wave per row (four rows of a wave at a time, their loads in
+    // flight together), lanes stride the columns
+    for (int i0 = 4 * wave; i0 < d; i0 += 16) {
+      double t[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+      for (int j = lane; j < d; j += 64) {
+        const double vj = v[j];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (i0 + q < d) t[q] += C[(int64_t)(i0 + q) * d + j] * vj;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        double tq = t[q];
+        for (int m = 32; m >= 1; m >>= 1) tq += shfl_xor_d(tq, m);
+        if (lane == 0 && i0 + q < d) w[i0 + q] = tq;
+      }
     }
     __syncthreads();
     double vw = 0.0, ww = 0.0;
@@ -324,7 +343,15 @@ __global__ __launch_bounds__(kThreads) void k_normalise(Geometry g, Bufs B) {
   } else {
     for (int col = tid; col < d; col += kThreads) {
       const double xb = B.i_xbar[col];
-      for (int64_t i = row0; i < row1; ++i) one(i, col, xb);
+      int64_t i = row0;
+      for (; i + 7 < row1; i += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = B.X[(i + u) * d + col];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) B.X[(i + u) * d + col] = (float)(((double)v[u] - xb) / a);
+      }
+      for (; i < row1; ++i) one(i, col, xb);
     }
   }
 }

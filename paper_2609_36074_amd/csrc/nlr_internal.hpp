@@ -15,7 +15,7 @@ constexpr int kHistCap = 4096;    // per-iteration record ring
 constexpr int kTPA = 64;          // rows per pass-A tile
 constexpr int kTPB = 128;         // rows per pass-B super-tile (4 waves x 32 rows)
 constexpr int kMaxR = 256;        // largest supported rank
-constexpr int kPowerIters = 64;   // refinement power iterations after the squaring phase
+constexpr int kPowerIters = 16;   // refinement power iterations after the squaring phase
 constexpr int kSquarings = 20;    // C -> C^(2^20) before the refinement
 
 // Device control block.  Written only by single-workgroup control kernels and
