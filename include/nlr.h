@@ -213,7 +213,10 @@ nlr_status nlr_normaliser(nlr_ctx* ctx, double* a, double* xbar_host);
 
 /* Diagnostic read-back (synchronises): what = 0 copies Theta = Xhat^T U of the
  * latest iteration as d*r row-major floats; 1 copies p = U^T 1 (r floats) of
- * the current U; 2 copies s = U^T ybar (r floats) of the latest iteration. */
+ * the current U; 2 copies s = U^T ybar (r floats) of the latest iteration's
+ * starting factor -- in the one-pass form (split products, 97..128 features,
+ * 33..64 columns) of the current U instead, formed after each pass for the next
+ * one with the step arguments of that call. */
 nlr_status nlr_inspect(nlr_ctx* ctx, int32_t what, void* host_dst, size_t bytes);
 
 /* Per-kernel timing with HIP events recorded on the context's stream around
