@@ -219,7 +219,7 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}): the NLR path here is the "
-              "single-GPU kernel set; multi-GPU row sharding is described in DESIGN.md but not built.",
+              "single-GPU kernel set; sharding the rows over several GPUs is designed but not built.",
               file=sys.stderr)
         sys.exit(2)
 
