@@ -168,3 +168,25 @@ def test_onepass_resume_flags():
     c = nlr.Context(to_dev(Xh.astype(np.float32)), K, b.U, b.y, alpha=alpha, beta=beta, flags=flags, **kw)
     c.run(59)
     assert rel_max_err(host(c.U), host(a.U)) < U_TOL
+
+
+def test_onepass_nondefault_stream_and_profiling():
+    """The one-pass form on a non-default stream gives the same iterate bitwise; with
+    profiling on, its launches are timed under the pass and control kinds."""
+    import torch
+    X, Z, K, beta, alpha = _gated(128, 64)
+    kw = dict(eps_d=3e-3, eps_c=1e-7, T_min=0, flags=SPLIT)
+    a = make_ctx(X, Z, K, alpha, beta, **kw)
+    a.run(40)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        b = make_ctx(X, Z, K, alpha, beta, stream=s, **kw)
+        b.set_profiling(1)
+        b.run(20)
+        b.run(20)
+    s.synchronize()
+    assert np.array_equal(host(a.U), host(b.U)) and np.array_equal(host(a.y), host(b.y))
+    times = {k: v for k, v in b.kernel_times().items() if v[1]}
+    log(f"  one-pass launches timed: { {k: v[1] for k, v in times.items()} }")
+    assert times["pass_bf"][1] == 40 and times["reduce_theta"][1] == 40
+    assert all(v[0] > 0 for v in times.values())
