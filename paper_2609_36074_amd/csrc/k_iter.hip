@@ -480,6 +480,132 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
 }
 
 // ---------------------------------------------------------------------------
+// Row pass and finish pass of the single-Xhat-pass form for narrow factors (r <= 16,
+// r even): eight lanes per row (two columns each, 8-byte loads) and eight rows per
+// wave and step, so that the per-row work (the FP64 dot and its butterfly, q, the
+// dual step, ybar and the FP64 statistics) is not repeated over 16 lanes for a few
+// columns.  The row dot sums over the 8 lanes of a DPP half row (row8_sum_d); both
+// modes use it, so q, ytilde and ybar agree bitwise whichever of them does the row
+// work (nlr_run(T) equals T nlr_step).  Outputs as k_pass_a_rows.
+// ---------------------------------------------------------------------------
+template <int MODE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_rows_narrow(
+    Geometry g, Bufs B, StepArgs S) {
+  constexpr bool FINISH = MODE == kPassFinish;
+  static_assert(MODE == kPassFinish || MODE == kPassRows, "row work only");
+  const float* Usrc = B.ctl->ubuf ? B.U2 : B.U;
+  if (FINISH && B.ctl->breakdown != 0) {
+    if (B.ctl->ubuf) {
+      const int64_t tot = g.n * (int64_t)g.r;
+      for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < tot; e += (int64_t)gridDim.x * kThreads)
+        B.U[e] = B.U2[e];
+    }
+    return;
+  }
+  if (!FINISH && halted(B.ctl)) return;
+  const bool stopped = FINISH && (B.ctl->stop != 0);
+  constexpr int PF = 8;  // steps in flight
+  __shared__ double dred[kThreads + 8];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int grp = lane >> 3;  // row within the step
+  const int li = lane & 7;    // lane within the row
+  const int64_t n = g.n;
+  const int r = g.r;
+  const float cf = B.ctl->c_f;
+  const bool gate = (S.end_work != 0) && (B.ctl->gate != 0) && !stopped;
+  const float gam = S.gamma_f;
+  const int cu = 2 * li;
+  const bool cx = cu < r;  // r even: both columns of the lane are valid, or neither
+  const float pl[2] = {cx ? B.p[cu] : 0.f, cx ? B.p[cu + 1] : 0.f};
+
+  const int64_t steps = (n + 7) >> 3;
+  const int64_t wid = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t nw = (int64_t)g.GA * 4;
+  const int64_t k0 = wid * steps / nw;
+  const int64_t k1 = (wid + 1) * steps / nw;
+
+  double s_acc[2] = {0.0, 0.0};
+  double qq = 0.0, yq = 0.0;
+  float ur[PF][2];
+  float yr[PF];
+  auto issue = [&](int slot, int64_t k) {
+    const int64_t row = 8 * k + grp;
+    const bool ok = (k < k1) && (row < n);
+    const int64_t rr = ok ? row : 0;
+    load_vec<2>(ur[slot], Usrc + rr * r + (cx ? cu : 0), true);
+    yr[slot] = B.y[rr];
+  };
+#pragma unroll
+  for (int i = 0; i < PF; ++i) {
+    __builtin_amdgcn_sched_barrier(0);
+    issue(i, k0 + i);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  for (int64_t kb = k0; kb < k1; kb += PF) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      __builtin_amdgcn_sched_barrier(0);
+      const int64_t k = kb + i;
+      const int64_t row = 8 * k + grp;
+      const bool valid = (k < k1) && (row < n);
+      float u[2];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) u[c] = (valid && cx) ? ur[i][c] * cf : 0.f;
+      double dot = 0.0;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) dot += (double)u[c] * (double)pl[c];
+      dot = row8_sum_d(dot);
+      const float q = (float)(dot - 1.0);
+      float yt = valid ? yr[i] : 0.f;
+      if (gate) yt = fmaf(gam, q, yt);
+      const float ybar = fmaf(gam, q, yt);
+      if (gate) *(valid ? (B.y + row) : B.dump) = yt;  // the 8 lanes of a row store the same value
+#pragma unroll
+      for (int c = 0; c < 2; ++c) s_acc[c] += (double)ybar * (double)u[c];
+      const bool lead = valid && li == 0;
+      qq += lead ? (double)q * (double)q : 0.0;
+      yq += lead ? (double)yt * (double)q : 0.0;
+      if (FINISH) {
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        float* dst = (valid && cx) ? (B.U + row * r + cu) : B.dump;
+        *reinterpret_cast<f32x2*>(dst) = (f32x2){u[0], u[1]};
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      issue(i, k + PF);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // s: the eight rows of a step hold the same columns; waves hold disjoint rows
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    double v = s_acc[c] + shfl_xor_d(s_acc[c], 8);
+    v = v + shfl_xor_d(v, 16);
+    v = v + shfl_xor_d(v, 32);
+    if (grp == 0) dred[wave * 16 + cu + c] = v;
+  }
+  __syncthreads();
+  double* ap = B.a_part + (int64_t)blockIdx.x * (4 + g.r32);
+  for (int c = tid; c < g.r32; c += kThreads) {
+    double t = 0.0;
+    if (c < 16) t = ((dred[c] + dred[16 + c]) + dred[32 + c]) + dred[48 + c];
+    ap[4 + c] = FINISH ? 0.0 : t;
+  }
+  const double tq = block_sum_d(qq, dred + kThreads);
+  const double ty = block_sum_d(yq, dred + kThreads);
+  if (tid == 0) {
+    ap[0] = tq;
+    ap[1] = ty;
+    ap[2] = ap[3] = 0.0;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Segmented column sums, fixed order: out[s][c] = sum over rows of segment s of
 // P[row][c] (rows [s R/S, (s+1) R/S)).  Grid (ceil(C/64), S); thread (col, sub)
 // sums rows sub, sub+4, ... of the segment, then the four subs are added in order.
@@ -1351,6 +1477,16 @@ static hipError_t pass_a_rows_launch(const Geometry& g, const Bufs& b, const Ste
 
 static hipError_t pass_a_rows_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, int finish,
                                        hipStream_t st) {
+  // narrow factors in the single-Xhat-pass form: the row and finish passes (both, so
+  // that their row dots agree) pack eight lanes per row; pass A with its product keeps
+  // the 16-lane layout
+  if (g.fused && g.r <= 16 && g.r % 2 == 0 && (finish == kPassRows || finish == kPassFinish)) {
+    if (finish == kPassFinish)
+      hipLaunchKernelGGL((k_rows_narrow<kPassFinish>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
+    else
+      hipLaunchKernelGGL((k_rows_narrow<kPassRows>), dim3(g.GA), dim3(kThreads), 0, st, g, b, a);
+    return hipGetLastError();
+  }
   const int key = g.a_fv * 100 + g.a_ngf * 10 + g.a_cv;
   switch (key) {
     case 111: return pass_a_rows_launch<1, 1, 1>(g, b, a, finish, st);
