@@ -359,3 +359,45 @@ def test_profiling_levels():
     assert {"ctl_a", "ctl_b", "reduce_theta"} <= set(every)
     assert set(passes) <= {"pass_a", "pass_b", "pass_u", "pass_bf", "finish"} and passes
     assert all(v[0] > 0 for v in passes.values())
+
+
+def test_history_ring_wraps_in_order():
+    """Beyond 4096 iterations the history holds the latest 4096 records, oldest first, and
+    their iteration numbers and statistics match the record of the last iteration."""
+    X, Z, _, wl = _tiny()
+    K = wl.K
+    T = 4096 + 700
+    ctx = make_ctx(X, Z, K, onlr.default_step_size(K), eps_d=0.0, eps_c=0.0, T_min=T)
+    done, last = ctx.run(T)
+    assert done == T
+    hist = ctx.history(8192)
+    assert len(hist) == 4096
+    assert [h["t"] for h in hist] == list(range(T - 4096, T))
+    assert hist[-1]["t"] == last["t"] and hist[-1]["objective"] == last["objective"]
+    assert hist[-1]["delta"] == last["delta"] and hist[-1]["c"] == last["c"]
+    assert len(ctx.history(10)) == 10 and ctx.history(10)[-1]["t"] == T - 1
+
+
+def test_two_contexts_interleaved_on_two_streams():
+    """Two contexts on two streams, their runs interleaved call by call, give the same
+    iterates bitwise as each run alone (contexts share no state)."""
+    import torch
+    X1, Z1, _, wl = _tiny()
+    X2, _, _ = gaussian_mixture(3000, 16, 4, 16.0, seed=77)
+    Z2 = standard_normal_factor(3000, 4, seed=78).astype(np.float64)
+    K = wl.K
+    alpha = onlr.default_step_size(K)
+    ref1 = make_ctx(X1, Z1, K, alpha)
+    ref1.run(60)
+    ref2 = make_ctx(X2, Z2, K, alpha)
+    ref2.run(60)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    a = make_ctx(X1, Z1, K, alpha, stream=s1)
+    b = make_ctx(X2, Z2, K, alpha, stream=s2)
+    for _ in range(6):
+        a.step(with_stats=False)
+        b.run(10)
+        a.run(9)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(a.U), host(ref1.U)) and np.array_equal(host(a.y), host(ref1.y))
+    assert np.array_equal(host(b.U), host(ref2.U)) and np.array_equal(host(b.y), host(ref2.y))
