@@ -1366,6 +1366,20 @@ __device__ __forceinline__ void seg_ab_block(const Geometry& g, const Bufs& B, i
   if (tid < 8 && col < C) out[col] = red[tid];
 }
 
+// The segment sums after the fused pass B of the single-Xhat-pass form in one launch:
+// blockIdx.y < SAF the segments of the Theta partial rows, SAF .. SAF + SB - 1 those of
+// the statistics rows (b_part; the first (4 + r32 + 63) / 64 blocks of those rows).
+__global__ __launch_bounds__(kThreads) void k_seg_fused(Geometry g, Bufs B) {
+  if (halted(B.ctl)) return;
+  __shared__ double red[kThreads];
+  const int by = blockIdx.y;
+  if (by < g.SAF) {
+    seg_sum_block<float>(B.theta_part, g.GB, g.theta_cols, B.seg_theta, g.SAF, blockIdx.x, by, red);
+  } else if ((int)blockIdx.x < (4 + g.r32 + 63) / 64) {
+    seg_sum_block<double>(B.b_part, g.GB, 4 + g.r32, B.seg_b, g.SB, blockIdx.x, by - g.SAF, red);
+  }
+}
+
 // The segment sums after a one-pass kernel in one launch: blockIdx.y < nseg the
 // segments of the Theta and W^T W partial rows, nseg and nseg + 1 the statistics
 // (a_part, b_part; the first (4 + r32 + 7) / 8 blocks of those rows).
@@ -1637,6 +1651,18 @@ hipError_t launch_ctl_one(const Geometry& g, const Bufs& b, const StepArgs& a, h
 hipError_t launch_seg_onepass(const Geometry& g, const Bufs& b, hipStream_t st) {
   const int cx = (g.theta_cols + 63) / 64, ax = (4 + g.r32 + 7) / 8;
   hipLaunchKernelGGL(k_seg_onepass, dim3(cx > ax ? cx : ax, g.SAF + 2), dim3(kThreads), 0, st, g, b, g.SAF);
+  return hipGetLastError();
+}
+
+hipError_t launch_seg_fused(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const int cx = (g.theta_cols + 63) / 64, bx = (4 + g.r32 + 63) / 64;
+  hipLaunchKernelGGL(k_seg_fused, dim3(cx > bx ? cx : bx, g.SAF + g.SB), dim3(kThreads), 0, st, g, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_theta_fused(const Geometry& g, const Bufs& b, hipStream_t st) {
+  // the Theta segments come from k_seg_fused
+  hipLaunchKernelGGL(k_reduce_theta, dim3(g.RT), dim3(kThreads), 0, st, g, b, g.SAF, 1, -1.0f);
   return hipGetLastError();
 }
 

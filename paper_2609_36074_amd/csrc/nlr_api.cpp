@@ -453,9 +453,9 @@ static nlr_status enqueue_iteration(nlr_ctx* c, bool first) {
     LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
     LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
     LAUNCH(KK_PASS_BF, launch_pass_bf(c->g, c->b, a, c->stream));
-    LAUNCH(KK_CTL_B, launch_seg_b(c->g, c->b, c->stream));
+    LAUNCH(KK_CTL_B, launch_seg_fused(c->g, c->b, c->stream));  // statistics and Theta segments
     LAUNCH(KK_CTL_B, launch_ctl_b(c->g, c->b, a, c->stream));
-    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta(c->g, c->b, true, c->stream));
+    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta_fused(c->g, c->b, c->stream));
     c->pending = true;
     return NLR_OK;
   }

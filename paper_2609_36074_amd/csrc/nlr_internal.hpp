@@ -214,6 +214,8 @@ hipError_t launch_split_x8(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_seg_a_rows(const Geometry& g, const Bufs& b, int64_t rows, bool finish, hipStream_t st);
 hipError_t launch_ctl_one(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_seg_onepass(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_seg_fused(const Geometry& g, const Bufs& b, hipStream_t st);
+hipError_t launch_reduce_theta_fused(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_reduce_theta_onepass(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_s_gram(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
 hipError_t launch_reduce_theta_rows(const Geometry& g, const Bufs& b, int64_t rows, int nseg, bool scaled,
