@@ -451,6 +451,95 @@ __global__ __launch_bounds__(kThreads) void k_zero_y(Geometry g, Bufs B) {
 }
 
 // ---------------------------------------------------------------------------
+// The same power method for wide inputs (d > 256), the matrix-vector products
+// spread over workgroups: C does not stay in one compute unit's cache there, and
+// one workgroup streaming it each iteration dominates the initialisation.
+// v and w live in the squaring buffer the last squaring did not write (vw[0..d),
+// vw[d..2d)); state[0] the Rayleigh quotient.
+// ---------------------------------------------------------------------------
+// v = the column of Bf with the largest diagonal entry (lowest index on ties), normalised.
+__global__ __launch_bounds__(kThreads) void k_power_start(Geometry g, const double* __restrict__ Bf,
+                                                          double* __restrict__ vw) {
+  __shared__ double red[8];
+  __shared__ int shi[1];
+  __shared__ double sh[1];
+  const int d = g.d, tid = threadIdx.x;
+  if (tid == 0) {
+    double best = -1.0;
+    int arg = 0;
+    for (int j = 0; j < d; ++j) {
+      const double x = Bf[(int64_t)j * d + j];
+      if (x > best) {
+        best = x;
+        arg = j;
+      }
+    }
+    shi[0] = arg;
+  }
+  __syncthreads();
+  const int j0 = shi[0];
+  double nn = 0.0;
+  for (int i = tid; i < d; i += kThreads) {
+    const double x = Bf[(int64_t)i * d + j0];
+    nn += x * x;
+  }
+  nn = block_sum_d(nn, red);
+  if (tid == 0) sh[0] = nn;
+  __syncthreads();
+  const double inv = (sh[0] > 0.0) ? 1.0 / sqrt(sh[0]) : 0.0;
+  for (int i = tid; i < d; i += kThreads) vw[i] = Bf[(int64_t)i * d + j0] * inv;
+}
+
+// w = C v: workgroup b forms rows 64 b .. 64 b + 63; lane l row 64 b + l (column l of the
+// symmetric C, read row by row: coalesced), wave k the terms j = k, k + 4, ...; the four
+// partial sums are added in order.
+__global__ __launch_bounds__(kThreads) void k_power_mv(Geometry g, const double* __restrict__ C,
+                                                       double* __restrict__ vw) {
+  __shared__ double part[kThreads];
+  const int d = g.d, tid = threadIdx.x;
+  const int i = blockIdx.x * 64 + (tid & 63), sub = tid >> 6;
+  const double* v = vw;
+  double t = 0.0;
+  if (i < d)
+#pragma unroll 4
+    for (int j = sub; j < d; j += 4) t += C[(int64_t)j * d + i] * v[j];
+  part[tid] = t;
+  __syncthreads();
+  if (sub == 0 && i < d) vw[d + i] = ((part[tid] + part[64 + tid]) + part[128 + tid]) + part[192 + tid];
+}
+
+// Rayleigh quotient of v, then v = w / |w| (not after the last product); with last set,
+// a = sqrt(Rayleigh quotient) to the control block.
+__global__ __launch_bounds__(kThreads) void k_power_norm(Geometry g, Bufs B, double* __restrict__ vw, int last) {
+  __shared__ double red[8];
+  __shared__ double sh[2];
+  const int d = g.d, tid = threadIdx.x;
+  double s1 = 0.0, s2 = 0.0;
+  for (int i = tid; i < d; i += kThreads) {
+    s1 += vw[i] * vw[d + i];
+    s2 += vw[d + i] * vw[d + i];
+  }
+  s1 = block_sum_d(s1, red);
+  s2 = block_sum_d(s2, red);
+  if (tid == 0) {
+    sh[0] = s1;
+    sh[1] = s2;
+  }
+  __syncthreads();
+  if (last) {
+    if (tid == 0) {
+      const double lam = sh[0];
+      const double a = (lam > 0.0) ? sqrt(lam) : 0.0;
+      B.ctl->spectral_a = a;
+      if (!(a > 0.0) || !isfinite(a)) B.ctl->degenerate = 1;
+    }
+    return;
+  }
+  const double inv = (sh[1] > 0.0) ? 1.0 / sqrt(sh[1]) : 0.0;
+  for (int i = tid; i < d; i += kThreads) vw[i] = vw[d + i] * inv;
+}
+
+// ---------------------------------------------------------------------------
 hipError_t launch_ctl_init(const Bufs& b, float gamma_f, hipStream_t st) {
   hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, b, gamma_f);
   return hipGetLastError();
@@ -493,6 +582,17 @@ hipError_t launch_spectral(const Geometry& g, const Bufs& b, hipStream_t st) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (g.d > kThreads) {
+    // wide inputs: the products over workgroups; v and w in the buffer the last
+    // squaring did not write
+    double* vw = (in == b.i_B0) ? b.i_B1 : b.i_B0;
+    hipLaunchKernelGGL(k_power_start, dim3(1), dim3(kThreads), 0, st, g, in, vw);
+    for (int it = 0; it <= kPowerIters; ++it) {
+      hipLaunchKernelGGL(k_power_mv, dim3((g.d + 63) / 64), dim3(kThreads), 0, st, g, (const double*)b.i_C, vw);
+      hipLaunchKernelGGL(k_power_norm, dim3(1), dim3(kThreads), 0, st, g, b, vw, it == kPowerIters ? 1 : 0);
+    }
+    return hipGetLastError();
+  }
   const size_t lds = 2 * (size_t)g.d * sizeof(double);
   if (lds > (64u << 10)) {
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_power), hipFuncAttributeMaxDynamicSharedMemorySize,
