@@ -100,12 +100,13 @@ __global__ __launch_bounds__(kThreads) void k_colmean(Geometry g, Bufs B) {
 // workgroup (chunk gx, block pair bp) adds the 64 x 64 block (bi, bj), bi <= bj, of
 // the sum over the chunk's rows of (x - xbar)(x - xbar)^T.  Wave w owns the block
 // rows 16 w .. 16 w + 15 and all 64 columns (four 16 x 16 tiles).  A product step
-// takes 4 rows: lane l supplies row l / 16 of the step and feature l % 16 of its
-// tile (the A operand from the block's rows, the B operands from its columns), and
+// takes 4 data rows: lane l reads row l / 16 of the step and feature l % 16 of its
+// tile from LDS (the A operand from the block's rows, the B operands from its columns), and
 // holds result element (4 v + l / 16, l % 16) of a tile in entry v.  The blocks
 // below the diagonal are not formed (the sum is symmetric; k_gram_reduce reads
 // their mirror).
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
+static_assert(kThreads == 256, "k_gram stages a 32 x 64 operand as 8 elements per thread of 4 waves");
 __global__ __launch_bounds__(kThreads) void k_gram(Geometry g, Bufs B) {
   const int tid = threadIdx.x;
   const int d = g.d;
@@ -121,40 +122,50 @@ __global__ __launch_bounds__(kThreads) void k_gram(Geometry g, Bufs B) {
   const int64_t r1 = (int64_t)(blockIdx.x + 1) * n / g.GG;
   const int lane = tid & 63, w = tid >> 6;
   const int kq = lane >> 4, cl = lane & 15;
-  const int fa = 64 * bi + 16 * w + cl;
-  const bool oka = fa < d;
-  const double ma = oka ? B.i_xbar[fa] : 0.0;
-  int fbj[4];
-  bool okb[4];
-  double mb[4];
-#pragma unroll
-  for (int J = 0; J < 4; ++J) {
-    fbj[J] = 64 * bj + 16 * J + cl;
-    okb[J] = fbj[J] < d;
-    mb[J] = okb[J] ? B.i_xbar[fbj[J]] : 0.0;
-  }
   f64x4_t acc[4];
 #pragma unroll
   for (int J = 0; J < 4; ++J) acc[J] = (f64x4_t){0.0, 0.0, 0.0, 0.0};
-  // rounds of 8 steps (32 rows): the round's loads are issued together
-  for (int64_t t0 = r0; t0 < r1; t0 += 32) {
-    float va[8], vb[8][4];
-    bool okr[8];
+  // Rounds of 32 rows.  The round's centred values of the block's 64 row features
+  // and 64 column features are formed once in FP64 by the workgroup and staged in
+  // LDS (rows padded to 80 doubles, so that the 32 lanes of a read pass meet all 64
+  // banks); the next round's raw values are loaded while the matrix cores take this
+  // round's.
+  __shared__ double xs[2][32][80];
+  const bool same = bi == bj;
+  // element k = tid + 256 q (q = 0..7) of a 32 x 64 operand: row k / 64, feature k % 64
+  const int sf = tid & 63, sr = tid >> 6;  // feature, first row (rows sr + 4 q)
+  const int fsa = 64 * bi + sf, fsb = 64 * bj + sf;
+  const bool oksa = fsa < d, oksb = fsb < d;
+  const double msa = oksa ? B.i_xbar[fsa] : 0.0, msb = oksb ? B.i_xbar[fsb] : 0.0;
+  float ra[8], rb[8];
+  auto load_round = [&](int64_t t0) {
 #pragma unroll
-    for (int st = 0; st < 8; ++st) {
-      const int64_t row = t0 + 4 * st + kq;
-      okr[st] = row < r1;
-      const int64_t rb = (okr[st] ? row : r0) * (int64_t)d;
-      va[st] = B.X[rb + (oka ? fa : 0)];
-#pragma unroll
-      for (int J = 0; J < 4; ++J) vb[st][J] = B.X[rb + (okb[J] ? fbj[J] : 0)];
+    for (int q = 0; q < 8; ++q) {
+      const int64_t row = t0 + sr + 4 * q;
+      const int64_t rb0 = (row < r1 ? row : r0) * (int64_t)d;
+      ra[q] = B.X[rb0 + (oksa ? fsa : 0)];
+      rb[q] = same ? 0.f : B.X[rb0 + (oksb ? fsb : 0)];
     }
+  };
+  if (r0 < r1) load_round(r0);
+  for (int64_t t0 = r0; t0 < r1; t0 += 32) {
+    __syncthreads();  // the previous round's operands are consumed
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const bool okr = t0 + sr + 4 * q < r1;
+      xs[0][sr + 4 * q][sf] = (okr && oksa) ? (double)ra[q] - msa : 0.0;
+      if (!same) xs[1][sr + 4 * q][sf] = (okr && oksb) ? (double)rb[q] - msb : 0.0;
+    }
+    __syncthreads();
+    if (t0 + 32 < r1) load_round(t0 + 32);
+    const int ob = same ? 0 : 1;
 #pragma unroll
     for (int st = 0; st < 8; ++st) {
-      const double a = (okr[st] && oka) ? (double)va[st] - ma : 0.0;
+      const int row = 4 * st + kq;
+      const double a = xs[0][row][16 * w + cl];
 #pragma unroll
       for (int J = 0; J < 4; ++J) {
-        const double b = (okr[st] && okb[J]) ? (double)vb[st][J] - mb[J] : 0.0;
+        const double b = xs[ob][row][16 * J + cl];
         acc[J] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc[J], 0, 0, 0);
       }
     }
@@ -165,7 +176,7 @@ __global__ __launch_bounds__(kThreads) void k_gram(Geometry g, Bufs B) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int ia = 64 * bi + 16 * w + 4 * v + kq;
-      const int jb = fbj[J];
+      const int jb = 64 * bj + 16 * J + cl;
       if (ia < d && jb < d) out[(int64_t)ia * d + jb] = acc[J][v];
     }
 }
