@@ -101,8 +101,16 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
     g.GI = (int32_t)gi;
     const int64_t dd8 = (int64_t)d * d * 8;
     int64_t gg = ((int64_t)64 << 20) / (dd8 > 0 ? dd8 : 1);
-    if (gg < 1) gg = 1;
+    // every Gram workgroup resident at once: four per compute unit (their LDS), 256
+    // units, shared by the chunks of all nb (nb + 1) / 2 block pairs -- a second,
+    // partial wave of workgroups would take as long as the first (2e6 x 768: 14 chunks
+    // x 78 pairs, 34.5 ms; 13 chunks, 29.6 ms).  At most 256 chunks: more resident
+    // workgroups do not shorten the 128-feature Gram and lengthen its reduction.
+    const int64_t nbk = (d + 63) / 64;
+    const int64_t resident = 1024 / (nbk * (nbk + 1) / 2);
+    if (gg > resident) gg = resident;
     if (gg > 256) gg = 256;
+    if (gg < 1) gg = 1;
     const int64_t t64 = (n + 63) / 64;
     if (gg > t64) gg = t64;
     g.GG = (int32_t)gg;

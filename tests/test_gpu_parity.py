@@ -45,9 +45,10 @@ def _gated():
 
 # ---------------------------------------------------------------- initialisation
 # d = 1, 65 and 130 also cover the Gram kernel's ragged 64-feature blocks and the mirrored
-# blocks below its diagonal (one, two and three blocks per side)
+# blocks below its diagonal (one, two and three blocks per side); d = 300 the power method's
+# matrix-vector products spread over workgroups (above 256 features) with a ragged last one
 @pytest.mark.parametrize("n,d", [(2000, 16), (1037, 13), (5000, 128), (300, 768), (500, 1), (777, 65),
-                                 (3001, 130)])
+                                 (3001, 130), (1501, 300)])
 def test_normaliser(n, d):
     log(f"normaliser n={n} d={d}")
     X, _, _ = gaussian_mixture(n, d, 3, 9.0, seed=n + d)
