@@ -159,9 +159,26 @@ enum {
 nlr_status nlr_labels_spectral(nlr_ctx* ctx, int32_t K, const int64_t* seed_rows, int32_t max_iter,
                                int32_t* labels, int32_t* passes_done);
 
-/* Bytes of device workspace nlr_init needs for an (n, d, r) problem.  Depends
- * only on (n, d, r).  Returns 0 when the shape is invalid or unsupported. */
+/* Bytes of device workspace nlr_init needs for an (n, d, r) problem (the
+ * storage model of Section 4.4, eq. gpu-storage: besides Xhat, the one n x r
+ * factor and the stored dual, only per-workgroup partial sums -- fp32 Theta
+ * partials, FP64 statistics -- and a few d x r / r-vectors; the panel form adds
+ * ybar, n floats).  Depends only on (n, d, r).  Returns 0 when the shape is
+ * invalid or unsupported. */
 size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r);
+
+/* The iteration form nlr_init chooses for a shape and flags, assuming 16-byte
+ * aligned X and U (as any allocator's base address is); host-only, no HIP call.
+ * Every form computes Algorithm 1; they differ in how the passes over the rows
+ * are fused (Section 4.2) and by floating-point rounding only.  Returns an
+ * nlr_form value, or -1 for invalid arguments or an unsupported shape. */
+enum {
+  NLR_FORM_TWO_PASS = 0,     /* pass A (Theta = Xhat^T U, row work), pass B (Xhat Theta, epilogue) */
+  NLR_FORM_PANEL = 1,        /* two passes with LDS-tiled split-fp16 products (large d x r) */
+  NLR_FORM_SINGLE_PASS = 2,  /* row pass over U, then pass B that also forms Xhat^T W: Xhat read once */
+  NLR_FORM_ONE_PASS = 3      /* one kernel per iteration: row work, primal step, next Theta and s terms */
+};
+int32_t nlr_iteration_form(int64_t n, int32_t d, int32_t r, int32_t K, uint32_t flags);
 
 /* Prepares a problem and enqueues the initialisation on `stream`:
  *   1. centring and spectral normalisation of X in place (Section 3):
@@ -199,7 +216,12 @@ nlr_status nlr_step(nlr_ctx* ctx, nlr_iter_stats* stats);
 nlr_status nlr_run(nlr_ctx* ctx, int32_t T, int32_t* iters_done, nlr_iter_stats* last);
 
 /* Row-argmax labels of the current U: labels[i] = argmax_j U_ij, lowest j on
- * ties (int32, device pointer, n entries).  Asynchronous. */
+ * ties (int32, device pointer, n entries).  Appendix D ("Recover cluster labels
+ * from U"): under exact recovery with r = K the solution is U = H, one positive
+ * entry 1/sqrt(n_k) per row in the column of the row's cluster, so the argmax
+ * of a row is its cluster; for r > K use nlr_labels_spectral.  Argmax of W
+ * equals argmax of U = c W (c > 0).  Returns NLR_EINVAL for a NULL or
+ * misaligned labels pointer, NLR_ESTATE on a failed context.  Asynchronous. */
 nlr_status nlr_labels(nlr_ctx* ctx, int32_t* labels);
 
 /* Copies the records of the most recent iterations (oldest first, at most the

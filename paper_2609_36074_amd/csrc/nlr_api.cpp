@@ -535,6 +535,17 @@ size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r) {
   return m;
 }
 
+int32_t nlr_iteration_form(int64_t n, int32_t d, int32_t r, int32_t K, uint32_t flags) {
+  if (!shape_ok(n, d, r) || K < 1 || K > r || r > kMaxR) return -1;
+  const bool split = (flags & NLR_INIT_SPLIT_F16) != 0;
+  const Geometry g = make_geometry(n, d, r, K, true, split, (flags & NLR_INIT_TWO_PASS) == 0);
+  if (split && !g.split_b && !g.panel) return -1;
+  if (g.fused8) return NLR_FORM_ONE_PASS;
+  if (g.fused) return NLR_FORM_SINGLE_PASS;
+  if (g.panel) return NLR_FORM_PANEL;
+  return NLR_FORM_TWO_PASS;
+}
+
 nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, int32_t r, float* U, float* y,
                     const nlr_params* params, uint32_t flags, void* workspace, size_t workspace_bytes,
                     void* stream) {

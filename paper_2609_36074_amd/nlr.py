@@ -31,7 +31,14 @@ NLR_INIT_DATA_START = 32
 
 NLR_MAX_KERNEL_KINDS = 16
 
-EXPORTED = ["nlr_workspace_bytes", "nlr_init", "nlr_set_params", "nlr_step", "nlr_run", "nlr_labels",
+NLR_FORM_TWO_PASS = 0
+NLR_FORM_PANEL = 1
+NLR_FORM_SINGLE_PASS = 2
+NLR_FORM_ONE_PASS = 3
+FORM_NAMES = {NLR_FORM_TWO_PASS: "two-pass", NLR_FORM_PANEL: "two-pass-panel",
+              NLR_FORM_SINGLE_PASS: "single-Xhat-pass", NLR_FORM_ONE_PASS: "one-pass"}
+
+EXPORTED = ["nlr_workspace_bytes", "nlr_iteration_form", "nlr_init", "nlr_set_params", "nlr_step", "nlr_run", "nlr_labels",
             "nlr_labels_spectral",
             "nlr_history", "nlr_normaliser", "nlr_inspect", "nlr_set_profiling", "nlr_kernel_times",
             "nlr_destroy", "nlr_status_string", "nlr_version"]
@@ -77,6 +84,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     P, i32, i64, u32, sz, dbl = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_size_t, ctypes.c_double
     lib.nlr_workspace_bytes.argtypes = [i64, i32, i32]
     lib.nlr_workspace_bytes.restype = sz
+    lib.nlr_iteration_form.argtypes = [i64, i32, i32, i32, u32]
+    lib.nlr_iteration_form.restype = i32
     lib.nlr_init.argtypes = [ctypes.POINTER(P), P, i64, i32, i32, i32, P, P, ctypes.POINTER(NlrParams), u32, P, sz, P]
     lib.nlr_init.restype = ctypes.c_int
     lib.nlr_set_params.argtypes = [P, ctypes.POINTER(NlrParams)]
@@ -125,6 +134,10 @@ def _check(status: int, where: str) -> int:
 # ---------------------------------------------------------------------------
 def nlr_workspace_bytes(n: int, d: int, r: int) -> int:
     return int(load_library().nlr_workspace_bytes(n, d, r))
+
+
+def nlr_iteration_form(n: int, d: int, r: int, K: int, flags: int) -> int:
+    return int(load_library().nlr_iteration_form(n, d, r, K, flags))
 
 
 def nlr_init(X_ptr: int, n: int, d: int, K: int, r: int, U_ptr: int, y_ptr: int, params: NlrParams,

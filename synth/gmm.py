@@ -101,6 +101,9 @@ def cluster_sizes(n: int, K: int, rule: str, rng: np.random.Generator) -> np.nda
 
 
 def _fill_chunks(out: np.ndarray, seed_seq: np.random.SeedSequence, fill, threads: int) -> None:
+    # Child ci of a fresh SeedSequence is the same whatever the number spawned, so
+    # the rows of chunk ci do not depend on how many rows are drawn in all: the
+    # first m rows of an n-row draw are an m-row draw's rows (same labels given).
     n = out.shape[0]
     nchunks = (n + CHUNK_ROWS - 1) // CHUNK_ROWS
     children = seed_seq.spawn(nchunks)
@@ -120,12 +123,14 @@ def _fill_chunks(out: np.ndarray, seed_seq: np.random.SeedSequence, fill, thread
 
 def gaussian_mixture(n: int, d: int, K: int, center_var: float, *, sizes: str = "equal",
                      noise: str = "iso", l2_normalise: bool = False, seed: int = 0,
-                     threads: int | None = None):
-    """Draw (X float32 [n, d], labels int32 [n], centers float64 [K, d]).
+                     threads: int | None = None, rows: int | None = None):
+    """Draw (X float32 [m, d], labels int32 [m], centers float64 [K, d]), m = n or `rows`.
 
     Centers mu_k ~ N(0, center_var * I_d).  Noise eps_i ~ N(0, I_d) ("iso") or
     N(0, diag(v_{z_i})) with v_k ~ U[0.2, 2]^d ("aniso").  Labels are a
-    shuffled assignment with the requested cluster sizes.
+    shuffled assignment with the requested cluster sizes over all n rows.
+    With ``rows = m < n`` only the first m rows of the n-row draw are made:
+    bitwise the leading rows of the full draw.
     """
     threads = _threads() if threads is None else threads
     root = np.random.SeedSequence(seed)
@@ -143,7 +148,11 @@ def gaussian_mixture(n: int, d: int, K: int, center_var: float, *, sizes: str = 
         raise ValueError(f"unknown noise {noise!r}")
     c32 = centers.astype(np.float32)
     sd32 = None if sd is None else sd.astype(np.float32)
-    X = np.empty((n, d), dtype=np.float32)
+    m = n if rows is None else int(rows)
+    if not 0 < m <= n:
+        raise ValueError(f"rows must be in 1..{n}")
+    labels = labels[:m]
+    X = np.empty((m, d), dtype=np.float32)
 
     def fill(g: np.random.Generator, lo: int, hi: int) -> None:
         z = labels[lo:hi]
@@ -162,7 +171,10 @@ def gaussian_mixture(n: int, d: int, K: int, center_var: float, *, sizes: str = 
 
 
 def standard_normal_factor(n: int, r: int, seed: int, threads: int | None = None) -> np.ndarray:
-    """Z with i.i.d. N(0, 1) entries, float32 [n, r] (the raw draw behind U_0)."""
+    """Z with i.i.d. N(0, 1) entries, float32 [n, r] (the raw draw behind U_0).
+
+    Rows do not depend on n: the first m rows of an n-row draw are the m-row draw.
+    """
     threads = _threads() if threads is None else threads
     Z = np.empty((n, r), dtype=np.float32)
 
@@ -173,16 +185,20 @@ def standard_normal_factor(n: int, r: int, seed: int, threads: int | None = None
     return Z
 
 
-def make_workload(name_or_wl, n: int | None = None, threads: int | None = None):
+def make_workload(name_or_wl, n: int | None = None, threads: int | None = None,
+                  rows: int | None = None):
     """Inputs of a named workload: (X, Z, labels, workload).
 
-    ``n`` overrides the number of rows (a prefix-compatible smaller draw of the
-    same distribution, used for bounded CPU samples).
+    ``n`` replaces the number of rows: a new, smaller draw of the same
+    distribution (its cluster sizes and label shuffle are drawn for that n, so
+    its rows are not those of the full workload).  ``rows`` instead keeps the
+    full workload's n and returns only its first ``rows`` rows, bitwise equal to
+    the leading rows of the full draw (used for bounded CPU samples).
     """
     wl = WORKLOADS[name_or_wl] if isinstance(name_or_wl, str) else name_or_wl
     nn = wl.n if n is None else int(n)
     X, labels, _ = gaussian_mixture(nn, wl.d, wl.K, wl.center_var, sizes=wl.sizes,
                                     noise=wl.noise, l2_normalise=wl.l2_normalise,
-                                    seed=wl.seed, threads=threads)
-    Z = standard_normal_factor(nn, wl.r, wl.seed + 1, threads=threads)
+                                    seed=wl.seed, threads=threads, rows=rows)
+    Z = standard_normal_factor(X.shape[0], wl.r, wl.seed + 1, threads=threads)
     return X, Z, labels, wl

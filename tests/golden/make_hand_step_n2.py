@@ -22,7 +22,8 @@ g = {
         "a=||W||^2=1.22, b=||U||^2=1, h=<W,U>=1.1, c=sqrt(K/a), U1=cW (eq. projected-primal-step), "
         "delta^2=c^2 a+b-2ch=2-2.2/sqrt(1.22) (eq. movement-identity), p1=1.2/sqrt(1.22), "
         "q1=U1 p1-1=[1.32/1.22-1, 0.12/1.22-1], f(U0)=-Theta^2+beta/2*||q/sqrt2||^2=1/2 "
-        "(eq. normalized), gated dual step y1=(beta/sqrt2) q1 (Algorithm 1)."),
+        "(eq. normalized), gated dual step y1=(beta/sqrt2) q1 (Algorithm 1); the stored dual "
+        "ytilde=y/sqrt(n) takes (beta/n) q1 = 2 q1 (Section 3, storage convention)."),
     "X": [[-1.0], [3.0]], "U0": [[1.0], [0.0]], "K": 1, "alpha": 0.1, "beta": 4.0,
     "a_norm": 2.0 * math.sqrt(2.0),
     "Xhat": [[-1 / math.sqrt(2)], [1 / math.sqrt(2)]],
@@ -36,6 +37,7 @@ g = {
     "rho1": math.sqrt(q1[0] ** 2 + q1[1] ** 2) / math.sqrt(2.0),
     "objective0": 0.5,
     "y1_if_gated": [4.0 / math.sqrt(2.0) * q1[0], 4.0 / math.sqrt(2.0) * q1[1]],
+    "ytilde1_if_gated": [2.0 * q1[0], 2.0 * q1[1]],
 }
 with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "hand_step_n2.json"), "w") as f:
     json.dump(g, f, indent=1)

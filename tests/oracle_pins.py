@@ -344,6 +344,57 @@ def pin_random_start_recovery():
     assert kmeans.adjusted_rand_index(nlr.labels(res.U), lab) == 1.0
 
 
+def pin_stored_dual_convention():
+    """The dual buffer stores ytilde = y / sqrt(n), and the dual step y += (beta/sqrt(n)) q is
+    ytilde += (beta/n) q on it (Section 3, storage and penalty convention): hand values, the
+    hand-worked step's gated dual, and the effective multiplier of eq. (dualnormalized)."""
+    y = np.array([2.0, -4.0, 6.0, 0.0])           # n = 4, sqrt(n) = 2
+    assert np.array_equal(nlr.stored_dual(y), np.array([1.0, -2.0, 3.0, 0.0]))
+    assert np.array_equal(nlr.dual_from_stored(np.array([1.0, -2.0, 3.0, 0.0])), y)
+    g = json.load(open(os.path.join(GOLDEN, "hand_step_n2.json")))
+    yt = nlr.stored_dual(np.array(g["y1_if_gated"]))
+    assert np.allclose(yt, g["ytilde1_if_gated"], rtol=0, atol=1e-14), yt
+    assert np.allclose(nlr.dual_from_stored(np.array(g["ytilde1_if_gated"])), g["y1_if_gated"],
+                       rtol=0, atol=1e-14)
+    # ybar_eff = y/sqrt(n) + (beta/n) g(U): the stored dual plus the stored-scale penalty term
+    _, U, yr, beta = _random_state(31)
+    ybar = nlr.effective_multiplier(U, yr, beta)
+    n = U.shape[0]
+    assert np.allclose(ybar, nlr.stored_dual(yr) + (beta / n) * (U @ U.sum(axis=0) - 1.0),
+                       rtol=0, atol=1e-14)
+
+
+def pin_adjusted_rand_index():
+    """ARI by pair counting: a hand-worked contingency table (8/33), relabelling and
+    symmetry, and scikit-learn's adjusted_rand_score on random labelings."""
+    # table [[2,1,0],[0,1,2]]: sum C(n_ij,2) = 2, rows 6, cols 3, C(6,2) = 15:
+    # (2 - 6*3/15) / ((6+3)/2 - 6*3/15) = 0.8 / 3.3 = 8/33
+    a = np.array([0, 0, 0, 1, 1, 1])
+    b = np.array([0, 0, 1, 1, 2, 2])
+    assert abs(kmeans.adjusted_rand_index(a, b) - 8.0 / 33.0) < 1e-15
+    assert abs(kmeans.adjusted_rand_index(b, a) - 8.0 / 33.0) < 1e-15
+    assert kmeans.adjusted_rand_index(a, 5 - 3 * a) == 1.0
+    # one class against all-distinct labels: every pair split, ARI = 0
+    assert abs(kmeans.adjusted_rand_index(np.zeros(5, int), np.arange(5))) < 1e-15
+    from sklearn.metrics import adjusted_rand_score
+    rng = _rng(32)
+    for n, ka, kb in [(40, 3, 4), (200, 5, 5), (17, 2, 6)]:
+        x, z = rng.integers(0, ka, n), rng.integers(0, kb, n)
+        assert abs(kmeans.adjusted_rand_index(x, z) - adjusted_rand_score(x, z)) < 1e-12
+
+
+def pin_recovery_threshold():
+    """eq. (exact_recovery_threshold) at special cases: with d = 0 it is 8 log n (natural log);
+    with K d = 3 n log n the square root is 2, so the threshold is 12 log n; it grows with d."""
+    for n in (10, 1000, 123457):
+        assert abs(kmeans.exact_recovery_threshold_sq(n, 4, 0) - 8.0 * np.log(n)) < 1e-12 * np.log(n)
+        d = 3.0 * n * np.log(n)
+        assert abs(kmeans.exact_recovery_threshold_sq(n, 1, d) - 12.0 * np.log(n)) < 1e-12 * np.log(n)
+        assert abs(kmeans.exact_recovery_threshold_sq(n, 2, d / 2) - 12.0 * np.log(n)) < 1e-12 * np.log(n)
+    v = [kmeans.exact_recovery_threshold_sq(10_000, 8, d) for d in (1, 10, 100, 1000)]
+    assert all(x < y for x, y in zip(v, v[1:])), v
+
+
 # ---------------------------------------------------------------- brute force K-means
 def pin_partition_counts():
     """The partition enumerator yields S(n, k) partitions (Stirling numbers, golden table)."""

@@ -32,19 +32,53 @@ def test_algorithmic_bytes_per_point():
         bench.algorithmic_bytes("nonsense", n, d, r)
 
 
-@pytest.mark.parametrize("d,r,split,two_pass,form", [
-    (128, 64, True, False, "one-pass"), (97 + 3, 36, True, False, "one-pass"),
-    (128, 64, False, False, "single-Xhat-pass"), (64, 16, True, False, "single-Xhat-pass"),
-    (96, 64, True, False, "single-Xhat-pass"), (128, 32, True, False, "single-Xhat-pass"),
-    (128, 64, True, True, "two-pass")])
-def test_iteration_form(d, r, split, two_pass, form):
-    assert bench.iteration_form(d, r, split, two_pass) == form
+@pytest.mark.parametrize("name,n,d,r,split,two_pass,form", [
+    ("tiny", 2_000, 16, 4, True, False, "single-Xhat-pass"),
+    ("gmm1m", 1_000_000, 64, 16, True, False, "single-Xhat-pass"),
+    ("gmm10m", 10_000_000, 128, 64, True, False, "one-pass"),
+    ("gmm10m fp32", 10_000_000, 128, 64, False, False, "single-Xhat-pass"),
+    ("gmm10m two-pass", 10_000_000, 128, 64, True, True, "two-pass"),
+    ("gmm50m", 50_000_000, 32, 10, True, False, "single-Xhat-pass"),
+    ("embed2m", 2_000_000, 768, 256, True, False, "two-pass-panel"),
+    ("embed2m fp32", 2_000_000, 768, 256, False, False, "two-pass"),
+    ("d=100 r=36", 100_000, 100, 36, True, False, "one-pass"),
+    ("d=96", 100_000, 96, 64, True, False, "single-Xhat-pass"),
+    ("r=32", 100_000, 128, 32, True, False, "single-Xhat-pass"),
+    ("Table 2 d=50 fp32", 100_000, 50, 30, False, False, "two-pass"),
+])
+def test_iteration_form_comes_from_the_library(name, n, d, r, split, two_pass, form):
+    assert bench.iteration_form(n, d, r, r, split, two_pass) == form
 
 
-def test_traffic_record_matches_the_sources():
-    t = bench.load_traffic("pass_bf_split16", "gmm10m")
-    assert t is not None, "the committed traffic record no longer matches the kernel sources"
-    rec = json.load(open(os.path.join(ROOT, "profiles", "traffic_pass_bf_split16_gmm10m.json")))
-    assert rec["kernel_source_hash"] == bench.kernel_source_hash("pass_bf_split16")
+def test_iteration_form_rejects_unsupported_shapes():
+    with pytest.raises(ValueError):
+        bench.iteration_form(100_000, 50, 30, 20, True, False)  # split needs d % 4 == 0 (panel: d % 8)
+    with pytest.raises(ValueError):
+        bench.iteration_form(100_000, 128, 512, 64, False, False)  # r above the compiled family
+
+
+def test_physical_rate_counts_the_launched_kernels():
+    """achieved_hbm_gbs divides the bytes of the launched row and pass kernels, not the fixed
+    two-pass numerator (which the one-pass form does not move)."""
+    n, d, r = 10_000_000, 128, 64
+    kinfo = {"pass_bf": {"launches": 50}, "pass_u": {"launches": 1}, "finish": {"launches": 1},
+             "ctl_b": {"launches": 100}}
+    moved = bench.iteration_bytes(kinfo, n, d, r)
+    assert moved == 50 * 4.0 * (n * d + 2 * n * r + n) + 4.0 * (n * r + n) + 4.0 * (2 * n * r + n)
+    assert moved < 0.6 * 50 * bench.algorithmic_bytes("step", n, d, r)
+    two = {"pass_a": {"launches": 50}, "pass_b": {"launches": 50}, "finish": {"launches": 1}}
+    assert bench.iteration_bytes(two, n, d, r) == pytest.approx(
+        50 * bench.algorithmic_bytes("step", n, d, r) + 4.0 * (2 * n * r + n))
+
+
+def test_traffic_record_follows_the_sources():
+    """A traffic record is read only while the kernel sources hash to what it was measured on."""
+    path = os.path.join(ROOT, "profiles", "traffic_pass_bf_split16_gmm10m.json")
+    rec = json.load(open(path))
     assert 0.99 < rec["bytes_per_launch"] / rec["algorithmic_bytes_per_launch"] < 1.05
+    t = bench.load_traffic("pass_bf_split16", "gmm10m")
+    if rec["kernel_source_hash"] == bench.kernel_source_hash("pass_bf_split16"):
+        assert t == rec["bytes_per_launch"]
+    else:
+        assert t is None
     assert bench.load_traffic("pass_bf_split16", "no-such-workload") is None

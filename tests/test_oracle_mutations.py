@@ -41,6 +41,9 @@ MUTATIONS = [
     ("range finder with the transposed Cholesky factor", "MRinv = np.linalg.solve(L, M.T).T",
      "MRinv = np.linalg.solve(L.T, M.T).T"),
     ("range finder on Z instead of Xhat^T Z", "M = Xhat.T @ Z\n", "M = Z[: Xhat.shape[1]]\n"),
+    ("stored dual scaled up by sqrt(n)", "return y / np.sqrt(y.shape[0])", "return y * np.sqrt(y.shape[0])"),
+    ("stored dual read back divided by sqrt(n)", "* np.sqrt(ytilde.shape[0])", "/ np.sqrt(ytilde.shape[0])"),
+    ("stored dual scaled by n", "return y / np.sqrt(y.shape[0])", "return y / y.shape[0]"),
 ]
 
 
@@ -55,6 +58,20 @@ LABEL_MUTATIONS = [
     ("distance without the square", "np.sum((E - C[k][None, :]) ** 2, axis=1)", "np.sum(np.abs(E - C[k][None, :]) - 1.0, axis=1)"),
     ("right singular vectors", "Uq, _, _ = np.linalg.svd(np.asarray(U, dtype=np.float64), full_matrices=False)\n    return Uq[:, :K]",
      "_, _, Vt = np.linalg.svd(np.asarray(U, dtype=np.float64), full_matrices=False)\n    return Vt.T[:, :K]"),
+]
+
+
+KMEANS_SRC = open(os.path.join(ROOT, "oracle", "kmeans.py")).read()
+
+# (name, original text, mutated text) planted in oracle/kmeans.py
+KMEANS_MUTATIONS = [
+    ("ARI without the chance adjustment", "return float((s_ij - exp) / (mx - exp))", "return float(s_ij / mx)"),
+    ("ARI always one", "if mx == exp:", "if True:"),
+    ("ARI with the row pairs twice", "mx = 0.5 * (s_a + s_b)", "mx = s_a"),
+    ("recovery threshold in log10", "ln = np.log(n)", "ln = np.log10(n)"),
+    ("recovery threshold without the 1 + under the root", "np.sqrt(1.0 + K * d / (n * ln))",
+     "np.sqrt(K * d / (n * ln))"),
+    ("recovery threshold with K d / n", "K * d / (n * ln)", "K * d / n"),
 ]
 
 
@@ -90,6 +107,20 @@ def test_mutation_is_caught(monkeypatch, name, orig, new):
         try:
             pin()
         except Exception as e:  # any failure (assertion, error) counts as caught
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin catches the planted mistake: {name}"
+
+
+@pytest.mark.parametrize("name,orig,new", KMEANS_MUTATIONS, ids=[m[0] for m in KMEANS_MUTATIONS])
+def test_kmeans_mutation_is_caught(monkeypatch, name, orig, new):
+    mutant = _load_mutant(monkeypatch, orig, new, KMEANS_SRC, "oracle_kmeans_mutant")
+    monkeypatch.setattr(oracle_pins, "kmeans", mutant)
+    caught = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin()
+        except Exception:
             caught.append(pin.__name__)
             break
     assert caught, f"no pin catches the planted mistake: {name}"

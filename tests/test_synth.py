@@ -43,3 +43,15 @@ def test_embedding_rows_unit_norm():
     assert np.allclose(np.linalg.norm(X, axis=1), 1.0, atol=1e-5)
     counts = np.bincount(lab, minlength=256)
     assert counts[0] > counts[-1]
+
+
+def test_rows_is_a_true_prefix_of_the_full_draw():
+    """make_workload(rows=m) returns bitwise the first m rows of the full draw (the CPU
+    baseline's sample), across a generator chunk boundary; n=m is a different draw."""
+    full = make_workload("gmm1m")
+    m = 300_000  # beyond one 2^18-row chunk
+    pre = make_workload("gmm1m", rows=m)
+    for a, b in zip(full[:3], pre[:3]):
+        assert np.array_equal(a[:m], b)
+    other = make_workload("gmm1m", n=m)
+    assert not np.array_equal(other[0], pre[0])
