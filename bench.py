@@ -165,6 +165,7 @@ def measure(nlr, torch, np, X_host, Z_host, wl, steps, warm, split, two_pass):
         ctx.run(warm)
     torch.cuda.synchronize()
     ctx.set_profiling(2)  # events around the row and pass kernels only (the roofline's candidates)
+    rows0 = ctx.inspect("rows_run")
     stream = ctx.stream
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -176,6 +177,7 @@ def measure(nlr, torch, np, X_host, Z_host, wl, steps, warm, split, two_pass):
     t_ms = ev0.elapsed_time(ev1)
     kt = ctx.kernel_times()
     ctx.set_profiling(False)
+    rows_ran = ctx.inspect("rows_run") - rows0
     assert done == steps, (done, steps)
     hist = ctx.history(steps)
     ctx.close()
@@ -188,9 +190,16 @@ def measure(nlr, torch, np, X_host, Z_host, wl, steps, warm, split, two_pass):
     eff_gbs = algorithmic_bytes("step", n, d, r, dual_frac) * steps / (t_ms / 1e3) / 1e9
     kinfo = {k: {"total_ms": v[0], "launches": v[1], "avg_ms": (v[0] / v[1]) if v[1] else None}
              for k, v in kt.items() if v[1]}
-    # the bytes the form actually moved, over the timed region: a physical HBM rate
-    phys_gbs = iteration_bytes(kinfo, n, d, r, dual_frac) / (t_ms / 1e3) / 1e9
+    # the bytes the form actually moved, over the timed region: a physical HBM rate.  The
+    # one-pass form launches its row pass every iteration but it runs (and moves U) only
+    # where the previous iteration's stop may fire: count those, from the library's counter
+    kbytes = {k: dict(v) for k, v in kinfo.items()}
+    if "pass_u" in kbytes and split and iteration_form(n, d, r, K, split, two_pass) == "one-pass":
+        kbytes["pass_u"]["launches"] = rows_ran
+    phys_gbs = iteration_bytes(kbytes, n, d, r, dual_frac) / (t_ms / 1e3) / 1e9
     dom = max(("pass_a", "pass_b", "pass_u", "pass_bf"), key=lambda k: kinfo.get(k, {"total_ms": 0})["total_ms"])
+    if rows_ran:
+        kinfo["pass_u"]["row_passes_run"] = rows_ran
     dom_ms = kinfo[dom]["avg_ms"]
     dom_bytes = algorithmic_bytes(dom, n, d, r, dual_frac)
     achieved = dom_bytes / (dom_ms / 1e3) / 1e9

@@ -53,7 +53,9 @@ typedef enum {
   NLR_EDEGENERATE = 4,  /* centred data is zero, so a = ||X_c||_2 = 0 (Section 3 needs a > 0) */
   NLR_EHIP = 5,         /* a HIP runtime call failed */
   NLR_ESTATE = 6,       /* context failed earlier, or was used out of order */
-  NLR_EUNSUPPORTED = 7  /* shape outside the compiled kernel family (see nlr_init) */
+  NLR_EUNSUPPORTED = 7, /* shape outside the compiled kernel family (see nlr_init) */
+  NLR_ERANGE = 8        /* split-fp16 products: W left the range of its fp16 operand (see
+                           NLR_INIT_SPLIT_F16); sticky like NLR_EBREAKDOWN, U then holds W */
 } nlr_status;
 
 /* Algorithm parameters (Algorithm 1 "Require" line).  The paper fixes no
@@ -76,7 +78,8 @@ typedef struct {
  *   dual_step             : Delta < eps_d^2 K, the dual step taken at the end of iteration t
  *   rho                   : ||q_{t+1}||_2 / sqrt(n), q = U p - 1 of U_{t+1}
  *   stop                  : the stopping rule of Section 4.3 fired at iteration t
- *   breakdown             : normalisation breakdown at iteration t (U then holds W) */
+ *   breakdown             : 1 normalisation breakdown at iteration t (U then holds W);
+ *                           2 W out of the split-fp16 range at iteration t (NLR_ERANGE) */
 typedef struct {
   int64_t t;
   double objective;
@@ -114,7 +117,18 @@ enum {
    * held 4 consecutive features hold their 4 fp16 hi halves then their 4 fp16 lo
    * halves of x * s (s a power of two); in the panel form each 32 bytes that held
    * 8 features hold their 8 hi halves then their 8 lo halves.  U_0 must lie in
-   * Omega (|u| <= sqrt(K)); nlr_init projects it unless NLR_INIT_U_IN_OMEGA. */
+   * Omega (|u| <= sqrt(K)); nlr_init projects it unless NLR_INIT_U_IN_OMEGA.
+   * Range precondition of the single-Xhat-pass and one-pass forms: the fresh
+   * update W (before its normalisation) is split at the fixed scale 2^10, so
+   * every entry must stay at or below 65504 / 2^10 (about 64).  A factor in
+   * Omega has |u| <= sqrt(K) <= 8, and every gradient entry is at most
+   * sqrt(K) (2 + 2 ||y|| + 2 beta (K + 1)) in size, so a step size within the
+   * Prop. 1 bound at the current dual (alpha <= 1/L(y), eq. L) keeps
+   * |w| <= 2 sqrt(K) <= 16; a step several times larger may not (the dual grows
+   * with dual steps while alpha stays fixed).  An iteration whose W
+   * leaves the range stops with NLR_ERANGE before any operand that left fp16's
+   * range reaches Theta or s; fp32 products (without this flag) have no such
+   * limit. */
   NLR_INIT_SPLIT_F16 = 8,
   /* Use the two-pass iteration (pass A: Theta = Xhat^T U with the row work; pass
    * B: Xhat Theta with the fused epilogue) even where the single-Xhat-pass form
@@ -126,11 +140,11 @@ enum {
    * features, 33..64 columns (d % 4 == 0, r % 4 == 0) the default is the
    * one-pass form: the same kernel also does the row work (q, the gated dual
    * step, ybar), s = U^T ybar is formed from W^T W, W^T ytilde and the column sums
-   * of the previous pass's W, and the stopping rule of an iteration is decided
-   * after the next pass, which reads the factor from one buffer and writes W to a
-   * second n x r buffer in the workspace (discarded when the rule fires).  All
-   * forms compute the same iteration; they differ by floating-point rounding
-   * only. */
+   * of the previous pass's W, and W is written over U in place.  At iterations
+   * where the previous iteration's stopping rule can fire (its movement is below
+   * min(eps_d, eps_c) and t >= T_min; the residual rho is then still needed) the
+   * row work runs in a pass of its own first and settles the rule.  All forms
+   * compute the same iteration; they differ by floating-point rounding only. */
   NLR_INIT_TWO_PASS = 16,
   /* Data-informed start (Appendix D, "Initialization"): U holds Z on input (e.g.
    * i.i.d. N(0,1) entries) and is replaced by U_0 = Pi_Omega(Q), where Q is the
@@ -238,7 +252,11 @@ nlr_status nlr_normaliser(nlr_ctx* ctx, double* a, double* xbar_host);
  * the current U; 2 copies s = U^T ybar (r floats) of the latest iteration's
  * starting factor -- in the one-pass form (split products, 97..128 features,
  * 33..64 columns) of the current U instead, formed after each pass for the next
- * one with the step arguments of that call. */
+ * one with the step arguments of that call; 3 copies an int64: the number of
+ * one-pass iterations since nlr_init whose row work ran in a pass of its own
+ * before the primal step (the first iteration after nlr_init, and those at which
+ * the previous iteration's stopping rule could fire).  Other values, or `bytes`
+ * too small, return NLR_EINVAL. */
 nlr_status nlr_inspect(nlr_ctx* ctx, int32_t what, void* host_dst, size_t bytes);
 
 /* Per-kernel timing with HIP events recorded on the context's stream around

@@ -13,6 +13,17 @@ __device__ __forceinline__ bool halted(const DevCtl* ctl) {
   return (ctl->stop | ctl->breakdown) != 0;
 }
 
+// Whether the stopping rule of the previous iteration (Section 4.3) can still fire
+// at this one: its movement is below min(eps_d, eps_c) and t >= T_min; only the
+// residual rho of the current factor is then missing, which the row work computes.
+// The one-pass iteration writes W over the factor it reads when this is false; when
+// true, the row work runs in its own pass first and settles the rule.
+__device__ __forceinline__ bool stop_possible(const DevCtl* ctl, const StepArgs& S) {
+  const int64_t t = ctl->t_done;
+  return S.end_work != 0 && t > 0 && ctl->Delta < S.eps_d * S.eps_d * S.K && ctl->delta < S.eps_c &&
+         t >= S.T_min;
+}
+
 // Loads W consecutive floats; when !ok the (valid) address is still read and the
 // values are replaced by zeros, so no branch is needed.
 template <int W>

@@ -33,9 +33,15 @@
 
 namespace nlr {
 
-// Power-of-two scale of W in the split phase 2: |w| < 32 (= 4 sqrt(K) at the
-// largest split-supported K = 64; a normalised factor has |u| <= sqrt(K)).
+// Power-of-two scale of W in the split second product (and the one-pass kernel's
+// W^T W): w 2^10 stays a finite fp16 for w <= 65504 / 2^10 ~ 64.  A normalised factor
+// has |u| <= sqrt(K) <= 8 at the largest split-supported K = 64, and a step within
+// the Prop. 1 bound moves an entry by less than that; a larger step size or dual can
+// exceed it.  Each workgroup reports whether its W did (column 3 of its statistics
+// row: 1.0 if so), and the control kernel then stops the iteration with a range
+// error before the inf/NaN operands reach Theta or s.
 constexpr float kWScale = 1024.0f;
+constexpr float kWMax = 65504.0f / kWScale;
 
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef __fp16 h16x4 __attribute__((__vector_size__(4 * sizeof(__fp16))));
@@ -180,6 +186,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_
   __syncthreads();
 
   double sa = 0.0, sb = 0.0, sh = 0.0;
+  float wmx = 0.f;  // SPLIT: largest w of this lane (the fp16 range of the W operand)
   double colacc[NB];
 #pragma unroll
   for (int m = 0; m < NB; ++m) colacc[m] = 0.0;
@@ -420,6 +427,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_
           float w = fmaxf(t, 0.f);
           if (!vpt || c + e >= r) w = 0.f;
           wv[4 * qd + e] = w;
+          if constexpr (SPLIT) wmx = fmaxf(wmx, w);
           const double wd = (double)w, ud = (double)uu;
           sa = fma(wd, wd, sa);
           sb = fma(ud, ud, sb);
@@ -537,11 +545,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_
   const double ta = block_sum_d(sa, dred);
   const double tb2 = block_sum_d(sb, dred);
   const double th = block_sum_d(sh, dred);
+  // 1.0 when some w of this workgroup left the range of the split W operand (w != w: NaN)
+  const double over = block_sum_d((wmx > kWMax || wmx != wmx) ? 1.0 : 0.0, dred);
   if (tid == 0) {
     out[0] = ta;
     out[1] = tb2;
     out[2] = th;
-    out[3] = 0.0;
+    out[3] = over > 0.0 ? 1.0 : 0.0;
   }
 
   // ---- partial of Xhat^T W_{t+1}: ((wave0 + wave2) + (wave1 + wave3)) in [f][c] order ----
@@ -597,16 +607,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_
 // Row work (the end of the previous iteration): q = u.p - 1 in FP64, the pending
 // gated dual step (ytilde stored), ybar, ||q||^2 and ytilde^T q -- as the row
 // pass does, so that the row pass is not needed.  Its s = U^T ybar is instead
-// formed (by k_reduce_theta after the pass, or by k_s_gram at the start of a host
-// call) from terms this kernel accumulates while W is on chip: the
+// formed (by k_reduce_theta after the pass, or by k_onepass_begin at the start of
+// a host call) from terms this kernel accumulates while W is on chip: the
 // column sums of W and of W ytilde (FP64 across tiles) and the Gram W^T W (a
 // third product on the matrix cores, from the W tile; wave w adds the block
 // (rows 32 (w % 2) .., columns 32 (w / 4) ..) of the tile's row half w / 2 % 2).
-// The factor is read from one buffer and W written to the other (B.ctl->ubuf):
-// the stopping rule of the previous iteration is decided after this kernel, which
-// is then discarded if the rule fires.  W leaves through LDS: each wave stages its
-// slab's rows, packed as in U, in its own rows of the W tile and stores them as
-// whole contiguous 1 KiB pieces before the same rows take the split of W.
+// W is written over the factor in place.  The stopping rule of the previous
+// iteration needs the residual rho of the current factor, which the row work
+// computes; when that rule can fire at all (movement below min(eps_d, eps_c),
+// t >= T_min: known before the pass), the row pass runs first and decides it, and
+// this kernel then skips the dual step (rows_first).  W leaves through LDS: each
+// wave stages its slab's rows, packed as in U, in its own rows of the W tile and
+// stores them as whole contiguous 1 KiB pieces before the same rows take the
+// split of W.
 // ===========================================================================
 namespace bf8 {
 
@@ -787,12 +800,14 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
   const float gam = S.gamma_f;
   const float neg_alpha = -S.alpha_f;
   const float sx = B.ctl->x_scale;
-  // the factor of this iteration is read from one buffer, W_{t+1} written to the other
-  const int ubsel = B.ctl->ubuf;
-  const float* Usrc = ubsel ? B.U2 : B.U;
-  float* Udst = ubsel ? B.U : B.U2;
-  // the pending gated dual step (the end of the previous iteration)
-  const bool gate = (S.end_work != 0) && (B.ctl->gate != 0);
+  // W_{t+1} is written over the factor rows this workgroup has read (each tile's rows
+  // are read and written by the same workgroup, the reads first): the pass runs only
+  // once the previous iteration's stopping rule can no longer discard it
+  const float* Usrc = B.U;
+  float* Udst = B.U;
+  // the pending gated dual step (the end of the previous iteration), unless the row
+  // pass has applied it
+  const bool gate = (S.end_work != 0) && (B.ctl->gate != 0) && (B.ctl->rows_first == 0);
 
   // ---- Theta_t as the A operand of the first product: lane l of block (ks, cb)
   // holds column 16 cb + l % 16 and, for q = l / 16, features 32 ks + 4 q + e and
@@ -851,6 +866,7 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     }
 
   double sa = 0.0, sb = 0.0, sh = 0.0, colacc = 0.0, colyacc = 0.0, qq = 0.0, yq = 0.0;
+  float wmx = 0.f;  // largest w of this lane (the fp16 range of the split W operand)
   f32x16 acc2, accg;
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc2[v] = accg[v] = 0.f;
@@ -1030,6 +1046,7 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
         t = t + se[e];
         const float w = fmaxf(t, 0.f) * okf[cb];
         wv[4 * cb + e] = w;
+        wmx = fmaxf(wmx, w);
         const double wd = (double)w, ud = (double)uu;
         sa = fma(wd, wd, sa);
         sb = fma(ud, ud, sb);
@@ -1146,12 +1163,15 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     qq += shfl_xor_d(qq, m);
     yq += shfl_xor_d(yq, m);
   }
+  float wbad = (wmx > kWMax || wmx != wmx) ? 1.0f : 0.0f;  // w != w: NaN
+  for (int m = 32; m >= 1; m >>= 1) wbad = fmaxf(wbad, shfl_xor_f(wbad, m));
   if (lane == 0) {
     dred[8 * wave + 0] = sa;
     dred[8 * wave + 1] = sb;
     dred[8 * wave + 2] = sh;
     dred[8 * wave + 3] = qq;
     dred[8 * wave + 4] = yq;
+    fred[wave] = wbad;
   }
   // ---- partials of Xhat^T W_{t+1} (row splits in order, [f][c] order) and of
   // W^T W (the two halves of each block in order, [k][l] order) ----
@@ -1184,7 +1204,12 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     if (tid < 3) out[tid] = v;
     else aout[tid - 3] = v;  // ||q||^2, ytilde^T q
   }
-  if (tid == 5) out[3] = 0.0;
+  if (tid == 5) {
+    float bad = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) bad = fmaxf(bad, fred[w]);
+    out[3] = bad > 0.f ? 1.0 : 0.0;  // W left the range of its split operand
+  }
   if (tid == 6) aout[2] = 0.0;
   if (tid == 7) aout[3] = 0.0;
   float* part = B.theta_part + (int64_t)blockIdx.x * g.theta_cols;

@@ -21,11 +21,11 @@ __global__ void k_ctl_init(Bufs B, float gamma_f) {
     c->gate = 0;
     c->degenerate = 0;
     c->t_done = 0;
-    c->pad64 = 0;
     c->c_f = 1.0f;
     c->x_scale = 1.0f;
     c->th_scale = 1.0f;
-    c->ubuf = 0;
+    c->rows_first = 0;
+    c->rows_run = 0;
     c->a = c->b = c->h = 0.0;
     c->Delta = c->delta = 0.0;
     c->rho = c->objective = c->theta_fro2 = 0.0;

@@ -272,19 +272,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
     Geometry g, Bufs B, StepArgs S) {
   constexpr bool FINISH = MODE == kPassFinish;
   constexpr bool THETA = MODE == kPassIter;
-  // the iterate is in the workspace factor buffer after an odd number of one-pass
-  // iterations; the finish pass moves it to U
-  const float* Usrc = B.ctl->ubuf ? B.U2 : B.U;
-  if (FINISH && B.ctl->breakdown != 0) {
-    // the unnormalised update replaces the factor
-    if (B.ctl->ubuf) {
-      const int64_t tot = g.n * (int64_t)g.r;
-      for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < tot; e += (int64_t)gridDim.x * kThreads)
-        B.U[e] = B.U2[e];
-    }
-    return;
-  }
+  // on breakdown the unnormalised update W already holds the factor's place
+  const float* Usrc = B.U;
+  if (FINISH && B.ctl->breakdown != 0) return;
   if (!FINISH && halted(B.ctl)) return;
+  // the one-pass iteration launches the row pass every iteration; it runs only when
+  // the previous iteration's stopping rule may fire (the pass then does no row work)
+  if (MODE == kPassRows && g.fused8 && !B.ctl->rows_first) return;
   const bool stopped = FINISH && (B.ctl->stop != 0);
   constexpr int NBLK = FV * NGF * CV;  // 16x16 blocks of Theta
   // k-steps in flight: fewer when Theta takes 128 registers, more when only U and y stream
@@ -493,15 +487,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
     Geometry g, Bufs B, StepArgs S) {
   constexpr bool FINISH = MODE == kPassFinish;
   static_assert(MODE == kPassFinish || MODE == kPassRows, "row work only");
-  const float* Usrc = B.ctl->ubuf ? B.U2 : B.U;
-  if (FINISH && B.ctl->breakdown != 0) {
-    if (B.ctl->ubuf) {
-      const int64_t tot = g.n * (int64_t)g.r;
-      for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < tot; e += (int64_t)gridDim.x * kThreads)
-        B.U[e] = B.U2[e];
-    }
-    return;
-  }
+  const float* Usrc = B.U;
+  if (FINISH && B.ctl->breakdown != 0) return;
   if (!FINISH && halted(B.ctl)) return;
   const bool stopped = FINISH && (B.ctl->stop != 0);
   constexpr int PF = 8;  // steps in flight
@@ -627,11 +614,14 @@ __device__ __forceinline__ void seg_sum_block(const T* __restrict__ P, int64_t R
     out[(int64_t)by * C + col] = ((red[tid] + red[64 + tid]) + red[128 + tid]) + red[192 + tid];
 }
 
+// mode 0: run unless broken down (after the finish pass); 1: unless halted; 2: unless
+// halted or the one-pass iteration's row pass did not run (rows_first unset)
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_seg_sum(const T* __restrict__ P, int64_t R, int C,
                                                       double* __restrict__ out, int S, const DevCtl* ctl,
-                                                      int skip_if_halted) {
-  if (skip_if_halted ? halted(ctl) : (ctl->breakdown != 0)) return;
+                                                      int mode) {
+  if (mode == 0 ? (ctl->breakdown != 0) : halted(ctl)) return;
+  if (mode == 2 && !ctl->rows_first) return;
   __shared__ double red[kThreads];
   seg_sum_block<T>(P, R, C, out, S, blockIdx.x, blockIdx.y, red);
 }
@@ -708,16 +698,17 @@ __global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs
   if (ctl->breakdown) return;
   if (ctl->stop) {
     // stopped earlier in this call: the finish pass only materialised U
-    if (finish && threadIdx.x == 0) {
-      ctl->c_f = 1.0f;
-      ctl->ubuf = 0;
-    }
+    if (finish && threadIdx.x == 0) ctl->c_f = 1.0f;
     return;
   }
+  // one-pass iteration: after its row pass only (which runs when the stop may fire)
+  if (g.fused8 && !finish && !ctl->rows_first) return;
   __shared__ double red[8];
   const int tid = threadIdx.x;
   const int C = 4 + g.r32;
-  if (!finish) {
+  // (one-pass iteration with valid Gram terms, rows_first == 1: s is the Gram-derived
+  // one already in place, as when the pass does the row work itself)
+  if (!finish && !(g.fused8 && ctl->rows_first == 1)) {
     for (int c = tid; c < g.r32; c += kThreads) {
       double t = 0.0;
       for (int s = 0; s < g.SA; ++s) t += B.seg_a[(int64_t)s * C + 4 + c];
@@ -760,10 +751,8 @@ __global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs
       cur->stop = 0;
       cur->breakdown = 0;
     }
-    if (finish) {
-      ctl->c_f = 1.0f;
-      ctl->ubuf = 0;
-    }
+    if (finish) ctl->c_f = 1.0f;
+    if (g.fused8 && !finish) ctl->rows_run += 1;
   }
 }
 
@@ -1189,11 +1178,12 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
   const int tid = threadIdx.x;
   const int C = 4 + g.r32;
   if (tid == 0) {
-    double a = 0.0, b = 0.0, h = 0.0;
+    double a = 0.0, b = 0.0, h = 0.0, over = 0.0;
     for (int s = 0; s < g.SB; ++s) {
       a += B.seg_b[(int64_t)s * C + 0];
       b += B.seg_b[(int64_t)s * C + 1];
       h += B.seg_b[(int64_t)s * C + 2];
+      over += B.seg_b[(int64_t)s * C + 3];
     }
     const double nu = sqrt(a);
     const int64_t t = ctl->t_done;
@@ -1201,7 +1191,12 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
     rec->a = a;
     rec->b = b;
     rec->h = h;
-    if (!(nu > 1e-20) || !isfinite(a)) {
+    if (over > 0.0) {
+      // a split-fp16 operand of W left fp16's range (the fused pass's flag)
+      ctl->breakdown = kRangeError;
+      rec->breakdown = kRangeError;
+      cbuf[0] = 0.0;
+    } else if (!(nu > 1e-20) || !isfinite(a)) {
       ctl->breakdown = 1;
       rec->breakdown = 1;
       cbuf[0] = 0.0;
@@ -1239,98 +1234,92 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
 
 // ---------------------------------------------------------------------------
 // One-pass iteration (the eight-wave fused pass B does the row work too), control
-// after the pass (one workgroup).  The pass did the row work of this iteration --
-// the end of the previous one: its gated dual step, q and the objective terms --
-// before the primal step, so the stopping rule of the previous iteration is decided
-// here, after the fact: when it fires, this iteration's W (written to the other
-// factor buffer) and partials are discarded and the iterate stays the previous
-// one.  Otherwise as k_ctl_b, then the column sums P of W and W^T ytilde for the
-// next iteration's s (formed by the next one-pass kernel).  S.row_pass: the row pass did this iteration's
-// row work (k_ctl_a has already decided the stopping rule and the record).
+// after the pass (one workgroup).  Unless the row pass ran first (rows_first: the
+// previous iteration's stopping rule could fire, and k_ctl_a has decided it and
+// written the record), the pass did the row work of this iteration -- the end of
+// the previous one: its gated dual step, q and the objective terms -- before the
+// primal step; the stopping rule could not fire then, and rho and the objective
+// are recorded here.  Then as k_ctl_b, the column sums P of W and W^T ytilde for
+// the next iteration's s, and whether the next iteration's row pass runs first.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_ctl_one(Geometry g, Bufs B, StepArgs S) {
   DevCtl* ctl = B.ctl;
   if (halted(ctl)) return;
   __shared__ double red[8];
   __shared__ double cbuf[1];
-  __shared__ int sflag[1];
   const int tid = threadIdx.x;
   double th2 = 0.0;
   for (int k = tid; k < g.RT; k += kThreads) th2 += B.th2_part[k];
   th2 = block_sum_d(th2, red);
   if (tid == 0) {
-    int stopped = 0;
     const int64_t t = ctl->t_done;
-    if (!S.row_pass) {
+    if (!ctl->rows_first) {
       const double qq = B.seg_a[0], yq = B.seg_a[1];
       const double rho = sqrt(qq * S.inv_n);
       ctl->rho = rho;
       if (S.end_work && t > 0) {
         nlr_iter_stats* prev = &B.hist[(t - 1) % kHistCap];
-        const int stop = (ctl->Delta < S.eps_d * S.eps_d * S.K) && (ctl->delta < S.eps_c) &&
-                         (rho < S.eps_c) && (t >= S.T_min);
         prev->rho = rho;
-        prev->stop = stop;
-        if (stop) {
-          ctl->stop = 1;
-          stopped = 1;
-        }
+        prev->stop = 0;
       }
-      if (!stopped) {
-        const double obj = -th2 + yq + 0.5 * S.beta * S.inv_n * qq;
-        ctl->objective = obj;
-        ctl->theta_fro2 = th2;
-        nlr_iter_stats* cur = &B.hist[t % kHistCap];
-        cur->t = t;
-        cur->objective = obj;
-        cur->theta_fro2 = th2;
-        cur->rho = 0.0;
-        cur->stop = 0;
-      }
+      const double obj = -th2 + yq + 0.5 * S.beta * S.inv_n * qq;
+      ctl->objective = obj;
+      ctl->theta_fro2 = th2;
+      nlr_iter_stats* cur = &B.hist[t % kHistCap];
+      cur->t = t;
+      cur->objective = obj;
+      cur->theta_fro2 = th2;
+      cur->rho = 0.0;
+      cur->stop = 0;
     }
-    sflag[0] = stopped;
     cbuf[0] = 0.0;
-    if (!stopped) {
-      const double a = B.seg_b[0], b = B.seg_b[1], h = B.seg_b[2];
-      const double nu = sqrt(a);
-      nlr_iter_stats* rec = &B.hist[t % kHistCap];
-      rec->a = a;
-      rec->b = b;
-      rec->h = h;
-      rec->dual_step = 0;
-      rec->breakdown = 0;
-      // W_{t+1} is in the other buffer from here on (on breakdown it replaces the factor)
-      ctl->ubuf ^= 1;
-      if (!(nu > 1e-20) || !isfinite(a)) {
-        ctl->breakdown = 1;
-        rec->breakdown = 1;
-        rec->c = 0.f;
-        rec->delta = 0.0;
-      } else {
-        const float cf = (float)(sqrt(S.K) / nu);
-        const double c = (double)cf;
-        double D = c * c * a + b - 2.0 * c * h;
-        if (D < 0.0) D = 0.0;
-        const double delta = sqrt(D) / sqrt(S.K);
-        const int gate = D < S.eps_d * S.eps_d * S.K;
-        ctl->a = a;
-        ctl->b = b;
-        ctl->h = h;
-        ctl->Delta = D;
-        ctl->delta = delta;
-        ctl->gate = gate;
-        ctl->c_f = cf;
-        ctl->c_gram = c;
-        ctl->t_done = t + 1;
-        rec->c = cf;
-        rec->delta = delta;
-        rec->dual_step = gate;
-        cbuf[0] = c;
-      }
+    const double a = B.seg_b[0], b = B.seg_b[1], h = B.seg_b[2];
+    const double nu = sqrt(a);
+    nlr_iter_stats* rec = &B.hist[t % kHistCap];
+    rec->a = a;
+    rec->b = b;
+    rec->h = h;
+    rec->dual_step = 0;
+    rec->breakdown = 0;
+    if (B.seg_b[3] > 0.0) {
+      // the split W operand left fp16's range: stop before Theta and s use it
+      ctl->breakdown = kRangeError;
+      rec->breakdown = kRangeError;
+      rec->c = 0.f;
+      rec->delta = 0.0;
+    } else if (!(nu > 1e-20) || !isfinite(a)) {
+      // W_{t+1} has overwritten the factor (Algorithm 2 order)
+      ctl->breakdown = 1;
+      rec->breakdown = 1;
+      rec->c = 0.f;
+      rec->delta = 0.0;
+    } else {
+      const float cf = (float)(sqrt(S.K) / nu);
+      const double c = (double)cf;
+      double D = c * c * a + b - 2.0 * c * h;
+      if (D < 0.0) D = 0.0;
+      const double delta = sqrt(D) / sqrt(S.K);
+      const int gate = D < S.eps_d * S.eps_d * S.K;
+      ctl->a = a;
+      ctl->b = b;
+      ctl->h = h;
+      ctl->Delta = D;
+      ctl->delta = delta;
+      ctl->gate = gate;
+      ctl->c_f = cf;
+      ctl->c_gram = c;
+      ctl->t_done = t + 1;
+      rec->c = cf;
+      rec->delta = delta;
+      rec->dual_step = gate;
+      cbuf[0] = c;
+      // the next iteration of this call has this one's end-of-iteration work pending
+      StepArgs nx = S;
+      nx.end_work = 1;
+      ctl->rows_first = stop_possible(ctl, nx) ? 1 : 0;
     }
   }
   __syncthreads();
-  if (sflag[0]) return;
   const double c = cbuf[0];
   if (c > 0.0) {
     for (int col = tid; col < g.r32; col += kThreads) {
@@ -1415,11 +1404,18 @@ __device__ __forceinline__ float s_from_gram(const Bufs& B, int r32, int k, doub
   return (float)(c * wy + gmul * c * (c * c * gp - P));
 }
 
-__global__ __launch_bounds__(64) void k_s_gram(Geometry g, Bufs B, StepArgs S) {
+// At the start of a host call (one workgroup): s from the stored Gram terms with the
+// beta of this call when they are valid, and whether the first iteration's row pass
+// runs before its pass: 2 when there are no Gram terms (after nlr_init; s then comes
+// from the row pass), 1 when the stopping rule of the previous iteration may fire
+// under this call's arguments (eps, T_min; the row pass settles the rule, s stays
+// the Gram-derived one), else 0.
+__global__ __launch_bounds__(64) void k_onepass_begin(Geometry g, Bufs B, StepArgs S, int gram_valid) {
   if (halted(B.ctl)) return;
   const int r32 = g.r32;
   const int k = threadIdx.x;
-  if (k >= r32) return;
+  if (k == 0) B.ctl->rows_first = !gram_valid ? 2 : (stop_possible(B.ctl, S) ? 1 : 0);
+  if (!gram_valid || k >= r32) return;
   const float sk = s_from_gram(B, r32, k, B.gram_vec[2 * r32 + k], S.gamma_f);
   B.s[k] = (k < g.r) ? sk : 0.f;
 }
@@ -1561,11 +1557,13 @@ hipError_t launch_reduce_theta(const Geometry& g, const Bufs& b, bool fused_part
                         : launch_reduce_theta_rows(g, b, g.GA, g.SA, false, st);
 }
 
-// a_part rows -> g.SA segment sums (the segment count k_ctl_a reads)
+// a_part rows -> g.SA segment sums (the segment count k_ctl_a reads); in the one-pass
+// iteration they follow its row pass, and run when that did
 hipError_t launch_seg_a_rows(const Geometry& g, const Bufs& b, int64_t rows, bool finish, hipStream_t st) {
   const int C = 4 + g.r32;
+  const int mode = finish ? 0 : (g.fused8 ? 2 : 1);
   hipLaunchKernelGGL((k_seg_sum<double>), dim3((C + 63) / 64, g.SA), dim3(kThreads), 0, st,
-                     (const double*)b.a_part, rows, C, b.seg_a, g.SA, (const DevCtl*)b.ctl, finish ? 0 : 1);
+                     (const double*)b.a_part, rows, C, b.seg_a, g.SA, (const DevCtl*)b.ctl, mode);
   return hipGetLastError();
 }
 
@@ -1673,8 +1671,9 @@ hipError_t launch_reduce_theta_onepass(const Geometry& g, const Bufs& b, const S
   return hipGetLastError();
 }
 
-hipError_t launch_s_gram(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_s_gram, dim3(1), dim3(64), 0, st, g, b, a);
+hipError_t launch_onepass_begin(const Geometry& g, const Bufs& b, const StepArgs& a, bool gram_valid,
+                                hipStream_t st) {
+  hipLaunchKernelGGL(k_onepass_begin, dim3(1), dim3(64), 0, st, g, b, a, gram_valid ? 1 : 0);
   return hipGetLastError();
 }
 

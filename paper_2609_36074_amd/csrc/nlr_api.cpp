@@ -237,10 +237,7 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.i_xbar = reinterpret_cast<double*>(take(d * 8));
   b.dump = reinterpret_cast<float*>(take(256));
   b.thmax_part = reinterpret_cast<float*>(take((size_t)g.RT * 4));
-  if (g.fused8) {
-    b.U2 = reinterpret_cast<float*>(take((size_t)g.n * (size_t)g.r * 4));
-    b.gram_vec = reinterpret_cast<double*>(take(3 * r32 * 8));
-  }
+  if (g.fused8) b.gram_vec = reinterpret_cast<double*>(take(3 * r32 * 8));
   if (g.panel) {
     b.ybar = reinterpret_cast<float*>(take((size_t)g.n * 4));
     b.theta_split = take((size_t)((g.d + 15) / 16) * 64 * g.pnbw * 64);
@@ -251,7 +248,10 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.s_G = reinterpret_cast<double*>(take((size_t)g.r * g.r * 8));
   b.s_T = reinterpret_cast<double*>(take(d * (size_t)g.r * 8));
   // union: pass-A Theta partials | init temporaries
-  size_t prow = (size_t)(g.GA > g.GB ? g.GA : g.GB);  // pass A or fused pass B partials
+  // rows of Theta partials: pass A's (also the init's pass A of the fused forms), or
+  // the fused pass B's (the two-pass forms' pass B writes none)
+  size_t prow = (size_t)g.GA;
+  if (g.fused && (size_t)g.GB > prow) prow = (size_t)g.GB;
   if (g.panel && (size_t)g.PS > prow) prow = (size_t)g.PS;
   const size_t u_iter = align256(prow * (size_t)g.theta_cols * 4);
   size_t u_init = 0;
@@ -315,6 +315,7 @@ struct nlr_ctx {
   bool gram_valid;    // one-pass iteration: the Gram terms of the latest pass give the next s
   bool failed;        // sticky failure
   bool breakdown;
+  bool range_error;   // the breakdown is a split-fp16 range error (NLR_ERANGE)
   int64_t t_host;     // last known iteration counter
   bool t_host_valid;
   DevCtl* host_ctl;   // pinned mirror of the control block
@@ -428,28 +429,23 @@ static hipError_t prof_collect(nlr_ctx* c) {
 static nlr_status enqueue_iteration(nlr_ctx* c, bool first) {
   const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
   if (c->g.fused8) {
-    // one pass over the rows per iteration: the pass does the row work of the
-    // iteration (the end of the previous one) as well as the primal step, reading
-    // the factor from one buffer and writing W to the other; s comes from the Gram
-    // terms of the previous pass (formed after that pass with this call's step
-    // arguments, or anew at the start of a call), or, when there is no previous
-    // pass (after init or a stop), from the row pass.  Then one launch of segment
-    // sums (Theta and W^T W partials, the row statistics), the control, and Theta
-    // with (W^T W) P and the next s.
-    StepArgs ap = a;
-    if (!c->gram_valid) {
-      LAUNCH(KK_PASS_U, launch_pass_u(c->g, c->b, a, c->stream));
-      LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
-      LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
-      ap.end_work = 0;
-      ap.row_pass = 1;
-    } else if (first) {
-      LAUNCH(KK_CTL_A, launch_s_gram(c->g, c->b, a, c->stream));
-    }
-    LAUNCH(KK_PASS_BF, launch_pass_bf(c->g, c->b, ap, c->stream));
+    // one pass over the rows per iteration, writing W over the factor: the pass does
+    // the row work of the iteration (the end of the previous one) as well as the
+    // primal step; s comes from the Gram terms of the previous pass (formed after that
+    // pass with this call's step arguments, or anew at the start of a call).  When the
+    // previous iteration's stopping rule may fire (decided on the device before the
+    // pass), or there is no previous pass (after init or a stop), the row pass, its
+    // segment sums and k_ctl_a run first (they return at entry otherwise) and settle
+    // the rule and s.  Then one launch of segment sums (Theta and W^T W partials, the
+    // row statistics), the control, and Theta with (W^T W) P and the next s.
+    if (first) LAUNCH(KK_CTL_A, launch_onepass_begin(c->g, c->b, a, c->gram_valid, c->stream));
+    LAUNCH(KK_PASS_U, launch_pass_u(c->g, c->b, a, c->stream));
+    LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
+    LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
+    LAUNCH(KK_PASS_BF, launch_pass_bf(c->g, c->b, a, c->stream));
     LAUNCH(KK_CTL_B, launch_seg_onepass(c->g, c->b, c->stream));
-    LAUNCH(KK_CTL_B, launch_ctl_one(c->g, c->b, ap, c->stream));
-    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta_onepass(c->g, c->b, ap, c->stream));
+    LAUNCH(KK_CTL_B, launch_ctl_one(c->g, c->b, a, c->stream));
+    LAUNCH(KK_REDUCE_THETA, launch_reduce_theta_onepass(c->g, c->b, a, c->stream));
     c->gram_valid = true;
     c->pending = true;
     return NLR_OK;
@@ -580,6 +576,7 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   c->gram_valid = false;
   c->failed = false;
   c->breakdown = false;
+  c->range_error = false;
   c->t_host = 0;
   c->t_host_valid = true;
   c->prof = false;
@@ -662,11 +659,12 @@ nlr_status nlr_step(nlr_ctx* c, nlr_iter_stats* stats) {
     if (c->host_ctl->breakdown) {
       c->failed = true;
       c->breakdown = true;
+      c->range_error = c->host_ctl->breakdown == kRangeError;
     }
     const int64_t t = c->host_ctl->t_done - (c->host_ctl->breakdown ? 0 : 1);
     if (read_record(c, t < 0 ? 0 : t, stats) != NLR_OK) return NLR_EHIP;
     if (prof_collect(c) != hipSuccess) return hip_fail(c);
-    if (c->breakdown) return NLR_EBREAKDOWN;
+    if (c->breakdown) return c->range_error ? NLR_ERANGE : NLR_EBREAKDOWN;
   }
   return NLR_OK;
 }
@@ -692,12 +690,13 @@ nlr_status nlr_run(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* l
   if (prof_collect(c) != hipSuccess) return hip_fail(c);
   const int64_t t1 = c->host_ctl->t_done;
   if (iters_done) *iters_done = (int32_t)(t1 - t0);
-  // a stop may have discarded the latest pass of the one-pass iteration: the next
-  // iteration forms s from the rows again
-  if (c->host_ctl->stop || c->host_ctl->breakdown) c->gram_valid = false;
+  // (one-pass iteration: a stop fires after the row pass, before the pass; the Gram
+  // terms of the latest pass stay those of the current factor, with the dual step of
+  // its end counted by the stored gate, so they still give the next call's s)
   if (c->host_ctl->breakdown) {
     c->failed = true;
     c->breakdown = true;
+    c->range_error = c->host_ctl->breakdown == kRangeError;
   }
   if (last) {
     if (t1 > t0 || c->host_ctl->breakdown) {
@@ -708,7 +707,7 @@ nlr_status nlr_run(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* l
       last->t = -1;
     }
   }
-  return c->breakdown ? NLR_EBREAKDOWN : NLR_OK;
+  return c->breakdown ? (c->range_error ? NLR_ERANGE : NLR_EBREAKDOWN) : NLR_OK;
 }
 
 nlr_status nlr_labels(nlr_ctx* c, int32_t* labels) {
@@ -799,6 +798,13 @@ nlr_status nlr_inspect(nlr_ctx* c, int32_t what, void* host_dst, size_t bytes) {
       }
     return NLR_OK;
   }
+  if (what == 3) {
+    if (bytes < sizeof(int64_t)) return NLR_EINVAL;
+    if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+    const int64_t v = c->host_ctl->rows_run;
+    std::memcpy(host_dst, &v, sizeof v);
+    return NLR_OK;
+  }
   if (what == 1 || what == 2) {
     if (bytes < (size_t)g.r * 4) return NLR_EINVAL;
     if (hipMemcpyAsync(host_dst, what == 1 ? c->b.p : c->b.s, (size_t)g.r * 4, hipMemcpyDeviceToHost,
@@ -862,6 +868,7 @@ const char* nlr_status_string(nlr_status s) {
     case NLR_EHIP: return "HIP runtime error";
     case NLR_ESTATE: return "context failed earlier or used out of order";
     case NLR_EUNSUPPORTED: return "shape outside the compiled kernel family";
+    case NLR_ERANGE: return "split-fp16 products: W left the range of its fp16 operand (use fp32 products or a smaller step)";
   }
   return "unknown status";
 }

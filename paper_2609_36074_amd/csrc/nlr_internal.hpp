@@ -18,19 +18,26 @@ constexpr int kMaxR = 256;        // largest supported rank
 constexpr int kPowerIters = 16;   // refinement power iterations after the squaring phase
 constexpr int kSquarings = 20;    // C -> C^(2^20) before the refinement
 
+// DevCtl::breakdown values besides 0: the normalisation breakdown of Algorithm 1,
+// and a split-fp16 operand of W out of fp16's range (both stop the iteration, U then
+// holds W).
+constexpr int32_t kBreakdown = 1;
+constexpr int32_t kRangeError = 2;
+
 // Device control block.  Written only by single-workgroup control kernels and
 // read uniformly by every kernel at entry.
 struct alignas(16) DevCtl {
   int32_t stop;        // stopping rule fired during the current host call
-  int32_t breakdown;   // sticky: normalisation breakdown
+  int32_t breakdown;   // sticky: kBreakdown (normalisation breakdown) or kRangeError
   int32_t gate;        // dual gate of the latest primal step
   int32_t degenerate;  // init: a = ||X_c||_2 is zero or not finite
   int64_t t_done;      // completed primal steps
-  int64_t pad64;
+  int64_t rows_run;    // one-pass iterations whose row work ran in its own pass first
   float c_f;           // lazy scale of the factor buffer (1 when materialised)
   float x_scale;       // power of two keeping |Xhat| x_scale < 2^15 (split-fp16 products)
   float th_scale;      // power of two keeping |Theta| th_scale < 2^15 (panel pass B operand)
-  int32_t ubuf;        // factor buffer of the current iterate: 0 the caller's U, 1 the workspace copy
+  int32_t rows_first;  // one-pass iteration: the row pass runs before the pass -- 1 the stop may
+                       // fire (s from the Gram terms), 2 no Gram terms yet (s from the rows)
   double a, b, h;      // fused statistics of the latest primal step
   double Delta;        // squared movement estimate
   double delta;        // movement estimate
@@ -54,7 +61,7 @@ struct StepArgs {
   double inv_n;
   int64_t T_min;
   int32_t end_work;    // apply the pending end-of-iteration vector work (dual step, rho, stop test)
-  int32_t row_pass;    // one-pass iteration: the row pass already did this iteration's row work
+  int32_t pad32;
 };
 
 // Launch geometry; a pure function of (n, d, r) so that reduction orders,
@@ -127,7 +134,6 @@ struct Bufs {
   float* ybar;         // n: ybar of the current iteration (panel form: pass A -> pass B)
   void* theta_split;   // panel form: split Theta^T chunks, 64 bytes per (16 features, column)
   // one-pass iteration (eight-wave fused pass B)
-  float* U2;           // n x r: second factor buffer (pass reads one, writes the other)
   double* gram_vec;    // 3 r32: column sums P of W, W^T ytilde, (W^T W) P (fixed-order sums)
   // init temporaries (alias the pass-A partial region)
   double* i_colsum;    // GI x d
@@ -217,7 +223,10 @@ hipError_t launch_seg_onepass(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_seg_fused(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_reduce_theta_fused(const Geometry& g, const Bufs& b, hipStream_t st);
 hipError_t launch_reduce_theta_onepass(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
-hipError_t launch_s_gram(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st);
+// start of a host call of the one-pass iteration: s from the stored Gram terms (when
+// valid) and whether the first iteration's row pass runs before its pass
+hipError_t launch_onepass_begin(const Geometry& g, const Bufs& b, const StepArgs& a, bool gram_valid,
+                                hipStream_t st);
 hipError_t launch_reduce_theta_rows(const Geometry& g, const Bufs& b, int64_t rows, int nseg, bool scaled,
                                     hipStream_t st);
 

@@ -21,6 +21,7 @@ NLR_EDEGENERATE = 4
 NLR_EHIP = 5
 NLR_ESTATE = 6
 NLR_EUNSUPPORTED = 7
+NLR_ERANGE = 8
 
 NLR_INIT_U_IN_OMEGA = 1
 NLR_INIT_KEEP_Y = 2
@@ -260,6 +261,10 @@ class Context:
 
     def inspect(self, what: str):
         import numpy as np
+        if what == "rows_run":
+            v = ctypes.c_int64(0)
+            _check(load_library().nlr_inspect(self._ctx, 3, ctypes.byref(v), 8), "nlr_inspect")
+            return int(v.value)
         if what == "theta":
             out = np.zeros((self.d, self.r), dtype=np.float32)
             code = 0

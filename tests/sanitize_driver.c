@@ -32,7 +32,7 @@ static nlr_status init(float* X, int64_t n, int32_t d, int32_t K, int32_t r, flo
 
 int main(void) {
   CHECK(strncmp(nlr_version(), "nlr-gfx950", 10) == 0);
-  for (int s = 0; s < 8; ++s) CHECK(strcmp(nlr_status_string((nlr_status)s), "unknown status") != 0);
+  for (int s = 0; s < 9; ++s) CHECK(strcmp(nlr_status_string((nlr_status)s), "unknown status") != 0);
   CHECK(strcmp(nlr_status_string((nlr_status)99), "unknown status") == 0);
   CHECK(strcmp(nlr_status_string((nlr_status)-1), "unknown status") == 0);
 

@@ -33,9 +33,19 @@ def test_exports_every_declared_symbol(lib):
 
 def test_version_and_status_strings(lib):
     assert lib.nlr_version().decode().startswith("nlr-gfx950")
-    for s in range(8):
+    for s in range(9):
         assert lib.nlr_status_string(s).decode() != "unknown status"
     assert lib.nlr_status_string(99).decode() == "unknown status"
+
+
+def test_workspace_holds_no_factor_copy(lib):
+    """Section 4.4 (eq. gpu-storage): besides Xhat, one n x r factor and the stored dual, the
+    workspace holds partial sums and init temporaries only -- far below one n x r fp32 factor
+    (a second factor buffer would make it exceed 1.0)."""
+    for n, d, r in [(1_000_000, 64, 16), (10_000_000, 128, 64), (50_000_000, 32, 10),
+                    (2_000_000, 768, 256)]:
+        assert nlr.nlr_workspace_bytes(n, d, r) < 0.5 * n * r * 4, (n, d, r)
+    assert nlr.nlr_workspace_bytes(10_000_000, 128, 64) < 64 << 20
 
 
 def test_workspace_bytes(lib):

@@ -1,12 +1,12 @@
 """The one-pass iteration (97..128 features, 33..64 columns, split products): one
 pass over the rows per iteration does the row work of the iteration (the end of
-the previous one) and the primal step, reading the factor from one buffer and
-writing W to the other; s comes from the Gram terms of the previous pass, and
-the stopping rule of an iteration is decided after the next pass, which is then
-discarded.  Checked against the fp64 oracle as the other forms: trajectories
-with gated dual steps, bitwise equality of nlr_run and nlr_step, the stopping
-rule, and breakdown (the unnormalised update, written to the workspace buffer,
-replaces the factor).
+the previous one) and the primal step, writing W over the factor it reads; s
+comes from the Gram terms of the previous pass.  Where the previous iteration's
+stopping rule can fire (movement below min(eps_d, eps_c), t >= T_min), the row
+work runs in a pass of its own first and settles it.  Checked against the fp64
+oracle as the other forms: trajectories with gated dual steps, bitwise equality
+of nlr_run and nlr_step (also across iterations whose row pass runs first), the
+stopping rule, and breakdown (the unnormalised update replaces the factor).
 """
 import numpy as np
 import pytest
@@ -59,7 +59,7 @@ def test_onepass_run_equals_steps_bitwise():
     a = make_ctx(X, Z, K, alpha, beta, **kw)
     b = make_ctx(X, Z, K, alpha, beta, **kw)
     c = make_ctx(X, Z, K, alpha, beta, **kw)
-    T = 451  # odd: the last pass writes the workspace buffer; 162 dual steps in the first 450
+    T = 451  # 162 dual steps in the first 450
     done, _ = a.run(T)
     assert done == T
     done_c, _ = c.run(T)
@@ -102,6 +102,43 @@ def test_onepass_stop_rule(d, r, expect):
     # a second run continues from the stopped iterate
     more, _ = ctx.run(5)
     assert more >= 1
+
+
+@pytest.mark.parametrize("d,r", [(100, 36), (128, 64)])
+def test_onepass_rows_first_iterations(d, r):
+    """eps_c = 1e-3, T_min = 0: from the first iteration whose movement falls below 1e-3 until
+    the stop (432 / 564), nlr_run runs each iteration's row pass first (it settles the stopping
+    rule) and then the pass in place; nlr_step settles the rule in the finish pass of each call
+    instead.  The two stay bitwise equal (s comes from the Gram terms either way), follow the
+    oracle, and the counter of row-first iterations is as expected."""
+    X, Z, K, beta, alpha = _gated(d, r)
+    kw = dict(eps_d=3e-3, eps_c=1e-3, T_min=0, flags=SPLIT)
+    T = 420
+    a = make_ctx(X, Z, K, alpha, beta, **kw)
+    b = make_ctx(X, Z, K, alpha, beta, **kw)
+    done, last = a.run(T)
+    assert done == T and last["stop"] == 0
+    for _ in range(T):
+        b.step(with_stats=False)
+    assert np.array_equal(host(a.U), host(b.U)) and np.array_equal(host(a.y), host(b.y))
+    hist = a.history(T)
+    # the row pass runs first at t where delta_{t-1} < min(eps_d, eps_c) (and once after init)
+    expect = 1 + sum(1 for h in hist[:-1] if h["delta"] < 1e-3)
+    ra, rb = a.inspect("rows_run"), b.inspect("rows_run")
+    log(f"one-pass rows-first d={d} r={r}: {ra} of {T} iterations (expected {expect}); steps: {rb}")
+    assert ra == expect and ra > 20 and rb == 1
+    gates = [bool(h["dual_step"]) for h in hist]
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    ref = onlr.run(Xh, Z, K, alpha, beta, T=T, T_min=T, eps_d=3e-3, eps_c=1e-3, gates=gates)
+    assert rel_max_err(host(a.U), ref.U) < U_TOL
+    ys = onlr.stored_dual(ref.y)
+    assert np.abs(host(a.y) - ys).max() <= 1e-4 * np.abs(ys).max()
+    # one more iteration from the GPU's own iterate, taken by the oracle
+    U_t, y_t = host(a.U), host(a.y)
+    st = a.step()
+    one = onlr.run(Xh, U_t, K, alpha, beta, T=1, T_min=1, project_init=False,
+                   y0=onlr.dual_from_stored(y_t), gates=[bool(st["dual_step"])])
+    assert rel_max_err(host(a.U), one.U) < U_TOL / 10
 
 
 @pytest.mark.parametrize("steps_first", [0, 1])

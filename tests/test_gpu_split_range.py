@@ -1,0 +1,66 @@
+"""The split W operand out of fp16's range (NLR_ERANGE), on the GPU.
+
+With a step size far beyond the Prop. 1 bound (alpha = 1e5, about 4e4 times the default)
+the first update has entries near 180 (> 65504 / 2^10): the single-Xhat-pass form (16
+features, 4 columns) and the one-pass form (128 features, 64 columns) stop with NLR_ERANGE
+instead of iterating on inf/NaN operands; U holds the finite W; the context is then
+failed.  The same step with fp32 products (no such limit) gives a finite normalised
+iterate.  This is numeric overflow handled by the kernels' own flag, not a GPU fault."""
+import numpy as np
+import pytest
+
+from gpu_util import host, log, make_ctx
+from oracle import nlr as onlr
+from synth import gaussian_mixture, make_workload, standard_normal_factor
+
+pytestmark = pytest.mark.gpu
+
+SPLIT = 8  # NLR_INIT_SPLIT_F16
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_36074_amd import nlr
+    nlr.load_library()
+
+
+def _inputs(shape):
+    if shape == "tiny":
+        X, Z, _, wl = make_workload("tiny")
+        return X, Z.astype(np.float64), wl.K, 1.0
+    X, _, _ = gaussian_mixture(3000, 128, 4, 25.0, seed=1)
+    return X, standard_normal_factor(3000, 64, seed=2).astype(np.float64), 4, 2.0
+
+
+@pytest.mark.parametrize("shape,form", [("tiny", "single-Xhat-pass"), ("d128r64", "one-pass")])
+def test_split_range_error(shape, form):
+    from paper_2609_36074_amd import nlr
+    X, Z, K, beta = _inputs(shape)
+    n, r = Z.shape
+    assert nlr.FORM_NAMES[nlr.nlr_iteration_form(n, X.shape[1], r, K, SPLIT)] == form
+    alpha = 1e5
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    U0 = onlr.project_omega(Z, K)
+    W = np.maximum(U0 - alpha * onlr.gradient(Xh, U0, np.zeros(n), beta), 0.0)
+    log(f"range error {shape}: max w of the first update {W.max():.1f}")
+    assert W.max() > 2 * 65504 / 1024
+    ctx = make_ctx(X, Z, K, alpha, beta, flags=SPLIT)
+    with pytest.raises(nlr.NlrError) as e:
+        ctx.run(3)
+    assert e.value.status == nlr.NLR_ERANGE
+    U = host(ctx.U)
+    assert np.all(np.isfinite(U)) and U.max() > 64
+    h = ctx.history(8)
+    assert h[-1]["breakdown"] == 2 and h[-1]["t"] == 0
+    with pytest.raises(nlr.NlrError) as e:
+        ctx.run(1)
+    assert e.value.status == nlr.NLR_ESTATE
+    # fp32 products take the same step without a range limit
+    c32 = make_ctx(X, Z, K, alpha, beta, flags=0)
+    done, last = c32.run(3)
+    U32 = host(c32.U)
+    assert done == 3 and np.all(np.isfinite(U32)) and last["breakdown"] == 0
+    assert abs((U32 * U32).sum() - K) < 1e-3 * K
