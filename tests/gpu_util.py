@@ -88,3 +88,46 @@ def trajectory(X, Z, K, alpha, beta, T, eps_d=1e-4, eps_c=1e-4, one_step_tol=Non
             ystored = onlr.stored_dual(r1.y)
             assert np.abs(y_gpu[t + 1] - ystored).max() <= 1e-5 * max(1e-12, np.abs(ystored).max()) + 1e-12, t
     return ctx, ref, traj_err, obj_err, bad_gates, one, U_gpu, stats
+
+
+def lockstep(ctx, Xh, U0, K, alpha, beta, T, eps_d, t0=0):
+    """Steps the GPU context T times (nlr_step with its record) and the fp64 oracle along,
+    holding a few copies of U only (no stored trajectory), for the full-size workloads:
+      traj[t]  the oracle's own trajectory from U0 (the GPU's gate decisions replayed) at t+1;
+      one[t]   one oracle step from the GPU's own iterate U_t, y_t (same gate), at t+1;
+      yerr[t]  the stored dual after that step, relative to its max;
+      obj[t]   the objective f_{y_t}(U_t) of the record against the trajectory's.
+    The oracle steps run one after the other in this thread: BLAS calls made concurrently
+    from two Python threads have returned wrong products here."""
+    U_ref = np.asarray(U0, dtype=np.float64)
+    y_ref = np.zeros(U_ref.shape[0])
+    U_prev, y_prev = host(ctx.U), host(ctx.y)
+    out = {"traj": [], "one": [], "yerr": [], "obj": [], "bad_gates": [], "stats": []}
+
+    def oracle_step(U, y, gate, t):
+        return onlr.run(Xh, U, K, alpha, beta, T=1, T_min=1, project_init=False, y0=y, gates=[gate], t0=t)
+
+    for t in range(t0, t0 + T):
+        st = ctx.step()
+        out["stats"].append(st)
+        gate = bool(st["dual_step"])
+        U_gpu, y_gpu = host(ctx.U), host(ctx.y)
+        r = oracle_step(U_ref, y_ref, gate, t)
+        rec = r.records[0]
+        out["traj"].append(rel_max_err(U_gpu, r.U))
+        out["obj"].append(obj_rel_err(st["objective"], rec.objective, 1.0))
+        if gate != (rec.delta < eps_d) and abs(rec.delta - eps_d) > 1e-3 * eps_d:
+            out["bad_gates"].append(t)
+        U_ref, y_ref = r.U, r.y
+        del r
+        o = oracle_step(U_prev, onlr.dual_from_stored(y_prev), gate, t)
+        out["one"].append(rel_max_err(U_gpu, o.U))
+        ys = onlr.stored_dual(o.y)
+        ymax = float(np.abs(ys).max())
+        out["yerr"].append(float(np.abs(y_gpu - ys).max()) / ymax if ymax > 0 else float(np.abs(y_gpu).max()))
+        del o
+        U_prev, y_prev = U_gpu, y_gpu
+        log(f"  t={t}: traj {out['traj'][-1]:.2e} one {out['one'][-1]:.2e} obj {out['obj'][-1]:.2e} "
+            f"gate {int(gate)}")
+    out["U_ref"], out["U_gpu"] = U_ref, U_prev
+    return out

@@ -11,8 +11,8 @@ within 1e-3 relative of eps_d).
 import numpy as np
 import pytest
 
-from gpu_util import (OBJ_TOL, U_TOL, host, label_agreement, log, make_ctx, obj_rel_err, rel_max_err,
-                      trajectory)
+from gpu_util import (OBJ_TOL, U_TOL, host, label_agreement, lockstep, log, make_ctx, obj_rel_err,
+                      rel_max_err, trajectory)
 from oracle import nlr as onlr
 from synth import gaussian_mixture, make_workload, standard_normal_factor
 
@@ -178,15 +178,18 @@ def test_ragged_shapes(n, d, r, K):
 
 
 def test_gmm1m_parity():
+    """gmm1m over its configuration's 100 iterations with fp32 products, each iterate against
+    the oracle's trajectory and one oracle step from the GPU's own iterate."""
     X, Z, lab, wl = make_workload("gmm1m")
-    Z = Z.astype(np.float64)
-    K = wl.K
-    alpha = onlr.default_step_size(K)
-    log("gmm1m trajectory T=6")
-    ctx, ref, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, alpha, 1.0, 6, one_step_tol=True)
-    log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
-    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
-    bad, amb = label_agreement(ctx.labels().cpu().numpy(), ref.U)
+    K, alpha = wl.K, onlr.default_step_size(wl.K)
+    log(f"gmm1m lockstep T={wl.T}")
+    ctx = make_ctx(X, Z, K, alpha, 1.0, T_min=wl.T)
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    res = lockstep(ctx, Xh, onlr.project_omega(Z.astype(np.float64), K), K, alpha, 1.0, wl.T, 1e-4)
+    log(f"  traj {max(res['traj']):.2e} one {max(res['one']):.2e} obj {max(res['obj']):.2e}")
+    assert max(res["traj"]) < U_TOL and max(res["one"]) < U_TOL / 10 and max(res["obj"]) < OBJ_TOL
+    assert not res["bad_gates"]
+    bad, amb = label_agreement(ctx.labels().cpu().numpy(), res["U_ref"])
     log(f"  labels: {bad} mismatches, {amb} ambiguous")
     assert bad == 0
 

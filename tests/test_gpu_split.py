@@ -7,7 +7,7 @@ decision consistent with the oracle's own movement.
 import numpy as np
 import pytest
 
-from gpu_util import OBJ_TOL, U_TOL, host, label_agreement, log, make_ctx, trajectory
+from gpu_util import OBJ_TOL, U_TOL, host, label_agreement, lockstep, log, make_ctx, trajectory
 from oracle import nlr as onlr
 from synth import gaussian_mixture, make_workload, standard_normal_factor
 
@@ -109,15 +109,37 @@ def test_split_fused8_run_equals_steps_and_deterministic():
 
 
 def test_split_gmm1m():
+    """gmm1m over its configuration's 100 iterations in the bench's form (split products,
+    single-Xhat-pass), each iterate against the oracle's trajectory and one oracle step."""
     X, Z, _, wl = make_workload("gmm1m")
-    Z = Z.astype(np.float64)
-    log("split: gmm1m trajectory T=6")
-    ctx, ref, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, wl.K, onlr.default_step_size(wl.K), 1.0, 6,
-                                                           one_step_tol=True, flags=SPLIT)
-    log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
-    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
-    bad, amb = label_agreement(ctx.labels().cpu().numpy(), ref.U)
+    K, alpha = wl.K, onlr.default_step_size(wl.K)
+    log(f"split: gmm1m lockstep T={wl.T}")
+    ctx = make_ctx(X, Z, K, alpha, 1.0, T_min=wl.T, flags=SPLIT)
+    Xh, _, _ = onlr.centre_and_normalise(X)
+    res = lockstep(ctx, Xh, onlr.project_omega(Z.astype(np.float64), K), K, alpha, 1.0, wl.T, 1e-4)
+    log(f"  traj {max(res['traj']):.2e} one {max(res['one']):.2e} obj {max(res['obj']):.2e} "
+        f"y {max(res['yerr']):.2e}")
+    assert max(res["traj"]) < U_TOL and max(res["one"]) < U_TOL / 10 and max(res["obj"]) < OBJ_TOL
+    assert not res["bad_gates"]
+    bad, amb = label_agreement(ctx.labels().cpu().numpy(), res["U_ref"])
     assert bad == 0, (bad, amb)
+
+
+@pytest.mark.parametrize("flags", [SPLIT, 0])
+def test_tiny_dual_steps_at_config_tolerance(flags):
+    """tiny with the configurations' eps_d = 1e-4 and default step: the movement falls below
+    eps_d near iteration 800, so 1500 iterations take dual steps under the paper's gate."""
+    X, Z, _, wl = make_workload("tiny")
+    Z = Z.astype(np.float64)
+    K = wl.K
+    _, _, traj, obj, bad_gates, one, _, stats = trajectory(X, Z, K, onlr.default_step_size(K), 1.0, 1500,
+                                                           eps_d=1e-4, eps_c=1e-4, one_step_tol=True,
+                                                           flags=flags)
+    ngates = sum(s["dual_step"] for s in stats)
+    log(f"  tiny eps_d=1e-4 flags={flags}: {ngates} dual steps; traj {max(traj):.2e} one {max(one):.2e}")
+    assert ngates >= 1
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates, bad_gates
 
 
 def test_split_run_equals_steps_and_deterministic():
