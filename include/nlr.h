@@ -211,6 +211,26 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
                     float* U, float* y, const nlr_params* params, uint32_t flags,
                     void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): nlr_init followed by
+ * nlr_run(T) in one call that allocates nothing -- no workspace argument, no
+ * context left behind, no pinned host memory.  Arguments, in-place outputs (X
+ * becomes Xhat, U the iterate after the run, y the stored dual) and statuses are
+ * those of nlr_init and nlr_run; *iters_done and *last (both nullable) as in
+ * nlr_run.  Its scratch is a device array inside the library of
+ * NLR_STATIC_SCRATCH_BYTES (64 MiB), one per GPU the library runs on, held until
+ * the process ends: a shape whose nlr_workspace_bytes exceeds it returns
+ * NLR_EWORKSPACE before any HIP call (every benchmark shape up to 1e7 x 128 x 64
+ * fits; 2e6 x 768 x 256 does not).  Every call on a GPU uses that GPU's one
+ * array, and everything a call reads from it is written by the same call first;
+ * calls that overlap on one GPU (other threads, other streams) race on it and
+ * must be serialised by the caller.  Synchronises `stream` as nlr_init and
+ * nlr_run do. */
+#define NLR_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+nlr_status nlr_solve_static(float* X, int64_t n, int32_t d, int32_t K, int32_t r, float* U, float* y,
+                            const nlr_params* params, uint32_t flags, int32_t T, int32_t* iters_done,
+                            nlr_iter_stats* last, void* stream);
+
 /* Replaces the algorithm parameters of a context (takes effect at the next step). */
 nlr_status nlr_set_params(nlr_ctx* ctx, const nlr_params* params);
 

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -542,11 +543,13 @@ int32_t nlr_iteration_form(int64_t n, int32_t d, int32_t r, int32_t K, uint32_t 
   return NLR_FORM_TWO_PASS;
 }
 
-nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, int32_t r, float* U, float* y,
-                    const nlr_params* params, uint32_t flags, void* workspace, size_t workspace_bytes,
-                    void* stream) {
-  if (!ctx) return NLR_EINVAL;
-  *ctx = nullptr;
+}  // extern "C"
+
+// Argument checks of nlr_init (before any HIP call); on success *g0 is the geometry
+// and *need the workspace bytes it takes.
+static nlr_status check_init(const float* X, int64_t n, int32_t d, int32_t K, int32_t r, const float* U,
+                             const float* y, const nlr_params* params, uint32_t flags, Geometry* g0,
+                             size_t* need) {
   if (!X || !U || !y || !params_ok(params)) return NLR_EINVAL;
   if (!shape_ok(n, d, r) || K < 1 || K > r) return NLR_EINVAL;
   if (flags & ~(uint32_t)(NLR_INIT_U_IN_OMEGA | NLR_INIT_KEEP_Y | NLR_INIT_X_NORMALISED | NLR_INIT_SPLIT_F16 |
@@ -558,13 +561,16 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   const bool aligned16 = (((uintptr_t)X & 15) == 0) && (((uintptr_t)U & 15) == 0);
   const bool split = (flags & NLR_INIT_SPLIT_F16) != 0;
   const bool fused = (flags & NLR_INIT_TWO_PASS) == 0;
-  const Geometry g0 = make_geometry(n, d, r, K, aligned16, split, fused);
-  if (split && !g0.split_b && !g0.panel) return NLR_EUNSUPPORTED;
-  const size_t need = carve_workspace(g0, nullptr, nullptr);
-  if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
+  *g0 = make_geometry(n, d, r, K, aligned16, split, fused);
+  if (split && !g0->split_b && !g0->panel) return NLR_EUNSUPPORTED;
+  *need = carve_workspace(*g0, nullptr, nullptr);
+  return NLR_OK;
+}
 
-  nlr_ctx* c = new (std::nothrow) nlr_ctx();
-  if (!c) return NLR_EHIP;
+// Fills a constructed context (its host_ctl mirror already set) and enqueues the
+// initialisation; synchronises once.  Leaves releasing the context to the caller.
+static nlr_status init_ctx(nlr_ctx* c, const Geometry& g0, float* X, int32_t K, float* U, float* y,
+                           const nlr_params* params, uint32_t flags, void* workspace, void* stream) {
   c->g = g0;
   carve_workspace(c->g, reinterpret_cast<char*>(workspace), &c->b);
   c->b.X = X;
@@ -586,92 +592,49 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
     c->prof_ms[k] = 0.0;
     c->prof_n[k] = 0;
   }
-  if (hipGetDevice(&c->device) != hipSuccess) {
-    delete c;
-    return NLR_EHIP;
-  }
-  if (hipHostMalloc(reinterpret_cast<void**>(&c->host_ctl), sizeof(DevCtl), hipHostMallocDefault) != hipSuccess) {
-    delete c;
-    return NLR_EHIP;
-  }
+  if (hipGetDevice(&c->device) != hipSuccess) return NLR_EHIP;
   const Geometry& g = c->g;
   const Bufs& b = c->b;
+  const int64_t n = g.n;
+  const bool split = (flags & NLR_INIT_SPLIT_F16) != 0;
   hipStream_t st = c->stream;
-  auto fail = [&](nlr_status s) {
-    nlr_destroy(c);
-    return s;
-  };
-  if (launch_ctl_init(b, (float)(params->beta / (double)n), st) != hipSuccess) return fail(NLR_EHIP);
+  if (launch_ctl_init(b, (float)(params->beta / (double)n), st) != hipSuccess) return NLR_EHIP;
   if (!(flags & NLR_INIT_X_NORMALISED)) {
-    if (launch_colsum(g, b, st) != hipSuccess) return fail(NLR_EHIP);
-    if (launch_gram(g, b, st) != hipSuccess) return fail(NLR_EHIP);
-    if (launch_spectral(g, b, st) != hipSuccess) return fail(NLR_EHIP);
-    if (launch_normalise(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_colsum(g, b, st) != hipSuccess) return NLR_EHIP;
+    if (launch_gram(g, b, st) != hipSuccess) return NLR_EHIP;
+    if (launch_spectral(g, b, st) != hipSuccess) return NLR_EHIP;
+    if (launch_normalise(g, b, st) != hipSuccess) return NLR_EHIP;
   }
   if (split)
-    if (launch_xscale(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_xscale(g, b, st) != hipSuccess) return NLR_EHIP;
   if (flags & NLR_INIT_DATA_START) {
     // U holds Z: replace it by the range finder's orthonormal factor Q (Appendix D)
     const StepArgs a0 = make_step_args(c, 0);
-    if (launch_data_start(g, b, a0, (flags & NLR_INIT_X_NORMALISED) != 0, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_data_start(g, b, a0, (flags & NLR_INIT_X_NORMALISED) != 0, st) != hipSuccess) return NLR_EHIP;
   }
-  if (launch_project(g, b, (double)K, (flags & NLR_INIT_U_IN_OMEGA) ? 1 : 0, st) != hipSuccess)
-    return fail(NLR_EHIP);
+  if (launch_project(g, b, (double)K, (flags & NLR_INIT_U_IN_OMEGA) ? 1 : 0, st) != hipSuccess) return NLR_EHIP;
   if (!(flags & NLR_INIT_KEEP_Y))
-    if (launch_zero_y(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_zero_y(g, b, st) != hipSuccess) return NLR_EHIP;
   if (g.fused) {
     // Theta_0 = Xhat^T U_0: one pass A (its row partials are recomputed by the first row pass)
     const StepArgs a0 = make_step_args(c, 0);
-    if (launch_pass_a(g, b, a0, false, st) != hipSuccess) return fail(NLR_EHIP);
-    if (launch_reduce_theta(g, b, false, st) != hipSuccess) return fail(NLR_EHIP);
+    if (launch_pass_a(g, b, a0, false, st) != hipSuccess) return NLR_EHIP;
+    if (launch_reduce_theta(g, b, false, st) != hipSuccess) return NLR_EHIP;
     // split products: the fused pass B is then the only reader of X; store Xhat split once
     if (g.split_b)
-      if (launch_split_x(g, b, st) != hipSuccess) return fail(NLR_EHIP);
+      if (launch_split_x(g, b, st) != hipSuccess) return NLR_EHIP;
   }
   // panel form: both passes read Xhat only as split operands; store it so once
   if (g.panel)
-    if (launch_split_x8(g, b, st) != hipSuccess) return fail(NLR_EHIP);
-  if (read_ctl(c) != NLR_OK) return fail(NLR_EHIP);
-  if (c->host_ctl->degenerate) return fail(NLR_EDEGENERATE);
-  if (c->host_ctl->breakdown) return fail(NLR_EBREAKDOWN);
-  *ctx = c;
+    if (launch_split_x8(g, b, st) != hipSuccess) return NLR_EHIP;
+  if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+  if (c->host_ctl->degenerate) return NLR_EDEGENERATE;
+  if (c->host_ctl->breakdown) return NLR_EBREAKDOWN;
   return NLR_OK;
 }
 
-nlr_status nlr_set_params(nlr_ctx* c, const nlr_params* params) {
-  if (!c || !params_ok(params)) return NLR_EINVAL;
-  if (c->failed) return NLR_ESTATE;
-  c->prm = *params;
-  return NLR_OK;
-}
-
-nlr_status nlr_step(nlr_ctx* c, nlr_iter_stats* stats) {
-  if (!c) return NLR_EINVAL;
-  if (c->failed) return NLR_ESTATE;
-  if (launch_clear_stop(c->b, c->stream) != hipSuccess) return hip_fail(c);
-  nlr_status s = enqueue_iteration(c, true);
-  if (s != NLR_OK) return s;
-  s = enqueue_finish(c);
-  if (s != NLR_OK) return s;
-  c->t_host_valid = false;
-  if (stats) {
-    if (read_ctl(c) != NLR_OK) return NLR_EHIP;
-    if (c->host_ctl->breakdown) {
-      c->failed = true;
-      c->breakdown = true;
-      c->range_error = c->host_ctl->breakdown == kRangeError;
-    }
-    const int64_t t = c->host_ctl->t_done - (c->host_ctl->breakdown ? 0 : 1);
-    if (read_record(c, t < 0 ? 0 : t, stats) != NLR_OK) return NLR_EHIP;
-    if (prof_collect(c) != hipSuccess) return hip_fail(c);
-    if (c->breakdown) return c->range_error ? NLR_ERANGE : NLR_EBREAKDOWN;
-  }
-  return NLR_OK;
-}
-
-nlr_status nlr_run(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* last) {
-  if (!c || T < 0) return NLR_EINVAL;
-  if (c->failed) return NLR_ESTATE;
+// Up to T iterations and the finish pass (the body of nlr_run).
+static nlr_status run_iterations(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* last) {
   if (!c->t_host_valid)
     if (read_ctl(c) != NLR_OK) return NLR_EHIP;
   const int64_t t0 = c->t_host;
@@ -708,6 +671,117 @@ nlr_status nlr_run(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* l
     }
   }
   return c->breakdown ? (c->range_error ? NLR_ERANGE : NLR_EBREAKDOWN) : NLR_OK;
+}
+
+// ---- the allocation-free entry point ----
+// Device scratch that nlr_solve_static uses in place of a caller's workspace: one
+// copy per GPU the library runs on, held until the process ends, shared by every
+// such call on that GPU (calls that overlap on one GPU race on it).  In host code
+// the array's name is not a device address: the address of the current device's
+// copy comes from hipGetSymbolAddress, taken once per device by the first call
+// there and kept in g_scratch_ptr.
+static __device__ __align__(256) unsigned char scratch[NLR_STATIC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};
+
+static nlr_status static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return NLR_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return NLR_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return NLR_OK;
+}
+
+extern "C" {
+
+nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, int32_t r, float* U, float* y,
+                    const nlr_params* params, uint32_t flags, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  if (!ctx) return NLR_EINVAL;
+  *ctx = nullptr;
+  Geometry g0;
+  size_t need = 0;
+  const nlr_status chk = check_init(X, n, d, K, r, U, y, params, flags, &g0, &need);
+  if (chk != NLR_OK) return chk;
+  if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
+  nlr_ctx* c = new (std::nothrow) nlr_ctx();
+  if (!c) return NLR_EHIP;
+  if (hipHostMalloc(reinterpret_cast<void**>(&c->host_ctl), sizeof(DevCtl), hipHostMallocDefault) != hipSuccess) {
+    delete c;
+    return NLR_EHIP;
+  }
+  const nlr_status s = init_ctx(c, g0, X, K, U, y, params, flags, workspace, stream);
+  if (s != NLR_OK) {
+    nlr_destroy(c);
+    return s;
+  }
+  *ctx = c;
+  return NLR_OK;
+}
+
+nlr_status nlr_solve_static(float* X, int64_t n, int32_t d, int32_t K, int32_t r, float* U, float* y,
+                            const nlr_params* params, uint32_t flags, int32_t T, int32_t* iters_done,
+                            nlr_iter_stats* last, void* stream) {
+  if (T < 0) return NLR_EINVAL;
+  Geometry g0;
+  size_t need = 0;
+  const nlr_status chk = check_init(X, n, d, K, r, U, y, params, flags, &g0, &need);
+  if (chk != NLR_OK) return chk;
+  if (need > NLR_STATIC_SCRATCH_BYTES) return NLR_EWORKSPACE;
+  void* ws = nullptr;
+  if (static_scratch(&ws) != NLR_OK) return NLR_EHIP;
+  // the context lives on this stack frame; the control-block mirror is ordinary host
+  // memory (no pinned allocation); profiling stays off, so no events are created
+  nlr_ctx c;
+  DevCtl mirror;
+  std::memset(&mirror, 0, sizeof(mirror));
+  c.host_ctl = &mirror;
+  nlr_status s = init_ctx(&c, g0, X, K, U, y, params, flags, ws, stream);
+  if (s != NLR_OK) return s;
+  return run_iterations(&c, T, iters_done, last);
+}
+
+nlr_status nlr_set_params(nlr_ctx* c, const nlr_params* params) {
+  if (!c || !params_ok(params)) return NLR_EINVAL;
+  if (c->failed) return NLR_ESTATE;
+  c->prm = *params;
+  return NLR_OK;
+}
+
+nlr_status nlr_step(nlr_ctx* c, nlr_iter_stats* stats) {
+  if (!c) return NLR_EINVAL;
+  if (c->failed) return NLR_ESTATE;
+  if (launch_clear_stop(c->b, c->stream) != hipSuccess) return hip_fail(c);
+  nlr_status s = enqueue_iteration(c, true);
+  if (s != NLR_OK) return s;
+  s = enqueue_finish(c);
+  if (s != NLR_OK) return s;
+  c->t_host_valid = false;
+  if (stats) {
+    if (read_ctl(c) != NLR_OK) return NLR_EHIP;
+    if (c->host_ctl->breakdown) {
+      c->failed = true;
+      c->breakdown = true;
+      c->range_error = c->host_ctl->breakdown == kRangeError;
+    }
+    const int64_t t = c->host_ctl->t_done - (c->host_ctl->breakdown ? 0 : 1);
+    if (read_record(c, t < 0 ? 0 : t, stats) != NLR_OK) return NLR_EHIP;
+    if (prof_collect(c) != hipSuccess) return hip_fail(c);
+    if (c->breakdown) return c->range_error ? NLR_ERANGE : NLR_EBREAKDOWN;
+  }
+  return NLR_OK;
+}
+
+nlr_status nlr_run(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr_iter_stats* last) {
+  if (!c || T < 0) return NLR_EINVAL;
+  if (c->failed) return NLR_ESTATE;
+  return run_iterations(c, T, iters_done, last);
 }
 
 nlr_status nlr_labels(nlr_ctx* c, int32_t* labels) {

@@ -42,7 +42,9 @@ FORM_NAMES = {NLR_FORM_TWO_PASS: "two-pass", NLR_FORM_PANEL: "two-pass-panel",
 EXPORTED = ["nlr_workspace_bytes", "nlr_iteration_form", "nlr_init", "nlr_set_params", "nlr_step", "nlr_run", "nlr_labels",
             "nlr_labels_spectral",
             "nlr_history", "nlr_normaliser", "nlr_inspect", "nlr_set_profiling", "nlr_kernel_times",
-            "nlr_destroy", "nlr_status_string", "nlr_version"]
+            "nlr_destroy", "nlr_status_string", "nlr_version", "nlr_solve_static"]
+
+NLR_STATIC_SCRATCH_BYTES = 64 << 20
 
 
 class NlrParams(ctypes.Structure):
@@ -87,6 +89,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nlr_workspace_bytes.restype = sz
     lib.nlr_iteration_form.argtypes = [i64, i32, i32, i32, u32]
     lib.nlr_iteration_form.restype = i32
+    lib.nlr_solve_static.argtypes = [P, i64, i32, i32, i32, P, P, ctypes.POINTER(NlrParams), u32, i32,
+                                     ctypes.POINTER(i32), ctypes.POINTER(NlrIterStats), P]
+    lib.nlr_solve_static.restype = ctypes.c_int
     lib.nlr_init.argtypes = [ctypes.POINTER(P), P, i64, i32, i32, i32, P, P, ctypes.POINTER(NlrParams), u32, P, sz, P]
     lib.nlr_init.restype = ctypes.c_int
     lib.nlr_set_params.argtypes = [P, ctypes.POINTER(NlrParams)]
@@ -139,6 +144,16 @@ def nlr_workspace_bytes(n: int, d: int, r: int) -> int:
 
 def nlr_iteration_form(n: int, d: int, r: int, K: int, flags: int) -> int:
     return int(load_library().nlr_iteration_form(n, d, r, K, flags))
+
+
+def nlr_solve_static(X_ptr: int, n: int, d: int, K: int, r: int, U_ptr: int, y_ptr: int, params: NlrParams,
+                     flags: int, T: int, stream_ptr: int = 0):
+    """(status, iterations done, record of the last one): the allocation-free init + run."""
+    done = ctypes.c_int32(0)
+    last = NlrIterStats()
+    st = load_library().nlr_solve_static(X_ptr, n, d, K, r, U_ptr, y_ptr, ctypes.byref(params), flags, T,
+                                         ctypes.byref(done), ctypes.byref(last), stream_ptr)
+    return int(st), int(done.value), last.as_dict()
 
 
 def nlr_init(X_ptr: int, n: int, d: int, K: int, r: int, U_ptr: int, y_ptr: int, params: NlrParams,

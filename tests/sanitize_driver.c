@@ -114,6 +114,20 @@ int main(void) {
   CHECK(nlr_kernel_times(NULL, names, ms, launches, &cnt) == NLR_EINVAL);
   nlr_destroy(NULL);
 
+  /* nlr_solve_static: the same argument checks, and shapes beyond its scratch, before any HIP call */
+  done = -7;
+  CHECK(nlr_solve_static(X, 1000, 16, 4, 4, U, y, &ok, 0, -1, &done, &st, NULL) == NLR_EINVAL && done == -7);
+  CHECK(nlr_solve_static(NULL, 1000, 16, 4, 4, U, y, &ok, 0, 5, &done, &st, NULL) == NLR_EINVAL);
+  CHECK(nlr_solve_static(X, 1000, 16, 4, 4, U, y, NULL, 0, 5, &done, &st, NULL) == NLR_EINVAL);
+  CHECK(nlr_solve_static(X, 1000, 16, 5, 4, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EINVAL);
+  CHECK(nlr_solve_static(X, INT64_MAX, 16, 4, 4, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EINVAL);
+  CHECK(nlr_solve_static(X, 1000, 16, 4, 300, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EUNSUPPORTED);
+  CHECK(nlr_solve_static(X, 1000, 16, 4, 4, U, y, &ok, 1u << 7, 5, NULL, NULL, NULL) == NLR_EINVAL);
+  CHECK(nlr_workspace_bytes(2000000, 768, 256) > NLR_STATIC_SCRATCH_BYTES);
+  CHECK(nlr_solve_static(X, 2000000, 768, 256, 256, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EWORKSPACE);
+  CHECK(nlr_solve_static(X, ((int64_t)1 << 40) - 1, 4096, 256, 256, U, y, &ok, 0, 5, NULL, NULL, NULL) ==
+        NLR_EWORKSPACE);
+
   if (fails) fprintf(stderr, "%d checks failed\n", fails);
   else printf("all checks passed\n");
   return fails ? 1 : 0;

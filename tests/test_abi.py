@@ -133,3 +133,18 @@ def test_binding_fails_loudly_without_library(tmp_path):
             nlr.load_library(str(tmp_path / "libnlr.so"))
         finally:
             nlr._lib = saved
+
+
+def test_solve_static_rejects_before_any_hip_call(lib):
+    """The allocation-free entry point checks its arguments as nlr_init does, and rejects shapes
+    whose workspace exceeds its fixed device scratch with NLR_EWORKSPACE (no GPU needed)."""
+    p = nlr.NlrParams(0.01, 1.0, 1e-4, 1e-4, 0, 0)
+    assert nlr.nlr_workspace_bytes(10_000_000, 128, 64) <= nlr.NLR_STATIC_SCRATCH_BYTES
+    assert nlr.nlr_workspace_bytes(2_000_000, 768, 256) > nlr.NLR_STATIC_SCRATCH_BYTES
+    st, done, _ = nlr.nlr_solve_static(FAKE, 2_000_000, 768, 256, 256, FAKE, FAKE, p, 0, 5)
+    assert st == nlr.NLR_EWORKSPACE and done == 0
+    assert nlr.nlr_solve_static(FAKE, 1000, 16, 4, 4, FAKE, FAKE, p, 0, -1)[0] == nlr.NLR_EINVAL
+    assert nlr.nlr_solve_static(0, 1000, 16, 4, 4, FAKE, FAKE, p, 0, 5)[0] == nlr.NLR_EINVAL
+    assert nlr.nlr_solve_static(FAKE, 1000, 16, 4, 300, FAKE, FAKE, p, 0, 5)[0] == nlr.NLR_EUNSUPPORTED
+    assert nlr.nlr_solve_static(FAKE, 1000, 16, 8, 16, FAKE + 4, FAKE, p, nlr.NLR_INIT_SPLIT_F16, 5)[0] == \
+        nlr.NLR_EUNSUPPORTED

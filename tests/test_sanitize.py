@@ -41,8 +41,9 @@ def test_host_code_under_sanitizers(tmp_path):
         from paper_2609_36074_amd import _build
         _build.build()
     api_o = str(tmp_path / "nlr_api.o")
-    # host-side instrumentation only: each sanitizer flag applies to the host pass
-    _run([hipcc, "-xhip", "-O1", "-g", "-std=c++17", "--offload-arch=gfx950", "--offload-host-only", "-fPIC",
+    # host-side instrumentation only: each sanitizer flag applies to the host pass (the device
+    # pass compiles the file's device array without any)
+    _run([hipcc, "-xhip", "-O1", "-g", "-std=c++17", "--offload-arch=gfx950", "-fPIC",
           "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
           "-Xarch_host", "-fno-sanitize-recover=all",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
