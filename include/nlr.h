@@ -203,8 +203,9 @@ int32_t nlr_iteration_form(int64_t n, int32_t d, int32_t r, int32_t K, uint32_t 
  *   3. y <- 0 [skipped with KEEP_Y]
  * X: device n*d floats (in: data, out: Xhat).  U: device n*r floats (in: U_0,
  * e.g. the paper's random start Z with N(0,1) entries; out: Pi_Omega(U_0)).
- * y: device n floats (stored dual).  Requires 1 <= K <= r <= 256, r <= n,
- * 1 <= d <= 4096, n < 2^40 (r > 256 returns NLR_EUNSUPPORTED).  Synchronises `stream` once at the end to report
+ * y: device n floats (stored dual).  Requires 1 <= K <= r <= 448, r <= n,
+ * 1 <= d <= 4096, n < 2^40 (r > 448 returns NLR_EUNSUPPORTED; above 256 columns
+ * only the fp32 two-pass form runs).  Synchronises `stream` once at the end to report
  * NLR_EDEGENERATE / NLR_EBREAKDOWN (U_0 with no positive entry).  On success
  * *ctx receives a new context. */
 nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, int32_t r,

@@ -377,11 +377,22 @@ __global__ __launch_bounds__(kThreads) void k_proj_partial(Geometry g, Bufs B) {
   const int64_t r0 = (int64_t)blockIdx.x * n / g.GI;
   const int64_t r1 = (int64_t)(blockIdx.x + 1) * n / g.GI;
   double* out = B.i_proj + (int64_t)blockIdx.x * (4 + g.r32);
-  const int rstep = kThreads / r;   // r <= 256
+  // r <= 256: column tid % r, every (256 / r)-th row; else columns tid, tid + 256, every row
+  const int rstep = r <= kThreads ? kThreads / r : 1;
   const int col = tid % r;
-  const int rsub = tid / r;
+  const int rsub = r <= kThreads ? tid / r : 0;
   double cs = 0.0, sq = 0.0;
-  if (rsub < rstep) {
+  if (r > kThreads) {
+    for (int c = tid; c < r; c += kThreads) {
+      double csc = 0.0;
+      for (int64_t i = r0; i < r1; ++i) {
+        const float u = fmaxf(B.U[i * r + c], 0.f);
+        csc += (double)u;
+        sq += (double)u * (double)u;
+      }
+      out[4 + c] = csc;
+    }
+  } else if (rsub < rstep) {
     // sixteen rows' loads in flight, added in row order
     int64_t i = r0 + rsub;
     for (; i + 15 * rstep < r1; i += 16 * rstep) {
@@ -403,7 +414,7 @@ __global__ __launch_bounds__(kThreads) void k_proj_partial(Geometry g, Bufs B) {
   }
   red[tid] = cs;
   __syncthreads();
-  if (tid < r) {
+  if (tid < r && r <= kThreads) {
     double t = 0.0;
     for (int k = 0; k < rstep; ++k) t += red[tid + k * r];
     out[4 + tid] = t;

@@ -110,11 +110,13 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
     for (int c = tid; c < r32; c += kThreads) p_s[c] = (c < r) ? B.p[c] : 0.f;
 
   // row-work accumulators
-  double acc_qq = 0.0, acc_yq = 0.0, acc_s = 0.0;
-  // s ownership: column sc, points ps0, ps0 + pstep, ...
+  double acc_qq = 0.0, acc_yq = 0.0, acc_s = 0.0, acc_s2 = 0.0;
+  // s ownership: column sc, points ps0, ps0 + pstep, ...; above 256 columns every
+  // point, columns tid and tid + 256 (acc_s2)
   const int pstep = kThreads / r32 > 0 ? kThreads / r32 : 1;
   const int sc = tid % r32;
   const int ps0 = tid / r32;
+  const int sc2 = tid + kThreads;
 
   // matrix-core accumulators
   const int mb = wave % MBG;
@@ -177,6 +179,8 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
         for (int pt = ps0; pt < kTPA; pt += pstep)
           acc_s += (double)ybar_s[pt] * (double)Us[pt * us_stride + sc];
       }
+      if (!FINISH && sc2 < r)
+        for (int pt = 0; pt < kTPA; ++pt) acc_s2 += (double)ybar_s[pt] * (double)Us[pt * us_stride + sc2];
     }
 
     if (!FINISH) {
@@ -250,6 +254,7 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
       for (int k = 0; k < pstep; ++k) t += dred[tid + k * r32];
       ap[4 + tid] = FINISH ? 0.0 : t;
     }
+    if (sc2 < r32) ap[4 + sc2] = FINISH ? 0.0 : acc_s2;
   }
 }
 
@@ -966,6 +971,195 @@ __global__ __launch_bounds__(kThreads) void k_pass_b(Geometry g, Bufs B, StepArg
 }
 
 // ---------------------------------------------------------------------------
+// Pass B above 256 columns (NB = 10, 12 or 14 blocks of 32).  As k_pass_b, with
+// the columns taken two blocks at a time: per 128-row super-tile each wave forms
+// q = u.p - 1 over the whole row first, then for each pair of column blocks the
+// product (the Xhat row chunks re-read from cache), the epilogue and W; column
+// sums go to the wave's row of LDS per tile (lanes l and l^1 combined first).
+// ---------------------------------------------------------------------------
+template <bool THETA_LDS, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_pass_b_wide(Geometry g, Bufs B, StepArgs S) {
+  if (halted(B.ctl)) return;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  float* th_s = reinterpret_cast<float*>(smem_raw);                 // d32*r32 if THETA_LDS
+  float* ps = th_s + (THETA_LDS ? g.d32 * g.r32 : 0);               // r32
+  float* ss = ps + g.r32;                                           // r32
+  double* colred = reinterpret_cast<double*>(ss + g.r32);          // 4 x r32
+  double* dred = colred + 4 * g.r32;                                // 8
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int h = lane >> 5;
+  const int li = lane & 31;
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r, r32 = g.r32, NBt = g.NB;
+  const int nch = g.nch;
+  const float cf = B.ctl->c_f;
+  const float gam = S.gamma_f;
+  const float two_alpha = S.two_alpha_f;
+  const float neg_alpha = -S.alpha_f;
+
+  if (THETA_LDS) {
+    const int tot4 = (g.d32 * r32) >> 2;
+    const f32x4* src = reinterpret_cast<const f32x4*>(B.theta);
+    f32x4* dst = reinterpret_cast<f32x4*>(th_s);
+    for (int v = tid; v < tot4; v += kThreads) dst[v] = src[v];
+  }
+  for (int c = tid; c < r32; c += kThreads) {
+    ps[c] = B.p[c];
+    ss[c] = B.s[c];
+  }
+  for (int c = tid; c < 4 * r32; c += kThreads) colred[c] = 0.0;
+  __syncthreads();
+  const float* theta = THETA_LDS ? th_s : B.theta;
+
+  double sa = 0.0, sb = 0.0, sh = 0.0;
+  int base = 0;  // local index (8 qd + e ordering) of the column sum this lane keeps
+  if (li & 16) base += 8;
+  if (li & 8) base += 4;
+  if (li & 4) base += 2;
+  if (li & 2) base += 1;
+
+  const int64_t sb0 = (int64_t)blockIdx.x * g.tilesB / g.GB;
+  const int64_t sb1 = (int64_t)(blockIdx.x + 1) * g.tilesB / g.GB;
+  for (int64_t st = sb0; st < sb1; ++st) {
+    const int64_t pt = st * kTPB + wave * 32 + li;
+    const bool vpt = pt < n;
+    const float* xrow = B.X + (vpt ? pt : 0) * (int64_t)d;
+    float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
+    auto load_u4 = [&](int c, float out[4]) {
+      if (VEC) {
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+        if (vpt && c < r) t = *reinterpret_cast<const f32x4*>(urow + c);
+        out[0] = t.x * cf;
+        out[1] = t.y * cf;
+        out[2] = t.z * cf;
+        out[3] = t.w * cf;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) out[e] = (vpt && c + e < r) ? urow[c + e] * cf : 0.f;
+      }
+    };
+    // q = u.p - 1 over the whole row (fp32 dot over the lane's half, then the other half)
+    float dotf = 0.f;
+    for (int m = 0; m < NBt; ++m)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int c = 32 * m + 8 * qd + 4 * h;
+        float u4[4];
+        load_u4(c, u4);
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(ps + c);
+        dotf = fmaf(u4[0], pv.x, dotf);
+        dotf = fmaf(u4[1], pv.y, dotf);
+        dotf = fmaf(u4[2], pv.z, dotf);
+        dotf = fmaf(u4[3], pv.w, dotf);
+      }
+    dotf += shfl_xor_f(dotf, 32);
+    float ybar = 0.f;
+    if (vpt) ybar = fmaf(gam, dotf - 1.0f, B.y[pt]);
+
+    for (int cg = 0; cg < NBt; cg += 2) {
+      f32x16 acc[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+      for (int ch = 0; ch < nch; ++ch) {
+        const int fb = ch * 32 + h * 16;
+        float xv[16];
+        if (VEC) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            f32x4 t = {0.f, 0.f, 0.f, 0.f};
+            if (vpt && fb + 4 * q < d) t = *reinterpret_cast<const f32x4*>(xrow + fb + 4 * q);
+            xv[4 * q + 0] = t.x;
+            xv[4 * q + 1] = t.y;
+            xv[4 * q + 2] = t.z;
+            xv[4 * q + 3] = t.w;
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) xv[q] = (vpt && fb + q < d) ? xrow[fb + q] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+          for (int m = 0; m < 2; ++m) {
+            const f32x4 a =
+                *reinterpret_cast<const f32x4*>(theta + ((((int64_t)ch * 4 + j) * NBt + cg + m) * 64 + lane) * 4);
+            acc[m] = mfma32x32x2(a.x, xv[4 * j + 0], acc[m]);
+            acc[m] = mfma32x32x2(a.y, xv[4 * j + 1], acc[m]);
+            acc[m] = mfma32x32x2(a.z, xv[4 * j + 2], acc[m]);
+            acc[m] = mfma32x32x2(a.w, xv[4 * j + 3], acc[m]);
+          }
+        }
+      }
+      // ---- epilogue of the pair: lane holds row pt, columns 32 (cg + m) + 8 qd + 4 h + e ----
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        float wv[16];
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const int c = 32 * (cg + m) + 8 * qd + 4 * h;
+          float u4[4];
+          load_u4(c, u4);
+          const f32x4 pv = *reinterpret_cast<const f32x4*>(ps + c);
+          const f32x4 sv = *reinterpret_cast<const f32x4*>(ss + c);
+          const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+          const float se[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float uu = u4[e];
+            float t = fmaf(two_alpha, acc[m][4 * qd + e], uu);
+            t = fmaf(neg_alpha, ybar * pe[e], t);
+            t = fmaf(neg_alpha, se[e], t);
+            float w = fmaxf(t, 0.f);
+            if (!vpt || c + e >= r) w = 0.f;
+            wv[4 * qd + e] = w;
+            const double wd = (double)w, ud = (double)uu;
+            sa = fma(wd, wd, sa);
+            sb = fma(ud, ud, sb);
+            sh = fma(wd, ud, sh);
+          }
+          if (vpt) {
+            if (VEC) {
+              if (c < r) {
+                f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
+                *reinterpret_cast<f32x4*>(urow + c) = o;
+              }
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (c + e < r) urow[c + e] = wv[4 * qd + e];
+            }
+          }
+        }
+        reduce_scatter<16, 16>(wv, li);
+        double v = (double)wv[0];
+        v += shfl_xor_d(v, 1);
+        if ((li & 1) == 0) colred[wave * r32 + 32 * (cg + m) + 8 * (base >> 2) + 4 * h + (base & 3)] += v;
+      }
+    }
+  }
+
+  // ---- workgroup partials ----
+  __syncthreads();
+  double* out = B.b_part + (int64_t)blockIdx.x * (4 + r32);
+  for (int c = tid; c < r32; c += kThreads)
+    out[4 + c] = ((colred[c] + colred[r32 + c]) + colred[2 * r32 + c]) + colred[3 * r32 + c];
+  const double ta = block_sum_d(sa, dred);
+  const double tb2 = block_sum_d(sb, dred);
+  const double th = block_sum_d(sh, dred);
+  if (tid == 0) {
+    out[0] = ta;
+    out[1] = tb2;
+    out[2] = th;
+    out[3] = 0.0;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Pass B, resident-tile form (d <= 128, r <= 128, 16-byte rows).  Same
 // arithmetic and partial layout as k_pass_b; each wave holds its tile's whole
 // Xhat slab (NCH chunks) and U slab in registers: the U loads of a tile are
@@ -1626,6 +1820,22 @@ hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hi
       case 44: return pass_b_res_launch<4, 4>(g, b, a, st);
       default: return hipErrorInvalidValue;
     }
+  }
+  if (g.NB > 8) {
+    // more than 256 columns, in pairs of column blocks
+    if (g.NB % 2 != 0 || g.NB > kMaxR / 32) return hipErrorInvalidValue;
+    const size_t lds = g.ldsB_bytes;
+    if (lds > (64u << 10)) return hipErrorInvalidValue;
+    const dim3 grid(g.GB), blk(kThreads);
+    const bool vec = g.vec_x && g.vec_u;
+    if (g.theta_lds) {
+      if (vec) hipLaunchKernelGGL((k_pass_b_wide<true, true>), grid, blk, lds, st, g, b, a);
+      else hipLaunchKernelGGL((k_pass_b_wide<true, false>), grid, blk, lds, st, g, b, a);
+    } else {
+      if (vec) hipLaunchKernelGGL((k_pass_b_wide<false, true>), grid, blk, lds, st, g, b, a);
+      else hipLaunchKernelGGL((k_pass_b_wide<false, false>), grid, blk, lds, st, g, b, a);
+    }
+    return hipGetLastError();
   }
   switch (g.NB) {
     case 1: return pass_b_nb<1>(g, b, a, st);

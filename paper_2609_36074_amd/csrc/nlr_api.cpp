@@ -32,11 +32,13 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   g.K = K;
   g.d32 = round_up(d, 32);
   g.MB = g.d32 / 32;
-  g.NB = next_pow2((r + 31) / 32);  // 1, 2, 4 or 8 column blocks
+  // 1, 2, 4 or 8 column blocks; above 256 columns an even number (10, 12, 14), which
+  // the two-pass kernels take in groups of two blocks
+  g.NB = r <= 256 ? next_pow2((r + 31) / 32) : 2 * ((r + 63) / 64);
   g.r32 = 32 * g.NB;
-  // pass A groups: MBG in {1, 2, 4}, NBG in {1, 2, 4}
+  // pass A groups: MBG in {1, 2, 4}, NBG in {1, 2, 4} dividing NB
   g.MBG = g.MB >= 3 ? 4 : g.MB;
-  g.NBG = g.NB >= 4 ? 4 : g.NB;
+  g.NBG = g.NB % 4 == 0 ? 4 : (g.NB % 2 == 0 ? 2 : 1);
   g.mgroups = (g.MB + g.MBG - 1) / g.MBG;
   g.ngroups = (g.NB + g.NBG - 1) / g.NBG;
   g.tilesA = (n + kTPA - 1) / kTPA;
@@ -147,7 +149,7 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   g.GAF = g.a_rows ? g.GA : (int32_t)(g.tilesA < 1024 ? g.tilesA : 1024);
   // split-fp16 panel form: the shapes the single-pass and resident kernels do not take
   g.panel = 0;
-  if (split && !g.fused && !g.split_b && aligned16 && d % 8 == 0 && r % 4 == 0 && r <= kMaxR) {
+  if (split && !g.fused && !g.split_b && aligned16 && d % 8 == 0 && r % 4 == 0 && r <= kMaxPanelR) {
     g.panel = 1;
     g.pnbw = g.NB >= 2 ? g.NB / 2 : 1;
     g.pfb = (d + 255) / 256;
@@ -328,6 +330,13 @@ struct nlr_ctx {
   size_t ev_used;
   double prof_ms[KK_COUNT];
   int64_t prof_n[KK_COUNT];
+  // nlr_run replays the iterations after a call's first one as captured graphs (one
+  // and eight iterations) while profiling is off: one submission instead of a launch
+  // per kernel.  Captured on a private stream when first needed, dropped when the
+  // step arguments change.
+  bool graphs_allowed;  // false for the allocation-free entry point (instantiation allocates)
+  hipStream_t cap_stream;
+  hipGraphExec_t graph1, graph8;
 };
 
 static nlr_status hip_fail(nlr_ctx* c) {
@@ -489,6 +498,65 @@ static nlr_status enqueue_iteration(nlr_ctx* c, bool first) {
   return NLR_OK;
 }
 
+static void drop_graphs(nlr_ctx* c) {
+  if (c->graph1) (void)hipGraphExecDestroy(c->graph1);
+  if (c->graph8) (void)hipGraphExecDestroy(c->graph8);
+  c->graph1 = c->graph8 = nullptr;
+}
+
+// Captures `iters` iterations that follow the first of a host call (their step
+// arguments are fixed: the end-of-iteration work of the previous one is pending) as an
+// executable graph.  The kernels read the device control block when they run, so a
+// replay behaves as the same launches made one by one.  No memset is recorded.
+static hipError_t capture_iterations(nlr_ctx* c, int iters, hipGraphExec_t* out) {
+  *out = nullptr;
+  hipError_t e = hipSuccess;
+  if (!c->cap_stream) {
+    e = hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+  }
+  const hipStream_t user = c->stream;
+  c->stream = c->cap_stream;
+  e = hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeRelaxed);
+  if (e != hipSuccess) {
+    c->stream = user;
+    return e;
+  }
+  nlr_status s = NLR_OK;
+  for (int k = 0; k < iters && s == NLR_OK; ++k) s = enqueue_iteration(c, false);
+  hipGraph_t graph = nullptr;
+  e = hipStreamEndCapture(c->cap_stream, &graph);
+  c->stream = user;
+  if (s != NLR_OK && e == hipSuccess) e = hipErrorUnknown;
+  if (e == hipSuccess) e = hipGraphInstantiate(out, graph, nullptr, nullptr, 0);
+  if (graph) (void)hipGraphDestroy(graph);
+  return e;
+}
+
+// Enqueues `nb` iterations that follow the first of the call: as graph replays when
+// allowed and profiling is off (the events of profiling are per launch), else one by one.
+static nlr_status enqueue_steady(nlr_ctx* c, int nb) {
+  if (c->graphs_allowed && !c->prof) {
+    if (!c->graph1 || !c->graph8) {
+      drop_graphs(c);
+      if (capture_iterations(c, 1, &c->graph1) != hipSuccess || capture_iterations(c, 8, &c->graph8) != hipSuccess) {
+        drop_graphs(c);
+        return hip_fail(c);
+      }
+    }
+    for (; nb >= 8; nb -= 8)
+      if (hipGraphLaunch(c->graph8, c->stream) != hipSuccess) return hip_fail(c);
+    for (; nb > 0; --nb)
+      if (hipGraphLaunch(c->graph1, c->stream) != hipSuccess) return hip_fail(c);
+    return NLR_OK;
+  }
+  for (; nb > 0; --nb) {
+    const nlr_status s = enqueue_iteration(c, false);
+    if (s != NLR_OK) return s;
+  }
+  return NLR_OK;
+}
+
 static nlr_status enqueue_finish(nlr_ctx* c) {
   const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
   LAUNCH(KK_FINISH, launch_pass_a(c->g, c->b, a, true, c->stream));
@@ -592,6 +660,8 @@ static nlr_status init_ctx(nlr_ctx* c, const Geometry& g0, float* X, int32_t K, 
     c->prof_ms[k] = 0.0;
     c->prof_n[k] = 0;
   }
+  c->cap_stream = nullptr;
+  c->graph1 = c->graph8 = nullptr;
   if (hipGetDevice(&c->device) != hipSuccess) return NLR_EHIP;
   const Geometry& g = c->g;
   const Bufs& b = c->b;
@@ -639,13 +709,23 @@ static nlr_status run_iterations(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr
     if (read_ctl(c) != NLR_OK) return NLR_EHIP;
   const int64_t t0 = c->t_host;
   if (launch_clear_stop(c->b, c->stream) != hipSuccess) return hip_fail(c);
-  for (int32_t k = 0; k < T; ++k) {
+  // the stop flag is polled every 32 iterations; kernels after a stop return at entry
+  for (int32_t k = 0; k < T;) {
     if (k > 0 && (k % 32) == 0) {
       if (read_ctl(c) != NLR_OK) return NLR_EHIP;
       if (c->host_ctl->stop || c->host_ctl->breakdown) break;
     }
-    nlr_status s = enqueue_iteration(c, k == 0);
+    if (k == 0) {
+      nlr_status s = enqueue_iteration(c, true);
+      if (s != NLR_OK) return s;
+      ++k;
+      continue;
+    }
+    const int32_t to_poll = 32 - (k % 32);
+    const int32_t nb = (T - k) < to_poll ? (T - k) : to_poll;
+    nlr_status s = enqueue_steady(c, nb);
     if (s != NLR_OK) return s;
+    k += nb;
   }
   nlr_status s = enqueue_finish(c);
   if (s != NLR_OK) return s;
@@ -712,6 +792,7 @@ nlr_status nlr_init(nlr_ctx** ctx, float* X, int64_t n, int32_t d, int32_t K, in
   if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need) return NLR_EWORKSPACE;
   nlr_ctx* c = new (std::nothrow) nlr_ctx();
   if (!c) return NLR_EHIP;
+  c->graphs_allowed = true;
   if (hipHostMalloc(reinterpret_cast<void**>(&c->host_ctl), sizeof(DevCtl), hipHostMallocDefault) != hipSuccess) {
     delete c;
     return NLR_EHIP;
@@ -739,6 +820,7 @@ nlr_status nlr_solve_static(float* X, int64_t n, int32_t d, int32_t K, int32_t r
   // the context lives on this stack frame; the control-block mirror is ordinary host
   // memory (no pinned allocation); profiling stays off, so no events are created
   nlr_ctx c;
+  c.graphs_allowed = false;  // graph instantiation allocates
   DevCtl mirror;
   std::memset(&mirror, 0, sizeof(mirror));
   c.host_ctl = &mirror;
@@ -751,6 +833,7 @@ nlr_status nlr_set_params(nlr_ctx* c, const nlr_params* params) {
   if (!c || !params_ok(params)) return NLR_EINVAL;
   if (c->failed) return NLR_ESTATE;
   c->prm = *params;
+  drop_graphs(c);  // their kernels carry the old step arguments
   return NLR_OK;
 }
 
@@ -923,6 +1006,8 @@ nlr_status nlr_kernel_times(nlr_ctx* c, const char** names, double* total_ms, in
 
 void nlr_destroy(nlr_ctx* c) {
   if (!c) return;
+  drop_graphs(c);
+  if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
   for (auto e : c->ev_pool) (void)hipEventDestroy(e);
   if (c->host_ctl) (void)hipHostFree(c->host_ctl);
   delete c;

@@ -14,7 +14,8 @@ constexpr int kThreads = 256;     // every kernel uses 256-thread workgroups (4 
 constexpr int kHistCap = 4096;    // per-iteration record ring
 constexpr int kTPA = 64;          // rows per pass-A tile
 constexpr int kTPB = 128;         // rows per pass-B super-tile (4 waves x 32 rows)
-constexpr int kMaxR = 256;        // largest supported rank
+constexpr int kMaxR = 448;        // largest supported rank (fp32 two-pass form above 256)
+constexpr int kMaxPanelR = 256;   // largest rank of the split-fp16 panel form
 constexpr int kPowerIters = 16;   // refinement power iterations after the squaring phase
 constexpr int kSquarings = 20;    // C -> C^(2^20) before the refinement
 

@@ -213,7 +213,7 @@ class Context:
         self.n, self.d, self.r, self.K = int(n), int(d), int(r), int(K)
         ws = int(lib.nlr_workspace_bytes(n, d, r))
         if ws == 0:
-            raise NlrError(NLR_EUNSUPPORTED if r > 256 else NLR_EINVAL, "nlr_workspace_bytes")
+            raise NlrError(NLR_EUNSUPPORTED if r > 448 else NLR_EINVAL, "nlr_workspace_bytes")
         self.workspace = torch.empty(ws + 256, dtype=torch.uint8, device=X.device)
         base = self.workspace.data_ptr()
         self._ws_ptr = (base + 255) & ~255

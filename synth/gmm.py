@@ -44,6 +44,7 @@ class Workload:
     l2_normalise: bool = False    # rows scaled to unit L2 norm after sampling
     seed: int = 0
     extra: dict = field(default_factory=dict)
+    gamma: float | None = None    # set: centres scaled to min separation gamma * CNRbar (Table 2)
 
 
 # The five shapes.  Seeds: data seed 0; the U_0 draw uses seed + 1.
@@ -56,6 +57,23 @@ WORKLOADS = {
                         sizes="zipf1.1", noise="aniso", l2_normalise=True),
 }
 WORKLOAD_ORDER = ["tiny", "gmm1m", "gmm10m", "gmm50m", "embed2m"]
+
+# The two smallest Table 2 settings (balanced mixture, minimum centre separation
+# gamma * CNRbar with gamma = 1, unit noise): shapes for parity and timing beside
+# the five above.
+TABLE2 = {
+    "t2k20": Workload("t2k20", 1_000_000, 50, 20, 30, 100, 1.0, gamma=1.0),
+    "t2k100": Workload("t2k100", 1_000_000, 200, 100, 300, 100, 1.0, gamma=1.0),
+}
+WORKLOADS.update(TABLE2)
+
+
+def cnr_bar(n: int, K: int, d: int) -> float:
+    """CNRbar = sqrt(4 (1 + sqrt(1 + K d / (n log n))) log n): the exact-recovery
+    threshold on the centroid-to-noise ratio (Section 2), the separation scale of
+    the paper's simulated mixtures (Section 5, Table 2).  A generator parameter."""
+    ln = np.log(n)
+    return float(np.sqrt(4.0 * (1.0 + np.sqrt(1.0 + K * d / (n * ln))) * ln))
 
 
 def _threads() -> int:
@@ -123,10 +141,13 @@ def _fill_chunks(out: np.ndarray, seed_seq: np.random.SeedSequence, fill, thread
 
 def gaussian_mixture(n: int, d: int, K: int, center_var: float, *, sizes: str = "equal",
                      noise: str = "iso", l2_normalise: bool = False, seed: int = 0,
-                     threads: int | None = None, rows: int | None = None):
+                     threads: int | None = None, rows: int | None = None,
+                     min_separation: float | None = None):
     """Draw (X float32 [m, d], labels int32 [m], centers float64 [K, d]), m = n or `rows`.
 
-    Centers mu_k ~ N(0, center_var * I_d).  Noise eps_i ~ N(0, I_d) ("iso") or
+    Centers mu_k ~ N(0, center_var * I_d); with ``min_separation`` = Delta (and
+    K >= 2) the same draw is then scaled so that min_{k != l} ||mu_k - mu_l|| =
+    Delta.  Noise eps_i ~ N(0, I_d) ("iso") or
     N(0, diag(v_{z_i})) with v_k ~ U[0.2, 2]^d ("aniso").  Labels are a
     shuffled assignment with the requested cluster sizes over all n rows.
     With ``rows = m < n`` only the first m rows of the n-row draw are made:
@@ -137,6 +158,11 @@ def gaussian_mixture(n: int, d: int, K: int, center_var: float, *, sizes: str = 
     s_meta, s_noise = root.spawn(2)
     meta = np.random.Generator(np.random.PCG64(s_meta))
     centers = meta.standard_normal((K, d)) * np.sqrt(center_var)
+    if min_separation is not None and K >= 2:
+        diff = centers[:, None, :] - centers[None, :, :]
+        dist = np.sqrt(np.einsum("kld,kld->kl", diff, diff))
+        dist[np.arange(K), np.arange(K)] = np.inf
+        centers = centers * (float(min_separation) / dist.min())
     sz = cluster_sizes(n, K, sizes, meta)
     labels = np.repeat(np.arange(K, dtype=np.int32), sz)
     meta.shuffle(labels)
@@ -197,8 +223,9 @@ def make_workload(name_or_wl, n: int | None = None, threads: int | None = None,
     """
     wl = WORKLOADS[name_or_wl] if isinstance(name_or_wl, str) else name_or_wl
     nn = wl.n if n is None else int(n)
+    sep = None if wl.gamma is None else wl.gamma * cnr_bar(nn, wl.K, wl.d)
     X, labels, _ = gaussian_mixture(nn, wl.d, wl.K, wl.center_var, sizes=wl.sizes,
                                     noise=wl.noise, l2_normalise=wl.l2_normalise,
-                                    seed=wl.seed, threads=threads, rows=rows)
+                                    seed=wl.seed, threads=threads, rows=rows, min_separation=sep)
     Z = standard_normal_factor(X.shape[0], wl.r, wl.seed + 1, threads=threads)
     return X, Z, labels, wl

@@ -40,7 +40,7 @@ int main(void) {
   const int64_t ns[] = {1, 2, 3, 255, 256, 257, 1000, 10000000, (int64_t)1 << 31, ((int64_t)1 << 40) - 1,
                         (int64_t)1 << 40, INT64_MAX / 2, INT64_MAX, 0, -1, INT64_MIN};
   const int32_t ds[] = {1, 3, 4, 13, 16, 64, 65, 100, 128, 129, 256, 768, 4096, 4097, 0, -1, INT32_MAX, INT32_MIN};
-  const int32_t rs[] = {1, 2, 4, 10, 16, 33, 64, 65, 128, 256, 257, 0, -1, INT32_MAX, INT32_MIN};
+  const int32_t rs[] = {1, 2, 4, 10, 16, 33, 64, 65, 128, 256, 257, 300, 448, 449, 0, -1, INT32_MAX, INT32_MIN};
   for (size_t a = 0; a < sizeof(ns) / sizeof(ns[0]); ++a)
     for (size_t b = 0; b < sizeof(ds) / sizeof(ds[0]); ++b)
       for (size_t c = 0; c < sizeof(rs) / sizeof(rs[0]); ++c) {
@@ -48,7 +48,7 @@ int main(void) {
         const int32_t d = ds[b], r = rs[c];
         const size_t w = nlr_workspace_bytes(n, d, r);
         CHECK(w == nlr_workspace_bytes(n, d, r));
-        const int valid = n >= 1 && n < ((int64_t)1 << 40) && d >= 1 && d <= 4096 && r >= 1 && r <= 256 && r <= n;
+        const int valid = n >= 1 && n < ((int64_t)1 << 40) && d >= 1 && d <= 4096 && r >= 1 && r <= 448 && r <= n;
         if (!valid) CHECK(w == 0);
         else CHECK(w > 0 && w < ((size_t)1 << 60));
       }
@@ -72,7 +72,7 @@ int main(void) {
   CHECK(init(X, INT64_MIN, 16, 4, 4, U, y, &ok, 0, FAKE, wsb, NULL) == NLR_EINVAL);
   CHECK(init(X, 1000, INT32_MAX, 4, 4, U, y, &ok, 0, FAKE, wsb, NULL) == NLR_EINVAL);
   CHECK(init(X, 1000, 16, INT32_MAX, INT32_MAX, U, y, &ok, 0, FAKE, wsb, NULL) == NLR_EINVAL);
-  CHECK(init(X, 1000, 16, 4, 300, U, y, &ok, 0, FAKE, wsb, NULL) == NLR_EUNSUPPORTED);
+  CHECK(init(X, 1000, 16, 4, 449, U, y, &ok, 0, FAKE, wsb, NULL) == NLR_EUNSUPPORTED);
   const nlr_params bad[] = {{0.0, 1.0, 1e-4, 1e-4, 0, 0}, {INFINITY, 1.0, 1e-4, 1e-4, 0, 0},
                             {NAN, 1.0, 1e-4, 1e-4, 0, 0},  {0.1, -1.0, 1e-4, 1e-4, 0, 0},
                             {0.1, 1.0, -1.0, 1e-4, 0, 0},  {0.1, 1.0, 1e-4, NAN, 0, 0},
@@ -121,7 +121,7 @@ int main(void) {
   CHECK(nlr_solve_static(X, 1000, 16, 4, 4, U, y, NULL, 0, 5, &done, &st, NULL) == NLR_EINVAL);
   CHECK(nlr_solve_static(X, 1000, 16, 5, 4, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EINVAL);
   CHECK(nlr_solve_static(X, INT64_MAX, 16, 4, 4, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EINVAL);
-  CHECK(nlr_solve_static(X, 1000, 16, 4, 300, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EUNSUPPORTED);
+  CHECK(nlr_solve_static(X, 1000, 16, 4, 449, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EUNSUPPORTED);
   CHECK(nlr_solve_static(X, 1000, 16, 4, 4, U, y, &ok, 1u << 7, 5, NULL, NULL, NULL) == NLR_EINVAL);
   CHECK(nlr_workspace_bytes(2000000, 768, 256) > NLR_STATIC_SCRATCH_BYTES);
   CHECK(nlr_solve_static(X, 2000000, 768, 256, 256, U, y, &ok, 0, 5, NULL, NULL, NULL) == NLR_EWORKSPACE);

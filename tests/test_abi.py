@@ -56,7 +56,8 @@ def test_workspace_bytes(lib):
     assert nlr.nlr_workspace_bytes(100, 0, 4) == 0      # d < 1
     assert nlr.nlr_workspace_bytes(100, 16, 0) == 0     # r < 1
     assert nlr.nlr_workspace_bytes(3, 16, 4) == 0       # r > n
-    assert nlr.nlr_workspace_bytes(1000, 16, 257) == 0  # r above the kernel family
+    assert nlr.nlr_workspace_bytes(1000, 16, 449) == 0  # r above the kernel family
+    assert nlr.nlr_workspace_bytes(1000, 16, 448) > 0 and nlr.nlr_workspace_bytes(1000, 200, 300) > 0
     assert nlr.nlr_workspace_bytes(1000, 4097, 4) == 0  # d above the limit
 
 
@@ -67,7 +68,7 @@ def _init(lib, X=FAKE, n=1000, d=16, K=4, r=4, U=FAKE, y=FAKE, params=None, flag
     if params is None:
         params = nlr.NlrParams(0.01, 1.0, 1e-4, 1e-4, 0, 0)
     if ws_bytes is None:
-        ws_bytes = nlr.nlr_workspace_bytes(n, d, r) if r <= 256 else 1 << 30
+        ws_bytes = nlr.nlr_workspace_bytes(n, d, r) if r <= 448 else 1 << 30
     ctx = ctypes.c_void_p(123)
     st = lib.nlr_init(ctypes.byref(ctx), X, n, d, K, r, U, y, ctypes.byref(params), flags, ws, ws_bytes, None)
     return st, ctx
@@ -82,7 +83,7 @@ def test_init_argument_errors(lib):
     assert _init(lib, K=5, r=4)[0] == nlr.NLR_EINVAL            # K > r
     assert _init(lib, n=3, r=4, K=2)[0] == nlr.NLR_EINVAL       # r > n
     assert _init(lib, d=0)[0] == nlr.NLR_EINVAL
-    assert _init(lib, r=300, K=4)[0] == nlr.NLR_EUNSUPPORTED
+    assert _init(lib, r=449, K=4, n=3000)[0] == nlr.NLR_EUNSUPPORTED
     assert _init(lib, params=P(0.0, 1.0, 1e-4, 1e-4, 0, 0))[0] == nlr.NLR_EINVAL      # alpha <= 0
     assert _init(lib, params=P(float("inf"), 1.0, 1e-4, 1e-4, 0, 0))[0] == nlr.NLR_EINVAL
     assert _init(lib, params=P(0.1, -1.0, 1e-4, 1e-4, 0, 0))[0] == nlr.NLR_EINVAL     # beta <= 0
@@ -145,6 +146,6 @@ def test_solve_static_rejects_before_any_hip_call(lib):
     assert st == nlr.NLR_EWORKSPACE and done == 0
     assert nlr.nlr_solve_static(FAKE, 1000, 16, 4, 4, FAKE, FAKE, p, 0, -1)[0] == nlr.NLR_EINVAL
     assert nlr.nlr_solve_static(0, 1000, 16, 4, 4, FAKE, FAKE, p, 0, 5)[0] == nlr.NLR_EINVAL
-    assert nlr.nlr_solve_static(FAKE, 1000, 16, 4, 300, FAKE, FAKE, p, 0, 5)[0] == nlr.NLR_EUNSUPPORTED
+    assert nlr.nlr_solve_static(FAKE, 1000, 16, 4, 449, FAKE, FAKE, p, 0, 5)[0] == nlr.NLR_EUNSUPPORTED
     assert nlr.nlr_solve_static(FAKE, 1000, 16, 8, 16, FAKE + 4, FAKE, p, nlr.NLR_INIT_SPLIT_F16, 5)[0] == \
         nlr.NLR_EUNSUPPORTED

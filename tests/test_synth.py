@@ -55,3 +55,24 @@ def test_rows_is_a_true_prefix_of_the_full_draw():
         assert np.array_equal(a[:m], b)
     other = make_workload("gmm1m", n=m)
     assert not np.array_equal(other[0], pre[0])
+
+
+def test_table2_workloads_separation():
+    """The Table 2 stand-ins: balanced mixtures whose closest pair of centres sits at
+    gamma * CNRbar (gamma = 1); CNRbar agrees with the oracle's exact-recovery threshold
+    (Section 2), written there independently."""
+    from oracle import kmeans
+    from synth import TABLE2, cnr_bar
+    for name, (n, d, K, r) in {"t2k20": (1_000_000, 50, 20, 30), "t2k100": (1_000_000, 200, 100, 300)}.items():
+        wl = TABLE2[name]
+        assert (wl.n, wl.d, wl.K, wl.r, wl.sizes) == (n, d, K, r, "equal")
+        assert abs(cnr_bar(n, K, d) ** 2 / kmeans.exact_recovery_threshold_sq(n, K, d) - 1.0) < 1e-12
+        X, lab, C = gaussian_mixture(n, d, K, 1.0, seed=0, rows=20_000, min_separation=cnr_bar(n, K, d))
+        dist = np.sqrt(((C[:, None, :] - C[None, :, :]) ** 2).sum(-1)) + np.diag([np.inf] * K)
+        assert abs(dist.min() / cnr_bar(n, K, d) - 1.0) < 1e-12
+        # unit within-cluster noise; the prefix is a true prefix of the make_workload draw
+        k0 = lab[0]
+        R = X[lab == k0] - C[k0]
+        assert abs(R.var() - 1.0) < 0.05
+        Xw, Zw, lw, _ = make_workload(name, rows=2000)
+        assert np.array_equal(Xw, X[:2000]) and np.array_equal(lw, lab[:2000]) and Zw.shape == (2000, r)
