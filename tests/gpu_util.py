@@ -3,6 +3,7 @@ binding, run the fp64 oracle on the same seeded inputs, compare."""
 from __future__ import annotations
 
 import sys
+import time
 
 import numpy as np
 
@@ -12,8 +13,11 @@ U_TOL = 1e-4     # max_ij |U_gpu - U_ref| / max_ij |U_ref| per iteration
 OBJ_TOL = 1e-5   # relative error of the objective
 
 
+_T0 = time.time()
+
+
 def log(msg: str) -> None:
-    print(msg, flush=True)
+    print(f"[{time.time() - _T0:7.1f}s] {msg}", flush=True)
     sys.stdout.flush()
 
 
@@ -131,3 +135,136 @@ def lockstep(ctx, Xh, U0, K, alpha, beta, T, eps_d, t0=0):
             f"gate {int(gate)}")
     out["U_ref"], out["U_gpu"] = U_ref, U_prev
     return out
+
+
+# ---------------------------------------------------------------- full-size lockstep in parallel
+# The GPU's iterates of a full-size run are saved first (float32, as read back); then one
+# worker process runs the oracle's trajectory from U_0 (the GPU's gate decisions
+# replayed) and the others run one oracle step from each saved GPU iterate.  The oracle
+# steps of a worker run one after another (BLAS in several threads of one process has
+# returned wrong products here); the workers are spawned processes that never touch
+# the GPU and read Xhat and the iterates from files mapped into memory.
+
+def _scratch_dir(need_bytes: int) -> str:
+    import shutil
+    import tempfile
+    for base in ("/dev/shm", tempfile.gettempdir()):
+        try:
+            if shutil.disk_usage(base).free > 1.5 * need_bytes:
+                return tempfile.mkdtemp(prefix="nlr_lock_", dir=base)
+        except OSError:
+            continue
+    raise RuntimeError(f"no scratch space for {need_bytes / 2**30:.1f} GiB of iterates")
+
+
+def _load(path: str, dtype=np.float64) -> np.ndarray:
+    return np.asarray(np.load(path, mmap_mode="r"), dtype=dtype)
+
+
+def _blas_threads(threads):
+    import threadpoolctl
+    return threadpoolctl.threadpool_limits(threads)
+
+
+def _traj_task(d, K, alpha, beta, gates, eps_d, sources, threads):
+    """Oracle trajectory from U_0 with the gates given; per iteration the relative error
+    against each source's saved iterate, the objective and the movement; and the label
+    agreement of each source's labels with the trajectory at the source's last iteration."""
+    _blas_threads(threads)
+    Xh = np.load(f"{d}/Xh.npy", mmap_mode="r")
+    U = _load(f"{d}/U0.npy")
+    y = np.zeros(U.shape[0])
+    out = {"err": {s: [] for s, _ in sources}, "obj": [], "delta": [], "labels": {}}
+    for t, gate in enumerate(gates):
+        r = onlr.run(Xh, U, K, alpha, beta, T=1, T_min=1, project_init=False, y0=y, gates=[gate], t0=t)
+        U, y = r.U, r.y
+        out["obj"].append(r.records[0].objective)
+        out["delta"].append(r.records[0].delta)
+        for s, T_s in sources:
+            if t < T_s:
+                out["err"][s].append(rel_max_err(_load(f"{d}/{s}_U{t + 1}.npy"), U))
+            if t + 1 == T_s:  # the source's labels were taken after its last iteration
+                out["labels"][s] = label_agreement(np.load(f"{d}/{s}_labels.npy"), U)
+        del r
+        log(f"    oracle trajectory: iteration {t} done")
+    return out
+
+
+def _one_task(d, K, alpha, beta, src, t, gate, threads):
+    """One oracle step from a source's saved iterate t; (U error, stored-dual error) at t+1."""
+    _blas_threads(threads)
+    Xh = np.load(f"{d}/Xh.npy", mmap_mode="r")
+    U_t, y_t = _load(f"{d}/{src}_U{t}.npy"), _load(f"{d}/{src}_y{t}.npy")
+    o = onlr.run(Xh, U_t, K, alpha, beta, T=1, T_min=1, project_init=False,
+                 y0=onlr.dual_from_stored(y_t), gates=[gate], t0=t)
+    del U_t
+    err = rel_max_err(_load(f"{d}/{src}_U{t + 1}.npy"), o.U)
+    ys = onlr.stored_dual(o.y)
+    y1 = _load(f"{d}/{src}_y{t + 1}.npy")
+    ymax = float(np.abs(ys).max())
+    yerr = float(np.abs(y1 - ys).max()) / ymax if ymax > 0 else float(np.abs(y1).max())
+    log(f"    oracle step from {src} iterate {t} done")
+    return src, t, err, yerr
+
+
+def lockstep_parallel(runs, Xh, U0, K, alpha, beta, eps_d, workers=3):
+    """runs: {name: (ctx, T)}, contexts started from the same Xhat and U0 = Pi_Omega(Z).
+    Steps each context T times (one host call per iteration) saving every iterate, then
+    checks them against the oracle as ``lockstep`` does, in `workers` processes:
+    traj, one, yerr, obj and bad_gates per run, and the label agreement after its last step."""
+    import multiprocessing as mp
+    import shutil
+    from concurrent.futures import ProcessPoolExecutor
+
+    n, r = U0.shape
+    need = Xh.nbytes + U0.nbytes + sum((T + 1) * (n * r * 4 + n * 4) for _, T in runs.values())
+    d = _scratch_dir(need)
+    try:
+        np.save(f"{d}/Xh.npy", Xh)
+        np.save(f"{d}/U0.npy", U0)
+        res = {}
+        for s, (ctx, T) in runs.items():
+            np.save(f"{d}/{s}_U0.npy", ctx.U.detach().cpu().numpy())
+            np.save(f"{d}/{s}_y0.npy", ctx.y.detach().cpu().numpy())
+            stats = []
+            for t in range(T):
+                stats.append(ctx.step())
+                np.save(f"{d}/{s}_U{t + 1}.npy", ctx.U.detach().cpu().numpy())
+                np.save(f"{d}/{s}_y{t + 1}.npy", ctx.y.detach().cpu().numpy())
+            np.save(f"{d}/{s}_labels.npy", ctx.labels().cpu().numpy())
+            res[s] = {"stats": stats, "gates": [bool(x["dual_step"]) for x in stats]}
+            log(f"  {s}: {T} GPU iterations saved")
+        # one trajectory per gate sequence: a run whose gates are a prefix of an earlier
+        # run's shares that run's trajectory
+        groups = []  # (gates, [(source, T)])
+        for s, (_, T) in runs.items():
+            g = res[s]["gates"]
+            for gg, members in groups:
+                if gg[:len(g)] == g:
+                    members.append((s, T))
+                    break
+            else:
+                groups.append((g, [(s, T)]))
+        # BLAS threads per worker: the box's share of cores (16) split between the workers
+        threads = max(1, 16 // workers)
+        with ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn")) as ex:
+            fts = [ex.submit(_traj_task, d, K, alpha, beta, gg, eps_d, members, threads) for gg, members in groups]
+            fo = [ex.submit(_one_task, d, K, alpha, beta, s, t, res[s]["gates"][t], threads)
+                  for s, (_, T) in runs.items() for t in range(T)]
+            ones = [f.result() for f in fo]
+            trs = [f.result() for f in fts]
+        for s, (_, T) in runs.items():
+            tr = next(x for x, (_, members) in zip(trs, groups) if any(m == s for m, _ in members))
+            o = sorted([x for x in ones if x[0] == s], key=lambda x: x[1])
+            st = res[s]["stats"]
+            res[s].update(traj=tr["err"][s], one=[x[2] for x in o], yerr=[x[3] for x in o],
+                          obj=[obj_rel_err(st[t]["objective"], tr["obj"][t], 1.0) for t in range(T)],
+                          bad_gates=[t for t in range(T) if res[s]["gates"][t] != (tr["delta"][t] < eps_d)
+                                     and abs(tr["delta"][t] - eps_d) > 1e-3 * eps_d],
+                          labels=tr["labels"][s])
+            for t in range(T):
+                log(f"  {s} t={t}: traj {res[s]['traj'][t]:.2e} one {res[s]['one'][t]:.2e} "
+                    f"obj {res[s]['obj'][t]:.2e} y {res[s]['yerr'][t]:.2e} gate {int(res[s]['gates'][t])}")
+        return res
+    finally:
+        shutil.rmtree(d, ignore_errors=True)

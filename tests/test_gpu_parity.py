@@ -11,7 +11,7 @@ within 1e-3 relative of eps_d).
 import numpy as np
 import pytest
 
-from gpu_util import (OBJ_TOL, U_TOL, host, label_agreement, lockstep, log, make_ctx, obj_rel_err,
+from gpu_util import (OBJ_TOL, U_TOL, host, label_agreement, lockstep_parallel, log, make_ctx, obj_rel_err,
                       rel_max_err, trajectory)
 from oracle import nlr as onlr
 from synth import gaussian_mixture, make_workload, standard_normal_factor
@@ -178,20 +178,24 @@ def test_ragged_shapes(n, d, r, K):
 
 
 def test_gmm1m_parity():
-    """gmm1m over its configuration's 100 iterations with fp32 products, each iterate against
+    """gmm1m over its configuration's 100 iterations with split products (the bench's
+    single-Xhat-pass form) and with fp32 products, from the same start: each iterate against
     the oracle's trajectory and one oracle step from the GPU's own iterate."""
     X, Z, lab, wl = make_workload("gmm1m")
     K, alpha = wl.K, onlr.default_step_size(wl.K)
-    log(f"gmm1m lockstep T={wl.T}")
-    ctx = make_ctx(X, Z, K, alpha, 1.0, T_min=wl.T)
+    log(f"gmm1m lockstep T={wl.T}, split and fp32 products")
+    runs = {"split16": (make_ctx(X, Z, K, alpha, 1.0, T_min=wl.T, flags=8), wl.T),
+            "fp32": (make_ctx(X, Z, K, alpha, 1.0, T_min=wl.T), wl.T)}
     Xh, _, _ = onlr.centre_and_normalise(X)
-    res = lockstep(ctx, Xh, onlr.project_omega(Z.astype(np.float64), K), K, alpha, 1.0, wl.T, 1e-4)
-    log(f"  traj {max(res['traj']):.2e} one {max(res['one']):.2e} obj {max(res['obj']):.2e}")
-    assert max(res["traj"]) < U_TOL and max(res["one"]) < U_TOL / 10 and max(res["obj"]) < OBJ_TOL
-    assert not res["bad_gates"]
-    bad, amb = label_agreement(ctx.labels().cpu().numpy(), res["U_ref"])
-    log(f"  labels: {bad} mismatches, {amb} ambiguous")
-    assert bad == 0
+    res = lockstep_parallel(runs, Xh, onlr.project_omega(Z.astype(np.float64), K), K, alpha, 1.0, 1e-4)
+    for s, r in res.items():
+        bad, amb = r["labels"]
+        log(f"  {s}: traj {max(r['traj']):.2e} one {max(r['one']):.2e} obj {max(r['obj']):.2e} "
+            f"y {max(r['yerr']):.2e} dual steps {sum(r['gates'])}; labels {bad} bad / {amb} ambiguous")
+        assert max(r["traj"]) < U_TOL and max(r["one"]) < U_TOL / 10 and max(r["obj"]) < OBJ_TOL
+        assert max(r["yerr"]) <= 1e-5
+        assert not r["bad_gates"]
+        assert bad == 0
 
 
 # ---------------------------------------------------------------- API semantics
