@@ -659,7 +659,8 @@ struct Shape {
   static constexpr int LDS = OFF_F + 8 * 4;
   static_assert(RS2 * NCH * NB == 8, "eight waves share the second product");
   static_assert(RS2 * D32 * R32 * 4 <= kRows * XRS, "the partial combine fits the Xhat tile");
-  static_assert(2 * R32 * R32 * 4 <= kRows * WRS, "the Gram combine fits the W tile");
+  static constexpr int GS = NB == 1 ? 8 : 2;              // Gram partials per workgroup
+  static_assert(GS * R32 * R32 * 4 <= kRows * WRS, "the Gram combine fits the W tile");
 };
 
 // Byte offset within a tile (rows of RS bytes) of this lane's transposing read
@@ -756,6 +757,15 @@ __device__ __forceinline__ void reduce_scatter16_row(float* v, int li) {
   rs_step<4, 2, 0x4E>(v, li);    // quad_perm [2, 3, 0, 1]
   rs_step<2, 1, 0xB1>(v, li);    // quad_perm [1, 0, 3, 2]
 }
+// The same for 8 values: lanes li and 15 - li first add all 8 (each half row then
+// covers the 16 rows), then the half-row steps; lane li keeps element li % 8.
+__device__ __forceinline__ void reduce_scatter8_row(float* v, int li) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = v[k] + dpp_f<0x140>(v[k]);  // row_mirror
+  rs_step<8, 4, 0x141>(v, li);
+  rs_step<4, 2, 0x4E>(v, li);
+  rs_step<2, 1, 0xB1>(v, li);
+}
 
 // A 16-byte unit (hi halves, lo halves) into its LDS slot, its two 8-byte halves
 // exchanged when `odd` (by address: two 8-byte writes, no data movement).
@@ -774,8 +784,9 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
   using P = bf8::Shape<NB, NCH>;
   constexpr int CB16 = P::CB16, R32 = P::R32, D32 = P::D32;
   constexpr int KPW = P::KPW;
-  // the row work's dot and the Gram blocks are laid out for 64 columns, 128 features
-  static_assert(NB == 2 && NCH == 4, "one-pass form: 33..64 columns, 97..128 features");
+  // the row work's dot and the Gram blocks are laid out for 33..64 columns and 97..128
+  // features, or for at most 16 columns (one 32-column block) and at most 64 features
+  static_assert((NB == 2 && NCH == 4) || (NB == 1 && NCH <= 2), "one-pass shapes");
   if (halted(B.ctl)) return;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   f16x8* th_h = reinterpret_cast<f16x8*>(smem_raw);
@@ -920,8 +931,9 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     int64_t tb;
     const uint32_t rr = lane_row(st, lo & 15, tb);
     const char* base = reinterpret_cast<const char*>(Usrc + tb * (int64_t)r);
+    // (one column block: at most 16 columns, all in the first 16-column block)
 #pragma unroll
-    for (int cb = 0; cb < CB16; ++cb) {
+    for (int cb = 0; cb < (NB == 1 ? 1 : CB16); ++cb) {
       const int c = 16 * cb + 4 * gq;
       const uint32_t off = 4u * (rr * (uint32_t)r + (uint32_t)(c < r ? c : 0));
       b.u[cb] = *reinterpret_cast<const f32x4*>(base + off);
@@ -929,8 +941,8 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     b.y = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(B.y + tb) + 4u * rr);
   };
 
-  UBuf ub;
-  auto tile = [&](Buf& bx, int64_t st, int64_t nst) {
+  // nst: the tile whose rows replace this tile's in bx and ub once they are consumed
+  auto tile = [&](Buf& bx, UBuf& ub, int64_t st, int64_t nst) {
     __builtin_amdgcn_sched_barrier(0);
     const int lane = opaque_lane();
     const int j = lane & 15, gq = lane >> 4;
@@ -983,39 +995,54 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     for (int cb = 0; cb < CB16; ++cb) {
       okf[cb] = (vpt && (16 * cb + 4 * gq) < r) ? 1.0f : 0.0f;
       const float sc = cf * okf[cb];
-      u[cb][0] = ub.u[cb].x * sc;
-      u[cb][1] = ub.u[cb].y * sc;
-      u[cb][2] = ub.u[cb].z * sc;
-      u[cb][3] = ub.u[cb].w * sc;
+      const f32x4 uv = (NB == 1 && cb > 0) ? (f32x4){0.f, 0.f, 0.f, 0.f} : ub.u[cb];
+      u[cb][0] = uv.x * sc;
+      u[cb][1] = uv.y * sc;
+      u[cb][2] = uv.z * sc;
+      u[cb][3] = uv.w * sc;
     }
     // q = u.p - 1 (FP64): the partial of each group of four columns, then the pairs
     // (columns 4k.. with 4(k^1).., then 4(k^2)..), then the groups of 16 and 32 --
     // the order of the row pass and the finish pass, so that q, the stored dual and
     // ybar are bitwise the same whichever kernel does the row work
-    double pd[CB16];
+    double dot;
+    typedef double f64x2 __attribute__((ext_vector_type(2)));
+    if constexpr (NB == 1) {
+      // at most 16 columns, all in block 0: the order of the narrow row pass -- pairs of
+      // columns, then groups of 4, 8 and 16 (the products are exact in FP64)
+      const f64x2 p01 = *reinterpret_cast<const f64x2*>(pdl + 4 * gq);
+      const f64x2 p23 = *reinterpret_cast<const f64x2*>(pdl + 4 * gq + 2);
+      const double a01 = (double)u[0][0] * p01.x + (double)u[0][1] * p01.y;
+      const double a23 = (double)u[0][2] * p23.x + (double)u[0][3] * p23.y;
+      double v = a01 + a23;
+      v += shfl_xor_d(v, 16);
+      v += shfl_xor_d(v, 32);
+      dot = v;
+    } else {
+      double pd[CB16];
 #pragma unroll
-    for (int cb = 0; cb < CB16; ++cb) {
-      typedef double f64x2 __attribute__((ext_vector_type(2)));
-      const f64x2 p01 = *reinterpret_cast<const f64x2*>(pdl + 16 * cb + 4 * gq);
-      const f64x2 p23 = *reinterpret_cast<const f64x2*>(pdl + 16 * cb + 4 * gq + 2);
-      const double pe[4] = {p01.x, p01.y, p23.x, p23.y};
-      double dd = 0.0;
+      for (int cb = 0; cb < CB16; ++cb) {
+        const f64x2 p01 = *reinterpret_cast<const f64x2*>(pdl + 16 * cb + 4 * gq);
+        const f64x2 p23 = *reinterpret_cast<const f64x2*>(pdl + 16 * cb + 4 * gq + 2);
+        const double pe[4] = {p01.x, p01.y, p23.x, p23.y};
+        double dd = 0.0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) dd += (double)u[cb][e] * pe[e];
-      pd[cb] = dd;
+        for (int e = 0; e < 4; ++e) dd += (double)u[cb][e] * pe[e];
+        pd[cb] = dd;
+      }
+#pragma unroll
+      for (int cb = 0; cb < CB16; ++cb) pd[cb] += shfl_xor_d(pd[cb], 16);
+#pragma unroll
+      for (int cb = 0; cb < CB16; ++cb) pd[cb] += shfl_xor_d(pd[cb], 32);
+      dot = (pd[0] + pd[1]) + (pd[2] + pd[3]);
     }
-#pragma unroll
-    for (int cb = 0; cb < CB16; ++cb) pd[cb] += shfl_xor_d(pd[cb], 16);
-#pragma unroll
-    for (int cb = 0; cb < CB16; ++cb) pd[cb] += shfl_xor_d(pd[cb], 32);
-    const double dot = (pd[0] + pd[1]) + (pd[2] + pd[3]);
     const float q = (float)(dot - 1.0);
     float yt = vpt ? ub.y : 0.f;
     if (gate) yt = fmaf(gam, q, yt);
     const float ybar = fmaf(gam, q, yt);
     // the factor rows and ytilde of this tile are consumed: request the next tile's
     __builtin_amdgcn_sched_barrier(0);
-    load_u(ub, st + step);
+    load_u(ub, nst);
     __builtin_amdgcn_sched_barrier(0);
     if (gate) *(vpt ? (B.y + pt) : B.dump) = yt;  // the four lanes of a row store the same value
     {
@@ -1094,8 +1121,14 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
       float wy[4 * CB16];
 #pragma unroll
       for (int k = 0; k < 4 * CB16; ++k) wy[k] = wv[k] * yt;
-      bf8::reduce_scatter16_row(wv, j);
-      bf8::reduce_scatter16_row(wy, j);
+      if constexpr (NB == 1) {
+        // 8 values: lane j keeps element j % 8
+        bf8::reduce_scatter8_row(wv, j);
+        bf8::reduce_scatter8_row(wy, j);
+      } else {
+        bf8::reduce_scatter16_row(wv, j);
+        bf8::reduce_scatter16_row(wy, j);
+      }
       colacc += (double)wv[0];
       colyacc += (double)wy[0];
     }
@@ -1131,26 +1164,49 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
         accg = mfma32x32x16h(gah, wh, accg);
       }
     };
-    rebase(1);
-    p2(std::integral_constant<int, 0>{});
-    p2(std::integral_constant<int, 1>{});
-    p2(std::integral_constant<int, 2>{});
-    p2(std::integral_constant<int, 3>{});
-    rebase(-1);
-    p2(std::integral_constant<int, 4>{});
-    p2(std::integral_constant<int, 5>{});
-    p2(std::integral_constant<int, 6>{});
-    p2(std::integral_constant<int, 7>{});
+    if constexpr (NB == 1) {
+      // one column block: wave w does its KPW steps of block (fb, 0) and the Gram block
+      // W^T W over the tile's 16-row step w, one of its own steps (k = w - KPW rsp), from
+      // the W operand just read (as A it is W^T)
+      const int gk = wave - KPW * rsp;
+      auto p2n = [&](auto kc) {
+        constexpr int K = decltype(kc)::value;
+        f16x8 xh, xl, wh, wl;
+        bf8::step_reads<16 * K * P::XRS, 16 * K * P::WRS>(xa, wa, xh, xl, wh, wl);
+        acc2 = mfma32x32x16h(xh, wl, acc2);
+        acc2 = mfma32x32x16h(xl, wh, acc2);
+        acc2 = mfma32x32x16h(xh, wh, acc2);
+        if (gk == K) {
+          accg = mfma32x32x16h(wh, wl, accg);
+          accg = mfma32x32x16h(wl, wh, accg);
+          accg = mfma32x32x16h(wh, wh, accg);
+        }
+      };
+      p2n(std::integral_constant<int, 0>{});
+      if constexpr (KPW > 1) p2n(std::integral_constant<int, 1>{});
+    } else {
+      rebase(1);
+      p2(std::integral_constant<int, 0>{});
+      p2(std::integral_constant<int, 1>{});
+      p2(std::integral_constant<int, 2>{});
+      p2(std::integral_constant<int, 3>{});
+      rebase(-1);
+      p2(std::integral_constant<int, 4>{});
+      p2(std::integral_constant<int, 5>{});
+      p2(std::integral_constant<int, 6>{});
+      p2(std::integral_constant<int, 7>{});
+    }
     __syncthreads();
   };
 
   Buf A;
+  UBuf ub;
   load_x(A, blockIdx.x, -1);
   load_u(ub, blockIdx.x);
-  for (int64_t st = blockIdx.x; st < T; st += step) tile(A, st, st + step);
+  for (int64_t st = blockIdx.x; st < T; st += step) tile(A, ub, st, st + step);
 
   // ---- statistics of this workgroup ----
-  {
+  if (NB == 2 || j < 8) {  // (one column block: lanes j and j + 8 hold the same element)
     const int col = 16 * (j >> 2) + 4 * gq + (j & 3);
     colred[wave * R32 + col] = colacc;
     colyred[wave * R32 + col] = colyacc;
@@ -1176,7 +1232,7 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
   // ---- partials of Xhat^T W_{t+1} (row splits in order, [f][c] order) and of
   // W^T W (the two halves of each block in order, [k][l] order) ----
   float* comb = reinterpret_cast<float*>(xt);   // RS2 x D32 x R32 (the tiles are no longer read)
-  float* gcomb = reinterpret_cast<float*>(wt);  // 2 x R32 x R32
+  float* gcomb = reinterpret_cast<float*>(wt);  // GS x R32 x R32
   const float unscale = (1.0f / sx) * (1.0f / kWScale);
   {
     const int h = lane >> 5, li = lane & 31;
@@ -1185,7 +1241,8 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
       const int f = 32 * fb + 8 * (v >> 2) + 4 * h + (v & 3);
       comb[(rsp * D32 + f) * R32 + 32 * cb2 + li] = acc2[v] * unscale;
       const int k = 32 * ga + 8 * (v >> 2) + 4 * h + (v & 3);
-      gcomb[(gh * R32 + k) * R32 + 32 * cb2 + li] = accg[v] * (1.0f / (kWScale * kWScale));
+      const int gs = NB == 1 ? wave : gh;  // the Gram split this wave holds
+      gcomb[(gs * R32 + (NB == 1 ? k - 32 * ga : k)) * R32 + 32 * cb2 + li] = accg[v] * (1.0f / (kWScale * kWScale));
     }
   }
   __syncthreads();
@@ -1220,7 +1277,14 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     part[e] = acc;
   }
   float* gpart = part + D32 * R32;  // W^T W follows Theta in the row
-  for (int e = tid; e < R32 * R32; e += bf8::kThreads8) gpart[e] = gcomb[e] + gcomb[R32 * R32 + e];
+  for (int e = tid; e < R32 * R32; e += bf8::kThreads8) {
+    const float* gc = gcomb + e;
+    constexpr int RR = R32 * R32;
+    if constexpr (NB == 1)
+      gpart[e] = ((gc[0] + gc[RR]) + (gc[2 * RR] + gc[3 * RR])) + ((gc[4 * RR] + gc[5 * RR]) + (gc[6 * RR] + gc[7 * RR]));
+    else
+      gpart[e] = gc[0] + gc[RR];
+  }
 }
 
 template <int NB, int NCH>
@@ -1235,11 +1299,15 @@ static hipError_t pass_bf8_launch(const Geometry& g, const Bufs& b, const StepAr
 }
 
 // shapes of the eight-wave form
-bool fused8_shape(int NB, int nch) { return (NB == 2 && nch == 4); }
+// 33..64 columns with 97..128 features; or at most 16 columns (the narrow row pass's
+// order of the row dot) with at most 64 features
+bool fused8_shape(int NB, int nch, int r) { return (NB == 2 && nch == 4) || (NB == 1 && nch <= 2 && r <= 16); }
 
 static hipError_t pass_bf8_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   switch (g.NB * 10 + g.nch) {
     case 24: return pass_bf8_launch<2, 4>(g, b, a, st);
+    case 11: return pass_bf8_launch<1, 1>(g, b, a, st);
+    case 12: return pass_bf8_launch<1, 2>(g, b, a, st);
     default: return hipErrorInvalidValue;
   }
 }

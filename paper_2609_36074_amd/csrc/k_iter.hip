@@ -495,8 +495,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
   const float* Usrc = B.U;
   if (FINISH && B.ctl->breakdown != 0) return;
   if (!FINISH && halted(B.ctl)) return;
+  // the one-pass iteration launches the row pass every iteration; it runs only when
+  // the previous iteration's stopping rule may fire (the pass then does no row work)
+  if (MODE == kPassRows && g.fused8 && !B.ctl->rows_first) return;
   const bool stopped = FINISH && (B.ctl->stop != 0);
-  constexpr int PF = 8;  // steps in flight
+  constexpr int PF = 8;  // steps in flight (16 halves the waves per SIMD: no more bytes in flight)
   __shared__ double dred[kThreads + 8];
 
   const int tid = threadIdx.x;

@@ -127,7 +127,7 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   const bool uflat = r % 4 != 0;
   g.fused = (fused && shape_f && fused_lds_need(g.NB, g.nch, split, uflat) <= kMaxFusedLds) ? 1 : 0;
   g.uflat = (g.fused && uflat) ? 1 : 0;
-  g.fused8 = (g.fused && split && !uflat && fused8_shape(g.NB, g.nch)) ? 1 : 0;
+  g.fused8 = (g.fused && split && !uflat && fused8_shape(g.NB, g.nch, r)) ? 1 : 0;
   // the one-pass iteration's W^T W partials follow its Theta partials in one row
   g.theta_cols = g.d32 * g.r32 + (g.fused8 ? g.r32 * g.r32 : 0);
   g.SAF = g.SA;
@@ -337,6 +337,7 @@ struct nlr_ctx {
   bool graphs_allowed;  // false for the allocation-free entry point (instantiation allocates)
   hipStream_t cap_stream;
   hipGraphExec_t graph1, graph8;
+  hipGraphExec_t lean1, lean8;  // one-pass iterations without the row pass (see enqueue_iteration)
 };
 
 static nlr_status hip_fail(nlr_ctx* c) {
@@ -435,8 +436,11 @@ static hipError_t prof_collect(nlr_ctx* c) {
   } while (0)
 
 // first: the first iteration of a host call (nlr_step, nlr_run), whose step
-// arguments may differ from those of the pass before it
-static nlr_status enqueue_iteration(nlr_ctx* c, bool first) {
+// arguments may differ from those of the pass before it.  lean (one-pass form, not the
+// first iteration): the caller knows that the previous iteration's stopping rule
+// cannot fire (t < T_min), so the row pass, its segment sums and k_ctl_a would
+// return at entry; they are not launched.
+static nlr_status enqueue_iteration(nlr_ctx* c, bool first, bool lean = false) {
   const StepArgs a = make_step_args(c, c->pending ? 1 : 0);
   if (c->g.fused8) {
     // one pass over the rows per iteration, writing W over the factor: the pass does
@@ -449,9 +453,11 @@ static nlr_status enqueue_iteration(nlr_ctx* c, bool first) {
     // the rule and s.  Then one launch of segment sums (Theta and W^T W partials, the
     // row statistics), the control, and Theta with (W^T W) P and the next s.
     if (first) LAUNCH(KK_CTL_A, launch_onepass_begin(c->g, c->b, a, c->gram_valid, c->stream));
-    LAUNCH(KK_PASS_U, launch_pass_u(c->g, c->b, a, c->stream));
-    LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
-    LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
+    if (first || !lean) {
+      LAUNCH(KK_PASS_U, launch_pass_u(c->g, c->b, a, c->stream));
+      LAUNCH(KK_CTL_A, launch_seg_a(c->g, c->b, false, c->stream));
+      LAUNCH(KK_CTL_A, launch_ctl_a(c->g, c->b, a, false, c->stream));
+    }
     LAUNCH(KK_PASS_BF, launch_pass_bf(c->g, c->b, a, c->stream));
     LAUNCH(KK_CTL_B, launch_seg_onepass(c->g, c->b, c->stream));
     LAUNCH(KK_CTL_B, launch_ctl_one(c->g, c->b, a, c->stream));
@@ -499,16 +505,17 @@ static nlr_status enqueue_iteration(nlr_ctx* c, bool first) {
 }
 
 static void drop_graphs(nlr_ctx* c) {
-  if (c->graph1) (void)hipGraphExecDestroy(c->graph1);
-  if (c->graph8) (void)hipGraphExecDestroy(c->graph8);
-  c->graph1 = c->graph8 = nullptr;
+  for (hipGraphExec_t* gp : {&c->graph1, &c->graph8, &c->lean1, &c->lean8}) {
+    if (*gp) (void)hipGraphExecDestroy(*gp);
+    *gp = nullptr;
+  }
 }
 
 // Captures `iters` iterations that follow the first of a host call (their step
 // arguments are fixed: the end-of-iteration work of the previous one is pending) as an
 // executable graph.  The kernels read the device control block when they run, so a
 // replay behaves as the same launches made one by one.  No memset is recorded.
-static hipError_t capture_iterations(nlr_ctx* c, int iters, hipGraphExec_t* out) {
+static hipError_t capture_iterations(nlr_ctx* c, int iters, bool lean, hipGraphExec_t* out) {
   *out = nullptr;
   hipError_t e = hipSuccess;
   if (!c->cap_stream) {
@@ -523,7 +530,7 @@ static hipError_t capture_iterations(nlr_ctx* c, int iters, hipGraphExec_t* out)
     return e;
   }
   nlr_status s = NLR_OK;
-  for (int k = 0; k < iters && s == NLR_OK; ++k) s = enqueue_iteration(c, false);
+  for (int k = 0; k < iters && s == NLR_OK; ++k) s = enqueue_iteration(c, false, lean);
   hipGraph_t graph = nullptr;
   e = hipStreamEndCapture(c->cap_stream, &graph);
   c->stream = user;
@@ -535,23 +542,25 @@ static hipError_t capture_iterations(nlr_ctx* c, int iters, hipGraphExec_t* out)
 
 // Enqueues `nb` iterations that follow the first of the call: as graph replays when
 // allowed and profiling is off (the events of profiling are per launch), else one by one.
-static nlr_status enqueue_steady(nlr_ctx* c, int nb) {
+static nlr_status enqueue_steady(nlr_ctx* c, int nb, bool lean) {
+  lean = lean && c->g.fused8;
   if (c->graphs_allowed && !c->prof) {
-    if (!c->graph1 || !c->graph8) {
-      drop_graphs(c);
-      if (capture_iterations(c, 1, &c->graph1) != hipSuccess || capture_iterations(c, 8, &c->graph8) != hipSuccess) {
+    hipGraphExec_t& g1 = lean ? c->lean1 : c->graph1;
+    hipGraphExec_t& g8 = lean ? c->lean8 : c->graph8;
+    if (!g1 || !g8) {
+      if (capture_iterations(c, 1, lean, &g1) != hipSuccess || capture_iterations(c, 8, lean, &g8) != hipSuccess) {
         drop_graphs(c);
         return hip_fail(c);
       }
     }
     for (; nb >= 8; nb -= 8)
-      if (hipGraphLaunch(c->graph8, c->stream) != hipSuccess) return hip_fail(c);
+      if (hipGraphLaunch(g8, c->stream) != hipSuccess) return hip_fail(c);
     for (; nb > 0; --nb)
-      if (hipGraphLaunch(c->graph1, c->stream) != hipSuccess) return hip_fail(c);
+      if (hipGraphLaunch(g1, c->stream) != hipSuccess) return hip_fail(c);
     return NLR_OK;
   }
   for (; nb > 0; --nb) {
-    const nlr_status s = enqueue_iteration(c, false);
+    const nlr_status s = enqueue_iteration(c, false, lean);
     if (s != NLR_OK) return s;
   }
   return NLR_OK;
@@ -661,7 +670,7 @@ static nlr_status init_ctx(nlr_ctx* c, const Geometry& g0, float* X, int32_t K, 
     c->prof_n[k] = 0;
   }
   c->cap_stream = nullptr;
-  c->graph1 = c->graph8 = nullptr;
+  c->graph1 = c->graph8 = c->lean1 = c->lean8 = nullptr;
   if (hipGetDevice(&c->device) != hipSuccess) return NLR_EHIP;
   const Geometry& g = c->g;
   const Bufs& b = c->b;
@@ -709,6 +718,9 @@ static nlr_status run_iterations(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr
     if (read_ctl(c) != NLR_OK) return NLR_EHIP;
   const int64_t t0 = c->t_host;
   if (launch_clear_stop(c->b, c->stream) != hipSuccess) return hip_fail(c);
+  // no iteration of this call can stop while t < T_min: its row pass would not run
+  // (one-pass form), so it is not launched
+  const bool lean = t0 + T - 1 < (int64_t)c->prm.T_min;
   // the stop flag is polled every 32 iterations; kernels after a stop return at entry
   for (int32_t k = 0; k < T;) {
     if (k > 0 && (k % 32) == 0) {
@@ -723,7 +735,7 @@ static nlr_status run_iterations(nlr_ctx* c, int32_t T, int32_t* iters_done, nlr
     }
     const int32_t to_poll = 32 - (k % 32);
     const int32_t nb = (T - k) < to_poll ? (T - k) : to_poll;
-    nlr_status s = enqueue_steady(c, nb);
+    nlr_status s = enqueue_steady(c, nb, lean);
     if (s != NLR_OK) return s;
     k += nb;
   }

@@ -177,7 +177,7 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
                        bool fused = false);
 // dynamic LDS of the fused pass B for (NB, nch, split, U moved as whole slabs)
 int fused_lds_need(int NB, int nch, bool split, bool uflat);
-bool fused8_shape(int NB, int nch);
+bool fused8_shape(int NB, int nch, int r);
 constexpr int kMaxFusedLds = 160 << 10;
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
 

@@ -33,8 +33,10 @@ def test_algorithmic_bytes_per_point():
 
 
 @pytest.mark.parametrize("name,n,d,r,split,two_pass,form", [
-    ("tiny", 2_000, 16, 4, True, False, "single-Xhat-pass"),
-    ("gmm1m", 1_000_000, 64, 16, True, False, "single-Xhat-pass"),
+    ("tiny", 2_000, 16, 4, True, False, "one-pass"),
+    ("tiny fp32", 2_000, 16, 4, False, False, "single-Xhat-pass"),
+    ("gmm1m", 1_000_000, 64, 16, True, False, "one-pass"),
+    ("d=64 r=20", 100_000, 64, 20, True, False, "single-Xhat-pass"),
     ("gmm10m", 10_000_000, 128, 64, True, False, "one-pass"),
     ("gmm10m fp32", 10_000_000, 128, 64, False, False, "single-Xhat-pass"),
     ("gmm10m two-pass", 10_000_000, 128, 64, True, True, "two-pass"),
@@ -45,6 +47,7 @@ def test_algorithmic_bytes_per_point():
     ("d=96", 100_000, 96, 64, True, False, "single-Xhat-pass"),
     ("r=32", 100_000, 128, 32, True, False, "single-Xhat-pass"),
     ("Table 2 d=50 fp32", 100_000, 50, 30, False, False, "two-pass"),
+    ("Table 2 d=200 r=300 fp32", 100_000, 200, 300, False, False, "two-pass"),
 ])
 def test_iteration_form_comes_from_the_library(name, n, d, r, split, two_pass, form):
     assert bench.iteration_form(n, d, r, r, split, two_pass) == form
@@ -54,7 +57,7 @@ def test_iteration_form_rejects_unsupported_shapes():
     with pytest.raises(ValueError):
         bench.iteration_form(100_000, 50, 30, 20, True, False)  # split needs d % 4 == 0 (panel: d % 8)
     with pytest.raises(ValueError):
-        bench.iteration_form(100_000, 128, 512, 64, False, False)  # r above the compiled family
+        bench.iteration_form(100_000, 128, 512, 64, False, False)  # r above the compiled family (448)
 
 
 def test_physical_rate_counts_the_launched_kernels():

@@ -27,24 +27,26 @@ def _need_gpu():
     nlr.load_library()
 
 
-# (n, d, r, flags, form): one shape per iteration form
-FORMS = [(2000, 16, 4, 0, "single-Xhat-pass"), (2000, 16, 4, TWO_PASS, "two-pass"),
-         (3000, 32, 10, SPLIT, "single-Xhat-pass"), (3000, 100, 36, SPLIT, "one-pass"),
-         (3000, 256, 40, SPLIT, "two-pass-panel"), (1000, 13, 5, 0, "two-pass")]
+# (n, d, r, flags, form, T_min): one shape per iteration form; with T_min above every
+# iteration of the plan the one-pass form's replays leave out the row pass
+FORMS = [(2000, 16, 4, 0, "single-Xhat-pass", 0), (2000, 16, 4, TWO_PASS, "two-pass", 0),
+         (3000, 32, 10, SPLIT, "single-Xhat-pass", 0), (3000, 100, 36, SPLIT, "one-pass", 0),
+         (3000, 100, 36, SPLIT, "one-pass", 10**6), (2000, 16, 4, SPLIT, "one-pass", 10**6),
+         (3000, 256, 40, SPLIT, "two-pass-panel", 0), (1000, 13, 5, 0, "two-pass", 0)]
 
 
-@pytest.mark.parametrize("n,d,r,flags,form", FORMS)
-def test_graph_replay_equals_steps(n, d, r, flags, form):
+@pytest.mark.parametrize("n,d,r,flags,form,T_min", FORMS)
+def test_graph_replay_equals_steps(n, d, r, flags, form, T_min):
     from paper_2609_36074_amd import nlr
     K, beta = 4, 2.0
     assert nlr.FORM_NAMES[nlr.nlr_iteration_form(n, d, r, K, flags)] == form
     X, _, _ = gaussian_mixture(n, d, K, 25.0, seed=1)
     Z = standard_normal_factor(n, r, seed=2).astype(np.float64)
     alpha = 1.8 * onlr.default_step_size(K, beta)
-    kw = dict(eps_d=3e-3, eps_c=1e-9, T_min=0, flags=flags)
+    kw = dict(eps_d=3e-3, eps_c=1e-9, T_min=T_min, flags=flags)
     a = make_ctx(X, Z, K, alpha, beta, **kw)
     b = make_ctx(X, Z, K, alpha, beta, **kw)
-    log(f"graph replay {form} n={n} d={d} r={r} flags={flags}")
+    log(f"graph replay {form} n={n} d={d} r={r} flags={flags} T_min={T_min}")
 
     def same(tag):
         for name in ("U", "y"):
