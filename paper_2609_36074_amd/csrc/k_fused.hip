@@ -778,10 +778,13 @@ __device__ __forceinline__ void put_unit(unsigned char* slot, f32x4 v, bool odd)
 
 }  // namespace bf8
 
-template <int NB, int NCH>
+// PAIRS (one column block, r % 4 == 2): the rows of U are 8-byte aligned only; the
+// factor moves in column pairs (8-byte loads, and 8-byte pieces of the packed slab).
+template <int NB, int NCH, bool PAIRS>
 __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_bf8(
     Geometry g, Bufs B, StepArgs S) {
   using P = bf8::Shape<NB, NCH>;
+  static_assert(!PAIRS || NB == 1, "column pairs: one column block");
   constexpr int CB16 = P::CB16, R32 = P::R32, D32 = P::D32;
   constexpr int KPW = P::KPW;
   // the row work's dot and the Gram blocks are laid out for 33..64 columns and 97..128
@@ -932,11 +935,23 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     const uint32_t rr = lane_row(st, lo & 15, tb);
     const char* base = reinterpret_cast<const char*>(Usrc + tb * (int64_t)r);
     // (one column block: at most 16 columns, all in the first 16-column block)
+    if constexpr (PAIRS) {
+      // columns c, c + 1 and c + 2, c + 3 as two 8-byte loads; a pair at or beyond r reads
+      // column 0 of the row instead (its values are masked)
+      typedef float f32x2 __attribute__((ext_vector_type(2)));
+      const int c = 4 * gq;
+      const uint32_t o0 = 4u * (rr * (uint32_t)r + (uint32_t)(c < r ? c : 0));
+      const uint32_t o1 = 4u * (rr * (uint32_t)r + (uint32_t)(c + 2 < r ? c + 2 : 0));
+      const f32x2 v0 = *reinterpret_cast<const f32x2*>(base + o0);
+      const f32x2 v1 = *reinterpret_cast<const f32x2*>(base + o1);
+      b.u[0] = (f32x4){v0.x, v0.y, v1.x, v1.y};
+    } else {
 #pragma unroll
-    for (int cb = 0; cb < (NB == 1 ? 1 : CB16); ++cb) {
-      const int c = 16 * cb + 4 * gq;
-      const uint32_t off = 4u * (rr * (uint32_t)r + (uint32_t)(c < r ? c : 0));
-      b.u[cb] = *reinterpret_cast<const f32x4*>(base + off);
+      for (int cb = 0; cb < (NB == 1 ? 1 : CB16); ++cb) {
+        const int c = 16 * cb + 4 * gq;
+        const uint32_t off = 4u * (rr * (uint32_t)r + (uint32_t)(c < r ? c : 0));
+        b.u[cb] = *reinterpret_cast<const f32x4*>(base + off);
+      }
     }
     b.y = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(B.y + tb) + 4u * rr);
   };
@@ -989,17 +1004,19 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
     const float* nasl = nass + lds_off;
     // okf: 1 for a valid row and column, else 0 (masked lanes compute on finite
     // values and their results are multiplied away: no branches)
-    float okf[CB16];
+    // (okf2: the same for the group's second column pair, which PAIRS can lose alone)
+    float okf[CB16], okf2[CB16];
     float u[CB16][4];
 #pragma unroll
     for (int cb = 0; cb < CB16; ++cb) {
       okf[cb] = (vpt && (16 * cb + 4 * gq) < r) ? 1.0f : 0.0f;
-      const float sc = cf * okf[cb];
+      okf2[cb] = PAIRS ? ((vpt && (16 * cb + 4 * gq + 2) < r) ? 1.0f : 0.0f) : okf[cb];
+      const float sc = cf * okf[cb], sc2 = cf * okf2[cb];
       const f32x4 uv = (NB == 1 && cb > 0) ? (f32x4){0.f, 0.f, 0.f, 0.f} : ub.u[cb];
       u[cb][0] = uv.x * sc;
       u[cb][1] = uv.y * sc;
-      u[cb][2] = uv.z * sc;
-      u[cb][3] = uv.w * sc;
+      u[cb][2] = uv.z * sc2;
+      u[cb][3] = uv.w * sc2;
     }
     // q = u.p - 1 (FP64): the partial of each group of four columns, then the pairs
     // (columns 4k.. with 4(k^1).., then 4(k^2)..), then the groups of 16 and 32 --
@@ -1071,7 +1088,7 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
         float t = fmaf(two_alpha_s, acc1[cb][e], uu);
         t = fmaf(ybar, pe[e], t);
         t = t + se[e];
-        const float w = fmaxf(t, 0.f) * okf[cb];
+        const float w = fmaxf(t, 0.f) * (e < 2 ? okf[cb] : okf2[cb]);
         wv[4 * cb + e] = w;
         wmx = fmaxf(wmx, w);
         const double wd = (double)w, ud = (double)uu;
@@ -1080,21 +1097,38 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
         sh = fma(wd, ud, sh);
       }
       const f32x4 o = {wv[4 * cb + 0], wv[4 * cb + 1], wv[4 * cb + 2], wv[4 * cb + 3]};
-      // unit j ru + c / 4 of the packed slab (columns >= r to the last unit, never stored)
-      const int uq = (c < r) ? (j * ru + 4 * cb + gq) : (16 * P::WU - 1);
-      *reinterpret_cast<f32x4*>(wst + 16 * bf8::stage_slot(uq)) = o;
+      if constexpr (PAIRS) {
+        // floats j r + c .. of the packed slab as two 8-byte pieces (unit (j r + c) / 4,
+        // half ((j r + c) / 2) % 2); pairs at or beyond r to the last unit, never stored
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        const int f0 = j * r + c;
+        const int q0 = (c < r) ? (f0 >> 2) : (16 * P::WU - 1), h0 = (c < r) ? ((f0 >> 1) & 1) : 0;
+        const int q1 = (c + 2 < r) ? ((f0 + 2) >> 2) : (16 * P::WU - 1), h1 = (c + 2 < r) ? (((f0 + 2) >> 1) & 1) : 1;
+        *reinterpret_cast<f32x2*>(wst + 16 * bf8::stage_slot(q0) + 8 * h0) = (f32x2){o.x, o.y};
+        *reinterpret_cast<f32x2*>(wst + 16 * bf8::stage_slot(q1) + 8 * h1) = (f32x2){o.z, o.w};
+      } else {
+        // unit j ru + c / 4 of the packed slab (columns >= r to the last unit, never stored)
+        const int uq = (c < r) ? (j * ru + 4 * cb + gq) : (16 * P::WU - 1);
+        *reinterpret_cast<f32x4*>(wst + 16 * bf8::stage_slot(uq)) = o;
+      }
     }
     __builtin_amdgcn_wave_barrier();
     {
       const int64_t row0 = st * bf8::kRows + 16 * wave;
       const int64_t rows = n - row0 < 16 ? n - row0 : 16;
-      const int nvalid = rows > 0 ? (int)rows * ru : 0;  // 16-byte units of the slab in U
+      // 16-byte units of the slab in U (PAIRS: rows r floats, a last half unit when rows r % 4 == 2)
+      const int nfl = rows > 0 ? (int)rows * r : 0;
+      const int nvalid = nfl >> 2;
       char* sbase = reinterpret_cast<char*>(Udst + (rows > 0 ? row0 : 0) * (int64_t)r);
 #pragma unroll
       for (int i = 0; i < 2 * NB; ++i) {  // 16 rows x R32 floats = 128 NB units
         const int q = lane + 64 * i;
         const f32x4 v = *reinterpret_cast<const f32x4*>(wst + 16 * bf8::stage_slot(q));
         if (q < nvalid) *reinterpret_cast<f32x4*>(sbase + 16u * (uint32_t)q) = v;
+        if (PAIRS && q == nvalid && (nfl & 3) != 0) {
+          typedef float f32x2 __attribute__((ext_vector_type(2)));
+          *reinterpret_cast<f32x2*>(sbase + 16u * (uint32_t)q) = (f32x2){v.x, v.y};
+        }
       }
     }
     __builtin_amdgcn_wave_barrier();
@@ -1287,27 +1321,29 @@ __global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(
   }
 }
 
-template <int NB, int NCH>
+template <int NB, int NCH, bool PAIRS>
 static hipError_t pass_bf8_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   constexpr int lds = bf8::Shape<NB, NCH>::LDS;
   static_assert(lds <= kMaxFusedLds, "LDS");
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_bf8<NB, NCH>),
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_bf8<NB, NCH, PAIRS>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_pass_bf8<NB, NCH>), dim3(g.GB), dim3(bf8::kThreads8), lds, st, g, b, a);
+  hipLaunchKernelGGL((k_pass_bf8<NB, NCH, PAIRS>), dim3(g.GB), dim3(bf8::kThreads8), lds, st, g, b, a);
   return hipGetLastError();
 }
 
 // shapes of the eight-wave form
-// 33..64 columns with 97..128 features; or at most 16 columns (the narrow row pass's
-// order of the row dot) with at most 64 features
-bool fused8_shape(int NB, int nch, int r) { return (NB == 2 && nch == 4) || (NB == 1 && nch <= 2 && r <= 16); }
+// 33..64 columns (r % 4 == 0) with 97..128 features; or at most 16 columns, r even (the
+// narrow row pass's order of the row dot), with at most 64 features
+bool fused8_shape(int NB, int nch, int r) {
+  return (NB == 2 && nch == 4 && r % 4 == 0) || (NB == 1 && nch <= 2 && r <= 16 && r % 2 == 0);
+}
 
 static hipError_t pass_bf8_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   switch (g.NB * 10 + g.nch) {
-    case 24: return pass_bf8_launch<2, 4>(g, b, a, st);
-    case 11: return pass_bf8_launch<1, 1>(g, b, a, st);
-    case 12: return pass_bf8_launch<1, 2>(g, b, a, st);
+    case 24: return g.r % 4 == 0 ? pass_bf8_launch<2, 4, false>(g, b, a, st) : hipErrorInvalidValue;
+    case 11: return g.r % 4 == 0 ? pass_bf8_launch<1, 1, false>(g, b, a, st) : pass_bf8_launch<1, 1, true>(g, b, a, st);
+    case 12: return g.r % 4 == 0 ? pass_bf8_launch<1, 2, false>(g, b, a, st) : pass_bf8_launch<1, 2, true>(g, b, a, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -127,7 +127,7 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   const bool uflat = r % 4 != 0;
   g.fused = (fused && shape_f && fused_lds_need(g.NB, g.nch, split, uflat) <= kMaxFusedLds) ? 1 : 0;
   g.uflat = (g.fused && uflat) ? 1 : 0;
-  g.fused8 = (g.fused && split && !uflat && fused8_shape(g.NB, g.nch, r)) ? 1 : 0;
+  g.fused8 = (g.fused && split && fused8_shape(g.NB, g.nch, r)) ? 1 : 0;
   // the one-pass iteration's W^T W partials follow its Theta partials in one row
   g.theta_cols = g.d32 * g.r32 + (g.fused8 ? g.r32 * g.r32 : 0);
   g.SAF = g.SA;

@@ -40,7 +40,8 @@ def test_algorithmic_bytes_per_point():
     ("gmm10m", 10_000_000, 128, 64, True, False, "one-pass"),
     ("gmm10m fp32", 10_000_000, 128, 64, False, False, "single-Xhat-pass"),
     ("gmm10m two-pass", 10_000_000, 128, 64, True, True, "two-pass"),
-    ("gmm50m", 50_000_000, 32, 10, True, False, "single-Xhat-pass"),
+    ("gmm50m", 50_000_000, 32, 10, True, False, "one-pass"),
+    ("d=32 r=18", 100_000, 32, 18, True, False, "single-Xhat-pass"),
     ("embed2m", 2_000_000, 768, 256, True, False, "two-pass-panel"),
     ("embed2m fp32", 2_000_000, 768, 256, False, False, "two-pass"),
     ("d=100 r=36", 100_000, 100, 36, True, False, "one-pass"),

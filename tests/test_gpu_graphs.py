@@ -30,7 +30,8 @@ def _need_gpu():
 # (n, d, r, flags, form, T_min): one shape per iteration form; with T_min above every
 # iteration of the plan the one-pass form's replays leave out the row pass
 FORMS = [(2000, 16, 4, 0, "single-Xhat-pass", 0), (2000, 16, 4, TWO_PASS, "two-pass", 0),
-         (3000, 32, 10, SPLIT, "single-Xhat-pass", 0), (3000, 100, 36, SPLIT, "one-pass", 0),
+         (3000, 32, 18, SPLIT, "single-Xhat-pass", 0), (3000, 100, 36, SPLIT, "one-pass", 0),
+         (3000, 32, 10, SPLIT, "one-pass", 10**6),
          (3000, 100, 36, SPLIT, "one-pass", 10**6), (2000, 16, 4, SPLIT, "one-pass", 10**6),
          (3000, 256, 40, SPLIT, "two-pass-panel", 0), (1000, 13, 5, 0, "two-pass", 0)]
 

@@ -1,5 +1,6 @@
 """The one-pass iteration (split products; 97..128 features with 33..64 columns, or
-at most 64 features with at most 16 columns, r % 4 == 0): one
+at most 64 features with at most 16 columns, r even -- r % 4 == 2 moves U in column
+pairs): one
 pass over the rows per iteration does the row work of the iteration (the end of
 the previous one) and the primal step, writing W over the factor it reads; s
 comes from the Gram terms of the previous pass.  Where the previous iteration's
@@ -34,7 +35,8 @@ def _gated(d, r):
     """A 3000-row mixture (seed 1) on which, with alpha = 1.8/(2 L0), beta = 2, eps_d = 3e-3 and
     eps_c = 1e-3, the oracle stops after 432 iterations with 144 dual steps at d = 100, r = 36, and
     after 564 with 244 at d = 128, r = 64 (first dual steps near iteration 25); after 769 at
-    d = 64, r = 16, 545 at d = 32, r = 12, 834 at d = 16, r = 4 and 538 at d = 48, r = 8."""
+    d = 64, r = 16, 545 at d = 32, r = 12, 834 at d = 16, r = 4, 538 at d = 48, r = 8, 596 at
+    d = 32, r = 10 and 625 at d = 64, r = 14."""
     K, beta = 4, 2.0
     X, lab, _ = gaussian_mixture(3000, d, K, 25.0, seed=1)
     Z = standard_normal_factor(3000, r, seed=2).astype(np.float64)
@@ -45,7 +47,8 @@ def _gated(d, r):
 # 280 in 600 (d = 128), 260 in 700 (d = 64, r = 16), 97 in 450 (d = 32, r = 12) and 258 in
 # 800 (d = 16, r = 4)
 @pytest.mark.parametrize("d,r,T,gates", [(100, 36, 450, 100), (128, 64, 600, 100), (64, 16, 700, 100),
-                                         (32, 12, 450, 50), (16, 4, 800, 100)])
+                                         (32, 12, 450, 50), (16, 4, 800, 100), (32, 10, 600, 100),
+                                         (64, 14, 600, 100)])
 def test_onepass_gated_trajectory(d, r, T, gates):
     from paper_2609_36074_amd import nlr
     assert nlr.FORM_NAMES[nlr.nlr_iteration_form(3000, d, r, 4, SPLIT)] == "one-pass"
@@ -60,8 +63,9 @@ def test_onepass_gated_trajectory(d, r, T, gates):
     assert not bad_gates, bad_gates
 
 
-# dual steps in the first 451 iterations: 162 (d = 100), 13 (d = 64), 2 (d = 16)
-@pytest.mark.parametrize("d,r,gates", [(100, 36, 50), (64, 16, 5), (16, 4, 1)])
+# dual steps in the first 451 iterations: 162 (d = 100), 13 (d = 64), 2 (d = 16), 83 (d = 32,
+# r = 10: column pairs), 5 (d = 16, r = 6)
+@pytest.mark.parametrize("d,r,gates", [(100, 36, 50), (64, 16, 5), (16, 4, 1), (32, 10, 50), (16, 6, 2)])
 def test_onepass_run_equals_steps_bitwise(d, r, gates):
     X, Z, K, beta, alpha = _gated(d, r)
     kw = dict(eps_d=3e-3, eps_c=1e-7, T_min=0, flags=SPLIT)
@@ -86,7 +90,8 @@ def test_onepass_run_equals_steps_bitwise(d, r, gates):
     assert np.array_equal(host(d.U), host(a.U)) and np.array_equal(host(d.y), host(a.y))
 
 
-@pytest.mark.parametrize("d,r,expect", [(100, 36, 432), (128, 64, 564), (64, 16, 769), (32, 12, 545)])
+@pytest.mark.parametrize("d,r,expect", [(100, 36, 432), (128, 64, 564), (64, 16, 769), (32, 12, 545),
+                                        (32, 10, 596), (64, 14, 625)])
 def test_onepass_stop_rule(d, r, expect):
     X, Z, K, beta, alpha = _gated(d, r)
     eps_d, eps_c = 3e-3, 1e-3

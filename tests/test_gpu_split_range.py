@@ -2,8 +2,8 @@
 
 With a step size far beyond the Prop. 1 bound (alpha = 1e5, about 4e4 times the default)
 the first update has entries near 180 (> 65504 / 2^10): the single-Xhat-pass form (16
-features, 10 columns) and the one-pass form (16 features, 4 columns; 128 features, 64
-columns) stop with NLR_ERANGE
+features, 18 columns) and the one-pass form (16 features, 4 or 10 columns; 128 features,
+64 columns) stop with NLR_ERANGE
 instead of iterating on inf/NaN operands; U holds the finite W; the context is then
 failed.  The same step with fp32 products (no such limit) gives a finite normalised
 iterate.  This is numeric overflow handled by the kernels' own flag, not a GPU fault."""
@@ -32,15 +32,16 @@ def _inputs(shape):
     if shape == "tiny":
         X, Z, _, wl = make_workload("tiny")
         return X, Z.astype(np.float64), wl.K, 1.0
-    if shape == "tiny r10":
+    if shape in ("tiny r10", "tiny r18"):
         X, _, _, wl = make_workload("tiny")
-        return X, standard_normal_factor(X.shape[0], 10, seed=2).astype(np.float64), wl.K, 1.0
+        r = int(shape[6:])
+        return X, standard_normal_factor(X.shape[0], r, seed=2).astype(np.float64), wl.K, 1.0
     X, _, _ = gaussian_mixture(3000, 128, 4, 25.0, seed=1)
     return X, standard_normal_factor(3000, 64, seed=2).astype(np.float64), 4, 2.0
 
 
-@pytest.mark.parametrize("shape,form", [("tiny r10", "single-Xhat-pass"), ("tiny", "one-pass"),
-                                        ("d128r64", "one-pass")])
+@pytest.mark.parametrize("shape,form", [("tiny r18", "single-Xhat-pass"), ("tiny", "one-pass"),
+                                        ("tiny r10", "one-pass"), ("d128r64", "one-pass")])
 def test_split_range_error(shape, form):
     from paper_2609_36074_amd import nlr
     X, Z, K, beta = _inputs(shape)
@@ -63,8 +64,8 @@ def test_split_range_error(shape, form):
     with pytest.raises(nlr.NlrError) as e:
         ctx.run(1)
     assert e.value.status == nlr.NLR_ESTATE
-    # fp32 products take the same step without a range limit (at 10 columns the oracle's
-    # second step with this alpha leaves no positive entry, so one step for every shape)
+    # fp32 products take the same step without a range limit (at 10 and 18 columns the
+    # oracle's second step with this alpha leaves no positive entry: one step for every shape)
     c32 = make_ctx(X, Z, K, alpha, beta, flags=0)
     done, last = c32.run(1)
     U32 = host(c32.U)
