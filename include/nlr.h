@@ -137,7 +137,8 @@ enum {
    * the partials of Xhat^T W_{t+1}, and Theta_{t+1} = c_{t+1} Xhat^T W_{t+1}
    * (U_{t+1} = c_{t+1} W_{t+1}, Algorithm 1), while a row pass over U and ytilde
    * does the rest of pass A's work.  With NLR_INIT_SPLIT_F16 and 97..128
-   * features, 33..64 columns (d % 4 == 0, r % 4 == 0) the default is the
+   * features with 33..64 columns (d % 4 == 0, r % 4 == 0), or at most 64
+   * features with at most 16 columns (d % 4 == 0, r even) the default is the
    * one-pass form: the same kernel also does the row work (q, the gated dual
    * step, ybar), s = U^T ybar is formed from W^T W, W^T ytilde and the column sums
    * of the previous pass's W, and W is written over U in place.  At iterations
@@ -247,7 +248,11 @@ nlr_status nlr_step(nlr_ctx* ctx, nlr_iter_stats* stats);
  * decides; the host polls a flag every 32 iterations and synchronises once
  * at the end.  *iters_done (nullable) receives the iterations done by this
  * call; *last (nullable) the record of the last one.  nlr_run(T) and T calls
- * of nlr_step give bitwise-identical U and y. */
+ * of nlr_step give bitwise-identical U and y.  While profiling is off, the
+ * iterations after the call's first are replayed from HIP graphs the context
+ * captures on first use (on a private stream; held until nlr_destroy, dropped
+ * by nlr_set_params); when every iteration of the call has t < T_min, the
+ * one-pass form leaves out the row pass that only the stopping rule needs. */
 nlr_status nlr_run(nlr_ctx* ctx, int32_t T, int32_t* iters_done, nlr_iter_stats* last);
 
 /* Row-argmax labels of the current U: labels[i] = argmax_j U_ij, lowest j on
@@ -271,8 +276,8 @@ nlr_status nlr_normaliser(nlr_ctx* ctx, double* a, double* xbar_host);
 /* Diagnostic read-back (synchronises): what = 0 copies Theta = Xhat^T U of the
  * latest iteration as d*r row-major floats; 1 copies p = U^T 1 (r floats) of
  * the current U; 2 copies s = U^T ybar (r floats) of the latest iteration's
- * starting factor -- in the one-pass form (split products, 97..128 features,
- * 33..64 columns) of the current U instead, formed after each pass for the next
+ * starting factor -- in the one-pass form (split products at the shapes listed
+ * under NLR_INIT_TWO_PASS) of the current U instead, formed after each pass for the next
  * one with the step arguments of that call; 3 copies an int64: the number of
  * one-pass iterations since nlr_init whose row work ran in a pass of its own
  * before the primal step (the first iteration after nlr_init, and those at which
