@@ -102,10 +102,12 @@ constexpr int fused_lds_bytes(int NB, int NCH, bool split, bool uflat) {
 template <int NB, int NCH>
 constexpr int fused_waves_per_simd() { return (NB == 1 && NCH <= 2) ? 2 : 1; }
 
-template <int NB, int NCH, bool SPLIT, bool UFLAT>
+// X2 (fp32 products, d % 4 == 2): rows of Xhat are 8-byte aligned only and load as 8-byte pieces.
+template <int NB, int NCH, bool SPLIT, bool UFLAT, bool X2>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_waves_per_simd<NB, NCH>(),
                                                                             fused_waves_per_simd<NB, NCH>()))) void k_pass_bf(
     Geometry g, Bufs B, StepArgs S) {
+  static_assert(!(SPLIT && X2), "the split Xhat needs 16-byte units of 4 features");
   if (halted(B.ctl)) return;
   constexpr int KS = 2 * NCH;                      // 16-feature k-steps (split phase 1)
   constexpr int D32 = 32 * NCH, R32 = 32 * NB;
@@ -222,11 +224,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_
       const int f = ch * 32 + h * 16 + 4 * q;
       // raw values: features >= d meet zero rows of Theta_t (and their rows of the
       // new partial are discarded by the reduction); rows >= n have w = 0
-      const f32x4 t = *reinterpret_cast<const f32x4*>(xrow + (f < d ? f : 0));
-      xv[ch][4 * q + 0] = t.x;
-      xv[ch][4 * q + 1] = t.y;
-      xv[ch][4 * q + 2] = t.z;
-      xv[ch][4 * q + 3] = t.w;
+      if constexpr (X2) {
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        const f32x2 t0 = *reinterpret_cast<const f32x2*>(xrow + (f < d ? f : 0));
+        const f32x2 t1 = *reinterpret_cast<const f32x2*>(xrow + (f + 2 < d ? f + 2 : 0));
+        xv[ch][4 * q + 0] = t0.x;
+        xv[ch][4 * q + 1] = t0.y;
+        xv[ch][4 * q + 2] = t1.x;
+        xv[ch][4 * q + 3] = t1.y;
+      } else {
+        const f32x4 t = *reinterpret_cast<const f32x4*>(xrow + (f < d ? f : 0));
+        xv[ch][4 * q + 0] = t.x;
+        xv[ch][4 * q + 1] = t.y;
+        xv[ch][4 * q + 2] = t.z;
+        xv[ch][4 * q + 3] = t.w;
+      }
     }
   };
   f32x4 unext[NB][4];
@@ -1348,30 +1360,30 @@ static hipError_t pass_bf8_dispatch(const Geometry& g, const Bufs& b, const Step
   }
 }
 
-template <int NB, int NCH, bool SPLIT, bool UFLAT>
+template <int NB, int NCH, bool SPLIT, bool UFLAT, bool X2>
 static hipError_t pass_bf_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   constexpr int lds = fused_lds_bytes(NB, NCH, SPLIT, UFLAT);
   if (lds > kMaxFusedLds) return hipErrorInvalidValue;
   if (lds > (64 << 10)) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_bf<NB, NCH, SPLIT, UFLAT>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_bf<NB, NCH, SPLIT, UFLAT, X2>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((k_pass_bf<NB, NCH, SPLIT, UFLAT>), dim3(g.GB), dim3(kThreads), lds, st, g, b, a);
+  hipLaunchKernelGGL((k_pass_bf<NB, NCH, SPLIT, UFLAT, X2>), dim3(g.GB), dim3(kThreads), lds, st, g, b, a);
   return hipGetLastError();
 }
 
-template <bool SPLIT, bool UFLAT>
+template <bool SPLIT, bool UFLAT, bool X2>
 static hipError_t pass_bf_dispatch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   switch (g.NB * 10 + g.nch) {
-    case 11: return pass_bf_launch<1, 1, SPLIT, UFLAT>(g, b, a, st);
-    case 12: return pass_bf_launch<1, 2, SPLIT, UFLAT>(g, b, a, st);
-    case 13: return pass_bf_launch<1, 3, SPLIT, UFLAT>(g, b, a, st);
-    case 14: return pass_bf_launch<1, 4, SPLIT, UFLAT>(g, b, a, st);
-    case 21: return pass_bf_launch<2, 1, SPLIT, UFLAT>(g, b, a, st);
-    case 22: return pass_bf_launch<2, 2, SPLIT, UFLAT>(g, b, a, st);
-    case 23: return pass_bf_launch<2, 3, SPLIT, UFLAT>(g, b, a, st);
-    case 24: return pass_bf_launch<2, 4, SPLIT, UFLAT>(g, b, a, st);
+    case 11: return pass_bf_launch<1, 1, SPLIT, UFLAT, X2>(g, b, a, st);
+    case 12: return pass_bf_launch<1, 2, SPLIT, UFLAT, X2>(g, b, a, st);
+    case 13: return pass_bf_launch<1, 3, SPLIT, UFLAT, X2>(g, b, a, st);
+    case 14: return pass_bf_launch<1, 4, SPLIT, UFLAT, X2>(g, b, a, st);
+    case 21: return pass_bf_launch<2, 1, SPLIT, UFLAT, X2>(g, b, a, st);
+    case 22: return pass_bf_launch<2, 2, SPLIT, UFLAT, X2>(g, b, a, st);
+    case 23: return pass_bf_launch<2, 3, SPLIT, UFLAT, X2>(g, b, a, st);
+    case 24: return pass_bf_launch<2, 4, SPLIT, UFLAT, X2>(g, b, a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1380,8 +1392,12 @@ int fused_lds_need(int NB, int nch, bool split, bool uflat) { return fused_lds_b
 
 hipError_t launch_pass_bf(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   if (g.fused8) return pass_bf8_dispatch(g, b, a, st);
-  if (g.uflat) return g.split_b ? pass_bf_dispatch<true, true>(g, b, a, st) : pass_bf_dispatch<false, true>(g, b, a, st);
-  return g.split_b ? pass_bf_dispatch<true, false>(g, b, a, st) : pass_bf_dispatch<false, false>(g, b, a, st);
+  if (g.d % 4 != 0) {  // fp32 products only (even d)
+    if (g.split_b || g.d % 2 != 0) return hipErrorInvalidValue;
+    return g.uflat ? pass_bf_dispatch<false, true, true>(g, b, a, st) : pass_bf_dispatch<false, false, true>(g, b, a, st);
+  }
+  if (g.uflat) return g.split_b ? pass_bf_dispatch<true, true, false>(g, b, a, st) : pass_bf_dispatch<false, true, false>(g, b, a, st);
+  return g.split_b ? pass_bf_dispatch<true, false, false>(g, b, a, st) : pass_bf_dispatch<false, false, false>(g, b, a, st);
 }
 
 }  // namespace nlr

@@ -1702,6 +1702,12 @@ static hipError_t pass_a_rows_dispatch(const Geometry& g, const Bufs& b, const S
     case 211: return pass_a_rows_launch<2, 1, 1>(g, b, a, finish, st);
     case 212: return pass_a_rows_launch<2, 1, 2>(g, b, a, finish, st);
     case 214: return pass_a_rows_launch<2, 1, 4>(g, b, a, finish, st);
+    case 221: return pass_a_rows_launch<2, 2, 1>(g, b, a, finish, st);
+    case 222: return pass_a_rows_launch<2, 2, 2>(g, b, a, finish, st);
+    case 224: return pass_a_rows_launch<2, 2, 4>(g, b, a, finish, st);
+    case 241: return pass_a_rows_launch<2, 4, 1>(g, b, a, finish, st);
+    case 242: return pass_a_rows_launch<2, 4, 2>(g, b, a, finish, st);
+    case 244: return pass_a_rows_launch<2, 4, 4>(g, b, a, finish, st);
     case 411: return pass_a_rows_launch<4, 1, 1>(g, b, a, finish, st);
     case 412: return pass_a_rows_launch<4, 1, 2>(g, b, a, finish, st);
     case 414: return pass_a_rows_launch<4, 1, 4>(g, b, a, finish, st);

@@ -64,14 +64,16 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   {
     int fv = 1;
     while (fv < 4 && 16 * fv < d) fv <<= 1;
-    if (d % fv != 0) fv = 1;
+    if (d % fv != 0) fv = (fv == 4 && d % 2 == 0) ? 2 : 1;  // even d: 8-byte loads
     const int ngf = (d + 16 * fv - 1) / (16 * fv);
     int cv = 1;
     while (cv < 4 && 16 * cv < r) cv <<= 1;
     const bool fits = (16 * cv >= r) && (r % cv == 0);
     const int key = fv * 100 + ngf * 10 + cv;
     const bool known = key == 111 || key == 112 || key == 114 || key == 211 || key == 212 || key == 214 ||
-                       key == 411 || key == 412 || key == 414 || key == 421 || key == 422 || key == 424;
+                       key == 221 || key == 222 || key == 224 || key == 241 || key == 242 || key == 244 ||
+                       key == 411 || key == 412 || key == 414 ||
+                       key == 421 || key == 422 || key == 424;
     g.a_rows = (known && fits && aligned16) ? 1 : 0;
     g.a_fv = fv;
     g.a_ngf = ngf;
@@ -123,7 +125,9 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   // register-resident shapes (d <= 128, r <= 64, 16-byte aligned X and U rows of
   // X; U rows of any length move as whole slabs) and its LDS; one persistent
   // workgroup per compute unit
-  const bool shape_f = aligned16 && d <= 128 && r <= 64 && d % 4 == 0 && g.a_rows;
+  // (fp32 products also for even d: X rows then move in 8-byte pieces; the split X stays
+  // in 16-byte units of 4 features per row, so split products need d % 4 == 0)
+  const bool shape_f = aligned16 && d <= 128 && r <= 64 && (d % 4 == 0 || (!split && d % 2 == 0)) && g.a_rows;
   const bool uflat = r % 4 != 0;
   g.fused = (fused && shape_f && fused_lds_need(g.NB, g.nch, split, uflat) <= kMaxFusedLds) ? 1 : 0;
   g.uflat = (g.fused && uflat) ? 1 : 0;

@@ -47,7 +47,9 @@ def test_algorithmic_bytes_per_point():
     ("d=100 r=36", 100_000, 100, 36, True, False, "one-pass"),
     ("d=96", 100_000, 96, 64, True, False, "single-Xhat-pass"),
     ("r=32", 100_000, 128, 32, True, False, "single-Xhat-pass"),
-    ("Table 2 d=50 fp32", 100_000, 50, 30, False, False, "two-pass"),
+    ("Table 2 d=50 fp32", 100_000, 50, 30, False, False, "single-Xhat-pass"),
+    ("d=110 fp32", 100_000, 110, 32, False, False, "single-Xhat-pass"),
+    ("d=51 fp32", 100_000, 51, 30, False, False, "two-pass"),
     ("Table 2 d=200 r=300 fp32", 100_000, 200, 300, False, False, "two-pass"),
 ])
 def test_iteration_form_comes_from_the_library(name, n, d, r, split, two_pass, form):

@@ -165,7 +165,10 @@ def test_trajectory_with_dual_steps():
 @pytest.mark.parametrize("n,d,r,K", [(1037, 13, 10, 7), (777, 64, 16, 16), (4099, 128, 64, 64),
                                      (300, 33, 33, 5), (513, 200, 100, 20), (64, 3, 1, 1),
                                      (1500, 768, 256, 256), (1037, 16, 10, 7), (999, 32, 10, 10),
-                                     (4001, 64, 30, 12), (70, 8, 1, 1), (2050, 128, 50, 20)])
+                                     (4001, 64, 30, 12), (70, 8, 1, 1), (2050, 128, 50, 20),
+                                     # even d, d % 4 == 2: the single-Xhat-pass form with 8-byte X rows
+                                     (4099, 50, 30, 20), (3001, 110, 32, 10), (1037, 18, 4, 4),
+                                     (2001, 46, 12, 6), (999, 126, 60, 12), (513, 2, 2, 2)])
 def test_ragged_shapes(n, d, r, K):
     log(f"ragged n={n} d={d} r={r} K={K}")
     X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 7 + d)

@@ -1,7 +1,8 @@
 """The two smallest simulation settings of Table 2 (balanced mixture, closest centres
 at CNRbar): n = 1e6 with (d, K, r) = (50, 20, 30) and (200, 100, 300).  Neither has the
-split products' shapes (d % 4 != 0; r > 256), so both run the fp32 two-pass form, the
-second with the pass B that takes the columns two blocks at a time.  Checked against
+split products' shapes (d % 4 != 0; r > 256), so both run fp32 products: the first in
+the single-Xhat-pass form with 8-byte Xhat rows, the second in the two-pass form with the
+pass B that takes the columns two blocks at a time.  Checked against
 the fp64 oracle: trajectories with one-step checks on leading-row samples of the draw
 (several tiles and a ragged tail) and the label recovery of Appendix D (r > K) on the
 GPU's factor there, dual steps at the larger shape, and the full 1e6 rows in lockstep.
@@ -30,9 +31,9 @@ def _need_gpu():
 
 def test_table2_forms():
     from paper_2609_36074_amd import nlr
-    for name in ("t2k20", "t2k100"):
+    for name, form in (("t2k20", "single-Xhat-pass"), ("t2k100", "two-pass")):
         _, _, _, wl = make_workload(name, rows=64)
-        assert nlr.FORM_NAMES[nlr.nlr_iteration_form(wl.n, wl.d, wl.r, wl.K, 0)] == "two-pass"
+        assert nlr.FORM_NAMES[nlr.nlr_iteration_form(wl.n, wl.d, wl.r, wl.K, 0)] == form
         assert nlr.nlr_iteration_form(wl.n, wl.d, wl.r, wl.K, nlr.NLR_INIT_SPLIT_F16) == -1
 
 
