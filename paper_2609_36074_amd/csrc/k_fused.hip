@@ -793,7 +793,7 @@ __device__ __forceinline__ void put_unit(unsigned char* slot, f32x4 v, bool odd)
 // PAIRS (one column block, r % 4 == 2): the rows of U are 8-byte aligned only; the
 // factor moves in column pairs (8-byte loads, and 8-byte pieces of the packed slab).
 template <int NB, int NCH, bool PAIRS>
-__global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_bf8(
+__global__ __launch_bounds__(bf8::kThreads8) __attribute__((amdgpu_waves_per_eu(NB * NCH == 1 ? 4 : 2, NB * NCH == 1 ? 4 : 2))) void k_pass_bf8(
     Geometry g, Bufs B, StepArgs S) {
   using P = bf8::Shape<NB, NCH>;
   static_assert(!PAIRS || NB == 1, "column pairs: one column block");

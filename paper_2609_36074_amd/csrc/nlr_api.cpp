@@ -136,8 +136,10 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   g.theta_cols = g.d32 * g.r32 + (g.fused8 ? g.r32 * g.r32 : 0);
   g.SAF = g.SA;
   if (g.fused) {
-    // persistent grid: one (two for the shapes with two waves per SIMD) workgroup per CU
-    const int64_t gmax = (!g.fused8 && g.NB == 1 && g.nch <= 2) ? 512 : 256;
+    // persistent grid: one workgroup per CU; two for the shapes whose kernel holds two
+    // workgroups' waves (the four-wave form with one column block and <= 64 features; the
+    // one-pass form with one column block and <= 32 features: 73 KiB of LDS, 128 VGPRs)
+    const int64_t gmax = (g.NB == 1 && (g.fused8 ? g.nch == 1 : g.nch <= 2)) ? 512 : 256;
     g.GB = (int32_t)(g.tilesB < gmax ? g.tilesB : gmax);
     g.SB = (g.GB + 31) / 32;
     g.SAF = (g.GB + 31) / 32;
