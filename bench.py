@@ -191,6 +191,16 @@ def measure(nlr, torch, np, X_host, Z_host, wl, steps, warm, split, two_pass):
     torch.cuda.synchronize()
     t_graph_ms = ev0.elapsed_time(ev1)
     assert done_g == steps, (done_g, steps)
+    # the row-argmax labels of the final factor (not part of the iteration): one call
+    # after a warm one, HIP events on the library's stream
+    lab = torch.empty(n, dtype=torch.int32, device=X_dev.device)
+    ctx.labels(out=lab)
+    ev0.record(stream)
+    ctx.labels(out=lab)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t_lab_ms = ev0.elapsed_time(ev1)
+    del lab
     ctx.close()
     del Ut, X_dev
     torch.cuda.empty_cache()
@@ -233,7 +243,7 @@ def measure(nlr, torch, np, X_host, Z_host, wl, steps, warm, split, two_pass):
            f"{eff_gbs:.0f} GB/s; graph replays {t_graph_ms / steps:.3f} ms/step")
     for k, v in kinfo.items():
         eprint(f"[bench]   {k:13s} {v['avg_ms'] * 1e3:9.1f} us x {v['launches']}")
-    return {"value": value, "t_ms": t_ms, "t_graph_ms": t_graph_ms, "eff_gbs": eff_gbs, "phys_gbs": phys_gbs, "dual_frac": dual_frac,
+    return {"value": value, "t_ms": t_ms, "t_graph_ms": t_graph_ms, "t_lab_ms": t_lab_ms, "eff_gbs": eff_gbs, "phys_gbs": phys_gbs, "dual_frac": dual_frac,
             "alpha": alpha, "roofline": roofline, "kernels": kinfo, "form": form}
 
 
@@ -241,9 +251,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=20,
-                    help="untimed iterations first (the clock and caches settle: the timed ms per iteration is "
-                         "about 2%% higher after 3 than after 20 at the headline shape)")
+    ap.add_argument("--warmup", type=int, default=50,
+                    help="untimed iterations first (the clock and caches settle: at the headline shape the timed "
+                         "ms per iteration is about 2%% higher after 3 than after 20, and 0.5%% after 50)")
     ap.add_argument("--workload", default="gmm10m")
     ap.add_argument("--gemm", choices=("fp32", "split16"), default="split16",
                     help="split16 (default): two-term fp16 splits of the operands on the fp16 matrix cores "
@@ -335,6 +345,9 @@ def main():
         "hbm_frac": round(m["phys_gbs"] / HBM_PEAK_GBS, 4),
         "effective_two_pass_gbs": round(m["eff_gbs"], 1),
         "roofline": m["roofline"],
+        "labels": {"ms": round(m["t_lab_ms"], 4), "bytes": 4 * n * r + 4 * n,
+                   "gbs": round((4 * n * r + 4 * n) / (m["t_lab_ms"] / 1e3) / 1e9, 1),
+                   "note": "one nlr_labels call (row argmax) on the final factor, outside the timed region"},
         "graph_replay": {"ms_per_step": m["t_graph_ms"] / args.steps, "value": n * args.steps / (m["t_graph_ms"] / 1e3),
                          "note": "the next `steps` iterations as an unprofiled nlr_run makes them: graph replays "
                                  "after the call's first iteration, no events"},

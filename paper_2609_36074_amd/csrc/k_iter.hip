@@ -1618,23 +1618,59 @@ __global__ __launch_bounds__(64) void k_onepass_begin(Geometry g, Bufs B, StepAr
 }
 
 // ---------------------------------------------------------------------------
-// Row-argmax labels, lowest index on ties.
+// Row-argmax labels, lowest index on ties.  A row is read by the 16 lanes of a DPP
+// row, four rows per wave and step: with 16-byte rows (VEC) lane j reads columns
+// 4j .. 4j + 3, 64 + 4j .., so one load instruction covers 256 contiguous bytes of
+// each of its four rows; otherwise lane j reads columns j, j + 16, ...  Each lane
+// keeps its first maximum (columns in increasing order, strict >), then the 16
+// candidates are reduced pairwise: the larger value, the lower column on equal values.
 // ---------------------------------------------------------------------------
+template <bool VEC>
 __global__ __launch_bounds__(kThreads) void k_labels(Geometry g, const float* __restrict__ U,
                                                      int32_t* __restrict__ labels) {
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (i >= g.n) return;
-  const float* row = U + i * g.r;
-  float best = row[0];
-  int arg = 0;
-  for (int c = 1; c < g.r; ++c) {
-    const float v = row[c];
-    if (v > best) {
-      best = v;
-      arg = c;
+  const int lane = threadIdx.x & 63;
+  const int j = lane & 15;
+  const int64_t n = g.n;
+  const int r = g.r;
+  const int64_t rows_per_step = (int64_t)gridDim.x * (kThreads / 16);
+  for (int64_t i = (int64_t)blockIdx.x * (kThreads / 16) + (threadIdx.x >> 4); i - (threadIdx.x >> 4) < n;
+       i += rows_per_step) {
+    const bool vrow = i < n;
+    const float* row = U + (vrow ? i : 0) * (int64_t)r;
+    constexpr int kNone = 0x7fffffff;  // no column seen yet
+    float best = 0.f;
+    int arg = kNone;
+    if (VEC) {
+      for (int c0 = 4 * j; c0 < r; c0 += 64) {  // r % 4 == 0: c0 + 3 < r
+        const f32x4 v = *reinterpret_cast<const f32x4*>(row + c0);
+        const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (arg == kNone || e[k] > best) {
+            best = e[k];
+            arg = c0 + k;
+          }
+      }
+    } else {
+      for (int c = j; c < r; c += 16) {
+        const float v = row[c];
+        if (arg == kNone || v > best) {
+          best = v;
+          arg = c;
+        }
+      }
     }
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1) {
+      const float ob = shfl_xor_f(best, m);
+      const int oa = __shfl_xor(arg, m, 64);
+      if (oa != kNone && (arg == kNone || ob > best || (ob == best && oa < arg))) {
+        best = ob;
+        arg = oa;
+      }
+    }
+    if (vrow && j == 0) labels[i] = arg;
   }
-  labels[i] = arg;
 }
 
 // ---------------------------------------------------------------------------
@@ -1897,8 +1933,13 @@ hipError_t launch_onepass_begin(const Geometry& g, const Bufs& b, const StepArgs
 }
 
 hipError_t launch_labels(const Geometry& g, const Bufs& b, int32_t* labels, hipStream_t st) {
-  const int64_t blocks = (g.n + kThreads - 1) / kThreads;
-  hipLaunchKernelGGL(k_labels, dim3((unsigned)blocks), dim3(kThreads), 0, st, g, (const float*)b.U, labels);
+  // 16 rows per workgroup and step; enough workgroups for eight per CU
+  int64_t blocks = (g.n + 15) / 16;
+  if (blocks > 2048) blocks = 2048;
+  if (g.vec_u)
+    hipLaunchKernelGGL((k_labels<true>), dim3((unsigned)blocks), dim3(kThreads), 0, st, g, (const float*)b.U, labels);
+  else
+    hipLaunchKernelGGL((k_labels<false>), dim3((unsigned)blocks), dim3(kThreads), 0, st, g, (const float*)b.U, labels);
   return hipGetLastError();
 }
 

@@ -412,3 +412,26 @@ def test_two_contexts_interleaved_on_two_streams():
     torch.cuda.synchronize()
     assert np.array_equal(host(a.U), host(ref1.U)) and np.array_equal(host(a.y), host(ref1.y))
     assert np.array_equal(host(b.U), host(ref2.U)) and np.array_equal(host(b.y), host(ref2.y))
+
+
+@pytest.mark.parametrize("r", [1, 4, 10, 64, 300])
+def test_labels_argmax_ties_and_layouts(r):
+    """nlr_labels on factors written directly into the context's U: exact ties (lowest
+    column wins, as numpy's argmax), all-equal rows, the maximum in every column position,
+    16-byte rows (r % 4 == 0) and others; the oracle's labels are the plain argmax."""
+    import torch
+    n = 4099
+    K = min(r, 4)
+    X, _, _ = gaussian_mixture(n, 8, 2, 9.0, seed=5)
+    Z = standard_normal_factor(n, r, seed=6)
+    ctx = make_ctx(X, Z, K, 0.01)
+    rng = np.random.default_rng(r)
+    U = rng.integers(0, 4, size=(n, r)).astype(np.float32)  # small integers: many exact ties
+    U[::7] = 1.0                                             # all-equal rows
+    for c in range(r):                                       # a unique maximum in each column
+        U[11 * c % n, :] = 0.0
+        U[11 * c % n, c] = 5.0
+    ctx.U.copy_(torch.from_numpy(U))
+    lab = ctx.labels().cpu().numpy()
+    assert np.array_equal(lab, onlr.labels(U.astype(np.float64)))
+    assert np.array_equal(lab, np.argmax(U, axis=1).astype(np.int32))
