@@ -168,7 +168,10 @@ def test_trajectory_with_dual_steps():
                                      (4001, 64, 30, 12), (70, 8, 1, 1), (2050, 128, 50, 20),
                                      # even d, d % 4 == 2: the single-Xhat-pass form with 8-byte X rows
                                      (4099, 50, 30, 20), (3001, 110, 32, 10), (1037, 18, 4, 4),
-                                     (2001, 46, 12, 6), (999, 126, 60, 12), (513, 2, 2, 2)])
+                                     (2001, 46, 12, 6), (999, 126, 60, 12), (513, 2, 2, 2),
+                                     # above 256 columns (pass B in pairs of column blocks): Theta in
+                                     # LDS, rows not 16-byte aligned, the largest rank
+                                     (2001, 16, 300, 8), (1501, 24, 301, 5), (999, 40, 448, 4)])
 def test_ragged_shapes(n, d, r, K):
     log(f"ragged n={n} d={d} r={r} K={K}")
     X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 7 + d)
