@@ -67,10 +67,17 @@ __device__ __forceinline__ void stage_tile(float* __restrict__ dst, int ls, cons
 // range of kTPA-row tiles and the Theta blocks of group gy (MBG x NBG blocks of
 // 32 x 32).  Wave w owns m-block w % MBG and all NBG n-blocks, over the k-slice
 // w / MBG of each tile (KS = 4 / MBG slices).  Group 0 also does the row work.
-// FINISH: no matrix product; materialise U and do the row work only.
+// MODE kAFinish: no matrix product; materialise U and do the row work only.
+// Above 128 columns the iteration's pass A runs as two launches: kARows (grid GA x 1:
+// the row work, staging all columns of U) and kATheta (every group stages only its
+// own columns, so a workgroup's LDS is a third of the combined form's).
 // ---------------------------------------------------------------------------
-template <int MBG, int NBG, bool FINISH>
+constexpr int kAIter = 0, kAFinish = 1, kARows = 2, kATheta = 3;
+template <int MBG, int NBG, int MODE>
 __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArgs S) {
+  constexpr bool FINISH = MODE == kAFinish;
+  constexpr bool THETA = MODE == kAIter || MODE == kATheta;  // the matrix product
+  constexpr bool ROWS = MODE != kATheta;                     // the row work (group 0)
   // The finish pass runs after a stop (it still materialises U) but not after a breakdown.
   if (FINISH ? (B.ctl->breakdown != 0) : halted(B.ctl)) return;
   const bool stopped = FINISH && (B.ctl->stop != 0);
@@ -78,9 +85,9 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
   extern __shared__ __align__(16) unsigned char smem_raw[];
   float* smem = reinterpret_cast<float*>(smem_raw);
   const int xs_stride = g.xs_stride;  // MBG*32
-  const int us_stride = g.us_stride;  // r32 + 4
+  const int us_stride = MODE == kATheta ? NBG * 32 + 4 : g.us_stride;  // staged columns + 4
   float* Xs = smem;                                  // kTPA x xs_stride
-  float* Us = Xs + (FINISH ? 0 : kTPA * xs_stride);  // kTPA x us_stride
+  float* Us = Xs + (THETA ? kTPA * xs_stride : 0);   // kTPA x us_stride
   float* ybar_s = Us + kTPA * us_stride;             // kTPA
   float* p_s = ybar_s + kTPA;                        // r32
   double* dred = reinterpret_cast<double*>(p_s + g.r32);  // 256 + 8 doubles (8-byte aligned: r32 even)
@@ -92,7 +99,7 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
   const int gy = blockIdx.y;
   const int mg = gy / g.ngroups;
   const int ng = gy - mg * g.ngroups;
-  const bool do_rows = (gy == 0);
+  const bool do_rows = ROWS && (gy == 0);
   const int64_t n = g.n;
   const int d = g.d, r = g.r, r32 = g.r32;
   const int f0 = mg * MBG * 32;       // first feature of the group
@@ -102,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
   const bool gate = (S.end_work != 0) && (B.ctl->gate != 0) && !stopped;
   const float gam = S.gamma_f;
 
-  // the grid is GA (Theta product) or GAF (finish pass)
+  // the grid is GA (Theta product) or GAF (finish pass, row-work launch)
   const int64_t tb = (int64_t)gx * g.tilesA / gridDim.x;
   const int64_t te = (int64_t)(gx + 1) * g.tilesA / gridDim.x;
 
@@ -134,7 +141,7 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
   for (int64_t tile = tb; tile < te; ++tile) {
     const int64_t row0 = tile * kTPA;
     __syncthreads();
-    if (!FINISH)
+    if (THETA)
       stage_tile(Xs, xs_stride, B.X, d, n, row0, f0, MBG * 32, d, 1.0f, g.vec_x != 0);
     stage_tile(Us, us_stride, B.U, r, n, row0, ucol0, ucols, r, cf, g.vec_u != 0);
     __syncthreads();
@@ -183,7 +190,7 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
         for (int pt = 0; pt < kTPA; ++pt) acc_s2 += (double)ybar_s[pt] * (double)Us[pt * us_stride + sc2];
     }
 
-    if (!FINISH) {
+    if (THETA) {
       // Theta_blk += Xs^T Us over this wave's k-slice (2 rows per instruction).
       const int kbeg = ks * (kTPA / KS);
       const int kend = kbeg + kTPA / KS;
@@ -202,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
   }
 
   // ---- write partials ----
-  if (!FINISH) {
+  if (THETA) {
     // combine k-slices (waves with the same m-block) in a fixed order
     __syncthreads();
     float* comb = smem;  // MBG * NBG * 16 * 64 floats
@@ -1685,23 +1692,49 @@ static hipError_t allow_lds(F* kern, size_t lds) {
                              (int)lds);
 }
 
-template <int MBG, int NBG, bool FIN>
+// Dynamic LDS of k_pass_a in a mode: the staged tiles, ybar and p, the reductions; the
+// k-slice combine of the Theta modes overlaps the tiles
+template <int MBG, int NBG, int MODE>
+static size_t pass_a_lds(const Geometry& g) {
+  const bool theta = MODE == kAIter || MODE == kATheta;
+  const int64_t us = MODE == kATheta ? NBG * 32 + 4 : g.us_stride;
+  const int64_t floats = (theta ? (int64_t)kTPA * g.xs_stride : 0) + (int64_t)kTPA * us + kTPA + g.r32;
+  int64_t bytes = floats * 4 + (256 + 8) * 8;
+  const int64_t comb = (int64_t)MBG * NBG * 16 * 64 * 4;
+  if (theta && comb > floats * 4) bytes = comb + (256 + 8) * 8 + 64;
+  return (size_t)((bytes + 15) & ~15);
+}
+
+template <int MBG, int NBG, int MODE>
 static hipError_t pass_a_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  // the finish pass writes no Theta partials: its grid is sized for the rows alone
-  const dim3 grid(FIN ? g.GAF : g.GA, FIN ? 1 : g.mgroups * g.ngroups);
-  const size_t lds = g.ldsA_bytes;
-  hipError_t e = allow_lds(k_pass_a<MBG, NBG, FIN>, lds);
+  // the finish pass and the row-work launch of the split form write no Theta partials:
+  // their grid is sized for the rows alone
+  const bool rows_only = MODE == kAFinish || MODE == kARows;
+  const dim3 grid(rows_only ? g.GAF : g.GA, rows_only ? 1 : g.mgroups * g.ngroups);
+  const size_t lds = pass_a_lds<MBG, NBG, MODE>(g);
+  if (lds > (160u << 10)) return hipErrorInvalidValue;
+  hipError_t e = allow_lds(k_pass_a<MBG, NBG, MODE>, lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_pass_a<MBG, NBG, FIN>), grid, dim3(kThreads), lds, st, g, b, a);
+  hipLaunchKernelGGL((k_pass_a<MBG, NBG, MODE>), grid, dim3(kThreads), lds, st, g, b, a);
   return hipGetLastError();
 }
 
-template <int MBG, bool FIN>
+template <int MBG, int MODE>
 static hipError_t pass_a_nbg(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   switch (g.NBG) {
-    case 1: return pass_a_launch<MBG, 1, FIN>(g, b, a, st);
-    case 2: return pass_a_launch<MBG, 2, FIN>(g, b, a, st);
-    case 4: return pass_a_launch<MBG, 4, FIN>(g, b, a, st);
+    case 1: return pass_a_launch<MBG, 1, MODE>(g, b, a, st);
+    case 2: return pass_a_launch<MBG, 2, MODE>(g, b, a, st);
+    case 4: return pass_a_launch<MBG, 4, MODE>(g, b, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int MODE>
+static hipError_t pass_a_mbg(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  switch (g.MBG) {
+    case 1: return pass_a_nbg<1, MODE>(g, b, a, st);
+    case 2: return pass_a_nbg<2, MODE>(g, b, a, st);
+    case 4: return pass_a_nbg<4, MODE>(g, b, a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1761,13 +1794,14 @@ hipError_t launch_pass_u(const Geometry& g, const Bufs& b, const StepArgs& a, hi
 
 hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bool finish, hipStream_t st) {
   if (g.a_rows) return pass_a_rows_dispatch(g, b, a, finish ? kPassFinish : kPassIter, st);
-  if (finish) return pass_a_nbg<4, true>(g, b, a, st);
-  switch (g.MBG) {
-    case 1: return pass_a_nbg<1, false>(g, b, a, st);
-    case 2: return pass_a_nbg<2, false>(g, b, a, st);
-    case 4: return pass_a_nbg<4, false>(g, b, a, st);
-    default: return hipErrorInvalidValue;
+  if (finish) return pass_a_nbg<4, kAFinish>(g, b, a, st);
+  if (pass_a_split(g)) {
+    // wide factors: the row work (all columns staged) and the product (own columns only)
+    const hipError_t e = pass_a_mbg<kARows>(g, b, a, st);
+    if (e != hipSuccess) return e;
+    return pass_a_mbg<kATheta>(g, b, a, st);
   }
+  return pass_a_mbg<kAIter>(g, b, a, st);
 }
 
 hipError_t launch_seg_theta(const Geometry& g, const Bufs& b, int64_t rows, int nseg, hipStream_t st) {
@@ -1807,8 +1841,9 @@ hipError_t launch_seg_a_rows(const Geometry& g, const Bufs& b, int64_t rows, boo
 }
 
 hipError_t launch_seg_a(const Geometry& g, const Bufs& b, bool finish, hipStream_t st) {
-  // the register-resident finish runs on the pass-A grid; the generic one on GAF
-  const int64_t rows = (finish && !g.a_rows) ? g.GAF : g.GA;
+  // the register-resident finish runs on the pass-A grid; the generic one, and the
+  // row-work launch of the split generic pass A, on GAF
+  const int64_t rows = ((finish && !g.a_rows) || (!finish && pass_a_split(g))) ? g.GAF : g.GA;
   return launch_seg_a_rows(g, b, rows, finish, st);
 }
 

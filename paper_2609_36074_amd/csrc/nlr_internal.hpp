@@ -178,6 +178,9 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
 // dynamic LDS of the fused pass B for (NB, nch, split, U moved as whole slabs)
 int fused_lds_need(int NB, int nch, bool split, bool uflat);
 bool fused8_shape(int NB, int nch, int r);
+// generic pass A above 128 columns: a row-work launch (GAF workgroups, all columns of U
+// staged) and a Theta launch whose workgroups stage only their own columns
+inline bool pass_a_split(const Geometry& g) { return !g.a_rows && g.r32 > 128; }
 constexpr int kMaxFusedLds = 160 << 10;
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
 
