@@ -51,9 +51,6 @@ __device__ __forceinline__ double dpp_d(double v) {
   const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, 0xF, 0xF, false);
   return __hiloint2double(hi, lo);
 }
-// Sum over the 16 lanes of a DPP row with involution pairings (xor 1, xor 2,
-// half-row mirror, row mirror): every step adds two equal partial sums, so all
-// lanes end with the same bits.
 // Sum over the 8 lanes of each DPP half row, bitwise the same in all 8 lanes.
 __device__ __forceinline__ double row8_sum_d(double v) {
   v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
@@ -62,6 +59,9 @@ __device__ __forceinline__ double row8_sum_d(double v) {
   return v;
 }
 
+// Sum over the 16 lanes of a DPP row with involution pairings (xor 1, xor 2,
+// half-row mirror, row mirror): every step adds two equal partial sums, so all
+// lanes end with the same bits.
 __device__ __forceinline__ double row16_sum_d(double v) {
   v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
   v += dpp_d<0x4E>(v);   // quad_perm [2,3,0,1]

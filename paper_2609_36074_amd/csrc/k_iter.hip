@@ -68,11 +68,11 @@ __device__ __forceinline__ void stage_tile(float* __restrict__ dst, int ls, cons
 // 32 x 32).  Wave w owns m-block w % MBG and all NBG n-blocks, over the k-slice
 // w / MBG of each tile (KS = 4 / MBG slices).  Group 0 also does the row work.
 // MODE kAFinish: no matrix product; materialise U and do the row work only.
-// Above 128 columns the iteration's pass A runs as two launches: kARows (grid GA x 1:
-// the row work, staging all columns of U) and kATheta (every group stages only its
-// own columns, so a workgroup's LDS is a third of the combined form's).
+// Above 128 columns the iteration's pass A runs as two launches: the row work
+// (k_rows_wide, below) and kATheta: the product alone, every group staging only its
+// own columns of U, so that a workgroup's LDS is about a third of the combined form's.
 // ---------------------------------------------------------------------------
-constexpr int kAIter = 0, kAFinish = 1, kARows = 2, kATheta = 3;
+constexpr int kAIter = 0, kAFinish = 1, kATheta = 2;
 template <int MBG, int NBG, int MODE>
 __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArgs S) {
   constexpr bool FINISH = MODE == kAFinish;
@@ -262,6 +262,125 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
       ap[4 + tid] = FINISH ? 0.0 : t;
     }
     if (sc2 < r32) ap[4 + sc2] = FINISH ? 0.0 : acc_s2;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Row work of the generic pass A above 128 columns (its first launch): no LDS
+// staging; each wave streams whole rows of U, lane l holding the columns
+// l + 64 j (CPL = ceil(r / 64) of them), RPI rows at a time.  Per row: u = fl(c_f w),
+// q = u.p - 1 (FP64, summed over the wave by an xor butterfly, so every lane has
+// the same bits), the gated dual step (eq. of the stored dual), ybar; then
+// s += ybar u, ||q||^2 and ytilde^T q in FP64.  Grid GAF; workgroup gx takes a
+// contiguous range of rows, its waves every fourth row of it, and writes partial row
+// gx in the layout of pass A (qq, yq, 0, 0, s).
+// ---------------------------------------------------------------------------
+template <int CPL>
+__global__ __launch_bounds__(kThreads) void k_rows_wide(Geometry g, Bufs B, StepArgs S) {
+  if (halted(B.ctl)) return;
+  constexpr int RPI = 4;  // rows per wave and step
+  __shared__ double sred[4 * 64 * CPL];
+  __shared__ double dred[kThreads + 8];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t n = g.n;
+  const int r = g.r;
+  const float cf = B.ctl->c_f;
+  const bool gate = (S.end_work != 0) && (B.ctl->gate != 0);
+  const float gam = S.gamma_f;
+
+  float pl[CPL];
+  bool okc[CPL];
+  int colo[CPL];  // column read (0 for the lanes past the last column)
+#pragma unroll
+  for (int j = 0; j < CPL; ++j) {
+    const int col = lane + 64 * j;
+    okc[j] = col < r;
+    colo[j] = okc[j] ? col : 0;
+    pl[j] = okc[j] ? B.p[col] : 0.f;
+  }
+  double sacc[CPL];
+#pragma unroll
+  for (int j = 0; j < CPL; ++j) sacc[j] = 0.0;
+  double acc_qq = 0.0, acc_yq = 0.0;
+
+  const int64_t rb = (int64_t)blockIdx.x * n / gridDim.x;
+  const int64_t re = (int64_t)(blockIdx.x + 1) * n / gridDim.x;
+  for (int64_t base = rb + (int64_t)wave * RPI; base < re; base += 4 * RPI) {
+    float u[RPI][CPL];
+    float yt[RPI];
+    // every load reads a valid address (row rb, column 0 in place of those out of range)
+    // and the value is dropped afterwards, so that no load sits behind a branch; all
+    // loads of the step are issued before any of their values is used
+#pragma unroll
+    for (int i = 0; i < RPI; ++i) {
+      const int64_t row = base + i;
+      const float* src = B.U + (row < re ? row : rb) * r;
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) u[i][j] = src[colo[j]];
+      yt[i] = B.y[row < re ? row : rb];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < RPI; ++i) {
+      const bool okr = base + i < re;
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) u[i][j] = (okr && okc[j]) ? u[i][j] * cf : 0.f;
+      yt[i] = okr ? yt[i] : 0.f;
+    }
+    double dot[RPI];
+#pragma unroll
+    for (int i = 0; i < RPI; ++i) {
+      dot[i] = 0.0;
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) dot[i] += (double)u[i][j] * (double)pl[j];
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1)
+#pragma unroll
+      for (int i = 0; i < RPI; ++i) dot[i] += shfl_xor_d(dot[i], m);
+#pragma unroll
+    for (int i = 0; i < RPI; ++i) {
+      const int64_t row = base + i;
+      if (row < re) {
+        const float q = (float)(dot[i] - 1.0);
+        float y = yt[i];
+        if (gate) {
+          y = fmaf(gam, q, y);
+          if (lane == 0) B.y[row] = y;
+        }
+        const float ybar = fmaf(gam, q, y);
+        if (lane == 0) {
+          acc_qq += (double)q * (double)q;
+          acc_yq += (double)y * (double)q;
+        }
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) sacc[j] += (double)ybar * (double)u[i][j];
+      }
+    }
+  }
+
+  double* ap = B.a_part + (int64_t)blockIdx.x * (4 + g.r32);
+  const double qq = block_sum_d(acc_qq, dred);
+  const double yq = block_sum_d(acc_yq, dred);
+  if (tid == 0) {
+    ap[0] = qq;
+    ap[1] = yq;
+    ap[2] = ap[3] = 0.0;
+  }
+  // s: the four waves' sums of a column, added in wave order
+#pragma unroll
+  for (int j = 0; j < CPL; ++j) sred[(wave * CPL + j) * 64 + lane] = sacc[j];
+  __syncthreads();
+  for (int c = tid; c < g.r32; c += kThreads) {
+    double t = 0.0;
+    if (c < 64 * CPL) {
+      const int j = c >> 6, l = c & 63;
+      t = ((sred[(0 * CPL + j) * 64 + l] + sred[(1 * CPL + j) * 64 + l]) + sred[(2 * CPL + j) * 64 + l]) +
+          sred[(3 * CPL + j) * 64 + l];
+    }
+    ap[4 + c] = t;
   }
 }
 
@@ -1693,7 +1812,7 @@ static hipError_t allow_lds(F* kern, size_t lds) {
 }
 
 // Dynamic LDS of k_pass_a in a mode: the staged tiles, ybar and p, the reductions; the
-// k-slice combine of the Theta modes overlaps the tiles
+// combine of the k-slices (MBG < 4) overlaps the tiles
 template <int MBG, int NBG, int MODE>
 static size_t pass_a_lds(const Geometry& g) {
   const bool theta = MODE == kAIter || MODE == kATheta;
@@ -1701,16 +1820,14 @@ static size_t pass_a_lds(const Geometry& g) {
   const int64_t floats = (theta ? (int64_t)kTPA * g.xs_stride : 0) + (int64_t)kTPA * us + kTPA + g.r32;
   int64_t bytes = floats * 4 + (256 + 8) * 8;
   const int64_t comb = (int64_t)MBG * NBG * 16 * 64 * 4;
-  if (theta && comb > floats * 4) bytes = comb + (256 + 8) * 8 + 64;
+  if (theta && MBG < 4 && comb > floats * 4) bytes = comb + (256 + 8) * 8 + 64;
   return (size_t)((bytes + 15) & ~15);
 }
 
 template <int MBG, int NBG, int MODE>
 static hipError_t pass_a_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  // the finish pass and the row-work launch of the split form write no Theta partials:
-  // their grid is sized for the rows alone
-  const bool rows_only = MODE == kAFinish || MODE == kARows;
-  const dim3 grid(rows_only ? g.GAF : g.GA, rows_only ? 1 : g.mgroups * g.ngroups);
+  // the finish pass writes no Theta partials: its grid is sized for the rows alone
+  const dim3 grid(MODE == kAFinish ? g.GAF : g.GA, MODE == kAFinish ? 1 : g.mgroups * g.ngroups);
   const size_t lds = pass_a_lds<MBG, NBG, MODE>(g);
   if (lds > (160u << 10)) return hipErrorInvalidValue;
   hipError_t e = allow_lds(k_pass_a<MBG, NBG, MODE>, lds);
@@ -1725,8 +1842,23 @@ static hipError_t pass_a_nbg(const Geometry& g, const Bufs& b, const StepArgs& a
     case 1: return pass_a_launch<MBG, 1, MODE>(g, b, a, st);
     case 2: return pass_a_launch<MBG, 2, MODE>(g, b, a, st);
     case 4: return pass_a_launch<MBG, 4, MODE>(g, b, a, st);
+    case 5: return pass_a_launch<MBG, 5, MODE>(g, b, a, st);
+    case 7: return pass_a_launch<MBG, 7, MODE>(g, b, a, st);
     default: return hipErrorInvalidValue;
   }
+}
+
+static hipError_t launch_rows_wide(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  const dim3 grid(g.GAF), blk(kThreads);
+  switch ((g.r + 63) / 64) {
+    case 3: hipLaunchKernelGGL(k_rows_wide<3>, grid, blk, 0, st, g, b, a); break;
+    case 4: hipLaunchKernelGGL(k_rows_wide<4>, grid, blk, 0, st, g, b, a); break;
+    case 5: hipLaunchKernelGGL(k_rows_wide<5>, grid, blk, 0, st, g, b, a); break;
+    case 6: hipLaunchKernelGGL(k_rows_wide<6>, grid, blk, 0, st, g, b, a); break;
+    case 7: hipLaunchKernelGGL(k_rows_wide<7>, grid, blk, 0, st, g, b, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 template <int MODE>
@@ -1797,7 +1929,7 @@ hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bo
   if (finish) return pass_a_nbg<4, kAFinish>(g, b, a, st);
   if (pass_a_split(g)) {
     // wide factors: the row work (all columns staged) and the product (own columns only)
-    const hipError_t e = pass_a_mbg<kARows>(g, b, a, st);
+    const hipError_t e = launch_rows_wide(g, b, a, st);
     if (e != hipSuccess) return e;
     return pass_a_mbg<kATheta>(g, b, a, st);
   }

@@ -36,9 +36,11 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   // the two-pass kernels take in groups of two blocks
   g.NB = r <= 256 ? next_pow2((r + 31) / 32) : 2 * ((r + 63) / 64);
   g.r32 = 32 * g.NB;
-  // pass A groups: MBG in {1, 2, 4}, NBG in {1, 2, 4} dividing NB
+  // pass A groups: MBG in {1, 2, 4}, NBG in {1, 2, 4, 5, 7} dividing NB; 10 and 14 blocks
+  // (above 256 columns, where the product runs in a launch of its own) in two groups
   g.MBG = g.MB >= 3 ? 4 : g.MB;
   g.NBG = g.NB % 4 == 0 ? 4 : (g.NB % 2 == 0 ? 2 : 1);
+  if (g.NB == 10 || g.NB == 14) g.NBG = g.NB / 2;
   g.mgroups = (g.MB + g.MBG - 1) / g.MBG;
   g.ngroups = (g.NB + g.NBG - 1) / g.NBG;
   g.tilesA = (n + kTPA - 1) / kTPA;
@@ -53,13 +55,6 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   }
   g.xs_stride = g.MBG * 32;
   g.us_stride = g.r32 + 4;
-  {
-    const int64_t floats = (int64_t)kTPA * g.xs_stride + (int64_t)kTPA * g.us_stride + kTPA + g.r32;
-    int64_t bytes = floats * 4 + (256 + 8) * 8;
-    const int64_t comb = (int64_t)g.MBG * g.NBG * 16 * 64 * 4;
-    if (comb > floats * 4) bytes = comb + (256 + 8) * 8 + 64;  // combine scratch overlaps the tiles
-    g.ldsA_bytes = (int32_t)((bytes + 15) & ~15);
-  }
   // register-resident pass A (16x16x4 blocks): all of Theta in one wave, FV*NGF*CV <= 32
   {
     int fv = 1;

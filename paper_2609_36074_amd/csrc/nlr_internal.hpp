@@ -73,11 +73,10 @@ struct Geometry {
   int32_t d32, r32;     // d, r rounded up to multiples of 32
   int32_t MB, NB;       // 32-wide blocks of d and r
   // pass A
-  int32_t MBG, NBG;     // m-blocks / n-blocks per workgroup group (1, 2 or 4)
+  int32_t MBG, NBG;     // m-blocks (1, 2 or 4) / n-blocks (1, 2, 4, 5 or 7) per workgroup group
   int32_t mgroups, ngroups;
   int32_t GA;           // row-chunk workgroups per group
   int64_t tilesA;       // ceil(n / kTPA)
-  int32_t ldsA_bytes;   // dynamic LDS of pass A
   int32_t xs_stride, us_stride;
   int32_t a_rows;       // 1: register-resident pass A (k_pass_a_rows)
   int32_t a_fv, a_ngf, a_cv;  // its features per lane, feature groups, columns per lane
@@ -178,8 +177,8 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
 // dynamic LDS of the fused pass B for (NB, nch, split, U moved as whole slabs)
 int fused_lds_need(int NB, int nch, bool split, bool uflat);
 bool fused8_shape(int NB, int nch, int r);
-// generic pass A above 128 columns: a row-work launch (GAF workgroups, all columns of U
-// staged) and a Theta launch whose workgroups stage only their own columns
+// generic pass A above 128 columns: a row-work launch (GAF workgroups streaming rows
+// of U) and a Theta launch whose workgroups stage only their own columns
 inline bool pass_a_split(const Geometry& g) { return !g.a_rows && g.r32 > 128; }
 constexpr int kMaxFusedLds = 160 << 10;
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
