@@ -266,6 +266,163 @@ __global__ __launch_bounds__(kThreads) void k_pass_a(Geometry g, Bufs B, StepArg
 }
 
 // ---------------------------------------------------------------------------
+// Theta = Xhat^T U of the generic pass A above 128 columns for 16-byte aligned rows
+// (d % 4 == 0, r % 4 == 0): the product of k_pass_a's Theta mode (same groups, waves,
+// k-slices and summation order, so the same bits) with the next tile's rows loaded
+// into registers while the matrix cores work on the current one.  Per tile a thread
+// holds XV + UV 16-byte pieces; loads past the last row or column read a valid
+// address and are zeroed, so none waits behind a branch.  The waves whose m-block
+// lies past the last feature skip the product (their partial rows are not written).
+// ---------------------------------------------------------------------------
+template <int MBG, int NBG>
+__global__ __launch_bounds__(kThreads) void k_theta_wide(Geometry g, Bufs B) {
+  if (halted(B.ctl)) return;
+  constexpr int KS = 4 / MBG;
+  constexpr int XS = MBG * 32 + 4;                // LDS row strides (floats)
+  constexpr int US = NBG * 32 + 4;
+  constexpr int XR4 = MBG * 8, UR4 = NBG * 8;     // 16-byte pieces per tile row
+  constexpr int XV = kTPA * XR4 / kThreads;       // pieces per thread and tile
+  constexpr int UV = kTPA * UR4 / kThreads;
+  static_assert(XV * kThreads == kTPA * XR4 && UV * kThreads == kTPA * UR4, "whole pieces per thread");
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  float* Xs = reinterpret_cast<float*>(smem_raw);  // kTPA x XS
+  float* Us = Xs + kTPA * XS;                      // kTPA x US
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int gx = blockIdx.x;
+  const int gy = blockIdx.y;
+  const int mg = gy / g.ngroups;
+  const int ng = gy - mg * g.ngroups;
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r, r32 = g.r32;
+  const int f0 = mg * MBG * 32;
+  const int c0 = ng * NBG * 32;
+  const float cf = B.ctl->c_f;
+  const int64_t tb = (int64_t)gx * g.tilesA / gridDim.x;
+  const int64_t te = (int64_t)(gx + 1) * g.tilesA / gridDim.x;
+  const int mb = wave % MBG;
+  const int ks = wave / MBG;
+  const bool active = f0 + mb * 32 < g.d32;
+
+  // this thread's pieces: tile row and column offset (fixed), validity of the column
+  int xo[XV], uo[UV];
+  bool xk[XV], uk[UV];
+#pragma unroll
+  for (int i = 0; i < XV; ++i) {
+    const int v = tid + i * kThreads, row = v / XR4, c = 4 * (v - row * XR4);
+    xk[i] = f0 + c < d;
+    xo[i] = row * d + (xk[i] ? f0 + c : 0);
+  }
+#pragma unroll
+  for (int i = 0; i < UV; ++i) {
+    const int v = tid + i * kThreads, row = v / UR4, c = 4 * (v - row * UR4);
+    uk[i] = c0 + c < r;
+    uo[i] = row * r + (uk[i] ? c0 + c : 0);
+  }
+  f32x4 xr[XV], ur[UV];
+  // rows of tile t: a row past the last is read as row 0 of the tile and zeroed
+  auto load = [&](int64_t tile) {
+    const int64_t row0 = tile * kTPA;
+    const int valid = (int)((n - row0) < kTPA ? (n - row0) : kTPA);
+    const float* xb = B.X + row0 * d;
+    const float* ub = B.U + row0 * r;
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int row = (tid + i * kThreads) / XR4;
+      xr[i] = *reinterpret_cast<const f32x4*>(xb + (row < valid ? xo[i] : xo[i] - row * d));
+    }
+#pragma unroll
+    for (int i = 0; i < UV; ++i) {
+      const int row = (tid + i * kThreads) / UR4;
+      ur[i] = *reinterpret_cast<const f32x4*>(ub + (row < valid ? uo[i] : uo[i] - row * r));
+    }
+  };
+
+  f32x16 acc[NBG];
+#pragma unroll
+  for (int j = 0; j < NBG; ++j)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+
+  if (tb < te) load(tb);
+  for (int64_t tile = tb; tile < te; ++tile) {
+    const int64_t row0 = tile * kTPA;
+    const int valid = (int)((n - row0) < kTPA ? (n - row0) : kTPA);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int v = tid + i * kThreads, row = v / XR4, c = 4 * (v - row * XR4);
+      const bool ok = xk[i] && row < valid;
+      const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+      *reinterpret_cast<f32x4*>(Xs + row * XS + c) = ok ? xr[i] : zero;
+    }
+#pragma unroll
+    for (int i = 0; i < UV; ++i) {
+      const int v = tid + i * kThreads, row = v / UR4, c = 4 * (v - row * UR4);
+      const bool ok = uk[i] && row < valid;
+      f32x4 t = ur[i];
+      t.x = ok ? t.x * cf : 0.f;
+      t.y = ok ? t.y * cf : 0.f;
+      t.z = ok ? t.z * cf : 0.f;
+      t.w = ok ? t.w * cf : 0.f;
+      *reinterpret_cast<f32x4*>(Us + row * US + c) = t;
+    }
+    __syncthreads();
+    if (tile + 1 < te) load(tile + 1);
+    if (active) {
+      const int kbeg = ks * (kTPA / KS);
+      const int kend = kbeg + kTPA / KS;
+      const int lr = lane >> 5;
+      const int lc = lane & 31;
+#pragma unroll 4
+      for (int k = kbeg; k < kend; k += 2) {
+        const float a = Xs[(k + lr) * XS + mb * 32 + lc];
+#pragma unroll
+        for (int j = 0; j < NBG; ++j) {
+          const float bv = Us[(k + lr) * US + j * 32 + lc];
+          acc[j] = mfma32x32x2(a, bv, acc[j]);
+        }
+      }
+    }
+  }
+
+  // combine k-slices (waves with the same m-block) in a fixed order, then write
+  __syncthreads();
+  float* comb = Xs;  // MBG * NBG * 16 * 64 floats
+  for (int slice = 1; slice < KS; ++slice) {
+    if (ks == slice) {
+#pragma unroll
+      for (int j = 0; j < NBG; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) comb[((mb * NBG + j) * 16 + v) * 64 + lane] = acc[j][v];
+    }
+    __syncthreads();
+    if (ks == 0) {
+#pragma unroll
+      for (int j = 0; j < NBG; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[j][v] += comb[((mb * NBG + j) * 16 + v) * 64 + lane];
+    }
+    __syncthreads();
+  }
+  if (ks == 0 && active) {
+    float* part = B.theta_part + (int64_t)gx * g.theta_cols;
+    const int lr = lane >> 5, lc = lane & 31;
+#pragma unroll
+    for (int j = 0; j < NBG; ++j) {
+      const int col = c0 + j * 32 + lc;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int f = f0 + mb * 32 + 8 * (v >> 2) + 4 * lr + (v & 3);
+        if (f < g.d32 && col < r32) part[(int64_t)f * r32 + col] = acc[j][v];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Row work of the generic pass A above 128 columns (its first launch): no LDS
 // staging; each wave streams whole rows of U, lane l holding the columns
 // l + 64 j (CPL = ceil(r / 64) of them), RPI rows at a time.  Per row: u = fl(c_f w),
@@ -1848,6 +2005,36 @@ static hipError_t pass_a_nbg(const Geometry& g, const Bufs& b, const StepArgs& a
   }
 }
 
+template <int MBG, int NBG>
+static hipError_t theta_wide_launch(const Geometry& g, const Bufs& b, hipStream_t st) {
+  const size_t tiles = (size_t)kTPA * ((MBG * 32 + 4) + (NBG * 32 + 4)) * 4;
+  const size_t comb = MBG < 4 ? (size_t)MBG * NBG * 16 * 64 * 4 : 0;
+  const size_t lds = tiles > comb ? tiles : comb;
+  hipError_t e = allow_lds(k_theta_wide<MBG, NBG>, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_theta_wide<MBG, NBG>), dim3(g.GA, g.mgroups * g.ngroups), dim3(kThreads), lds, st, g, b);
+  return hipGetLastError();
+}
+
+template <int MBG>
+static hipError_t theta_wide_nbg(const Geometry& g, const Bufs& b, hipStream_t st) {
+  switch (g.NBG) {
+    case 4: return theta_wide_launch<MBG, 4>(g, b, st);
+    case 5: return theta_wide_launch<MBG, 5>(g, b, st);
+    case 7: return theta_wide_launch<MBG, 7>(g, b, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+static hipError_t launch_theta_wide(const Geometry& g, const Bufs& b, hipStream_t st) {
+  switch (g.MBG) {
+    case 1: return theta_wide_nbg<1>(g, b, st);
+    case 2: return theta_wide_nbg<2>(g, b, st);
+    case 4: return theta_wide_nbg<4>(g, b, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 static hipError_t launch_rows_wide(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   const dim3 grid(g.GAF), blk(kThreads);
   switch ((g.r + 63) / 64) {
@@ -1931,6 +2118,8 @@ hipError_t launch_pass_a(const Geometry& g, const Bufs& b, const StepArgs& a, bo
     // wide factors: the row work (all columns staged) and the product (own columns only)
     const hipError_t e = launch_rows_wide(g, b, a, st);
     if (e != hipSuccess) return e;
+    // 16-byte rows: the product with the next tile prefetched into registers
+    if (g.vec_x && g.vec_u && (g.NBG == 4 || g.NBG == 5 || g.NBG == 7)) return launch_theta_wide(g, b, st);
     return pass_a_mbg<kATheta>(g, b, a, st);
   }
   return pass_a_mbg<kAIter>(g, b, a, st);
