@@ -1257,6 +1257,239 @@ __global__ __launch_bounds__(kThreads) void k_pass_b(Geometry g, Bufs B, StepArg
 }
 
 // ---------------------------------------------------------------------------
+// Pass B with Theta streamed through LDS, for a Theta larger than LDS holds whole
+// (d32 r32 4 > 64 KiB) and 16-byte rows.  As k_pass_b (waves, rows, the operand
+// layout of Theta and the k-order of the products), with the columns in NB / CG
+// groups of CG blocks: per 128-row super-tile, for each group and each 32-feature
+// chunk, the workgroup stages the chunk's Theta operands (4 CG KiB) in one of two
+// LDS buffers and every wave multiplies its rows by them.  The next chunk's Theta
+// operands and Xhat features are loaded into registers while the matrix cores work
+// on the current one: one barrier per chunk.  Loads past the last row, feature or
+// column read a valid address and are zeroed, so that no load waits behind a branch.
+// ---------------------------------------------------------------------------
+template <int CG>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_pass_b_stream(
+    Geometry g, Bufs B, StepArgs S) {
+  if (halted(B.ctl)) return;
+  constexpr int TCF = 4 * CG * 256;  // floats of a chunk's Theta operands
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  float* tbuf = reinterpret_cast<float*>(smem_raw);       // 2 x TCF
+  float* ps = tbuf + 2 * TCF;                              // r32
+  float* ss = ps + g.r32;                                  // r32
+  double* colred = reinterpret_cast<double*>(smem_raw);   // 4 x r32, after the tile loop
+  double* dred = reinterpret_cast<double*>(ss + g.r32);   // 4
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int h = lane >> 5;
+  const int li = lane & 31;
+  const int64_t n = g.n;
+  const int d = g.d, r = g.r, r32 = g.r32, NB = g.NB;
+  const int nch = g.nch;
+  const int ngr = NB / CG;  // column groups (1 or 2)
+  const float cf = B.ctl->c_f;
+  const float gam = S.gamma_f;
+  const float two_alpha = S.two_alpha_f;
+  const float neg_alpha = -S.alpha_f;
+
+  for (int c = tid; c < r32; c += kThreads) {
+    ps[c] = B.p[c];
+    ss[c] = B.s[c];
+  }
+
+  double sa = 0.0, sb = 0.0, sh = 0.0;
+  double colacc[2 * CG];
+#pragma unroll
+  for (int m = 0; m < 2 * CG; ++m) colacc[m] = 0.0;
+  int base = 0;  // local index (8 qd + e ordering) of the column sum this lane keeps
+  if (li & 16) base += 8;
+  if (li & 8) base += 4;
+  if (li & 4) base += 2;
+  if (li & 2) base += 1;
+
+  const int64_t sb0 = (int64_t)blockIdx.x * g.tilesB / g.GB;
+  const int64_t sb1 = (int64_t)(blockIdx.x + 1) * g.tilesB / g.GB;
+
+  // Theta operands of chunk (group cgi, chunk ch): piece v = tid + 256 i of the chunk is
+  // j = v / (64 CG), block m = v / 64 % CG, lane v % 64 of the pass-B layout
+  int toff[CG];  // piece of chunk (0, 0) this thread stages, in pieces of 16 bytes
+#pragma unroll
+  for (int i = 0; i < CG; ++i) {
+    const int v = tid + kThreads * i;
+    toff[i] = ((v / (64 * CG)) * NB + (v / 64) % CG) * 64 + (v & 63);
+  }
+  f32x4 tr[CG];
+  f32x4 xr[4];
+  // chunk ch of group cgi: pieces ch 4 NB 64 + cgi CG 64 + toff
+  auto load_chunk = [&](int64_t st, int cgi, int ch) {
+    const float* tsrc = B.theta + ((int64_t)ch * 4 * NB * 64 + cgi * CG * 64) * 4;
+#pragma unroll
+    for (int i = 0; i < CG; ++i) tr[i] = *reinterpret_cast<const f32x4*>(tsrc + toff[i] * 4);
+    const int64_t pt = st * kTPB + wave * 32 + li;
+    const float* xrow = B.X + (pt < n ? pt : 0) * (int64_t)d;
+    const int fb = ch * 32 + h * 16;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) xr[q] = *reinterpret_cast<const f32x4*>(xrow + (fb + 4 * q < d ? fb + 4 * q : 0));
+  };
+
+  if (sb0 < sb1) load_chunk(sb0, 0, 0);
+  int kbuf = 0;
+  for (int64_t st = sb0; st < sb1; ++st) {
+    const int64_t pt = st * kTPB + wave * 32 + li;
+    const bool vpt = pt < n;
+    float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
+    // (the opaque copy keeps the p/s reads inside the tile loop instead of hoisting
+    // 2*16*NB loop-invariant registers out of it)
+    int lds_off = 0;
+    asm volatile("" : "+v"(lds_off));
+    const float* psl = ps + lds_off;
+    const float* ssl = ss + lds_off;
+    auto load_u4 = [&](int c, float out[4]) {
+      const f32x4 t = *reinterpret_cast<const f32x4*>(urow + (c < r ? c : 0));
+      const bool ok = vpt && c < r;
+      out[0] = ok ? t.x * cf : 0.f;
+      out[1] = ok ? t.y * cf : 0.f;
+      out[2] = ok ? t.z * cf : 0.f;
+      out[3] = ok ? t.w * cf : 0.f;
+    };
+    // q = u.p - 1 over the whole row (fp32 dot over the lane's half, then the other half)
+    float dotf = 0.f;
+    for (int m = 0; m < NB; ++m)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int c = 32 * m + 8 * qd + 4 * h;
+        float u4[4];
+        load_u4(c, u4);
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+        dotf = fmaf(u4[0], pv.x, dotf);
+        dotf = fmaf(u4[1], pv.y, dotf);
+        dotf = fmaf(u4[2], pv.z, dotf);
+        dotf = fmaf(u4[3], pv.w, dotf);
+      }
+    dotf += shfl_xor_f(dotf, 32);
+    const float yv = B.y[vpt ? pt : 0];
+    const float ybar = vpt ? fmaf(gam, dotf - 1.0f, yv) : 0.f;
+
+    for (int cgi = 0; cgi < ngr; ++cgi) {
+      f32x16 acc[CG];
+#pragma unroll
+      for (int m = 0; m < CG; ++m)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[m][v] = 0.f;
+      for (int ch = 0; ch < nch; ++ch) {
+        // stage this chunk's Theta operands; the barrier also ends every wave's reads
+        // of the buffer two chunks back
+        float* tb = tbuf + kbuf * TCF;
+#pragma unroll
+        for (int i = 0; i < CG; ++i) *reinterpret_cast<f32x4*>(tb + (tid + kThreads * i) * 4) = tr[i];
+        const bool xok = vpt;
+        float xv[16];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const bool ok = xok && (ch * 32 + h * 16 + 4 * q < d);
+          xv[4 * q + 0] = ok ? xr[q].x : 0.f;
+          xv[4 * q + 1] = ok ? xr[q].y : 0.f;
+          xv[4 * q + 2] = ok ? xr[q].z : 0.f;
+          xv[4 * q + 3] = ok ? xr[q].w : 0.f;
+        }
+        __syncthreads();
+        // prefetch the next chunk: next feature chunk, else next group, else next super-tile
+        {
+          const bool nc = ch + 1 < nch, ng = !nc && cgi + 1 < ngr;
+          const int64_t st2 = (nc || ng) ? st : st + 1;
+          if (st2 < sb1) load_chunk(st2, nc ? cgi : (ng ? cgi + 1 : 0), nc ? ch + 1 : 0);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          f32x4 a[CG];
+#pragma unroll
+          for (int m = 0; m < CG; ++m) a[m] = *reinterpret_cast<const f32x4*>(tb + ((j * CG + m) * 64 + lane) * 4);
+#pragma unroll
+          for (int m = 0; m < CG; ++m) {
+            acc[m] = mfma32x32x2(a[m].x, xv[4 * j + 0], acc[m]);
+            acc[m] = mfma32x32x2(a[m].y, xv[4 * j + 1], acc[m]);
+            acc[m] = mfma32x32x2(a[m].z, xv[4 * j + 2], acc[m]);
+            acc[m] = mfma32x32x2(a[m].w, xv[4 * j + 3], acc[m]);
+          }
+          // the operands of one feature quad at a time (4 CG registers)
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        kbuf ^= 1;
+      }
+      // ---- epilogue of the group: lane holds row pt, columns 32 (CG cgi + m) + 8 qd + 4 h + e ----
+#pragma unroll
+      for (int m = 0; m < CG; ++m) {
+        const int mb = cgi * CG + m;
+        float wv[16];
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const int c = 32 * mb + 8 * qd + 4 * h;
+          float u4[4];
+          load_u4(c, u4);
+          const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+          const f32x4 sv = *reinterpret_cast<const f32x4*>(ssl + c);
+          const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+          const float se[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float uu = u4[e];
+            float t = fmaf(two_alpha, acc[m][4 * qd + e], uu);
+            t = fmaf(neg_alpha, ybar * pe[e], t);
+            t = fmaf(neg_alpha, se[e], t);
+            float w = fmaxf(t, 0.f);
+            if (!vpt || c + e >= r) w = 0.f;
+            wv[4 * qd + e] = w;
+            const double wd = (double)w, ud = (double)uu;
+            sa = fma(wd, wd, sa);
+            sb = fma(ud, ud, sb);
+            sh = fma(wd, ud, sh);
+          }
+          if (vpt && c < r) {
+            const f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
+            *reinterpret_cast<f32x4*>(urow + c) = o;
+          }
+        }
+        reduce_scatter<16, 16>(wv, li);
+        // colacc[cgi CG + m] (a constant index in each unrolled copy)
+        if (cgi == 0) colacc[m] += (double)wv[0];
+        else colacc[CG + m] += (double)wv[0];
+        // one column block at a time: its U loads are not hoisted above the previous block
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+
+  // ---- workgroup partials ----
+  __syncthreads();  // the Theta buffers become the column-sum table
+  for (int c = tid; c < 4 * r32; c += kThreads) colred[c] = 0.0;
+  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < 2 * CG; ++m) {
+    if (m < NB) {
+      const double v = colacc[m] + shfl_xor_d(colacc[m], 1);
+      if ((li & 1) == 0) {
+        const int col = 32 * m + 8 * (base >> 2) + 4 * h + (base & 3);
+        colred[wave * r32 + col] = v;
+      }
+    }
+  }
+  __syncthreads();
+  double* out = B.b_part + (int64_t)blockIdx.x * (4 + r32);
+  for (int c = tid; c < r32; c += kThreads)
+    out[4 + c] = ((colred[c] + colred[r32 + c]) + colred[2 * r32 + c]) + colred[3 * r32 + c];
+  const double ta = block_sum_d(sa, dred);
+  const double tb2 = block_sum_d(sb, dred);
+  const double th = block_sum_d(sh, dred);
+  if (tid == 0) {
+    out[0] = ta;
+    out[1] = tb2;
+    out[2] = th;
+    out[3] = 0.0;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Pass B above 256 columns (NB = 10, 12 or 14 blocks of 32).  As k_pass_b, with
 // the columns taken two blocks at a time: per 128-row super-tile each wave forms
 // q = u.p - 1 over the whole row first, then for each pair of column blocks the
@@ -2181,6 +2414,19 @@ hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, boo
   return hipGetLastError();
 }
 
+template <int CG>
+static hipError_t pass_b_stream_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
+  // Theta buffers (the column-sum table at the end, 4 r32 doubles <= 8 NB KiB, fits
+  // them: NB <= 2 CG), p, s, the reduction
+  const size_t tiles = (size_t)2 * 4 * CG * 256 * 4;
+  if ((size_t)4 * g.r32 * 8 > tiles || g.NB > 2 * CG || g.NB % CG != 0) return hipErrorInvalidValue;
+  const size_t lds = tiles + (size_t)2 * g.r32 * 4 + 4 * 8;
+  hipError_t e = allow_lds(k_pass_b_stream<CG>, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_pass_b_stream<CG>), dim3(g.GB), dim3(kThreads), lds, st, g, b, a);
+  return hipGetLastError();
+}
+
 template <int NB>
 static hipError_t pass_b_nb(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   const size_t lds = g.ldsB_bytes;
@@ -2219,6 +2465,19 @@ hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hi
       case 42: return pass_b_res_launch<4, 2>(g, b, a, st);
       case 43: return pass_b_res_launch<4, 3>(g, b, a, st);
       case 44: return pass_b_res_launch<4, 4>(g, b, a, st);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (!g.theta_lds && g.vec_x && g.vec_u) {
+    // Theta streamed through LDS in chunks, columns in one or two groups
+    switch (g.NB) {
+      case 1: return pass_b_stream_launch<1>(g, b, a, st);
+      case 2: return pass_b_stream_launch<2>(g, b, a, st);
+      case 4: return pass_b_stream_launch<4>(g, b, a, st);
+      case 8: return pass_b_stream_launch<4>(g, b, a, st);
+      case 10: return pass_b_stream_launch<5>(g, b, a, st);
+      case 12: return pass_b_stream_launch<6>(g, b, a, st);
+      case 14: return pass_b_stream_launch<7>(g, b, a, st);
       default: return hipErrorInvalidValue;
     }
   }

@@ -183,6 +183,25 @@ def test_ragged_shapes(n, d, r, K):
     assert not bad_gates
 
 
+# Two-pass fp32 form with a Theta larger than LDS holds whole (d32 * r32 * 4 > 64 KiB) and
+# 16-byte rows: pass B streams Theta through LDS in chunks, with the columns in one group of
+# 1..4 blocks or two groups of 4..7; the wide pass A (above 128 columns) as a streaming row
+# pass and the register-prefetched product
+@pytest.mark.parametrize("n,d,r,K", [(1037, 520, 32, 8), (1501, 300, 64, 16), (1037, 132, 128, 16), (2001, 96, 256, 32),
+                                     (999, 200, 300, 20), (1201, 44, 384, 12), (777, 40, 448, 4),
+                                     (3001, 252, 200, 16)])
+def test_two_pass_streamed_theta(n, d, r, K):
+    log(f"streamed theta n={n} d={d} r={r} K={K}")
+    X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 3 + d)
+    Z = standard_normal_factor(n, r, seed=n + 2 * r).astype(np.float64)
+    alpha = onlr.default_step_size(K)
+    _, _, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, alpha, 1.0, 6, one_step_tol=True,
+                                                       flags=TWO_PASS)
+    log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates
+
+
 def test_gmm1m_parity():
     """gmm1m over its configuration's 100 iterations with split products (the bench's
     single-Xhat-pass form) and with fp32 products, from the same start: each iterate against
