@@ -427,8 +427,8 @@ __global__ __launch_bounds__(kThreads) void k_theta_wide(Geometry g, Bufs B) {
 // staging; each wave streams whole rows of U, lane l holding the columns
 // l + 64 j (CPL = ceil(r / 64) of them), RPI rows at a time.  Per row: u = fl(c_f w),
 // q = u.p - 1 (FP64, summed over the wave by an xor butterfly, so every lane has
-// the same bits), the gated dual step (eq. of the stored dual), ybar; then
-// s += ybar u, ||q||^2 and ytilde^T q in FP64.  Grid GAF; workgroup gx takes a
+// the same bits), the gated dual step (eq. of the stored dual), ybar (stored for
+// pass B); then s += ybar u, ||q||^2 and ytilde^T q in FP64.  Grid GAF; workgroup gx takes a
 // contiguous range of rows, its waves every fourth row of it, and writes partial row
 // gx in the layout of pass A (qq, yq, 0, 0, s).
 // ---------------------------------------------------------------------------
@@ -509,6 +509,7 @@ __global__ __launch_bounds__(kThreads) void k_rows_wide(Geometry g, Bufs B, Step
         }
         const float ybar = fmaf(gam, q, y);
         if (lane == 0) {
+          B.ybar[row] = ybar;
           acc_qq += (double)q * (double)q;
           acc_yq += (double)y * (double)q;
         }
@@ -1259,13 +1260,18 @@ __global__ __launch_bounds__(kThreads) void k_pass_b(Geometry g, Bufs B, StepArg
 // ---------------------------------------------------------------------------
 // Pass B with Theta streamed through LDS, for a Theta larger than LDS holds whole
 // (d32 r32 4 > 64 KiB) and 16-byte rows.  As k_pass_b (waves, rows, the operand
-// layout of Theta and the k-order of the products), with the columns in NB / CG
-// groups of CG blocks: per 128-row super-tile, for each group and each 32-feature
-// chunk, the workgroup stages the chunk's Theta operands (4 CG KiB) in one of two
-// LDS buffers and every wave multiplies its rows by them.  The next chunk's Theta
-// operands and Xhat features are loaded into registers while the matrix cores work
-// on the current one: one barrier per chunk.  Loads past the last row, feature or
-// column read a valid address and are zeroed, so that no load waits behind a branch.
+// layout of Theta and the k-order of the products), with the columns in groups of
+// CG blocks (the last group may be short): per 128-row super-tile, for each group
+// and each 32-feature chunk, the workgroup stages the chunk's Theta operands (4 KiB
+// per block) in one of two LDS buffers and every wave multiplies its rows by them.
+// The next chunk's Theta operands and Xhat features are loaded into registers while
+// the matrix cores work on the current one (one barrier per chunk); during a group's
+// last chunk the rows of U its epilogue needs are loaded instead, and the next
+// group's first chunk during the epilogue.  Loads past the last row, feature, block
+// or column read a valid address and are zeroed or unused, so that no load waits
+// behind a branch.  Above 128 columns ybar comes from the row launch of pass A
+// (which stores it), else from q = u.p - 1 formed here.  Column sums: lanes l and
+// l ^ 1 combined, then added to the wave's row of an LDS table per super-tile.
 // ---------------------------------------------------------------------------
 template <int CG>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_pass_b_stream(
@@ -1273,11 +1279,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
   if (halted(B.ctl)) return;
   constexpr int TCF = 4 * CG * 256;  // floats of a chunk's Theta operands
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  float* tbuf = reinterpret_cast<float*>(smem_raw);       // 2 x TCF
-  float* ps = tbuf + 2 * TCF;                              // r32
-  float* ss = ps + g.r32;                                  // r32
-  double* colred = reinterpret_cast<double*>(smem_raw);   // 4 x r32, after the tile loop
-  double* dred = reinterpret_cast<double*>(ss + g.r32);   // 4
+  float* tbuf = reinterpret_cast<float*>(smem_raw);           // 2 x TCF
+  double* colred = reinterpret_cast<double*>(tbuf + 2 * TCF);  // 4 x r32
+  float* ps = reinterpret_cast<float*>(colred + 4 * g.r32);    // r32
+  float* ss = ps + g.r32;                                      // r32
+  double* dred = reinterpret_cast<double*>(ss + g.r32);       // 4
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -1287,7 +1293,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
   const int64_t n = g.n;
   const int d = g.d, r = g.r, r32 = g.r32, NB = g.NB;
   const int nch = g.nch;
-  const int ngr = NB / CG;  // column groups (1 or 2)
+  const int ngr = (NB + CG - 1) / CG;  // column groups
+  const bool ystored = pass_a_split(g);  // the row launch of pass A stored ybar
   const float cf = B.ctl->c_f;
   const float gam = S.gamma_f;
   const float two_alpha = S.two_alpha_f;
@@ -1297,11 +1304,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
     ps[c] = B.p[c];
     ss[c] = B.s[c];
   }
+  for (int c = tid; c < 4 * r32; c += kThreads) colred[c] = 0.0;
 
   double sa = 0.0, sb = 0.0, sh = 0.0;
-  double colacc[2 * CG];
-#pragma unroll
-  for (int m = 0; m < 2 * CG; ++m) colacc[m] = 0.0;
   int base = 0;  // local index (8 qd + e ordering) of the column sum this lane keeps
   if (li & 16) base += 8;
   if (li & 8) base += 4;
@@ -1312,21 +1317,28 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
   const int64_t sb1 = (int64_t)(blockIdx.x + 1) * g.tilesB / g.GB;
 
   // Theta operands of chunk (group cgi, chunk ch): piece v = tid + 256 i of the chunk is
-  // j = v / (64 CG), block m = v / 64 % CG, lane v % 64 of the pass-B layout
-  int toff[CG];  // piece of chunk (0, 0) this thread stages, in pieces of 16 bytes
+  // j = v / (64 CG), block m = v / 64 % CG (clamped to the last block), lane v % 64
+  int tj[CG], tm[CG];
 #pragma unroll
   for (int i = 0; i < CG; ++i) {
     const int v = tid + kThreads * i;
-    toff[i] = ((v / (64 * CG)) * NB + (v / 64) % CG) * 64 + (v & 63);
+    tj[i] = v / (64 * CG);
+    tm[i] = (v / 64) % CG;
   }
   f32x4 tr[CG];
   f32x4 xr[4];
-  // chunk ch of group cgi: pieces ch 4 NB 64 + cgi CG 64 + toff
   auto load_chunk = [&](int64_t st, int cgi, int ch) {
-    const float* tsrc = B.theta + ((int64_t)ch * 4 * NB * 64 + cgi * CG * 64) * 4;
+    // (an opaque zero keeps the address arithmetic here, not hoisted out of the loops
+    // into registers that would stay live across them)
+    int z = 0;
+    asm volatile("" : "+v"(z));
 #pragma unroll
-    for (int i = 0; i < CG; ++i) tr[i] = *reinterpret_cast<const f32x4*>(tsrc + toff[i] * 4);
-    const int64_t pt = st * kTPB + wave * 32 + li;
+    for (int i = 0; i < CG; ++i) {
+      const int mb = cgi * CG + tm[i] < NB ? cgi * CG + tm[i] : NB - 1;
+      const int64_t piece = (((int64_t)ch * 4 + tj[i]) * NB + mb) * 64 + ((tid + z) & 63);
+      tr[i] = *reinterpret_cast<const f32x4*>(B.theta + piece * 4);
+    }
+    const int64_t pt = st * kTPB + wave * 32 + li + z;
     const float* xrow = B.X + (pt < n ? pt : 0) * (int64_t)d;
     const int fb = ch * 32 + h * 16;
 #pragma unroll
@@ -1340,71 +1352,72 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
     const bool vpt = pt < n;
     float* urow = B.U + (vpt ? pt : 0) * (int64_t)r;
     // (the opaque copy keeps the p/s reads inside the tile loop instead of hoisting
-    // 2*16*NB loop-invariant registers out of it)
+    // loop-invariant registers out of it)
     int lds_off = 0;
     asm volatile("" : "+v"(lds_off));
     const float* psl = ps + lds_off;
     const float* ssl = ss + lds_off;
-    auto load_u4 = [&](int c, float out[4]) {
-      const f32x4 t = *reinterpret_cast<const f32x4*>(urow + (c < r ? c : 0));
-      const bool ok = vpt && c < r;
-      out[0] = ok ? t.x * cf : 0.f;
-      out[1] = ok ? t.y * cf : 0.f;
-      out[2] = ok ? t.z * cf : 0.f;
-      out[3] = ok ? t.w * cf : 0.f;
-    };
-    // q = u.p - 1 over the whole row (fp32 dot over the lane's half, then the other half)
-    float dotf = 0.f;
-    for (int m = 0; m < NB; ++m)
+    float ybar;
+    if (ystored) {
+      // ybar of the row pass of this iteration (q from an FP64 dot)
+      const float yb = B.ybar[vpt ? pt : 0];
+      ybar = vpt ? yb : 0.f;
+    } else {
+      // q = u.p - 1 over the whole row (fp32 dot over the lane's half, then the other half)
+      float dotf = 0.f;
+      for (int m = 0; m < NB; ++m)
 #pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        const int c = 32 * m + 8 * qd + 4 * h;
-        float u4[4];
-        load_u4(c, u4);
-        const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
-        dotf = fmaf(u4[0], pv.x, dotf);
-        dotf = fmaf(u4[1], pv.y, dotf);
-        dotf = fmaf(u4[2], pv.z, dotf);
-        dotf = fmaf(u4[3], pv.w, dotf);
-      }
-    dotf += shfl_xor_f(dotf, 32);
-    const float yv = B.y[vpt ? pt : 0];
-    const float ybar = vpt ? fmaf(gam, dotf - 1.0f, yv) : 0.f;
+        for (int qd = 0; qd < 4; ++qd) {
+          const int c = 32 * m + 8 * qd + 4 * h;
+          const f32x4 t = *reinterpret_cast<const f32x4*>(urow + (c < r ? c : 0));
+          const bool ok = vpt && c < r;
+          const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+          dotf = fmaf(ok ? t.x * cf : 0.f, pv.x, dotf);
+          dotf = fmaf(ok ? t.y * cf : 0.f, pv.y, dotf);
+          dotf = fmaf(ok ? t.z * cf : 0.f, pv.z, dotf);
+          dotf = fmaf(ok ? t.w * cf : 0.f, pv.w, dotf);
+        }
+      dotf += shfl_xor_f(dotf, 32);
+      const float yv = B.y[vpt ? pt : 0];
+      ybar = vpt ? fmaf(gam, dotf - 1.0f, yv) : 0.f;
+    }
 
     for (int cgi = 0; cgi < ngr; ++cgi) {
+      const int nbg = NB - cgi * CG < CG ? NB - cgi * CG : CG;  // blocks of this group
       f32x16 acc[CG];
 #pragma unroll
       for (int m = 0; m < CG; ++m)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[m][v] = 0.f;
-      for (int ch = 0; ch < nch; ++ch) {
-        // stage this chunk's Theta operands; the barrier also ends every wave's reads
-        // of the buffer two chunks back
+      // one chunk: stage its Theta operands (the barrier also ends every wave's reads of
+      // the buffer two chunks back), then `next` issues the loads that overlap the
+      // products, then the products
+      auto chunk = [&](int ch, auto&& next) {
         float* tb = tbuf + kbuf * TCF;
 #pragma unroll
         for (int i = 0; i < CG; ++i) *reinterpret_cast<f32x4*>(tb + (tid + kThreads * i) * 4) = tr[i];
-        const bool xok = vpt;
         float xv[16];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const bool ok = xok && (ch * 32 + h * 16 + 4 * q < d);
+          const bool ok = vpt && (ch * 32 + h * 16 + 4 * q < d);
           xv[4 * q + 0] = ok ? xr[q].x : 0.f;
           xv[4 * q + 1] = ok ? xr[q].y : 0.f;
           xv[4 * q + 2] = ok ? xr[q].z : 0.f;
           xv[4 * q + 3] = ok ? xr[q].w : 0.f;
         }
         __syncthreads();
-        // prefetch the next chunk: next feature chunk, else next group, else next super-tile
-        {
-          const bool nc = ch + 1 < nch, ng = !nc && cgi + 1 < ngr;
-          const int64_t st2 = (nc || ng) ? st : st + 1;
-          if (st2 < sb1) load_chunk(st2, nc ? cgi : (ng ? cgi + 1 : 0), nc ? ch + 1 : 0);
-        }
+        next();
+        // the loads are issued before the products (not sunk below them to reuse the
+        // registers of this chunk's X operands)
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           f32x4 a[CG];
 #pragma unroll
           for (int m = 0; m < CG; ++m) a[m] = *reinterpret_cast<const f32x4*>(tb + ((j * CG + m) * 64 + lane) * 4);
+          // every block of the group, also past the last of a short group (its operands
+          // are the last block's, its products unused): a conditional product would make
+          // the compiler copy the accumulators
 #pragma unroll
           for (int m = 0; m < CG; ++m) {
             acc[m] = mfma32x32x2(a[m].x, xv[4 * j + 0], acc[m]);
@@ -1412,68 +1425,74 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
             acc[m] = mfma32x32x2(a[m].z, xv[4 * j + 2], acc[m]);
             acc[m] = mfma32x32x2(a[m].w, xv[4 * j + 3], acc[m]);
           }
-          // the operands of one feature quad at a time (4 CG registers)
-          __builtin_amdgcn_sched_barrier(0);
         }
         kbuf ^= 1;
-      }
+      };
+      for (int ch = 0; ch + 1 < nch; ++ch) chunk(ch, [&]() { load_chunk(st, cgi, ch + 1); });
+      // the last chunk: the rows of U the epilogue needs are loaded meanwhile
+      f32x4 ua[CG][4];
+      chunk(nch - 1, [&]() {
+#pragma unroll
+        for (int m = 0; m < CG; ++m)
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const int c = 32 * (cgi * CG + m) + 8 * qd + 4 * h;
+            ua[m][qd] = *reinterpret_cast<const f32x4*>(urow + (c < r ? c : 0));
+          }
+      });
       // ---- epilogue of the group: lane holds row pt, columns 32 (CG cgi + m) + 8 qd + 4 h + e ----
 #pragma unroll
       for (int m = 0; m < CG; ++m) {
-        const int mb = cgi * CG + m;
-        float wv[16];
-#pragma unroll
-        for (int qd = 0; qd < 4; ++qd) {
-          const int c = 32 * mb + 8 * qd + 4 * h;
-          float u4[4];
-          load_u4(c, u4);
-          const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
-          const f32x4 sv = *reinterpret_cast<const f32x4*>(ssl + c);
-          const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
-          const float se[4] = {sv.x, sv.y, sv.z, sv.w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float uu = u4[e];
-            float t = fmaf(two_alpha, acc[m][4 * qd + e], uu);
-            t = fmaf(neg_alpha, ybar * pe[e], t);
-            t = fmaf(neg_alpha, se[e], t);
-            float w = fmaxf(t, 0.f);
-            if (!vpt || c + e >= r) w = 0.f;
-            wv[4 * qd + e] = w;
-            const double wd = (double)w, ud = (double)uu;
-            sa = fma(wd, wd, sa);
-            sb = fma(ud, ud, sb);
-            sh = fma(wd, ud, sh);
-          }
-          if (vpt && c < r) {
-            const f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
-            *reinterpret_cast<f32x4*>(urow + c) = o;
-          }
+        if (m == CG / 2) {
+          // the next group's (or super-tile's) first chunk, behind the rest of the epilogue
+          // (in the registers of the blocks done)
+          const bool ng = cgi + 1 < ngr;
+          const int64_t st2 = ng ? st : st + 1;
+          if (st2 < sb1) load_chunk(st2, ng ? cgi + 1 : 0, 0);
         }
-        reduce_scatter<16, 16>(wv, li);
-        // colacc[cgi CG + m] (a constant index in each unrolled copy)
-        if (cgi == 0) colacc[m] += (double)wv[0];
-        else colacc[CG + m] += (double)wv[0];
-        // one column block at a time: its U loads are not hoisted above the previous block
+        if (m < nbg) {
+          const int mb = cgi * CG + m;
+          float wv[16];
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const int c = 32 * mb + 8 * qd + 4 * h;
+            const bool ok = vpt && c < r;
+            const float u4[4] = {ok ? ua[m][qd].x * cf : 0.f, ok ? ua[m][qd].y * cf : 0.f,
+                                 ok ? ua[m][qd].z * cf : 0.f, ok ? ua[m][qd].w * cf : 0.f};
+            const f32x4 pv = *reinterpret_cast<const f32x4*>(psl + c);
+            const f32x4 sv = *reinterpret_cast<const f32x4*>(ssl + c);
+            const float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+            const float se[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float uu = u4[e];
+              float t = fmaf(two_alpha, acc[m][4 * qd + e], uu);
+              t = fmaf(neg_alpha, ybar * pe[e], t);
+              t = fmaf(neg_alpha, se[e], t);
+              float w = fmaxf(t, 0.f);
+              if (!vpt || c + e >= r) w = 0.f;
+              wv[4 * qd + e] = w;
+              const double wd = (double)w, ud = (double)uu;
+              sa = fma(wd, wd, sa);
+              sb = fma(ud, ud, sb);
+              sh = fma(wd, ud, sh);
+            }
+            if (ok) {
+              const f32x4 o = {wv[4 * qd + 0], wv[4 * qd + 1], wv[4 * qd + 2], wv[4 * qd + 3]};
+              *reinterpret_cast<f32x4*>(urow + c) = o;
+            }
+          }
+          reduce_scatter<16, 16>(wv, li);
+          const double v = (double)wv[0] + shfl_xor_d((double)wv[0], 1);
+          if ((li & 1) == 0) colred[wave * r32 + 32 * mb + 8 * (base >> 2) + 4 * h + (base & 3)] += v;
+        }
+        // one block at a time (its LDS reads are not hoisted above the previous block)
         __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
 
   // ---- workgroup partials ----
-  __syncthreads();  // the Theta buffers become the column-sum table
-  for (int c = tid; c < 4 * r32; c += kThreads) colred[c] = 0.0;
-  __syncthreads();
-#pragma unroll
-  for (int m = 0; m < 2 * CG; ++m) {
-    if (m < NB) {
-      const double v = colacc[m] + shfl_xor_d(colacc[m], 1);
-      if ((li & 1) == 0) {
-        const int col = 32 * m + 8 * (base >> 2) + 4 * h + (base & 3);
-        colred[wave * r32 + col] = v;
-      }
-    }
-  }
   __syncthreads();
   double* out = B.b_part + (int64_t)blockIdx.x * (4 + r32);
   for (int c = tid; c < r32; c += kThreads)
@@ -2416,11 +2435,9 @@ hipError_t launch_ctl_a(const Geometry& g, const Bufs& b, const StepArgs& a, boo
 
 template <int CG>
 static hipError_t pass_b_stream_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  // Theta buffers (the column-sum table at the end, 4 r32 doubles <= 8 NB KiB, fits
-  // them: NB <= 2 CG), p, s, the reduction
-  const size_t tiles = (size_t)2 * 4 * CG * 256 * 4;
-  if ((size_t)4 * g.r32 * 8 > tiles || g.NB > 2 * CG || g.NB % CG != 0) return hipErrorInvalidValue;
-  const size_t lds = tiles + (size_t)2 * g.r32 * 4 + 4 * 8;
+  // Theta buffers, the column-sum table, p, s, the reduction
+  const size_t lds = (size_t)2 * 4 * CG * 256 * 4 + (size_t)4 * g.r32 * 8 + (size_t)2 * g.r32 * 4 + 4 * 8;
+  if (lds > (160u << 10)) return hipErrorInvalidValue;
   hipError_t e = allow_lds(k_pass_b_stream<CG>, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_pass_b_stream<CG>), dim3(g.GB), dim3(kThreads), lds, st, g, b, a);
@@ -2469,16 +2486,11 @@ hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hi
     }
   }
   if (!g.theta_lds && g.vec_x && g.vec_u) {
-    // Theta streamed through LDS in chunks, columns in one or two groups
+    // Theta streamed through LDS in chunks, columns in groups of up to four blocks
     switch (g.NB) {
       case 1: return pass_b_stream_launch<1>(g, b, a, st);
       case 2: return pass_b_stream_launch<2>(g, b, a, st);
-      case 4: return pass_b_stream_launch<4>(g, b, a, st);
-      case 8: return pass_b_stream_launch<4>(g, b, a, st);
-      case 10: return pass_b_stream_launch<5>(g, b, a, st);
-      case 12: return pass_b_stream_launch<6>(g, b, a, st);
-      case 14: return pass_b_stream_launch<7>(g, b, a, st);
-      default: return hipErrorInvalidValue;
+      default: return pass_b_stream_launch<4>(g, b, a, st);  // groups of four blocks
     }
   }
   if (g.NB > 8) {

@@ -242,8 +242,8 @@ size_t carve_workspace(const Geometry& g, char* base, Bufs* out) {
   b.dump = reinterpret_cast<float*>(take(256));
   b.thmax_part = reinterpret_cast<float*>(take((size_t)g.RT * 4));
   if (g.fused8) b.gram_vec = reinterpret_cast<double*>(take(3 * r32 * 8));
+  if (g.panel || pass_a_split(g)) b.ybar = reinterpret_cast<float*>(take((size_t)g.n * 4));
   if (g.panel) {
-    b.ybar = reinterpret_cast<float*>(take((size_t)g.n * 4));
     b.theta_split = take((size_t)((g.d + 15) / 16) * 64 * g.pnbw * 64);
   }
   b.s_C = reinterpret_cast<double*>(take(d * d * 8));

@@ -178,8 +178,8 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
 int fused_lds_need(int NB, int nch, bool split, bool uflat);
 bool fused8_shape(int NB, int nch, int r);
 // generic pass A above 128 columns: a row-work launch (GAF workgroups streaming rows
-// of U) and a Theta launch whose workgroups stage only their own columns
-inline bool pass_a_split(const Geometry& g) { return !g.a_rows && g.r32 > 128; }
+// of U, storing ybar) and a Theta launch whose workgroups stage only their own columns
+__host__ __device__ inline bool pass_a_split(const Geometry& g) { return !g.a_rows && g.r32 > 128; }
 constexpr int kMaxFusedLds = 160 << 10;
 size_t carve_workspace(const Geometry& g, char* base, Bufs* out);  // base may be null (size only)
 
