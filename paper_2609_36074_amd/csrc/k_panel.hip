@@ -480,20 +480,21 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
 // ===========================================================================
 // Theta for pass B: split hi/lo of Theta * s_theta in the pass-B LDS image
 // ===========================================================================
-constexpr int kPBRows = 128;    // rows per pass-B tile (two row waves x 64)
-constexpr int kPBStages = 3;
-constexpr int kPBThreads = 256;
 
-template <int NBW>
+template <int NBW, int WR>
 struct PanelB {
+  static constexpr int ROWS = 64 * WR;            // rows per tile: WR row waves x 64
+  static constexpr int NT = 128 * WR;             // threads: WR row waves x 2 column waves
+  static constexpr int NW = NT / 64;
   static constexpr int RC = 64 * NBW;             // columns of the two column waves
   static constexpr int TH = RC * 64;              // Theta^T chunk: per column 16 features hi + lo
-  static constexpr int XB = kPBRows * 64;         // Xhat chunk: per row 16 features split
+  static constexpr int XB = ROWS * 64;            // Xhat chunk: per row 16 features split
   static constexpr int STAGE = TH + XB;
   static constexpr int INSTR = STAGE / 1024;
-  static constexpr int OPS = INSTR / 4;           // per wave
-  static constexpr int LDS = kPBStages * STAGE + 2 * RC * 4 + (2 * RC + 8) * 8;
-  static_assert(INSTR % 4 == 0, "equal share of the loads per wave");
+  static constexpr int OPS = INSTR / NW;          // per wave
+  static constexpr int STAGES = 3;  // ring of stages: loads two stages ahead
+  static constexpr int LDS = STAGES * STAGE + 2 * RC * 4 + (WR * RC + 8) * 8;
+  static_assert(INSTR % NW == 0, "equal share of the loads per wave");
 };
 
 // Stage k of the Theta image: column c owns 64 bytes = four 16-byte pieces
@@ -542,22 +543,28 @@ __global__ __launch_bounds__(kThreads) void k_theta_split_panel(Geometry g, Bufs
 // Pass B
 // ===========================================================================
 // Row R of a pass-B Xhat chunk: piece P = 2 unit + hl in slot P ^ ((R >> 2) & 3).
-template <int NBW>
-__global__ __launch_bounds__(kPBThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_b_panel(
+// WR row waves of 64 rows (2 WR waves): WR = 2, two 4-wave workgroups per compute unit;
+// WR = 4, one 8-wave workgroup per compute unit, so that each staged Theta chunk serves
+// twice the rows (half the Theta traffic from L2 per row).
+template <int NBW, int WR>
+__global__ __launch_bounds__(128 * WR) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pass_b_panel(
     Geometry g, Bufs B, StepArgs S) {
-  using P = PanelB<NBW>;
+  using P = PanelB<NBW, WR>;
+  constexpr int kPBRows = P::ROWS;
+  constexpr int kPBThreads = P::NT;
+  constexpr int kPBStages = P::STAGES;
   if (halted(B.ctl)) return;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   unsigned char* ring = smem_raw;
   float* ps = reinterpret_cast<float*>(smem_raw + kPBStages * P::STAGE);
   float* ss = ps + P::RC;
-  double* colred = reinterpret_cast<double*>(ss + P::RC);  // 2 x RC
-  double* dred = colred + 2 * P::RC;                       // 8
+  double* colred = reinterpret_cast<double*>(ss + P::RC);  // WR x RC
+  double* dred = colred + WR * P::RC;                      // 8
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
-  const int wr = wave >> 1;  // 64-row half of the tile
+  const int wr = wave >> 1;  // 64-row part of the tile
   const int cw = wave & 1;   // column half
   const int h = lane >> 5;
   const int li = lane & 31;
@@ -591,7 +598,7 @@ __global__ __launch_bounds__(kPBThreads) __attribute__((amdgpu_waves_per_eu(2, 2
     asm volatile("" : "+v"(ln));
 #pragma unroll
     for (int q = 0; q < P::OPS; ++q) {
-      const int i = wave + 4 * q;
+      const int i = wave + P::NW * q;
       const void* src;
       if (i < P::TH / 1024) {
         src = tb + (i * 1024 + ln * 16);
@@ -751,7 +758,7 @@ __global__ __launch_bounds__(kPBThreads) __attribute__((amdgpu_waves_per_eu(2, 2
 
   // ---- statistics of this workgroup ----
   __syncthreads();
-  for (int c = tid; c < 2 * P::RC; c += kPBThreads) colred[c] = 0.0;
+  for (int c = tid; c < WR * P::RC; c += kPBThreads) colred[c] = 0.0;
   __syncthreads();
 #pragma unroll
   for (int cb = 0; cb < NBW; ++cb) {
@@ -763,10 +770,14 @@ __global__ __launch_bounds__(kPBThreads) __attribute__((amdgpu_waves_per_eu(2, 2
   }
   __syncthreads();
   double* out = B.b_part + (int64_t)blockIdx.x * (4 + g.r32);
-  for (int c = tid; c < g.r32; c += kPBThreads) out[4 + c] = colred[c] + colred[P::RC + c];
-  const double ta = block_sum_d(sa, dred);
-  const double tb2 = block_sum_d(sb, dred);
-  const double th = block_sum_d(sh, dred);
+  for (int c = tid; c < g.r32; c += kPBThreads) {
+    double t = colred[c] + colred[P::RC + c];
+    if (WR == 4) t = t + (colred[2 * P::RC + c] + colred[3 * P::RC + c]);
+    out[4 + c] = t;
+  }
+  const double ta = WR == 4 ? block_sum8_d(sa, dred) : block_sum_d(sa, dred);
+  const double tb2 = WR == 4 ? block_sum8_d(sb, dred) : block_sum_d(sb, dred);
+  const double th = WR == 4 ? block_sum8_d(sh, dred) : block_sum_d(sh, dred);
   if (tid == 0) {
     out[0] = ta;
     out[1] = tb2;
@@ -806,14 +817,17 @@ static hipError_t pass_a_panel_launch(const Geometry& g, const Bufs& b, const St
   return hipGetLastError();
 }
 
-template <int NBW>
+template <int NBW, int WR>
 static hipError_t pass_b_panel_launch(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
-  constexpr int lds = PanelB<NBW>::LDS;
-  static_assert(lds <= (80 << 10), "two workgroups per compute unit");
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_b_panel<NBW>),
+  using P = PanelB<NBW, WR>;
+  constexpr int lds = P::LDS;
+  static_assert(WR == 4 || lds <= (80 << 10), "two workgroups per compute unit");
+  static_assert(lds <= (160 << 10), "LDS");
+  if (g.tilesP != (g.n + P::ROWS - 1) / P::ROWS) return hipErrorInvalidValue;  // geometry mismatch
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass_b_panel<NBW, WR>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_pass_b_panel<NBW>, dim3(g.GB), dim3(kPBThreads), lds, st, g, b, a);
+  hipLaunchKernelGGL((k_pass_b_panel<NBW, WR>), dim3(g.GB), dim3(P::NT), lds, st, g, b, a);
   return hipGetLastError();
 }
 
@@ -836,9 +850,9 @@ hipError_t launch_theta_split_panel(const Geometry& g, const Bufs& b, hipStream_
 
 hipError_t launch_pass_b_panel(const Geometry& g, const Bufs& b, const StepArgs& a, hipStream_t st) {
   switch (g.pnbw) {
-    case 1: return pass_b_panel_launch<1>(g, b, a, st);
-    case 2: return pass_b_panel_launch<2>(g, b, a, st);
-    case 4: return pass_b_panel_launch<4>(g, b, a, st);
+    case 1: return pass_b_panel_launch<1, 2>(g, b, a, st);
+    case 2: return pass_b_panel_launch<2, 2>(g, b, a, st);
+    case 4: return pass_b_panel_launch<4, 4>(g, b, a, st);
     default: return hipErrorInvalidValue;
   }
 }

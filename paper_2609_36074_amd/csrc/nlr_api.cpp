@@ -161,8 +161,12 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
     if (ps < 1) ps = 1;
     g.PS = (int32_t)ps;
     g.GPA = 8 * g.pfb * ((g.PS + 7) / 8);
-    g.tilesP = (n + 127) / 128;
-    g.GB = (int32_t)(g.tilesP < 512 ? g.tilesP : 512);  // two 4-wave workgroups per compute unit
+    // pass B: 256-row tiles in one 8-wave workgroup per compute unit at 128 columns per
+    // column wave (pnbw = 4), else 128-row tiles in two 4-wave workgroups per compute unit
+    const int prow = g.pnbw == 4 ? 256 : 128;
+    const int64_t pgrid = g.pnbw == 4 ? 256 : 512;
+    g.tilesP = (n + prow - 1) / prow;
+    g.GB = (int32_t)(g.tilesP < pgrid ? g.tilesP : pgrid);
     g.SB = (g.GB + 31) / 32;
     // |u| <= sqrt(K) for U in Omega (||U||_F^2 = K); 1% margin for rounding
     int e2;
