@@ -30,8 +30,9 @@
 // (workgroup ids congruent mod 8) and stream the same U rows at the same time,
 // so U is fetched from HBM about once.
 //
-// Pass B (k_pass_b_panel): workgroup of 4 waves (two per compute unit) over
-// 128-row tiles, 16 features per stage: Theta^T chunks (split and laid out once
+// Pass B (k_pass_b_panel): workgroups of 2 WR waves over 64 WR-row tiles (one 8-wave
+// workgroup per compute unit at 128 columns per column wave, else two of 4 waves),
+// 16 features per stage: Theta^T chunks (split and laid out once
 // per iteration by k_theta_split_panel) and Xhat row chunks in LDS, then the
 // epilogue on the accumulators: w = max(u + 2 alpha G - alpha ybar p - alpha s, 0),
 // FP64 a = ||W||^2, b = ||U||^2, h = <W, U>, column sums of W, W stored over U.
