@@ -203,6 +203,24 @@ def test_two_pass_streamed_theta(n, d, r, K):
     assert not bad_gates
 
 
+# Two-pass fp32 form above 128 columns at its edges: about one tile per workgroup (n = 301
+# just above r, a ragged last tile and super-tile), rows not 16-byte aligned (d % 4 == 2: the LDS-staged Theta product;
+# r % 4 != 0: the pair-wise pass B), the smallest split width (r = 129: three columns per lane
+# in the row launch)
+@pytest.mark.parametrize("n,d,r,K", [(301, 40, 300, 6), (777, 130, 160, 8), (1500, 64, 129, 9),
+                                     (2049, 132, 260, 10)])
+def test_two_pass_wide_edges(n, d, r, K):
+    log(f"two-pass wide edge n={n} d={d} r={r} K={K}")
+    X, _, _ = gaussian_mixture(n, d, max(K, 2), 16.0, seed=n * 5 + d)
+    Z = standard_normal_factor(n, r, seed=n + 3 * r).astype(np.float64)
+    alpha = onlr.default_step_size(K)
+    _, _, traj, obj, bad_gates, one, _, _ = trajectory(X, Z, K, alpha, 1.0, 6, one_step_tol=True,
+                                                       flags=TWO_PASS)
+    log(f"  traj {max(traj):.2e} one {max(one):.2e} obj {max(obj):.2e}")
+    assert max(traj) < U_TOL and max(one) < U_TOL / 10 and max(obj) < OBJ_TOL
+    assert not bad_gates
+
+
 def test_gmm1m_parity():
     """gmm1m over its configuration's 100 iterations with split products (the bench's
     single-Xhat-pass form) and with fp32 products, from the same start: each iterate against
