@@ -183,12 +183,13 @@ def test_ragged_shapes(n, d, r, K):
     assert not bad_gates
 
 
-# Two-pass fp32 form with a Theta larger than LDS holds whole (d32 * r32 * 4 > 64 KiB) and
-# 16-byte rows: pass B streams Theta through LDS in chunks, with the columns in groups of up
-# to four blocks (1, 2 and 4 blocks; 8..14 blocks in 2..4 groups, short last groups at 10 and
-# 14); the wide pass A (above 128 columns) as a streaming row pass and the register-prefetched
-# product
-@pytest.mark.parametrize("n,d,r,K", [(1037, 520, 32, 8), (1501, 300, 64, 16), (1037, 132, 128, 16), (2001, 96, 256, 32),
+# Two-pass fp32 form with a Theta that does not fit pass B's 64 KiB of LDS (beside p, s and
+# the reductions) and 16-byte rows: pass B streams Theta through LDS in chunks, with the
+# columns in groups of up to four blocks (1, 2 and 4 blocks; 8..14 blocks in 2..4 groups,
+# short last groups at 10 and 14); the wide pass A (above 128 columns) as a streaming row
+# pass and the register-prefetched product
+@pytest.mark.parametrize("n,d,r,K", [(1037, 520, 32, 8), (1501, 300, 64, 16), (1037, 132, 128, 16),
+                                     (2001, 96, 256, 32),
                                      (999, 200, 300, 20), (1201, 44, 384, 12), (777, 40, 448, 4),
                                      (3001, 252, 200, 16)])
 def test_two_pass_streamed_theta(n, d, r, K):
@@ -204,9 +205,10 @@ def test_two_pass_streamed_theta(n, d, r, K):
 
 
 # Two-pass fp32 form above 128 columns at its edges: about one tile per workgroup (n = 301
-# just above r, a ragged last tile and super-tile), rows not 16-byte aligned (d % 4 == 2: the LDS-staged Theta product;
-# r % 4 != 0: the pair-wise pass B), the smallest split width (r = 129: three columns per lane
-# in the row launch)
+# just above r, a ragged last tile and super-tile), rows not 16-byte aligned (d % 4 == 2: the
+# LDS-staged Theta product; r % 4 != 0: the pair-wise pass B), the smallest split width
+# (r = 129: three columns per lane in the row launch; its 64 x 256 Theta fills 64 KiB
+# exactly, so pass B takes it from L2)
 @pytest.mark.parametrize("n,d,r,K", [(301, 40, 300, 6), (777, 130, 160, 8), (1500, 64, 129, 9),
                                      (2049, 132, 260, 10)])
 def test_two_pass_wide_edges(n, d, r, K):
