@@ -1258,8 +1258,8 @@ __global__ __launch_bounds__(kThreads) void k_pass_b(Geometry g, Bufs B, StepArg
 }
 
 // ---------------------------------------------------------------------------
-// Pass B with Theta streamed through LDS, for a Theta larger than LDS holds whole
-// (d32 r32 4 > 64 KiB) and 16-byte rows.  As k_pass_b (waves, rows, the operand
+// Pass B with Theta streamed through LDS, for a Theta that does not fit pass B's 64 KiB
+// of LDS beside p, s and the reductions, and 16-byte rows.  As k_pass_b (waves, rows, the operand
 // layout of Theta and the k-order of the products), with the columns in groups of
 // CG blocks (the last group may be short): per 128-row super-tile, for each group
 // and each 32-feature chunk, the workgroup stages the chunk's Theta operands (4 KiB
@@ -2490,6 +2490,7 @@ hipError_t launch_pass_b(const Geometry& g, const Bufs& b, const StepArgs& a, hi
     switch (g.NB) {
       case 1: return pass_b_stream_launch<1>(g, b, a, st);
       case 2: return pass_b_stream_launch<2>(g, b, a, st);
+      case 10: return pass_b_stream_launch<2>(g, b, a, st);  // five exact groups of two
       default: return pass_b_stream_launch<4>(g, b, a, st);  // groups of four blocks
     }
   }

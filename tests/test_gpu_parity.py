@@ -185,9 +185,9 @@ def test_ragged_shapes(n, d, r, K):
 
 # Two-pass fp32 form with a Theta that does not fit pass B's 64 KiB of LDS (beside p, s and
 # the reductions) and 16-byte rows: pass B streams Theta through LDS in chunks, with the
-# columns in groups of up to four blocks (1, 2 and 4 blocks; 8..14 blocks in 2..4 groups,
-# short last groups at 10 and 14); the wide pass A (above 128 columns) as a streaming row
-# pass and the register-prefetched product
+# columns in groups of up to four blocks (1, 2 and 4 blocks; 8, 12 and 14 blocks in groups of
+# four, a short last group at 14; 10 blocks in five groups of two); the wide pass A (above
+# 128 columns) as a streaming row pass and the register-prefetched product
 @pytest.mark.parametrize("n,d,r,K", [(1037, 520, 32, 8), (1501, 300, 64, 16), (1037, 132, 128, 16),
                                      (2001, 96, 256, 32),
                                      (999, 200, 300, 20), (1201, 44, 384, 12), (777, 40, 448, 4),
