@@ -177,8 +177,8 @@ nlr_status nlr_labels_spectral(nlr_ctx* ctx, int32_t K, const int64_t* seed_rows
 /* Bytes of device workspace nlr_init needs for an (n, d, r) problem (the
  * storage model of Section 4.4, eq. gpu-storage: besides Xhat, the one n x r
  * factor and the stored dual, only per-workgroup partial sums -- fp32 Theta
- * partials, FP64 statistics -- and a few d x r / r-vectors; the panel form adds
- * ybar, n floats).  Depends only on (n, d, r).  Returns 0 when the shape is
+ * partials, FP64 statistics -- and a few d x r / r-vectors; the panel form and
+ * the two-pass form above 128 columns add ybar, n floats).  Depends only on (n, d, r).  Returns 0 when the shape is
  * invalid or unsupported. */
 size_t nlr_workspace_bytes(int64_t n, int32_t d, int32_t r);
 
