@@ -1305,6 +1305,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
     ss[c] = B.s[c];
   }
   for (int c = tid; c < 4 * r32; c += kThreads) colred[c] = 0.0;
+  __syncthreads();  // p and s are read before the first chunk's barrier (q below 129 columns)
 
   double sa = 0.0, sb = 0.0, sh = 0.0;
   int base = 0;  // local index (8 qd + e ordering) of the column sum this lane keeps
