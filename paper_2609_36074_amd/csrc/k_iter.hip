@@ -2156,38 +2156,82 @@ __global__ __launch_bounds__(64) void k_onepass_begin(Geometry g, Bufs B, StepAr
 // ---------------------------------------------------------------------------
 // Row-argmax labels, lowest index on ties.  A row is read by the 16 lanes of a DPP
 // row, four rows per wave and step: with 16-byte rows (VEC) lane j reads columns
-// 4j .. 4j + 3, 64 + 4j .., so one load instruction covers 256 contiguous bytes of
-// each of its four rows; otherwise lane j reads columns j, j + 16, ...  Each lane
-// keeps its first maximum (columns in increasing order, strict >), then the 16
-// candidates are reduced pairwise: the larger value, the lower column on equal values.
+// 4j .. 4j + 3, 64 + 4j .. (NCK = ceil(r / 64) pieces), so one load instruction covers
+// 256 contiguous bytes of each of its four rows, and a workgroup takes 16 RPS
+// consecutive rows per step, all their loads issued before any is compared (pieces
+// past the last column or row read a valid address and are skipped); otherwise lane j
+// reads columns
+// j, j + 16, ...  Each lane keeps its first maximum (columns in increasing order,
+// strict >), then the 16 candidates are reduced pairwise: the larger value, the lower
+// column on equal values.
 // ---------------------------------------------------------------------------
-template <bool VEC>
+__device__ __forceinline__ void label_reduce16(float& best, int& arg) {
+  constexpr int kNone = 0x7fffffff;
+#pragma unroll
+  for (int m = 1; m < 16; m <<= 1) {
+    const float ob = shfl_xor_f(best, m);
+    const int oa = __shfl_xor(arg, m, 64);
+    if (oa != kNone && (arg == kNone || ob > best || (ob == best && oa < arg))) {
+      best = ob;
+      arg = oa;
+    }
+  }
+}
+
+template <bool VEC, int NCK, int RPS>
 __global__ __launch_bounds__(kThreads) void k_labels(Geometry g, const float* __restrict__ U,
                                                      int32_t* __restrict__ labels) {
+  constexpr int kNone = 0x7fffffff;  // no column seen yet
   const int lane = threadIdx.x & 63;
   const int j = lane & 15;
   const int64_t n = g.n;
   const int r = g.r;
-  const int64_t rows_per_step = (int64_t)gridDim.x * (kThreads / 16);
-  for (int64_t i = (int64_t)blockIdx.x * (kThreads / 16) + (threadIdx.x >> 4); i - (threadIdx.x >> 4) < n;
-       i += rows_per_step) {
-    const bool vrow = i < n;
-    const float* row = U + (vrow ? i : 0) * (int64_t)r;
-    constexpr int kNone = 0x7fffffff;  // no column seen yet
-    float best = 0.f;
-    int arg = kNone;
-    if (VEC) {
-      for (int c0 = 4 * j; c0 < r; c0 += 64) {  // r % 4 == 0: c0 + 3 < r
-        const f32x4 v = *reinterpret_cast<const f32x4*>(row + c0);
-        const float e[4] = {v.x, v.y, v.z, v.w};
+  if (VEC) {
+    // a workgroup takes 16 RPS consecutive rows per step; group g its rows 16 k + g
+    const int64_t bstep = (int64_t)gridDim.x * 16 * RPS;
+    for (int64_t b0 = (int64_t)blockIdx.x * 16 * RPS; b0 < n; b0 += bstep) {
+      const int64_t i0 = b0 + (threadIdx.x >> 4);
+      f32x4 v[RPS][NCK];
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-          if (arg == kNone || e[k] > best) {
-            best = e[k];
-            arg = c0 + k;
-          }
+      for (int k = 0; k < RPS; ++k) {
+        const int64_t i = i0 + 16 * k;
+        const float* row = U + (i < n ? i : 0) * (int64_t)r;
+#pragma unroll
+        for (int q = 0; q < NCK; ++q) {
+          const int c0 = 4 * j + 64 * q;
+          v[k][q] = *reinterpret_cast<const f32x4*>(row + (c0 < r ? c0 : 0));
+        }
       }
-    } else {
+#pragma unroll
+      for (int k = 0; k < RPS; ++k) {
+        float best = 0.f;
+        int arg = kNone;
+#pragma unroll
+        for (int q = 0; q < NCK; ++q) {
+          const int c0 = 4 * j + 64 * q;  // r % 4 == 0: c0 + 3 < r when c0 < r
+          if (c0 < r) {
+            const float e[4] = {v[k][q].x, v[k][q].y, v[k][q].z, v[k][q].w};
+#pragma unroll
+            for (int e4 = 0; e4 < 4; ++e4)
+              if (arg == kNone || e[e4] > best) {
+                best = e[e4];
+                arg = c0 + e4;
+              }
+          }
+        }
+        label_reduce16(best, arg);
+        const int64_t i = i0 + 16 * k;
+        if (i < n && j == 0) labels[i] = arg;
+      }
+    }
+  } else {
+    const int64_t rows_per_step = (int64_t)gridDim.x * (kThreads / 16);
+    const int64_t first = (int64_t)blockIdx.x * (kThreads / 16) + (threadIdx.x >> 4);
+    for (int64_t i = first; i - (threadIdx.x >> 4) < n; i += rows_per_step) {
+      const bool vrow = i < n;
+      const float* row = U + (vrow ? i : 0) * (int64_t)r;
+      float best = 0.f;
+      int arg = kNone;
       for (int c = j; c < r; c += 16) {
         const float v = row[c];
         if (arg == kNone || v > best) {
@@ -2195,17 +2239,9 @@ __global__ __launch_bounds__(kThreads) void k_labels(Geometry g, const float* __
           arg = c;
         }
       }
+      label_reduce16(best, arg);
+      if (vrow && j == 0) labels[i] = arg;
     }
-#pragma unroll
-    for (int m = 1; m < 16; m <<= 1) {
-      const float ob = shfl_xor_f(best, m);
-      const int oa = __shfl_xor(arg, m, 64);
-      if (oa != kNone && (arg == kNone || ob > best || (ob == best && oa < arg))) {
-        best = ob;
-        arg = oa;
-      }
-    }
-    if (vrow && j == 0) labels[i] = arg;
   }
 }
 
@@ -2565,10 +2601,23 @@ hipError_t launch_labels(const Geometry& g, const Bufs& b, int32_t* labels, hipS
   // 16 rows per workgroup and step; enough workgroups for eight per CU
   int64_t blocks = (g.n + 15) / 16;
   if (blocks > 2048) blocks = 2048;
-  if (g.vec_u)
-    hipLaunchKernelGGL((k_labels<true>), dim3((unsigned)blocks), dim3(kThreads), 0, st, g, (const float*)b.U, labels);
-  else
-    hipLaunchKernelGGL((k_labels<false>), dim3((unsigned)blocks), dim3(kThreads), 0, st, g, (const float*)b.U, labels);
+  const dim3 grid((unsigned)blocks), blk(kThreads);
+  const float* U = b.U;
+  if (!g.vec_u) {
+    hipLaunchKernelGGL((k_labels<false, 1, 1>), grid, blk, 0, st, g, U, labels);
+  } else {
+    // rows per step so that a lane has four to eight pieces in flight
+    switch ((g.r + 63) / 64) {
+      case 1: hipLaunchKernelGGL((k_labels<true, 1, 4>), grid, blk, 0, st, g, U, labels); break;
+      case 2: hipLaunchKernelGGL((k_labels<true, 2, 4>), grid, blk, 0, st, g, U, labels); break;
+      case 3: hipLaunchKernelGGL((k_labels<true, 3, 2>), grid, blk, 0, st, g, U, labels); break;
+      case 4: hipLaunchKernelGGL((k_labels<true, 4, 2>), grid, blk, 0, st, g, U, labels); break;
+      case 5: hipLaunchKernelGGL((k_labels<true, 5, 1>), grid, blk, 0, st, g, U, labels); break;
+      case 6: hipLaunchKernelGGL((k_labels<true, 6, 1>), grid, blk, 0, st, g, U, labels); break;
+      case 7: hipLaunchKernelGGL((k_labels<true, 7, 1>), grid, blk, 0, st, g, U, labels); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
   return hipGetLastError();
 }
 

@@ -457,11 +457,12 @@ def test_two_contexts_interleaved_on_two_streams():
     assert np.array_equal(host(b.U), host(ref2.U)) and np.array_equal(host(b.y), host(ref2.y))
 
 
-@pytest.mark.parametrize("r", [1, 4, 10, 64, 300])
+@pytest.mark.parametrize("r", [1, 4, 10, 64, 128, 188, 256, 300, 384, 448])
 def test_labels_argmax_ties_and_layouts(r):
     """nlr_labels on factors written directly into the context's U: exact ties (lowest
     column wins, as numpy's argmax), all-equal rows, the maximum in every column position,
-    16-byte rows (r % 4 == 0) and others; the oracle's labels are the plain argmax."""
+    16-byte rows (r % 4 == 0: one to seven 256-byte pieces per row, one to four rows per
+    16-lane group and step) and others; the oracle's labels are the plain argmax."""
     import torch
     n = 4099
     K = min(r, 4)
