@@ -435,7 +435,7 @@ __global__ __launch_bounds__(kThreads) void k_theta_wide(Geometry g, Bufs B) {
 template <int CPL>
 __global__ __launch_bounds__(kThreads) void k_rows_wide(Geometry g, Bufs B, StepArgs S) {
   if (halted(B.ctl)) return;
-  constexpr int RPI = 4;  // rows per wave and step
+  constexpr int RPI = 8;  // rows per wave and step
   __shared__ double sred[4 * 64 * CPL];
   __shared__ double dred[kThreads + 8];
   const int tid = threadIdx.x;
