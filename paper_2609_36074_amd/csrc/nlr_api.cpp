@@ -48,6 +48,9 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
     const int64_t part_bytes = (int64_t)g.d32 * g.r32 * 4;
     int64_t lim = (int64_t)64 << 20;
     int64_t ga = lim / part_bytes;
+    // above 128 columns the product is a launch of its own (two workgroups per compute
+    // unit): one full round of them, without a partial second round
+    if (g.r32 > 128) ga = 512 / (g.mgroups * g.ngroups);
     if (ga < 16) ga = 16;
     if (ga > 1024) ga = 1024;
     if (ga > g.tilesA) ga = g.tilesA;
