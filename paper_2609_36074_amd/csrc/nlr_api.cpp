@@ -92,6 +92,9 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
   g.nch = g.d32 / 32;
   // Theta resident in pass B's LDS when it fits beside p, s and the reductions in 64 KiB
   g.theta_lds = ((int64_t)g.d32 * g.r32 * 4 + 2 * g.r32 * 4 + (4 * g.r32 + 8) * 8 <= (64 << 10)) ? 1 : 0;
+  // the streamed pass B (Theta from L2 through LDS, 16-byte rows): one persistent round of
+  // two workgroups per compute unit
+  if (!g.theta_lds && aligned16 && d % 4 == 0 && r % 4 == 0 && g.GB > 512) g.GB = 512;
   g.b_res = (g.nch <= 4 && g.NB <= 4 && g.NB * g.nch <= 8 && g.theta_lds && d % 4 == 0 && r % 4 == 0 &&
              aligned16) ? 1 : 0;
   g.ldsB_bytes = (int32_t)((g.theta_lds ? (int64_t)g.d32 * g.r32 * 4 : 0) + 2 * g.r32 * 4 +
