@@ -225,12 +225,23 @@ __global__ __launch_bounds__(kPAThreads) __attribute__((amdgpu_waves_per_eu(2, 2
     Geometry g, Bufs B, StepArgs S) {
   using P = PanelA<NBW>;
   if (halted(B.ctl)) return;
+  // full groups of eight splits (the blocks of a split congruent mod 8: one XCD), then
+  // a partial group of q splits (blocks congruent mod q) on the compute units left over
   const int per = 8 * g.pfb;
-  const int grp = blockIdx.x / per;
-  const int rem = blockIdx.x - grp * per;
-  const int fb = rem >> 3;
-  const int sp = grp * 8 + (rem & 7);
-  if (sp >= g.PS) return;
+  const int full = (g.PS / 8) * per;
+  int fb, sp;
+  if ((int)blockIdx.x < full) {
+    const int grp = blockIdx.x / per;
+    const int rem = blockIdx.x - grp * per;
+    fb = rem >> 3;
+    sp = grp * 8 + (rem & 7);
+  } else {
+    const int q = g.PS % 8;
+    const int rem = blockIdx.x - full;
+    fb = rem / q;
+    sp = (g.PS / 8) * 8 + rem % q;
+  }
+  if (sp >= g.PS || fb >= g.pfb) return;
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
   unsigned char* xring = smem_raw;

@@ -161,13 +161,15 @@ Geometry make_geometry(int64_t n, int32_t d, int32_t r, int32_t K, bool aligned1
     g.panel = 1;
     g.pnbw = g.NB >= 2 ? g.NB / 2 : 1;
     g.pfb = (d + 255) / 256;
-    // one 8-wave workgroup per compute unit; the feature blocks of a split on one XCD
+    // one 8-wave workgroup per compute unit; the feature blocks of a split on one XCD,
+    // then splits whose blocks are spread over XCDs on the compute units left over
     int64_t ps = 8 * (256 / (8 * g.pfb));
+    ps += (256 - ps * g.pfb) / g.pfb;
     const int64_t cap = n / 64 > 1 ? n / 64 : 1;  // at least four 16-row stages per split
     if (ps > cap) ps = cap;
     if (ps < 1) ps = 1;
     g.PS = (int32_t)ps;
-    g.GPA = 8 * g.pfb * ((g.PS + 7) / 8);
+    g.GPA = g.PS * g.pfb;
     // pass B: 256-row tiles in one 8-wave workgroup per compute unit at 128 columns per
     // column wave (pnbw = 4), else 128-row tiles in two 4-wave workgroups per compute unit
     const int prow = g.pnbw == 4 ? 256 : 128;

@@ -107,7 +107,7 @@ struct Geometry {
   int32_t pnbw;         // 32-column blocks per column wave (1, 2 or 4): 64 pnbw columns
   int32_t pfb;          // 256-feature blocks of pass A
   int32_t PS;           // row splits of pass A
-  int32_t GPA;          // pass A workgroups (8 pfb ceil(PS / 8), same XCD per split)
+  int32_t GPA;          // pass A workgroups (PS pfb: groups of 8 splits on one XCD each, then the rest)
   int64_t tilesP;       // 128-row tiles of pass B
   float su;             // power-of-two scale of U in the split (|u| <= sqrt(K))
 };
