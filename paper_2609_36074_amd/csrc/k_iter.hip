@@ -889,6 +889,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
 // P[row][c] (rows [s R/S, (s+1) R/S)).  Grid (ceil(C/64), S); thread (col, sub)
 // sums rows sub, sub+4, ... of the segment, then the four subs are added in order.
 // ---------------------------------------------------------------------------
+// sum over s < S of p[s * stride] in the order s = 0, 1, ...: the loads of eight terms
+// are issued before their additions (a clamped index, so that no load waits behind a
+// branch), which keeps the small reduction kernels from waiting on one load at a time
+template <typename T>
+__device__ __forceinline__ double seq_sum(const T* __restrict__ p, int64_t stride, int64_t S) {
+  double acc = 0.0;
+  for (int64_t s0 = 0; s0 < S; s0 += 8) {
+    double v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (double)p[(s0 + i < S ? s0 + i : S - 1) * stride];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (s0 + i < S) acc += v[i];
+  }
+  return acc;
+}
+
 template <typename T>
 __device__ __forceinline__ void seg_sum_block(const T* __restrict__ P, int64_t R, int C, double* __restrict__ out,
                                               int S, int bx, int by, double* red) {
@@ -898,8 +915,7 @@ __device__ __forceinline__ void seg_sum_block(const T* __restrict__ P, int64_t R
   const int64_t lo = (int64_t)by * R / S;
   const int64_t hi = (int64_t)(by + 1) * R / S;
   double acc = 0.0;
-  if (col < C)
-    for (int64_t row = lo + sub; row < hi; row += 4) acc += (double)P[row * C + col];
+  if (col < C && lo + sub < hi) acc = seq_sum<T>(P + (lo + sub) * C + col, 4 * (int64_t)C, (hi - lo - sub + 3) / 4);
   red[tid] = acc;
   __syncthreads();
   if (tid < 64 && col < C)
@@ -937,8 +953,7 @@ __global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, i
     const int r32 = g.r32;
     const int e = (blockIdx.x - g.RT) * kThreads + threadIdx.x;  // entry k r32 + l
     const int k = e / r32, l = e - k * r32;
-    double G = 0.0;
-    for (int s = 0; s < nseg; ++s) G += B.seg_theta[(int64_t)s * g.theta_cols + (int64_t)g.d32 * r32 + e];
+    const double G = seq_sum<double>(B.seg_theta + (int64_t)g.d32 * r32 + e, g.theta_cols, nseg);
     red[threadIdx.x] = G * B.gram_vec[l];
     __syncthreads();
     for (int w = r32 >> 1; w >= 1; w >>= 1) {
@@ -959,7 +974,7 @@ __global__ __launch_bounds__(kThreads) void k_reduce_theta(Geometry g, Bufs B, i
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   double sum = 0.0;
   if (e < tot) {
-    for (int s = 0; s < nseg; ++s) sum += B.seg_theta[(int64_t)s * g.theta_cols + e];
+    sum = seq_sum<double>(B.seg_theta + e, g.theta_cols, nseg);
     const int f = (int)(e / g.r32);
     // partials of Xhat^T W (fused pass B) carry the scale c of U = c W
     if (scaled) sum *= (double)B.ctl->c_f;
@@ -1002,17 +1017,15 @@ __global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs
   // one already in place, as when the pass does the row work itself)
   if (!finish && !(g.fused8 && ctl->rows_first == 1)) {
     for (int c = tid; c < g.r32; c += kThreads) {
-      double t = 0.0;
-      for (int s = 0; s < g.SA; ++s) t += B.seg_a[(int64_t)s * C + 4 + c];
+      const double t = seq_sum<double>(B.seg_a + 4 + c, C, g.SA);
       B.s[c] = (c < g.r) ? (float)t : 0.f;
     }
   }
   double qq = 0.0, yq = 0.0, th2 = 0.0;
-  if (tid == 0)
-    for (int s = 0; s < g.SA; ++s) {
-      qq += B.seg_a[(int64_t)s * C + 0];
-      yq += B.seg_a[(int64_t)s * C + 1];
-    }
+  if (tid == 0) {
+    qq = seq_sum<double>(B.seg_a + 0, C, g.SA);
+    yq = seq_sum<double>(B.seg_a + 1, C, g.SA);
+  }
   if (!finish)
     for (int k = tid; k < g.RT; k += kThreads) th2 += B.th2_part[k];
   th2 = block_sum_d(th2, red);
@@ -1911,13 +1924,10 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
   const int tid = threadIdx.x;
   const int C = 4 + g.r32;
   if (tid == 0) {
-    double a = 0.0, b = 0.0, h = 0.0, over = 0.0;
-    for (int s = 0; s < g.SB; ++s) {
-      a += B.seg_b[(int64_t)s * C + 0];
-      b += B.seg_b[(int64_t)s * C + 1];
-      h += B.seg_b[(int64_t)s * C + 2];
-      over += B.seg_b[(int64_t)s * C + 3];
-    }
+    const double a = seq_sum<double>(B.seg_b + 0, C, g.SB);
+    const double b = seq_sum<double>(B.seg_b + 1, C, g.SB);
+    const double h = seq_sum<double>(B.seg_b + 2, C, g.SB);
+    const double over = seq_sum<double>(B.seg_b + 3, C, g.SB);
     const double nu = sqrt(a);
     const int64_t t = ctl->t_done;
     nlr_iter_stats* rec = &B.hist[t % kHistCap];
@@ -1958,8 +1968,7 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
   const double c = cbuf[0];
   if (c > 0.0) {
     for (int col = tid; col < g.r32; col += kThreads) {
-      double t = 0.0;
-      for (int s = 0; s < g.SB; ++s) t += B.seg_b[(int64_t)s * C + 4 + col];
+      const double t = seq_sum<double>(B.seg_b + 4 + col, C, g.SB);
       B.p[col] = (col < g.r) ? (float)(c * t) : 0.f;
     }
   }
@@ -2077,8 +2086,7 @@ __device__ __forceinline__ void seg_ab_block(const Geometry& g, const Bufs& B, i
   const int col = bx * 8 + (tid & 7);
   const int sub = tid >> 3;
   double acc = 0.0;
-  if (col < C)
-    for (int64_t row = sub; row < g.GB; row += 32) acc += P[row * C + col];
+  if (col < C && sub < g.GB) acc = seq_sum<double>(P + (int64_t)sub * C + col, 32 * (int64_t)C, (g.GB - sub + 31) / 32);
   red[tid] = acc;
   __syncthreads();
   for (int w = 16; w >= 1; w >>= 1) {
