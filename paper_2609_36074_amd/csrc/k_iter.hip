@@ -1021,15 +1021,16 @@ __global__ __launch_bounds__(kThreads) void k_ctl_a(Geometry g, Bufs B, StepArgs
       B.s[c] = (c < g.r) ? (float)t : 0.f;
     }
   }
-  double qq = 0.0, yq = 0.0, th2 = 0.0;
-  if (tid == 0) {
-    qq = seq_sum<double>(B.seg_a + 0, C, g.SA);
-    yq = seq_sum<double>(B.seg_a + 1, C, g.SA);
-  }
+  // ||q||^2 and ytilde^T q summed by two threads at the same time (past those of s)
+  __shared__ double qy[2];
+  const int tq = g.r32 + 2 <= kThreads ? g.r32 : 0;
+  if (tid == tq || tid == tq + 1) qy[tid - tq] = seq_sum<double>(B.seg_a + (tid - tq), C, g.SA);
+  double th2 = 0.0;
   if (!finish)
     for (int k = tid; k < g.RT; k += kThreads) th2 += B.th2_part[k];
-  th2 = block_sum_d(th2, red);
+  th2 = block_sum_d(th2, red);  // (its barriers also publish qy)
   if (tid == 0) {
+    const double qq = qy[0], yq = qy[1];
     const double rho = sqrt(qq * S.inv_n);
     ctl->rho = rho;
     const int64_t t = ctl->t_done;
@@ -1921,13 +1922,14 @@ __global__ __launch_bounds__(kThreads) void k_ctl_b(Geometry g, Bufs B, StepArgs
   DevCtl* ctl = B.ctl;
   if (halted(ctl)) return;
   __shared__ double cbuf[1];
+  __shared__ double abh[4];
   const int tid = threadIdx.x;
   const int C = 4 + g.r32;
+  // a, b, h and the range flag summed by threads 0..3 at the same time
+  if (tid < 4) abh[tid] = seq_sum<double>(B.seg_b + tid, C, g.SB);
+  __syncthreads();
   if (tid == 0) {
-    const double a = seq_sum<double>(B.seg_b + 0, C, g.SB);
-    const double b = seq_sum<double>(B.seg_b + 1, C, g.SB);
-    const double h = seq_sum<double>(B.seg_b + 2, C, g.SB);
-    const double over = seq_sum<double>(B.seg_b + 3, C, g.SB);
+    const double a = abh[0], b = abh[1], h = abh[2], over = abh[3];
     const double nu = sqrt(a);
     const int64_t t = ctl->t_done;
     nlr_iter_stats* rec = &B.hist[t % kHistCap];
